@@ -1,0 +1,102 @@
+"""CPU oracle for paged decode attention.
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are the only callers. Nothing here is used by the HIP
+library or its Python binding, and nothing here imports them.
+
+Modules:
+  sf_oracle.c  fp64 attention over the gathered cache (C, OpenMP), wrapped below
+  dense_ref    numpy float64 dense softmax attention on tiny inputs
+  exact_ref    high-precision decimal attention for a handful of tokens
+  merge_ref    fp64 log-sum-exp merge of partial attention results
+  plan_ref     re-derivation of the split-K chunk plan from its stated rule
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sf_oracle.c")
+_LIB = os.path.join(_HERE, "libsf_oracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile sf_oracle.c with the host C compiler (plain -O2, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        p = ctypes.c_void_p
+        i = ctypes.c_int
+        L.sf_oracle_decode_attn.argtypes = [i, i, i, i, i, i, i, p, p, p, p, p, ctypes.c_double, p, p, i]
+        L.sf_oracle_decode_attn.restype = i
+        L.sf_oracle_gather.argtypes = [i, i, i, i, i, p, p, p, i, i, i, p, p]
+        L.sf_oracle_gather.restype = i
+        L.sf_oracle_max_threads.restype = i
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _u16(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    assert a.dtype == np.uint16, a.dtype
+    return a
+
+
+def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale, nthreads: int = 0):
+    """fp64 reference. q/k_pool/v_pool are uint16 bf16 bit arrays in the
+    documented layouts; returns (out [B,Hq,D] float64, lse [B,Hq] float64)."""
+    q = _u16(q)
+    k_pool = _u16(k_pool)
+    v_pool = _u16(v_pool)
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    b, hq, d = q.shape
+    n, hkv, p, d2 = k_pool.shape
+    assert d2 == d and v_pool.shape == (n, hkv, d, p) and bt.shape[0] == b and lens.shape == (b,)
+    out = np.empty((b, hq, d), dtype=np.float64)
+    lse = np.empty((b, hq), dtype=np.float64)
+    rc = lib().sf_oracle_decode_attn(b, hq, hkv, d, p, bt.shape[1], n, _ptr(q), _ptr(k_pool),
+                                     _ptr(v_pool), _ptr(bt), _ptr(lens), float(scale),
+                                     _ptr(out), _ptr(lse), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle rejected its input (code {rc})")
+    return out, lse
+
+
+def gather(k_pool, v_pool, block_table, seq: int, kvh: int, length: int):
+    """Dense [L, D] uint16 copies of one (sequence, KV head)'s cached K and V."""
+    k_pool = _u16(k_pool)
+    v_pool = _u16(v_pool)
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    n, hkv, p, d = k_pool.shape
+    kd = np.empty((length, d), dtype=np.uint16)
+    vd = np.empty((length, d), dtype=np.uint16)
+    rc = lib().sf_oracle_gather(hkv, d, p, bt.shape[1], n, _ptr(k_pool), _ptr(v_pool), _ptr(bt),
+                                int(seq), int(kvh), int(length), _ptr(kd), _ptr(vd))
+    if rc != 0:
+        raise ValueError("oracle gather hit an invalid page")
+    return kd, vd
+
+
+def max_threads() -> int:
+    return int(lib().sf_oracle_max_threads())
