@@ -1,0 +1,311 @@
+"""ctypes binding of libsf_decode_attn.so (argument marshalling only).
+
+The names mirror the C entry points declared in include/sf_decode_attn.h.
+Every step of the computation runs in the HIP library; PyTorch only supplies
+device memory and the stream. If the library is missing this module raises:
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libsf_decode_attn.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "sf_decode_attn.h")
+PAGE = 16
+ITEM_INTS = 8
+
+STATUS = {0: "SF_OK", 1: "SF_ERR_INVALID_ARG", 2: "SF_ERR_UNSUPPORTED", 3: "SF_ERR_CAPACITY",
+          4: "SF_ERR_PLAN_MISMATCH", 5: "SF_ERR_HIP"}
+
+
+class SfError(RuntimeError):
+    def __init__(self, where: str, status: int):
+        self.status = int(status)
+        super().__init__(f"{where}: {STATUS.get(self.status, self.status)} ({status_string(self.status)})")
+
+
+class sf_attn_desc(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("block_table_stride", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+
+
+class sf_plan_opts(ctypes.Structure):
+    _fields_ = [("num_cus", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
+                ("units_per_cu", ctypes.c_int32), ("min_chunk_pages", ctypes.c_int32),
+                ("max_chunk_pages", ctypes.c_int32)]
+
+
+class sf_plan_info(ctypes.Structure):
+    _fields_ = [("num_work", ctypes.c_int32), ("num_combine", ctypes.c_int32),
+                ("num_partials", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
+                ("work_bytes", ctypes.c_uint64), ("workspace_bytes", ctypes.c_uint64),
+                ("desc_key", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def lib():
+    """Loads the HIP library (raises if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing; build it with `python -m paper_2601_12784_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    vp = ctypes.c_void_p
+    L.sf_decode_attn_plan.argtypes = [P(sf_attn_desc), vp, P(sf_plan_opts), vp, ctypes.c_uint64,
+                                      P(sf_plan_info)]
+    L.sf_decode_attn.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp,
+                                 vp, ctypes.c_uint64, vp]
+    L.sf_decode_attn_combine.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, ctypes.c_uint64,
+                                         vp, vp, vp]
+    L.sf_debug_gather_kv.argtypes = [P(sf_attn_desc), vp, vp, vp, ctypes.c_int32, ctypes.c_int32,
+                                     ctypes.c_int32, vp, vp, vp]
+    for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv"):
+        getattr(L, fn).restype = ctypes.c_int
+    L.sf_status_string.argtypes = [ctypes.c_int]
+    L.sf_status_string.restype = ctypes.c_char_p
+    L.sf_version.restype = ctypes.c_int32
+    _lib = L
+    return L
+
+
+def header_functions() -> list[str]:
+    """Names of the functions include/sf_decode_attn.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sf_[a-z0-9_]+)\s*\(", text)))
+
+
+def status_string(status: int) -> str:
+    return lib().sf_status_string(int(status)).decode()
+
+
+def version() -> int:
+    return int(lib().sf_version())
+
+
+def make_desc(num_seqs, num_q_heads, num_kv_heads, head_dim, block_table_stride, num_pages,
+              softmax_scale, page_size=PAGE) -> sf_attn_desc:
+    return sf_attn_desc(int(num_seqs), int(num_q_heads), int(num_kv_heads), int(head_dim),
+                        int(page_size), int(block_table_stride), int(num_pages), float(softmax_scale))
+
+
+def make_opts(num_cus=0, chunk_pages=0, units_per_cu=0, min_chunk_pages=0, max_chunk_pages=0):
+    return sf_plan_opts(int(num_cus), int(chunk_pages), int(units_per_cu), int(min_chunk_pages),
+                        int(max_chunk_pages))
+
+
+def _addr(x) -> int | None:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if isinstance(x, torch.Tensor):
+        return x.data_ptr()
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    raise TypeError(type(x))
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(where, st):
+    if st != 0:
+        raise SfError(where, st)
+
+
+def _dev(t: torch.Tensor, name: str, dtype, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on the GPU (got {t.device})")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+# ----------------------------------------------------------------------------
+# the C entry points
+# ----------------------------------------------------------------------------
+def sf_decode_attn_plan(desc: sf_attn_desc, seq_lens, opts: sf_plan_opts | None = None,
+                        work_host=None):
+    """Plans one decode step on the host. seq_lens: int32 host array/tensor.
+
+    work_host: int32 host buffer (numpy or CPU tensor, pinned for async
+    uploads) or None to allocate a numpy buffer of the right size.
+    Returns (info, work_host)."""
+    if isinstance(seq_lens, torch.Tensor):
+        seq_lens = seq_lens.cpu().numpy()
+    lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    if lens.shape != (desc.num_seqs,):
+        raise ValueError("seq_lens must have num_seqs entries")
+    info = sf_plan_info()
+    L = lib()
+    op = ctypes.byref(opts) if opts is not None else None
+    if work_host is None:
+        _check("sf_decode_attn_plan", L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, op,
+                                                            None, 0, ctypes.byref(info)))
+        work_host = np.empty(max(1, info.work_bytes // 4), dtype=np.int32)
+    cap = work_host.numel() * 4 if isinstance(work_host, torch.Tensor) else work_host.nbytes
+    _check("sf_decode_attn_plan", L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, op,
+                                                        _addr(work_host), cap, ctypes.byref(info)))
+    return info, work_host
+
+
+def sf_decode_attn(desc, info, work_host, work_dev, q, k_pool, v_pool, block_table, out, lse=None,
+                   workspace=None, stream=None):
+    """Enqueues the attention kernel (and the work-list upload if work_host is given)."""
+    b, hq, hkv, d = desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
+    _dev(q, "q", torch.bfloat16, (b, hq, d))
+    _dev(k_pool, "k_pool", torch.bfloat16, (desc.num_pages, hkv, PAGE, d))
+    _dev(v_pool, "v_pool", torch.bfloat16, (desc.num_pages, hkv, d, PAGE))
+    _dev(block_table, "block_table", torch.int32, (b, desc.block_table_stride))
+    _dev(out, "out", torch.float32, (b, hq, d))
+    _dev(work_dev, "work_dev", torch.int32)
+    if work_dev.numel() * 4 < info.work_bytes:
+        raise ValueError("work_dev is smaller than the plan")
+    if lse is not None:
+        _dev(lse, "lse", torch.float32, (b, hq))
+    ws_bytes = 0
+    if workspace is not None:
+        _dev(workspace, "workspace", workspace.dtype)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check("sf_decode_attn", lib().sf_decode_attn(
+        ctypes.byref(desc), ctypes.byref(info), _addr(work_host), _addr(work_dev), _addr(q),
+        _addr(k_pool), _addr(v_pool), _addr(block_table), _addr(out), _addr(lse),
+        _addr(workspace), ws_bytes, _stream(stream)))
+
+
+def sf_decode_attn_combine(desc, info, work_dev, workspace, out, lse=None, stream=None):
+    """Enqueues the log-sum-exp merge of split sequences (no-op if none)."""
+    if info.num_combine == 0:
+        return
+    _dev(out, "out", torch.float32, (desc.num_seqs, desc.num_q_heads, desc.head_dim))
+    _dev(work_dev, "work_dev", torch.int32)
+    _dev(workspace, "workspace", workspace.dtype)
+    if lse is not None:
+        _dev(lse, "lse", torch.float32, (desc.num_seqs, desc.num_q_heads))
+    _check("sf_decode_attn_combine", lib().sf_decode_attn_combine(
+        ctypes.byref(desc), ctypes.byref(info), _addr(work_dev), _addr(workspace),
+        workspace.numel() * workspace.element_size(), _addr(out), _addr(lse), _stream(stream)))
+
+
+def sf_debug_gather_kv(desc, k_pool, v_pool, block_table, seq, kv_head, length, k_dense, v_dense,
+                       stream=None):
+    """Dense [length, D] bf16 copies of one (sequence, KV head) via the kernel's translation."""
+    d = desc.head_dim
+    _dev(k_pool, "k_pool", torch.bfloat16)
+    _dev(v_pool, "v_pool", torch.bfloat16)
+    _dev(block_table, "block_table", torch.int32)
+    _dev(k_dense, "k_dense", torch.bfloat16, (length, d))
+    _dev(v_dense, "v_dense", torch.bfloat16, (length, d))
+    _check("sf_debug_gather_kv", lib().sf_debug_gather_kv(
+        ctypes.byref(desc), _addr(k_pool), _addr(v_pool), _addr(block_table), int(seq),
+        int(kv_head), int(length), _addr(k_dense), _addr(v_dense), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------
+# convenience runner: owns the pinned work-list ring and the device buffers
+# ----------------------------------------------------------------------------
+class DecodeAttention:
+    """Plan + attention + combine for successive decode steps on one stream.
+
+    Host work lists go through a ring of pinned buffers; a buffer is rewritten
+    only after the event recorded behind its last upload has completed.
+    Device work list and workspace are torch allocations grown on demand.
+    """
+
+    def __init__(self, num_q_heads, num_kv_heads, head_dim, device=None, num_cus=None,
+                 ring: int = 4, opts: sf_plan_opts | None = None):
+        self.hq, self.hkv, self.d = int(num_q_heads), int(num_kv_heads), int(head_dim)
+        self.device = torch.device(device or "cuda")
+        if num_cus is None:
+            num_cus = torch.cuda.get_device_properties(self.device).multi_processor_count
+        self.opts = opts if opts is not None else make_opts(num_cus=num_cus)
+        if self.opts.num_cus == 0:
+            self.opts.num_cus = num_cus
+        self._ring = [None] * ring
+        self._events = [None] * ring
+        self._next = 0
+        self.work_dev = torch.empty(0, dtype=torch.int32, device=self.device)
+        self.workspace = torch.empty(0, dtype=torch.uint8, device=self.device)
+        self.last_info = None
+
+    def _pinned(self, nints: int) -> torch.Tensor:
+        i = self._next
+        self._next = (i + 1) % len(self._ring)
+        if self._events[i] is not None:
+            self._events[i].synchronize()
+        buf = self._ring[i]
+        if buf is None or buf.numel() < nints:
+            buf = torch.empty(max(nints, 1024), dtype=torch.int32, pin_memory=True)
+            self._ring[i] = buf
+        return i, buf
+
+    def plan(self, seq_lens, block_table_stride, num_pages, scale, chunk_pages=None):
+        desc = make_desc(len(seq_lens), self.hq, self.hkv, self.d, block_table_stride, num_pages, scale)
+        opts = self.opts
+        if chunk_pages is not None:
+            opts = sf_plan_opts(opts.num_cus, int(chunk_pages), opts.units_per_cu,
+                                opts.min_chunk_pages, opts.max_chunk_pages)
+        info, _ = self._plan_sizes(desc, seq_lens, opts)
+        slot, buf = self._pinned(info.work_bytes // 4)
+        info, _ = sf_decode_attn_plan(desc, seq_lens, opts, work_host=buf)
+        return desc, info, slot, buf
+
+    @staticmethod
+    def _plan_sizes(desc, seq_lens, opts):
+        if isinstance(seq_lens, torch.Tensor):
+            seq_lens = seq_lens.cpu().numpy()
+        lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+        info = sf_plan_info()
+        _check("sf_decode_attn_plan", lib().sf_decode_attn_plan(
+            ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts), None, 0, ctypes.byref(info)))
+        return info, None
+
+    def _ensure(self, info):
+        nints = info.work_bytes // 4
+        if self.work_dev.numel() < nints:
+            self.work_dev = torch.empty(max(nints, 1024), dtype=torch.int32, device=self.device)
+        if self.workspace.numel() < info.workspace_bytes:
+            self.workspace = torch.empty(int(info.workspace_bytes * 1.25) + 256, dtype=torch.uint8,
+                                         device=self.device)
+
+    def __call__(self, q, k_pool, v_pool, block_table, seq_lens, scale, out=None, lse=None,
+                 chunk_pages=None, stream=None):
+        b = q.shape[0]
+        if out is None:
+            out = torch.empty((b, self.hq, self.d), dtype=torch.float32, device=self.device)
+        desc, info, slot, buf = self.plan(seq_lens, block_table.shape[1], k_pool.shape[0], scale,
+                                          chunk_pages)
+        self._ensure(info)
+        st = _stream(stream)
+        sf_decode_attn(desc, info, buf, self.work_dev, q, k_pool, v_pool, block_table, out, lse,
+                       self.workspace, stream=st)
+        ev = torch.cuda.Event()
+        ev.record(torch.cuda.current_stream() if stream is None else torch.cuda.ExternalStream(st))
+        self._events[slot] = ev
+        sf_decode_attn_combine(desc, info, self.work_dev, self.workspace, out, lse, stream=st)
+        self.last_info = info
+        return out

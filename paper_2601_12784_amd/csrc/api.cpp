@@ -1,0 +1,139 @@
+// C entry points: argument checks on the host, then stream-ordered launches.
+// Nothing here allocates device memory or keeps state between calls.
+#include <cmath>
+#include <cstdint>
+
+#include "sf_internal.h"
+
+using namespace sf;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+sf_status check_plan(const sf_attn_desc* d, const sf_plan_info* info) {
+  if (!info) return SF_ERR_INVALID_ARG;
+  if (info->desc_key != desc_key(d)) return SF_ERR_PLAN_MISMATCH;
+  if (info->num_work < 0 || info->num_combine < 0 || info->num_partials < 0) return SF_ERR_INVALID_ARG;
+  if (info->work_bytes != uint64_t(info->num_work + info->num_combine) * kItemInts * 4)
+    return SF_ERR_PLAN_MISMATCH;
+  return SF_OK;
+}
+
+sf_status from_hip(hipError_t e) { return e == hipSuccess ? SF_OK : SF_ERR_HIP; }
+
+}  // namespace
+
+extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info* info,
+                                    const int32_t* work_host, int32_t* work_dev, const void* q,
+                                    const void* k_pool, const void* v_pool,
+                                    const int32_t* block_table, float* out, float* lse,
+                                    void* workspace, uint64_t workspace_bytes, void* stream) {
+  sf_status st = validate_desc(desc);
+  if (st != SF_OK) return st;
+  if ((st = check_plan(desc, info)) != SF_OK) return st;
+  if (info->num_work == 0) return SF_OK;
+  if (!work_dev || !q || !k_pool || !v_pool || !block_table || !out) return SF_ERR_INVALID_ARG;
+  if (!aligned16(work_dev) || !aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) ||
+      !aligned16(out) || !aligned4(block_table) || (lse && !aligned4(lse)))
+    return SF_ERR_INVALID_ARG;
+  if (workspace_bytes < info->workspace_bytes) return SF_ERR_CAPACITY;
+  if (info->workspace_bytes && (!workspace || !aligned16(workspace))) return SF_ERR_INVALID_ARG;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (work_host) {
+    hipError_t e = hipMemcpyAsync(work_dev, work_host, info->work_bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return SF_ERR_HIP;
+  }
+  const int32_t g = desc->num_q_heads / desc->num_kv_heads;
+  Workspace ws = carve_workspace(workspace, info->num_partials, g, desc->head_dim);
+  AttnArgs a;
+  a.work = work_dev;
+  a.num_work = info->num_work;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_table = block_table;
+  a.out = out;
+  a.lse = lse;
+  a.part_o = info->num_partials ? ws.part_o : nullptr;
+  a.part_lse = info->num_partials ? ws.part_lse : nullptr;
+  a.num_q_heads = desc->num_q_heads;
+  a.num_kv_heads = desc->num_kv_heads;
+  a.group = g;
+  a.head_dim = desc->head_dim;
+  a.bt_stride = desc->block_table_stride;
+  a.scale_log2 = float(double(desc->softmax_scale) * 1.4426950408889634074);
+  return from_hip(launch_attention(a, s));
+}
+
+extern "C" sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_plan_info* info,
+                                            const int32_t* work_dev, const void* workspace,
+                                            uint64_t workspace_bytes, float* out, float* lse,
+                                            void* stream) {
+  sf_status st = validate_desc(desc);
+  if (st != SF_OK) return st;
+  if ((st = check_plan(desc, info)) != SF_OK) return st;
+  if (info->num_combine == 0) return SF_OK;
+  if (!work_dev || !workspace || !out) return SF_ERR_INVALID_ARG;
+  if (!aligned16(work_dev) || !aligned16(workspace) || !aligned16(out) || (lse && !aligned4(lse)))
+    return SF_ERR_INVALID_ARG;
+  if (workspace_bytes < info->workspace_bytes) return SF_ERR_CAPACITY;
+  const int32_t g = desc->num_q_heads / desc->num_kv_heads;
+  Workspace ws = carve_workspace(const_cast<void*>(workspace), info->num_partials, g, desc->head_dim);
+  CombineArgs a;
+  a.items = work_dev + int64_t(info->num_work) * kItemInts;
+  a.num_items = info->num_combine;
+  a.part_o = ws.part_o;
+  a.part_lse = ws.part_lse;
+  a.out = out;
+  a.lse = lse;
+  a.num_q_heads = desc->num_q_heads;
+  a.group = g;
+  a.head_dim = desc->head_dim;
+  return from_hip(launch_combine(a, static_cast<hipStream_t>(stream)));
+}
+
+extern "C" sf_status sf_debug_gather_kv(const sf_attn_desc* desc, const void* k_pool,
+                                        const void* v_pool, const int32_t* block_table,
+                                        int32_t seq, int32_t kv_head, int32_t len, void* k_dense,
+                                        void* v_dense, void* stream) {
+  sf_status st = validate_desc(desc);
+  if (st != SF_OK) return st;
+  if (seq < 0 || seq >= desc->num_seqs || kv_head < 0 || kv_head >= desc->num_kv_heads || len < 0)
+    return SF_ERR_INVALID_ARG;
+  if ((int64_t(len) + kPage - 1) / kPage > desc->block_table_stride) return SF_ERR_INVALID_ARG;
+  if (len == 0) return SF_OK;
+  if (!k_pool || !v_pool || !block_table || !k_dense || !v_dense) return SF_ERR_INVALID_ARG;
+  if (!aligned16(k_pool) || !aligned16(v_pool) || !aligned4(block_table) || !aligned16(k_dense) ||
+      !aligned16(v_dense))
+    return SF_ERR_INVALID_ARG;
+  GatherArgs a;
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_table = block_table;
+  a.k_dense = static_cast<uint16_t*>(k_dense);
+  a.v_dense = static_cast<uint16_t*>(v_dense);
+  a.seq = seq;
+  a.kv_head = kv_head;
+  a.len = len;
+  a.num_kv_heads = desc->num_kv_heads;
+  a.head_dim = desc->head_dim;
+  a.bt_stride = desc->block_table_stride;
+  return from_hip(launch_gather(a, static_cast<hipStream_t>(stream)));
+}
+
+extern "C" const char* sf_status_string(sf_status s) {
+  switch (s) {
+    case SF_OK: return "ok";
+    case SF_ERR_INVALID_ARG: return "invalid argument";
+    case SF_ERR_UNSUPPORTED: return "unsupported shape (head_dim must be 64 or 128, page_size 16, Hq/Hkv <= 16)";
+    case SF_ERR_CAPACITY: return "buffer smaller than the plan requires";
+    case SF_ERR_PLAN_MISMATCH: return "plan was built for a different descriptor";
+    case SF_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+extern "C" int32_t sf_version(void) { return (1 << 16) | 0; }

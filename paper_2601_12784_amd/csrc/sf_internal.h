@@ -1,0 +1,83 @@
+// Internal declarations shared by the host-side API, the planner and the
+// kernel launchers of the decode-attention library.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "sf_decode_attn.h"
+
+namespace sf {
+
+constexpr int kPage = 16;       // tokens per KV page
+constexpr int kItemInts = 8;    // int32 fields per work-list row
+constexpr int kMaxGroup = 16;   // query heads per KV head handled by one MFMA column block
+
+// Defaults of the length-aware chunk rule (see sf_decode_attn_plan).
+constexpr int kDefaultNumCus = 256;
+constexpr int kDefaultUnitsPerCu = 8;
+constexpr int kDefaultMinChunk = 16;
+constexpr int kDefaultMaxChunk = 4096;
+
+sf_status validate_desc(const sf_attn_desc* d);
+uint64_t desc_key(const sf_attn_desc* d);
+uint64_t align256(uint64_t x);
+
+// Partial-result workspace: o [slots][g][D] fp32, then lse [slots][g] fp32 (log2 units).
+struct Workspace {
+  float* part_o;
+  float* part_lse;
+};
+Workspace carve_workspace(void* base, int32_t slots, int32_t g, int32_t d);
+
+struct AttnArgs {
+  const int32_t* work;
+  int32_t num_work;
+  const uint16_t* q;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_table;
+  float* out;
+  float* lse;
+  float* part_o;
+  float* part_lse;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;
+  int32_t head_dim;
+  int32_t bt_stride;
+  float scale_log2;   // softmax_scale * log2(e)
+};
+
+struct CombineArgs {
+  const int32_t* items;
+  int32_t num_items;
+  const float* part_o;
+  const float* part_lse;
+  float* out;
+  float* lse;
+  int32_t num_q_heads;
+  int32_t group;
+  int32_t head_dim;
+};
+
+struct GatherArgs {
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_table;
+  uint16_t* k_dense;
+  uint16_t* v_dense;
+  int32_t seq;
+  int32_t kv_head;
+  int32_t len;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t bt_stride;
+};
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
+
+}  // namespace sf

@@ -1,0 +1,240 @@
+"""Host-only checks of the C ABI: exported symbols, the split-K planner
+(bit-exact against the re-derivation in oracle/plan_ref.py), and argument
+checks that must reject bad calls before anything reaches the device."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from oracle import plan_ref
+from paper_2601_12784_amd import binding as B
+
+PAGE = 16
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.lib()
+
+
+def test_exports_every_declared_function(lib):
+    names = B.header_functions()
+    assert {"sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine",
+            "sf_debug_gather_kv", "sf_status_string", "sf_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_status_strings(lib):
+    assert B.version() >> 16 == 1
+    for st in range(6):
+        assert B.status_string(st)
+    assert B.status_string(99) == "unknown status"
+
+
+def test_struct_sizes_match_header():
+    assert ctypes.sizeof(B.sf_attn_desc) == 32
+    assert ctypes.sizeof(B.sf_plan_opts) == 20
+    assert ctypes.sizeof(B.sf_plan_info) == 40
+
+
+# ---------------------------------------------------------------------------
+# planner parity
+# ---------------------------------------------------------------------------
+def _plan_both(lens, hq, hkv, d, num_cus=256, chunk=0, upc=0, mn=0, mx=0, stride=None):
+    lens = np.asarray(lens, dtype=np.int32)
+    if stride is None:
+        stride = max(1, int(((lens.astype(np.int64) + PAGE - 1) // PAGE).max(initial=1)))
+    desc = B.make_desc(lens.size, hq, hkv, d, stride, 1, 0.1)
+    opts = B.make_opts(num_cus=num_cus, chunk_pages=chunk, units_per_cu=upc,
+                       min_chunk_pages=mn, max_chunk_pages=mx)
+    info, work = B.sf_decode_attn_plan(desc, lens, opts)
+    ref = plan_ref.plan(lens, hkv, hq, d, num_cus, chunk, upc or None, mn or None, mx or None)
+    return info, work[: info.work_bytes // 4].reshape(-1, 8), ref
+
+
+def _assert_same(info, work, ref):
+    assert info.chunk_pages == ref["chunk_pages"]
+    assert info.num_work == ref["items"].shape[0]
+    assert info.num_combine == ref["combine"].shape[0]
+    assert info.num_partials == ref["num_partials"]
+    assert info.workspace_bytes == ref["workspace_bytes"]
+    assert info.work_bytes == ref["work_bytes"]
+    assert np.array_equal(work[: info.num_work], ref["items"])
+    assert np.array_equal(work[info.num_work:], ref["combine"])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_plan_matches_rederivation_random(seed):
+    rng = np.random.default_rng(seed)
+    b = int(rng.integers(1, 300))
+    lens = np.exp(rng.normal(np.log(1500), 1.2, size=b)).astype(np.int64).clip(0, 40000)
+    lens[rng.random(b) < 0.05] = 0
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    g = int(rng.choice([1, 4, 5, 7, 16]))
+    info, work, ref = _plan_both(lens, hkv * g, hkv, 128, num_cus=int(rng.choice([8, 80, 256])))
+    _assert_same(info, work, ref)
+
+
+@pytest.mark.parametrize("chunk", [1, 2, 7, 64, 1 << 20])
+def test_plan_matches_rederivation_forced_chunk(chunk):
+    lens = [17, 64, 130, 300, 0, 1, 16, 33]
+    info, work, ref = _plan_both(lens, 4, 1, 64, chunk=chunk)
+    _assert_same(info, work, ref)
+
+
+def test_plan_matches_rederivation_knobs():
+    lens = np.arange(0, 5000, 37)
+    info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=32, upc=3, mn=5, mx=40)
+    _assert_same(info, work, ref)
+    assert info.chunk_pages == 40
+
+
+def test_tiny_plan_by_hand():
+    """L = {17, 64, 130, 300}: pages {2, 4, 9, 19}, T = 34 page-heads -> chunk 16
+    (clamped up); only the 19-page sequence splits, into pages [0,9) and [9,19).
+    The two 9-page items tie and go in sequence order."""
+    info, work, _ = _plan_both([17, 64, 130, 300], 4, 1, 64)
+    assert info.chunk_pages == 16 and info.num_work == 5 and info.num_combine == 1
+    assert info.num_partials == 2
+    expect = [[3, 0, 9, 19, 300, 1, 1, 2],
+              [2, 0, 0, 9, 130, -1, 0, 1],
+              [3, 0, 0, 9, 300, 0, 0, 2],
+              [1, 0, 0, 4, 64, -1, 0, 1],
+              [0, 0, 0, 2, 17, -1, 0, 1],
+              [3, 0, 0, 2, 0, 0, 0, 0]]
+    assert np.array_equal(work, np.array(expect, dtype=np.int32))
+    assert info.workspace_bytes == 2 * 4 * 64 * 4 + 256
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_plan_invariants(seed):
+    """Chunks tile [0, pages) exactly; none exceeds the chunk size; slots are
+    a permutation of [0, num_partials); order is by size, largest first."""
+    rng = np.random.default_rng(100 + seed)
+    lens = rng.integers(0, 20000, size=int(rng.integers(1, 200)))
+    hkv = 4
+    info, work, _ = _plan_both(lens, 28, hkv, 128, num_cus=int(rng.integers(1, 300)))
+    items = work[: info.num_work]
+    comb = work[info.num_work:]
+    sizes = items[:, 3] - items[:, 2]
+    assert np.all(np.diff(sizes) <= 0)
+    assert np.all(sizes <= info.chunk_pages)
+    slots = items[items[:, 5] >= 0, 5]
+    assert np.array_equal(np.sort(slots), np.arange(info.num_partials))
+    for s, L in enumerate(lens):
+        npg = (int(L) + PAGE - 1) // PAGE
+        for kvh in range(hkv):
+            mine = items[(items[:, 0] == s) & (items[:, 1] == kvh)]
+            assert np.all(mine[:, 4] == L)
+            mine = mine[np.argsort(mine[:, 6])]
+            n = mine.shape[0]
+            assert np.array_equal(mine[:, 6], np.arange(n)) and np.all(mine[:, 7] == n)
+            if npg == 0:
+                assert n == 1 and mine[0, 2] == mine[0, 3] == 0
+                continue
+            assert mine[0, 2] == 0 and mine[-1, 3] == npg
+            assert np.all(mine[1:, 2] == mine[:-1, 3]) and np.all(mine[:, 3] > mine[:, 2])
+            if n > 1:
+                row = comb[(comb[:, 0] == s) & (comb[:, 1] == kvh)]
+                assert row.shape[0] == 1 and row[0, 3] == n
+                assert np.array_equal(mine[:, 5], row[0, 2] + np.arange(n))
+            else:
+                assert mine[0, 5] == -1
+
+
+def test_plan_size_query_and_capacity(lib):
+    lens = np.array([100, 5000, 3], np.int32)
+    desc = B.make_desc(3, 8, 2, 128, 400, 1, 0.1)
+    info = B.sf_plan_info()
+    st = lib.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, None, None, 0, ctypes.byref(info))
+    assert st == 0 and info.work_bytes > 0
+    small = np.zeros(info.work_bytes // 4 - 1, np.int32)
+    st = lib.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, None, small.ctypes.data,
+                                 small.nbytes, ctypes.byref(info))
+    assert st == 3  # SF_ERR_CAPACITY
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, 2), ("page_size", 32, 2), ("num_q_heads", 34, 2),
+    ("num_q_heads", 31, 1), ("num_seqs", -1, 1), ("block_table_stride", 0, 1),
+    ("softmax_scale", float("nan"), 1),
+])
+def test_plan_rejects_bad_descriptor(lib, field, value, status):
+    desc = B.make_desc(2, 8, 2, 128, 10, 4, 0.1)
+    setattr(desc, field, value)
+    lens = np.array([10, 20], np.int32)
+    info = B.sf_plan_info()
+    assert lib.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, None, None, 0,
+                                   ctypes.byref(info)) == status
+
+
+def test_plan_rejects_bad_lengths(lib):
+    desc = B.make_desc(2, 8, 2, 128, 2, 4, 0.1)
+    info = B.sf_plan_info()
+    for lens in ([10, -1], [10, 33]):  # negative; 3 pages > stride 2
+        arr = np.array(lens, np.int32)
+        assert lib.sf_decode_attn_plan(ctypes.byref(desc), arr.ctypes.data, None, None, 0,
+                                       ctypes.byref(info)) == 1
+
+
+# ---------------------------------------------------------------------------
+# sf_decode_attn / combine argument checks (all fail before any HIP call)
+# ---------------------------------------------------------------------------
+FAKE = 0x10000  # aligned, never dereferenced: every case below must be rejected first
+
+
+def _planned(lens=(40, 3000)):
+    lens = np.array(lens, np.int32)
+    desc = B.make_desc(len(lens), 8, 2, 128, 200, 400, 0.1)
+    info, work = B.sf_decode_attn_plan(desc, lens, B.make_opts(num_cus=4, chunk_pages=16))
+    return desc, info, work
+
+
+def _call(lib, desc, info, **kw):
+    a = dict(work_host=None, work_dev=FAKE, q=FAKE, k=FAKE, v=FAKE, bt=FAKE, out=FAKE, lse=None,
+             ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return lib.sf_decode_attn(ctypes.byref(desc), ctypes.byref(info), a["work_host"], a["work_dev"],
+                              a["q"], a["k"], a["v"], a["bt"], a["out"], a["lse"], a["ws"],
+                              a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), 1), (dict(k=None), 1), (dict(v=None), 1), (dict(bt=None), 1),
+    (dict(out=None), 1), (dict(work_dev=None), 1),
+    (dict(q=FAKE + 8), 1), (dict(out=FAKE + 4), 1), (dict(bt=FAKE + 2), 1), (dict(lse=FAKE + 1), 1),
+    (dict(ws_bytes=0), 3), (dict(ws=None), 1), (dict(ws=FAKE + 8), 1),
+])
+def test_attn_rejects_bad_arguments(lib, kw, status):
+    desc, info, _ = _planned()
+    assert info.workspace_bytes > 0
+    assert _call(lib, desc, info, **kw) == status
+
+
+def test_attn_rejects_mismatched_plan(lib):
+    desc, info, _ = _planned()
+    other = B.make_desc(desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim,
+                        desc.block_table_stride + 1, desc.num_pages, desc.softmax_scale)
+    assert _call(lib, other, info) == 4
+    bad = B.sf_plan_info.from_buffer_copy(info)
+    bad.work_bytes += 32
+    assert _call(lib, desc, bad) == 4
+
+
+def test_combine_rejects_bad_arguments(lib):
+    desc, info, _ = _planned()
+    assert info.num_combine > 0
+    c = lib.sf_decode_attn_combine
+    assert c(ctypes.byref(desc), ctypes.byref(info), FAKE, FAKE, 0, FAKE, None, None) == 3
+    assert c(ctypes.byref(desc), ctypes.byref(info), None, FAKE, 1 << 30, FAKE, None, None) == 1
+    assert c(ctypes.byref(desc), ctypes.byref(info), FAKE, FAKE, 1 << 30, FAKE + 4, None, None) == 1
+
+
+def test_gather_rejects_bad_arguments(lib):
+    desc = B.make_desc(2, 8, 2, 128, 4, 10, 0.1)
+    g = lib.sf_debug_gather_kv
+    assert g(ctypes.byref(desc), FAKE, FAKE, FAKE, 2, 0, 5, FAKE, FAKE, None) == 1   # seq out of range
+    assert g(ctypes.byref(desc), FAKE, FAKE, FAKE, 0, 2, 5, FAKE, FAKE, None) == 1   # kv head
+    assert g(ctypes.byref(desc), FAKE, FAKE, FAKE, 0, 0, 65, FAKE, FAKE, None) == 1  # > stride pages
+    assert g(ctypes.byref(desc), FAKE, FAKE, FAKE, 0, 0, 5, FAKE + 8, FAKE, None) == 1

@@ -1,0 +1,260 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Acceptance for floating point (bf16 inputs, fp32 accumulation and output):
+elementwise |gpu - ref| <= 2e-3 + 1e-2 * |ref| for out and for lse.
+Integer and byte work (block-table gathers, plans) must match bit for bit.
+"""
+import functools
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2601_12784_amd import binding as B
+from paper_2601_12784_amd.workloads import (PAGE, bf16_bits, build_batch, make_batch,
+                                            make_straggler)
+
+pytestmark = pytest.mark.gpu
+
+ATOL, RTOL = 2e-3, 1e-2
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    _need_gpu()
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def to_dev(batch):
+    return dict(q=batch.q.cuda(), k=batch.k_pool.cuda(), v=batch.v_pool.cuda(),
+                bt=torch.from_numpy(batch.block_table).cuda())
+
+
+def run_gpu(batch, dev=None, chunk_pages=None, runner=None, lse=True):
+    dev = dev or to_dev(batch)
+    runner = runner or B.DecodeAttention(batch.num_q_heads, batch.num_kv_heads, batch.head_dim)
+    lse_t = torch.empty((batch.num_seqs, batch.num_q_heads), dtype=torch.float32, device="cuda") if lse else None
+    out = runner(dev["q"], dev["k"], dev["v"], dev["bt"], batch.seq_lens, batch.scale, lse=lse_t,
+                 chunk_pages=chunk_pages)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), (lse_t.cpu().numpy() if lse else None), runner
+
+
+def run_oracle(batch):
+    return oracle.decode_attn(bf16_bits(batch.q), bf16_bits(batch.k_pool), bf16_bits(batch.v_pool),
+                              batch.block_table, batch.seq_lens, batch.scale)
+
+
+def assert_close(gpu, ref, what=""):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    fin = np.isfinite(ref)
+    assert np.array_equal(np.isfinite(gpu), fin), f"{what}: finiteness differs"
+    assert np.array_equal(gpu[~fin], ref[~fin]), f"{what}: non-finite values differ"
+    err = np.abs(gpu[fin] - ref[fin])
+    bound = ATOL + RTOL * np.abs(ref[fin])
+    worst = float((err / bound).max(initial=0.0))
+    _say(f"  {what}: max|err| {err.max(initial=0):.3e}  worst err/bound {worst:.3f}  n={err.size}")
+    assert worst <= 1.0, f"{what}: tolerance exceeded ({worst:.3f} of bound)"
+
+
+def check_batch(batch, ref=None, chunk_pages=None, dev=None):
+    ref = ref or run_oracle(batch)
+    out, lse, runner = run_gpu(batch, dev=dev, chunk_pages=chunk_pages)
+    assert_close(out, ref[0], f"{batch.name} out chunk={chunk_pages}")
+    assert_close(lse, ref[1], f"{batch.name} lse chunk={chunk_pages}")
+    return out, lse, runner.last_info
+
+
+@functools.lru_cache(maxsize=None)
+def named(name):
+    return make_batch(name)
+
+
+@functools.lru_cache(maxsize=None)
+def named_ref(name):
+    return run_oracle(named(name))
+
+
+# ---------------------------------------------------------------------------
+# block-table translation: bit exact
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("which", ["tiny", "d128"])
+def test_gather_is_bit_exact(which):
+    if which == "tiny":
+        b = named("tiny")
+    else:
+        b = build_batch([1, 15, 16, 17, 300, 33], 8, 2, 128, 31, pool_pages=80)
+    dev = to_dev(b)
+    desc = B.make_desc(b.num_seqs, b.num_q_heads, b.num_kv_heads, b.head_dim,
+                       b.block_table.shape[1], b.num_pages, b.scale)
+    for s in range(b.num_seqs):
+        L = int(b.seq_lens[s])
+        for kvh in range(b.num_kv_heads):
+            kd = torch.empty((L, b.head_dim), dtype=torch.bfloat16, device="cuda")
+            vd = torch.empty_like(kd)
+            B.sf_debug_gather_kv(desc, dev["k"], dev["v"], dev["bt"], s, kvh, L, kd, vd)
+            torch.cuda.synchronize()
+            rk, rv = oracle.gather(bf16_bits(b.k_pool), bf16_bits(b.v_pool), b.block_table, s, kvh, L)
+            assert np.array_equal(bf16_bits(kd.cpu()), rk)
+            assert np.array_equal(bf16_bits(vd.cpu()), rv)
+
+
+# ---------------------------------------------------------------------------
+# the tiny config, every chunking
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("chunk", [None, 1, 2, 7, 64, 1 << 20])
+def test_tiny_parity(chunk):
+    _say(f"tiny chunk={chunk}")
+    check_batch(named("tiny"), named_ref("tiny"), chunk_pages=chunk)
+
+
+def test_chunk_count_invariance():
+    b = build_batch([1, 17, 100, 513, 2000, 4099], 28, 4, 128, 32)
+    dev = to_dev(b)
+    ref = run_oracle(b)
+    base, base_lse, _ = run_gpu(b, dev=dev, chunk_pages=1 << 20)
+    assert_close(base, ref[0], "unsplit")
+    for chunk in (1, 2, 7, 64):
+        out, lse, runner = run_gpu(b, dev=dev, chunk_pages=chunk)
+        assert runner.last_info.num_combine > 0
+        assert_close(out, ref[0], f"chunk={chunk}")
+        assert_close(lse, ref[1], f"lse chunk={chunk}")
+        assert np.allclose(out, base, rtol=1e-4, atol=1e-5), f"chunk={chunk} drifts from unsplit"
+
+
+# ---------------------------------------------------------------------------
+# exact special cases
+# ---------------------------------------------------------------------------
+def test_length_one_returns_v_row_bitwise():
+    b = build_batch([1] * 9, 28, 4, 128, 33)
+    out, lse, _ = run_gpu(b)
+    g = 7
+    vb = bf16_bits(b.v_pool)
+    for s in range(9):
+        pg = b.block_table[s, 0]
+        for h in range(28):
+            v = (vb[pg, h // g, :, 0].astype(np.uint32) << 16).view(np.float32)
+            assert np.array_equal(out[s, h], v)
+
+
+def test_dominant_key_returns_its_v_row_bitwise():
+    d, length, hot = 128, 200, 137
+    b = build_batch([length], 4, 1, d, 34)
+    q = np.zeros(d, np.float32)
+    q[0] = 64.0
+    bf16_bits(b.q)[0, :] = (q.view(np.uint32) >> 16).astype(np.uint16)
+    kb = bf16_bits(b.k_pool)
+    for t in range(length):
+        kb[b.block_table[0, t // PAGE], 0, t % PAGE, 0] = 0x4280 if t == hot else 0  # 64.0 / 0.0
+    out, _, _ = run_gpu(b)
+    pg = b.block_table[0, hot // PAGE]
+    v = (bf16_bits(b.v_pool)[pg, 0, :, hot % PAGE].astype(np.uint32) << 16).view(np.float32)
+    for h in range(4):
+        assert np.array_equal(out[0, h], v)
+
+
+def test_empty_sequences_give_zero_and_neg_inf():
+    b = build_batch([0, 40, 0, 1, 0], 8, 2, 128, 35)
+    ref = run_oracle(b)
+    out, lse, _ = run_gpu(b)
+    assert np.all(out[[0, 2, 4]] == 0.0) and np.all(np.isneginf(lse[[0, 2, 4]]))
+    assert_close(out, ref[0], "with empties")
+    assert_close(lse, ref[1], "lse with empties")
+
+
+def test_all_empty_batch():
+    b = build_batch([0, 0], 8, 2, 64, 36)
+    out, lse, _ = run_gpu(b)
+    assert np.all(out == 0.0) and np.all(np.isneginf(lse))
+
+
+def test_page_permutation_is_bitwise_invariant():
+    b = named("tiny")
+    out0, lse0, _ = run_gpu(b)
+    perm = np.random.default_rng(5).permutation(b.num_pages)
+    k2 = torch.empty_like(b.k_pool)
+    v2 = torch.empty_like(b.v_pool)
+    k2[torch.from_numpy(perm)] = b.k_pool
+    v2[torch.from_numpy(perm)] = b.v_pool
+    bt2 = b.block_table.copy()
+    bt2[bt2 >= 0] = perm[bt2[bt2 >= 0]]
+    dev = dict(q=b.q.cuda(), k=k2.cuda(), v=v2.cuda(), bt=torch.from_numpy(bt2).cuda())
+    out1, lse1, _ = run_gpu(b, dev=dev)
+    assert np.array_equal(out0, out1) and np.array_equal(lse0, lse1)
+
+
+def test_run_to_run_bitwise_determinism():
+    b = build_batch([3000, 17, 800, 12000], 28, 4, 128, 37)
+    dev = to_dev(b)
+    o1, l1, _ = run_gpu(b, dev=dev)
+    o2, l2, _ = run_gpu(b, dev=dev)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+def test_nan_poisoned_tails_do_not_leak():
+    b = build_batch([1, 15, 17, 31, 33, 47], 8, 2, 128, 38, pool_pages=20)
+    assert np.any(np.isnan(b.k_pool.float().numpy()))
+    out, lse, _ = run_gpu(b)
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse))
+
+
+# ---------------------------------------------------------------------------
+# ragged mid-size shapes: several tiles and partial pages, every group size
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("hq,hkv,d", [(28, 4, 128), (40, 8, 128), (16, 1, 128), (8, 8, 128),
+                                      (4, 1, 64), (32, 2, 64), (7, 7, 64), (64, 4, 128)])
+def test_ragged_shapes(hq, hkv, d):
+    lens = [1, 2, 15, 16, 17, 31, 32, 33, 255, 257, 1000, 4097]
+    b = build_batch(lens, hq, hkv, d, 40 + hq + hkv + d, pool_pages=sum((L + 15) // 16 for L in lens) + 7)
+    ref = run_oracle(b)
+    _say(f"ragged hq={hq} hkv={hkv} d={d}")
+    check_batch(b, ref)
+    check_batch(b, ref, chunk_pages=3)
+
+
+def test_sharp_softmax_scaled_keys():
+    """Keys scaled by 3 (the 32B-like workload's sharpening) at mid size."""
+    lens = np.random.default_rng(9).integers(1, 6000, size=24)
+    b = build_batch(lens, 40, 8, 128, 41, k_mult=3.0)
+    check_batch(b)
+
+
+# ---------------------------------------------------------------------------
+# the named workloads at full size
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["gqa7b", "longtail", "gqa32b"])
+def test_full_size_workload(name):
+    _say(f"full-size {name}: generating")
+    b = named(name)
+    _say(f"  {b.num_seqs} seqs, {int(b.seq_lens.sum())} tokens, {b.kv_bytes() / 1e9:.2f} GB KV")
+    ref = named_ref(name)
+    out, lse, info = check_batch(b, ref)
+    _say(f"  plan: {info.num_work} items, chunk {info.chunk_pages} pages, {info.num_combine} split pairs")
+
+
+def test_straggler_steps():
+    _say("straggler: generating")
+    run = make_straggler()
+    runner = B.DecodeAttention(28, 4, 128)
+    dev = dict(k=run.base.k_pool.cuda(), v=run.base.v_pool.cuda())
+    for t in (0, 1, 31, 63):
+        b = run.step_batch(t)
+        _say(f"  step {t}: {b.num_seqs} active")
+        d = dict(dev, q=b.q.cuda(), bt=torch.from_numpy(b.block_table).cuda())
+        ref = run_oracle(b)
+        out, lse, _ = run_gpu(b, dev=d, runner=runner)
+        assert_close(out, ref[0], f"straggler@{t}")
+        assert_close(lse, ref[1], f"straggler@{t} lse")
