@@ -38,63 +38,42 @@ def kernel_source_hash() -> str:
 
 
 class Stepper:
-    """Runs plan -> upload -> attention -> combine for a fixed batch on one stream."""
+    """Runs plan -> upload -> attention (+ merge) for a fixed batch on one stream."""
 
-    def __init__(self, batch, ring=4, chunk_pages=0):
+    def __init__(self, batch, chunk_pages=0, units_per_cu=0):
         import torch
         from paper_2601_12784_amd import binding as B
-        self.B, self.torch = B, torch
+        self.torch = torch
         self.batch = batch
         self.dev = dict(q=batch.q.cuda(), k=batch.k_pool.cuda(), v=batch.v_pool.cuda(),
                         bt=torch.from_numpy(batch.block_table).cuda())
         self.lens = np.ascontiguousarray(batch.seq_lens, dtype=np.int32)
+        self.chunk = chunk_pages or None
         cus = torch.cuda.get_device_properties(0).multi_processor_count
-        self.opts = B.make_opts(num_cus=cus, chunk_pages=chunk_pages)
-        self.desc = B.make_desc(batch.num_seqs, batch.num_q_heads, batch.num_kv_heads, batch.head_dim,
-                                batch.block_table.shape[1], batch.num_pages, batch.scale)
-        info, _ = B.sf_decode_attn_plan(self.desc, self.lens, self.opts)
-        self.info0 = info
-        n = info.work_bytes // 4
-        self.ring = [torch.empty(n, dtype=torch.int32, pin_memory=True) for _ in range(ring)]
-        self.ring_ev = [None] * ring
-        self.work_dev = torch.empty(n, dtype=torch.int32, device="cuda")
-        self.ws = torch.empty(max(int(info.workspace_bytes), 256), dtype=torch.uint8, device="cuda")
+        self.runner = B.DecodeAttention(batch.num_q_heads, batch.num_kv_heads, batch.head_dim,
+                                        opts=B.make_opts(num_cus=cus, units_per_cu=units_per_cu))
+        self.stream = torch.cuda.Stream()  # default priority
         self.out = torch.empty((batch.num_seqs, batch.num_q_heads, batch.head_dim), dtype=torch.float32,
                                device="cuda")
         self.lse = torch.empty((batch.num_seqs, batch.num_q_heads), dtype=torch.float32, device="cuda")
-        self.i = 0
+        self.step()
+        self.info0 = self.runner.last_info
 
     def step(self, ev_attn=None):
         """One decode step; ev_attn = (start, end) events bracketing the attention kernel."""
-        B, torch = self.B, self.torch
-        slot = self.i % len(self.ring)
-        self.i += 1
-        if self.ring_ev[slot] is not None:
-            self.ring_ev[slot].synchronize()
-        buf = self.ring[slot]
-        info, _ = B.sf_decode_attn_plan(self.desc, self.lens, self.opts, work_host=buf)
-        n = info.work_bytes // 4
-        self.work_dev[:n].copy_(buf[:n], non_blocking=True)
-        ev = torch.cuda.Event()
-        ev.record()
-        self.ring_ev[slot] = ev
-        if ev_attn is not None:
-            ev_attn[0].record()
-        B.sf_decode_attn(self.desc, info, None, self.work_dev, self.dev["q"], self.dev["k"], self.dev["v"],
-                         self.dev["bt"], self.out, self.lse, self.ws)
-        if ev_attn is not None:
-            ev_attn[1].record()
-        B.sf_decode_attn_combine(self.desc, info, self.work_dev, self.ws, self.out, self.lse)
-        return info
+        d = self.dev
+        self.runner(d["q"], d["k"], d["v"], d["bt"], self.lens, self.batch.scale, out=self.out, lse=self.lse,
+                    chunk_pages=self.chunk, stream=self.stream, attn_events=ev_attn)
 
 
 def time_steps(stepper, steps, warmup):
+    """Times `steps` decode steps after `warmup` untimed ones.
+    Returns (wall ms per step, mean and median attention-kernel ms from HIP events)."""
     torch = stepper.torch
     for _ in range(warmup):
         stepper.step()
     torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
         stepper.step(evs[i])
@@ -104,8 +83,9 @@ def time_steps(stepper, steps, warmup):
     return wall / steps * 1e3, float(np.mean(attn_ms)), float(np.median(attn_ms))
 
 
-def cpu_baseline(batch, budget_s=15.0):
-    """The fp64 oracle on a bounded prefix of the batch, timed on the host cores."""
+def cpu_baseline(batch, min_s=10.0, max_s=30.0):
+    """The fp64 oracle, timed on the host cores over repeated passes of the
+    batch (or of a prefix of it, if one pass would exceed max_s)."""
     import oracle
     from paper_2601_12784_amd.workloads import bf16_bits
     qb, kb, vb = bf16_bits(batch.q), bf16_bits(batch.k_pool), bf16_bits(batch.v_pool)
@@ -116,18 +96,20 @@ def cpu_baseline(batch, budget_s=15.0):
         oracle.decode_attn(qb[:n], kb, vb, batch.block_table[:n], batch.seq_lens[:n], batch.scale)
         return time.perf_counter() - t
 
-    n = min(8, batch.num_seqs)
-    dt = run(n)
-    per_tok = dt / max(1, int(batch.seq_lens[:n].sum()))
     cum = np.cumsum(batch.seq_lens.astype(np.int64))
-    target_tokens = budget_s / max(per_tok, 1e-12)
-    n = int(np.searchsorted(cum, target_tokens, side="right"))
+    n = min(8, batch.num_seqs)
+    per_tok = run(n) / max(1, int(cum[n - 1]))
+    n = int(np.searchsorted(cum, max_s / 2 / max(per_tok, 1e-12), side="right"))
     n = max(1, min(batch.num_seqs, n))
-    dt = run(n)
-    kv = batch.kv_bytes(batch.seq_lens[:n])
-    return {"value": kv / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n} of {batch.num_seqs} sequences ({int(cum[n - 1])} tokens, "
-                      f"{kv / 1e9:.3f} GB KV), fp64 C oracle, {dt:.2f} s"}
+    total, passes = 0.0, 0
+    while total < min_s and total < max_s - 1.0 and passes < 1000:
+        total += run(n)
+        passes += 1
+    kv = batch.kv_bytes(batch.seq_lens[:n]) * passes
+    return {"value": round(kv / total / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{passes} passes over the first {n} of {batch.num_seqs} sequences "
+                      f"({int(cum[n - 1])} tokens, {kv / passes / 1e9:.3f} GB KV per pass), "
+                      f"fp64 C oracle with {threads} OpenMP threads, {total:.1f} s"}
 
 
 def stored_traffic(kv_bytes_per_launch):
@@ -144,9 +126,11 @@ def stored_traffic(kv_bytes_per_launch):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--chunk-pages", type=int, default=0)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=1000,
+                    help="untimed steps first (the GPU leaves its idle clocks during these)")
+    ap.add_argument("--chunk-pages", type=int, default=0, help="force the chunk size (pages)")
+    ap.add_argument("--units-per-cu", type=int, default=0, help="planner target items per CU")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-skew", action="store_true", help="skip the equal-bytes uniform batch")
     ap.add_argument("--copy-probe", type=int, default=0,
@@ -180,15 +164,18 @@ def main():
     batch = make_batch("longtail")
     kv = batch.kv_bytes()
     log(f"  {batch.num_seqs} seqs, {int(batch.seq_lens.sum())} tokens, {kv / 1e9:.3f} GB KV/step")
-    st = Stepper(batch, chunk_pages=args.chunk_pages)
+    st = Stepper(batch, chunk_pages=args.chunk_pages, units_per_cu=args.units_per_cu)
     ms_step, attn_ms_mean, attn_ms_med = time_steps(st, args.steps, args.warmup)
     info = st.info0
     log(f"  step {ms_step * 1e3:.1f} us, attention kernel {attn_ms_mean * 1e3:.1f} us (median "
         f"{attn_ms_med * 1e3:.1f}), {info.num_work} items, chunk {info.chunk_pages}")
 
+    desc = B.make_desc(batch.num_seqs, batch.num_q_heads, batch.num_kv_heads, batch.head_dim,
+                       batch.block_table.shape[1], batch.num_pages, batch.scale)
+    hbuf = np.empty(info.work_bytes // 4, dtype=np.int32)
     t = time.perf_counter()
     for _ in range(50):
-        B.sf_decode_attn_plan(st.desc, st.lens, st.opts, work_host=st.ring[0])
+        B.sf_decode_attn_plan(desc, st.lens, st.runner.opts, work_host=hbuf)
     plan_us = (time.perf_counter() - t) / 50 * 1e6
 
     achieved = kv / (attn_ms_mean * 1e-3) / 1e9
@@ -227,7 +214,7 @@ def main():
         lens_u = uniform_lengths_like(batch.seq_lens.astype(np.int64))
         log("generating equal-token uniform batch")
         ub = build_batch(lens_u, 28, 4, 128, batch.seed + 100, name="uniform")
-        su = Stepper(ub, chunk_pages=args.chunk_pages)
+        su = Stepper(ub, chunk_pages=args.chunk_pages, units_per_cu=args.units_per_cu)
         ms_u, attn_u, _ = time_steps(su, args.steps, args.warmup)
         result["skew"] = {"uniform_ms_per_step": round(ms_u, 5), "uniform_kv_bytes": ub.kv_bytes(),
                           "skewed_over_uniform": round(ms_step / ms_u, 4),

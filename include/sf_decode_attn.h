@@ -29,7 +29,8 @@
  *   out          fp32  [B][Hq][D]
  *   lse          fp32  [B][Hq]                   optional (NULL = not written)
  * A (page, KV head) tile is 16*D*2 bytes (4 KiB at D = 128) and contiguous.
- * Supported: D in {64, 128}, page_size 16, 1 <= g <= 16.
+ * Supported: D in {64, 128}, page_size 16, 1 <= g <= 16. The pools may be NULL
+ * only when num_pages == 0, and then every sequence length must be 0.
  *
  * Ownership and ordering. The caller allocates every buffer; the library
  * allocates nothing, keeps no state between calls and is reentrant. Device
@@ -69,7 +70,7 @@ typedef struct sf_attn_desc {
   int32_t head_dim;            /* D: 64 or 128 */
   int32_t page_size;           /* tokens per page: 16 */
   int32_t block_table_stride;  /* int32 entries per block-table row, >= max_s ceil(L_s/16) */
-  int32_t num_pages;           /* pages in each pool */
+  int32_t num_pages;           /* pages in each pool (0: all lengths must be 0) */
   float softmax_scale;         /* multiplies q.k; must be finite */
 } sf_attn_desc;
 
@@ -90,13 +91,15 @@ typedef struct sf_plan_info {
   int32_t chunk_pages;       /* chunk size the plan used */
   uint64_t work_bytes;       /* bytes of the work list: (num_work + num_combine) * 32 */
   uint64_t workspace_bytes;  /* device scratch sf_decode_attn needs (0 if no partials) */
-  uint64_t desc_key;         /* fingerprint of the descriptor's shape fields */
+  uint64_t desc_key;         /* fingerprint of the descriptor's shape and pool-size fields */
 } sf_plan_info;
 
 /*
  * Builds the work list on the host (no device calls).
  *
- * Rule (the length-aware split-K partition):
+ * Rule (the length-aware split-K partition; the paper balances skewed
+ * trajectory lengths across rollout instances, Sec. 5.2, and this balances
+ * them across the compute units of one GPU):
  *   pages_s = ceil(L_s / 16);  T = sum_s pages_s * Hkv
  *   C   = opts.chunk_pages if > 0, else
  *         clamp(ceil(T / (units_per_cu * num_cus)), min_chunk_pages, max_chunk_pages)
@@ -106,8 +109,9 @@ typedef struct sf_plan_info {
  *   Items are ordered by page count, largest first, ties by (s, kvh, c).
  *   Pairs with n_s > 1 get consecutive partial slots in (s, kvh) order
  *   (chunk c -> slot_base + c) and one combine item each, in (s, kvh) order.
- * Work-list rows, int32 x 8 each, attention items first, then combine items:
- *   attention: seq, kv_head, page_begin, page_end, seq_len, slot (-1 = write out directly), c, n_s
+ * Work list, int32 rows of 8: attention items, then combine items:
+ *   attention: seq, kv_head, page_begin, page_end, seq_len,
+ *              slot (-1 = write out directly), combine index (-1 if n_s = 1), n_s
  *   combine:   seq, kv_head, slot_base, n_s, 0, 0, 0, 0
  *
  * seq_lens_host: B lengths on the host. opts may be NULL (all defaults).
@@ -125,7 +129,8 @@ sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t* seq_lens_
  * on the stream (work_host should be pinned memory for an asynchronous copy);
  * if it is NULL, work_dev must already hold this plan. Items whose sequence
  * fits in one chunk write out (and lse) directly; the others write partial
- * results into workspace, which sf_decode_attn_combine then merges.
+ * results into workspace, which sf_decode_attn_combine then merges. Calls
+ * that share a work_dev or workspace must not overlap on the device.
  * workspace: device buffer of workspace_bytes >= info->workspace_bytes
  * (may be NULL when that is 0). q, k_pool, v_pool, block_table, out: device
  * pointers in the layouts above. lse: device pointer or NULL.

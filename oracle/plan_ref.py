@@ -17,7 +17,8 @@ checked against it bit for bit:
   combine items: one per such pair, in (s, kvh) order
 
 Item rows (int32 x 8):
-  attention: seq, kv_head, page_begin, page_end, seq_len, slot (-1 = direct), c, n_s
+  attention: seq, kv_head, page_begin, page_end, seq_len, slot (-1 = direct),
+             combine index (-1 if n_s = 1), n_s
   combine:   seq, kv_head, slot_base, n_s, 0, 0, 0, 0
 """
 from __future__ import annotations
@@ -55,16 +56,19 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
     for s, (L, npg) in enumerate(zip(lens, pages)):
         for kvh in range(num_kv_heads):
             if npg == 0:
-                rows.append((0, s, kvh, 0, [s, kvh, 0, 0, L, -1, 0, 1]))
+                rows.append((0, s, kvh, 0, [s, kvh, 0, 0, L, -1, -1, 1]))
                 continue
             n = _ceil(npg, c_pages)
-            base = slot if n > 1 else -1
             for c in range(n):
                 b = c * npg // n
                 e = (c + 1) * npg // n
-                rows.append((e - b, s, kvh, c, [s, kvh, b, e, L, (base + c) if n > 1 else -1, c, n]))
+                if n > 1:
+                    row = [s, kvh, b, e, L, slot + c, len(combine), n]
+                else:
+                    row = [s, kvh, b, e, L, -1, -1, 1]
+                rows.append((e - b, s, kvh, c, row))
             if n > 1:
-                combine.append([s, kvh, base, n, 0, 0, 0, 0])
+                combine.append([s, kvh, slot, n, 0, 0, 0, 0])
                 slot += n
     rows.sort(key=lambda r: (-r[0], r[1], r[2], r[3]))
     items = np.array([r[4] for r in rows], dtype=np.int32).reshape(-1, 8)

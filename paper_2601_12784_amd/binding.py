@@ -226,14 +226,70 @@ def sf_debug_gather_kv(desc, k_pool, v_pool, block_table, seq, kv_head, length, 
 
 
 # ----------------------------------------------------------------------------
+# HIP runtime calls used by the runner for stream plumbing (copies and events)
+# ----------------------------------------------------------------------------
+_hip = None
+
+
+def hip():
+    global _hip
+    if _hip is None:
+        h = ctypes.CDLL("libamdhip64.so")
+        vp = ctypes.c_void_p
+        h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+        h.hipEventRecord.argtypes = [vp, vp]
+        h.hipStreamWaitEvent.argtypes = [vp, vp, ctypes.c_uint]
+        h.hipEventSynchronize.argtypes = [vp]
+        h.hipEventDestroy.argtypes = [vp]
+        h.hipMemcpyAsync.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, vp]
+        for fn in ("hipEventCreateWithFlags", "hipEventRecord", "hipStreamWaitEvent",
+                   "hipEventSynchronize", "hipEventDestroy", "hipMemcpyAsync"):
+            getattr(h, fn).restype = ctypes.c_int
+        _hip = h
+    return _hip
+
+
+def _hip_check(where, err):
+    if err != 0:
+        raise RuntimeError(f"{where} failed with hipError {err}")
+
+
+class _HipEvent:
+    """A timing-free HIP event (cheap to record and wait on)."""
+
+    def __init__(self):
+        self.ev = ctypes.c_void_p()
+        _hip_check("hipEventCreateWithFlags", hip().hipEventCreateWithFlags(ctypes.byref(self.ev), 0x2))
+        self.used = False
+
+    def record(self, stream_handle):
+        _hip_check("hipEventRecord", hip().hipEventRecord(self.ev, stream_handle))
+        self.used = True
+
+    def wait_on(self, stream_handle):
+        _hip_check("hipStreamWaitEvent", hip().hipStreamWaitEvent(stream_handle, self.ev, 0))
+
+    def synchronize(self):
+        if self.used:
+            _hip_check("hipEventSynchronize", hip().hipEventSynchronize(self.ev))
+
+    def __del__(self):
+        if _hip is not None and self.ev:
+            _hip.hipEventDestroy(self.ev)
+
+
+# ----------------------------------------------------------------------------
 # convenience runner: owns the pinned work-list ring and the device buffers
 # ----------------------------------------------------------------------------
 class DecodeAttention:
-    """Plan + attention + combine for successive decode steps on one stream.
+    """Plan + attention + combine for successive decode steps.
 
-    Host work lists go through a ring of pinned buffers; a buffer is rewritten
-    only after the event recorded behind its last upload has completed.
-    Device work list and workspace are torch allocations grown on demand.
+    The host plans each step into a ring of pinned buffers; the work list is
+    uploaded on a side stream (default priority) into one of two device
+    buffers, so the copy for step i+1 overlaps the kernels of step i and the
+    compute stream waits on that copy only. A pinned buffer is rewritten only
+    after its upload has completed, and a device buffer only after the step
+    that read it is done. Tensor checks run once per distinct set of tensors.
     """
 
     def __init__(self, num_q_heads, num_kv_heads, head_dim, device=None, num_cus=None,
@@ -245,67 +301,118 @@ class DecodeAttention:
         self.opts = opts if opts is not None else make_opts(num_cus=num_cus)
         if self.opts.num_cus == 0:
             self.opts.num_cus = num_cus
-        self._ring = [None] * ring
-        self._events = [None] * ring
-        self._next = 0
-        self.work_dev = torch.empty(0, dtype=torch.int32, device=self.device)
+        self.L = lib()
+        self._ring = [torch.empty(4096, dtype=torch.int32, pin_memory=True) for _ in range(ring)]
+        self._ring_ev = [_HipEvent() for _ in range(ring)]
+        self._n = 0
+        self.copy_stream = torch.cuda.Stream(device=self.device)
+        self._copy_h = self.copy_stream.cuda_stream
+        self._work = [torch.empty(4096, dtype=torch.int32, device=self.device) for _ in range(2)]
+        self._free_ev = [_HipEvent() for _ in range(2)]
         self.workspace = torch.empty(0, dtype=torch.uint8, device=self.device)
+        self._info = sf_plan_info()
+        self._checked = None
+        self._desc_key = None
+        self._desc = None
         self.last_info = None
+        self.last_work_dev = None
 
-    def _pinned(self, nints: int) -> torch.Tensor:
-        i = self._next
-        self._next = (i + 1) % len(self._ring)
-        if self._events[i] is not None:
-            self._events[i].synchronize()
-        buf = self._ring[i]
-        if buf is None or buf.numel() < nints:
-            buf = torch.empty(max(nints, 1024), dtype=torch.int32, pin_memory=True)
-            self._ring[i] = buf
-        return i, buf
+    def _opts(self, chunk_pages):
+        o = self.opts
+        if chunk_pages is None:
+            return o
+        return sf_plan_opts(o.num_cus, int(chunk_pages), o.units_per_cu, o.min_chunk_pages,
+                            o.max_chunk_pages)
 
-    def plan(self, seq_lens, block_table_stride, num_pages, scale, chunk_pages=None):
-        desc = make_desc(len(seq_lens), self.hq, self.hkv, self.d, block_table_stride, num_pages, scale)
-        opts = self.opts
-        if chunk_pages is not None:
-            opts = sf_plan_opts(opts.num_cus, int(chunk_pages), opts.units_per_cu,
-                                opts.min_chunk_pages, opts.max_chunk_pages)
-        info, _ = self._plan_sizes(desc, seq_lens, opts)
-        slot, buf = self._pinned(info.work_bytes // 4)
-        info, _ = sf_decode_attn_plan(desc, seq_lens, opts, work_host=buf)
-        return desc, info, slot, buf
+    def _check_tensors(self, q, k_pool, v_pool, block_table, out, lse):
+        key = (q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
+               out.data_ptr(), None if lse is None else lse.data_ptr(), tuple(q.shape),
+               tuple(k_pool.shape), tuple(v_pool.shape), tuple(block_table.shape))
+        if key == self._checked:
+            return
+        b, hkv, d = q.shape[0], self.hkv, self.d
+        _dev(q, "q", torch.bfloat16, (b, self.hq, d))
+        _dev(k_pool, "k_pool", torch.bfloat16, (k_pool.shape[0], hkv, PAGE, d))
+        _dev(v_pool, "v_pool", torch.bfloat16, (k_pool.shape[0], hkv, d, PAGE))
+        _dev(block_table, "block_table", torch.int32, (b, block_table.shape[1]))
+        _dev(out, "out", torch.float32, (b, self.hq, d))
+        if lse is not None:
+            _dev(lse, "lse", torch.float32, (b, self.hq))
+        self._checked = key
 
-    @staticmethod
-    def _plan_sizes(desc, seq_lens, opts):
-        if isinstance(seq_lens, torch.Tensor):
-            seq_lens = seq_lens.cpu().numpy()
-        lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
-        info = sf_plan_info()
-        _check("sf_decode_attn_plan", lib().sf_decode_attn_plan(
-            ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts), None, 0, ctypes.byref(info)))
-        return info, None
-
-    def _ensure(self, info):
-        nints = info.work_bytes // 4
-        if self.work_dev.numel() < nints:
-            self.work_dev = torch.empty(max(nints, 1024), dtype=torch.int32, device=self.device)
-        if self.workspace.numel() < info.workspace_bytes:
-            self.workspace = torch.empty(int(info.workspace_bytes * 1.25) + 256, dtype=torch.uint8,
-                                         device=self.device)
+    def _plan(self, desc, lens, opts):
+        L, info = self.L, self._info
+        slot = self._n % len(self._ring)
+        self._ring_ev[slot].synchronize()  # its previous upload has finished
+        buf = self._ring[slot]
+        st = L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts),
+                                   buf.data_ptr(), buf.numel() * 4, ctypes.byref(info))
+        if st == 3:  # SF_ERR_CAPACITY: grow this ring buffer and plan again
+            buf = torch.empty(info.work_bytes // 4 * 5 // 4 + 1024, dtype=torch.int32, pin_memory=True)
+            self._ring[slot] = buf
+            st = L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts),
+                                       buf.data_ptr(), buf.numel() * 4, ctypes.byref(info))
+        _check("sf_decode_attn_plan", st)
+        return slot, buf
 
     def __call__(self, q, k_pool, v_pool, block_table, seq_lens, scale, out=None, lse=None,
-                 chunk_pages=None, stream=None):
+                 chunk_pages=None, stream: torch.cuda.Stream | None = None, attn_events=None):
+        """One decode step on `stream` (default: the current stream). attn_events,
+        if given, is a (start, end) pair of torch events recorded around the
+        attention kernel."""
         b = q.shape[0]
+        main = stream or torch.cuda.current_stream(self.device)
+        main_h = main.cuda_stream
         if out is None:
             out = torch.empty((b, self.hq, self.d), dtype=torch.float32, device=self.device)
-        desc, info, slot, buf = self.plan(seq_lens, block_table.shape[1], k_pool.shape[0], scale,
-                                          chunk_pages)
-        self._ensure(info)
-        st = _stream(stream)
-        sf_decode_attn(desc, info, buf, self.work_dev, q, k_pool, v_pool, block_table, out, lse,
-                       self.workspace, stream=st)
-        ev = torch.cuda.Event()
-        ev.record(torch.cuda.current_stream() if stream is None else torch.cuda.ExternalStream(st))
-        self._events[slot] = ev
-        sf_decode_attn_combine(desc, info, self.work_dev, self.workspace, out, lse, stream=st)
-        self.last_info = info
+        self._check_tensors(q, k_pool, v_pool, block_table, out, lse)
+        dkey = (b, block_table.shape[1], k_pool.shape[0], float(scale))
+        if dkey != self._desc_key:
+            self._desc = make_desc(b, self.hq, self.hkv, self.d, block_table.shape[1], k_pool.shape[0], scale)
+            self._desc_key = dkey
+        desc = self._desc
+        if isinstance(seq_lens, torch.Tensor):
+            seq_lens = seq_lens.cpu().numpy()
+        lens = seq_lens if (isinstance(seq_lens, np.ndarray) and seq_lens.dtype == np.int32
+                            and seq_lens.flags.c_contiguous) else np.ascontiguousarray(seq_lens, np.int32)
+        if lens.shape != (b,):
+            raise ValueError("seq_lens must have one entry per sequence")
+        info = self._info
+        slot, buf = self._plan(desc, lens, self._opts(chunk_pages))
+
+        if self.workspace.numel() < info.workspace_bytes:
+            torch.cuda.synchronize(self.device)  # grown only while idle
+            self.workspace = torch.empty(int(info.workspace_bytes * 5 // 4) + 256, dtype=torch.uint8,
+                                         device=self.device)
+        j = self._n % 2
+        nbytes = info.work_bytes
+        if self._work[j].numel() * 4 < nbytes:
+            torch.cuda.synchronize(self.device)
+            self._work[j] = torch.empty(nbytes // 4 * 5 // 4 + 1024, dtype=torch.int32, device=self.device)
+        work = self._work[j]
+        # upload on the side stream once step n-2 (the last reader of work[j]) is done
+        if self._free_ev[j].used:
+            self._free_ev[j].wait_on(self._copy_h)
+        _hip_check("hipMemcpyAsync", hip().hipMemcpyAsync(work.data_ptr(), buf.data_ptr(), nbytes, 1,
+                                                          self._copy_h))
+        self._ring_ev[slot].record(self._copy_h)
+        self._ring_ev[slot].wait_on(main_h)
+
+        if attn_events is not None:
+            attn_events[0].record(main)
+        ws = self.workspace
+        _check("sf_decode_attn", self.L.sf_decode_attn(
+            ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
+            k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),
+            None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
+        if attn_events is not None:
+            attn_events[1].record(main)
+        if info.num_combine:
+            _check("sf_decode_attn_combine", self.L.sf_decode_attn_combine(
+                ctypes.byref(desc), ctypes.byref(info), work.data_ptr(), ws.data_ptr(), ws.numel(),
+                out.data_ptr(), None if lse is None else lse.data_ptr(), main_h))
+        self._free_ev[j].record(main_h)
+        self._n += 1
+        self.last_info = sf_plan_info.from_buffer_copy(info)
+        self.last_work_dev = work
         return out

@@ -34,7 +34,9 @@ extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info
   if (st != SF_OK) return st;
   if ((st = check_plan(desc, info)) != SF_OK) return st;
   if (info->num_work == 0) return SF_OK;
-  if (!work_dev || !q || !k_pool || !v_pool || !block_table || !out) return SF_ERR_INVALID_ARG;
+  if (!work_dev || !q || !block_table || !out) return SF_ERR_INVALID_ARG;
+  // An empty pool (num_pages == 0) only backs plans whose sequences are all empty.
+  if (desc->num_pages > 0 && (!k_pool || !v_pool)) return SF_ERR_INVALID_ARG;
   if (!aligned16(work_dev) || !aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) ||
       !aligned16(out) || !aligned4(block_table) || (lse && !aligned4(lse)))
     return SF_ERR_INVALID_ARG;

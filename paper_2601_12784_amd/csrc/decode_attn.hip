@@ -65,10 +65,129 @@ __device__ __forceinline__ float bf16_value(uint32_t bits) {
 // ---------------------------------------------------------------------------
 // attention over one chunk per wave
 // ---------------------------------------------------------------------------
+// K and V are streamed once and never reused, so they are read with
+// nontemporal loads; the next two-page block is fetched while the current one
+// is multiplied, which keeps 32 KiB in flight per wave.
+__device__ __forceinline__ u32x4 stream16(const uint16_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
+template <int D>
+struct KvBlock {
+  static constexpr int KB = D / 32;  // QK MFMA steps over the head dimension
+  static constexpr int JB = D / 16;  // PV output blocks of 16 dims
+  u32x4 k[2][KB];
+  u32x4 v[JB];
+};
+
+template <int D>
+struct ChunkCtx {
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* bt;  // this sequence's block-table row
+  int num_kv_heads;
+  int kvh;
+  int pe;             // end of this chunk (pages)
+  int k_page_sel;     // which page of the block this lane's K rows come from
+  int k_off;          // element offset of this lane's K row piece inside a tile
+  int v_page_sel;
+  int v_off;
+};
+
+// Loads the two-page block that starts at logical page pg (a single page if
+// pg + 1 == pe; the missing page then aliases the first and is masked later).
+template <int D>
+__device__ __forceinline__ void load_block(const ChunkCtx<D>& c, int pg, KvBlock<D>& b) {
+  const int pid0 = c.bt[pg];
+  int pid1 = pid0;
+  if (pg + 1 < c.pe) pid1 = c.bt[pg + 1];
+  const uint16_t* kp = c.k_pool + tile_offset(c.k_page_sel ? pid1 : pid0, c.num_kv_heads, c.kvh, D) + c.k_off;
+  const uint16_t* vp = c.v_pool + tile_offset(c.v_page_sel ? pid1 : pid0, c.num_kv_heads, c.kvh, D) + c.v_off;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int kb = 0; kb < KvBlock<D>::KB; ++kb) b.k[h][kb] = stream16(kp + k_elem(4 * h, kb * 32, D));
+#pragma unroll
+  for (int jb = 0; jb < KvBlock<D>::JB; ++jb) b.v[jb] = stream16(vp + v_elem(0, 16 * jb));
+}
+
+template <int D>
+struct SoftmaxState {
+  f32x4 o[KvBlock<D>::JB];  // O^T block jb: O[head col][16*jb + 4*grp + i]
+  float m;                  // running max of this lane's head, log2 units
+  float lsum;               // this lane's share of sum_t 2^(z_t - m)
+};
+
+// Scores, online-softmax update and P.V accumulation for one block.
+// nvalid = tokens of the block (from its first token) inside the sequence.
+template <int D>
+__device__ __forceinline__ void consume_block(KvBlock<D>& b, const u32x4* qf, int nvalid, int grp,
+                                              float scale_log2, SoftmaxState<D>& st) {
+  constexpr int KB = KvBlock<D>::KB;
+  constexpr int JB = KvBlock<D>::JB;
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f};
+  f32x4 s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    s0 = mfma_bf16(b.k[0][kb], qf[kb], s0);
+    s1 = mfma_bf16(b.k[1][kb], qf[kb], s1);
+  }
+  // This lane now holds head `col`, block tokens 8*grp + e (e < 4 from s0).
+  const int tok0 = 8 * grp;
+  float sc[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    sc[e] = (tok0 + e < nvalid) ? s0[e] * scale_log2 : -__builtin_inff();
+    sc[4 + e] = (tok0 + 4 + e < nvalid) ? s1[e] * scale_log2 : -__builtin_inff();
+  }
+  float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                   fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float mnew = fmaxf(st.m, mx);
+  const float alpha = fast_exp2(st.m - mnew);
+  st.m = mnew;
+
+  // P^T operand: the lane's eight weights as bf16 hi + lo parts, so the
+  // PV product keeps about 16 bits of each weight.
+  float ps = 0.f;
+  uint32_t hi[4], lo[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float p0 = fast_exp2(sc[2 * w] - mnew);
+    const float p1 = fast_exp2(sc[2 * w + 1] - mnew);
+    ps += p0 + p1;
+    const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
+    const uint32_t l0 = bf16_bits(p0 - bf16_value(h0)), l1 = bf16_bits(p1 - bf16_value(h1));
+    hi[w] = h0 | (h1 << 16);
+    lo[w] = l0 | (l1 << 16);
+  }
+  st.lsum = st.lsum * alpha + ps;
+  const u32x4 phi = {hi[0], hi[1], hi[2], hi[3]};
+  const u32x4 plo = {lo[0], lo[1], lo[2], lo[3]};
+
+  if (nvalid < 2 * kPage) {
+    // Slots past the sequence end may hold anything (even NaN): zero them,
+    // since a zero weight times NaN would still be NaN.
+    u32x4 mask;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      mask[w] = (tok0 + 2 * w < nvalid ? 0x0000FFFFu : 0u) | (tok0 + 2 * w + 1 < nvalid ? 0xFFFF0000u : 0u);
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) b.v[jb] &= mask;
+  }
+#pragma unroll
+  for (int jb = 0; jb < JB; ++jb) {
+    st.o[jb] *= alpha;
+    st.o[jb] = mfma_bf16(b.v[jb], phi, st.o[jb]);
+    st.o[jb] = mfma_bf16(b.v[jb], plo, st.o[jb]);
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(64) void attn_chunk_kernel(AttnArgs a) {
-  constexpr int KB = D / 32;  // QK MFMA steps over the head dimension
-  constexpr int JB = D / 16;  // PV output blocks of 16 dims
+  constexpr int KB = KvBlock<D>::KB;
+  constexpr int JB = KvBlock<D>::JB;
   const int lane = threadIdx.x;
   const int col = lane & 15;   // MFMA column (query head in group) and A-operand row
   const int grp = lane >> 4;   // MFMA k-group
@@ -84,6 +203,24 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(AttnArgs a) {
   const bool head_ok = col < g;
   const int head = kvh * g + col;
 
+  ChunkCtx<D> c;
+  c.k_pool = a.k_pool;
+  c.v_pool = a.v_pool;
+  c.bt = a.block_table + size_t(seq) * a.bt_stride;
+  c.num_kv_heads = a.num_kv_heads;
+  c.kvh = kvh;
+  c.pe = pe;
+  // K operand: A-row r = col holds block token 8*(r/4) + r%4 (+4 for the
+  // second MFMA): page r/8 of the block, slot 8*((r/4)%2) + r%4.
+  c.k_page_sel = col >> 3;
+  c.k_off = k_elem(8 * ((col >> 2) & 1) + (col & 3), grp * 8, D);
+  // V operand: A-row = dim 16*jb + col, k-group grp = block tokens 8*grp .. +7.
+  c.v_page_sel = grp >> 1;
+  c.v_off = v_elem(8 * (grp & 1), col);
+
+  KvBlock<D> blk[2];
+  if (pb < pe) load_block(c, pb, blk[0]);
+
   // Q as the B operand of S^T = K Q^T: column = head, k = 8 dims per group.
   u32x4 qf[KB];
   {
@@ -95,115 +232,40 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(AttnArgs a) {
     }
   }
 
-  f32x4 o[JB];
+  SoftmaxState<D> st;
 #pragma unroll
-  for (int jb = 0; jb < JB; ++jb) o[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m = -__builtin_inff();  // running max of this lane's head, log2 units
-  float lsum = 0.f;             // this lane's share of sum_t 2^(z_t - m)
+  for (int jb = 0; jb < JB; ++jb) st.o[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.m = -__builtin_inff();
+  st.lsum = 0.f;
 
-  // K operand: A-row r = col holds block token 8*(r/4) + r%4 (+4 for the
-  // second MFMA), i.e. page r/8 of the block, slot below.
-  const int k_page_sel = col >> 3;
-  const int k_slot = 8 * ((col >> 2) & 1) + (col & 3);
-  // V operand: A-row = dim 16*jb + col, k-group grp = block tokens 8*grp .. +7.
-  const int v_page_sel = grp >> 1;
-  const int v_slot = 8 * (grp & 1);
-
-  const int32_t* bt = a.block_table + size_t(seq) * a.bt_stride;
-  for (int pg = pb; pg < pe; pg += 2) {
-    const bool two = pg + 1 < pe;
-    const int pid0 = bt[pg];
-    int pid1 = pid0;
-    if (two) pid1 = bt[pg + 1];
-    const uint16_t* kt = a.k_pool + tile_offset(k_page_sel ? pid1 : pid0, a.num_kv_heads, kvh, D);
-    const uint16_t* vt = a.v_pool + tile_offset(v_page_sel ? pid1 : pid0, a.num_kv_heads, kvh, D);
-    const uint16_t* kp = kt + k_elem(k_slot, grp * 8, D);
-    const uint16_t* vp = vt + v_elem(v_slot, col);
-
-    u32x4 kr[2][KB];
-    u32x4 vr[JB];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) kr[h][kb] = load16(kp + k_elem(4 * h, kb * 32, D));
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) vr[jb] = load16(vp + v_elem(0, 16 * jb));
-
-    f32x4 s0 = {0.f, 0.f, 0.f, 0.f};
-    f32x4 s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      s0 = mfma_bf16(kr[0][kb], qf[kb], s0);
-      s1 = mfma_bf16(kr[1][kb], qf[kb], s1);
-    }
-
-    // This lane now holds head `col`, block tokens 8*grp + e (e < 4 from s0).
-    const int nvalid = min(len - pg * kPage, two ? 2 * kPage : kPage);
-    const int tok0 = 8 * grp;
-    float sc[8];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      sc[e] = (tok0 + e < nvalid) ? s0[e] * a.scale_log2 : -__builtin_inff();
-      sc[4 + e] = (tok0 + 4 + e < nvalid) ? s1[e] * a.scale_log2 : -__builtin_inff();
-    }
-    float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
-                     fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m, mx);
-    const float alpha = fast_exp2(m - mnew);
-    m = mnew;
-
-    float ps = 0.f;
-    uint32_t hi[4], lo[4];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float p0 = fast_exp2(sc[2 * w] - mnew);
-      const float p1 = fast_exp2(sc[2 * w + 1] - mnew);
-      ps += p0 + p1;
-      const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
-      const uint32_t l0 = bf16_bits(p0 - bf16_value(h0)), l1 = bf16_bits(p1 - bf16_value(h1));
-      hi[w] = h0 | (h1 << 16);
-      lo[w] = l0 | (l1 << 16);
-    }
-    lsum = lsum * alpha + ps;
-    const u32x4 phi = {hi[0], hi[1], hi[2], hi[3]};
-    const u32x4 plo = {lo[0], lo[1], lo[2], lo[3]};
-
-    if (nvalid < 2 * kPage) {
-      // Slots past the sequence end may hold anything (even NaN): zero them,
-      // since a zero weight times NaN would still be NaN.
-      u32x4 mask;
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        mask[w] = (tok0 + 2 * w < nvalid ? 0x0000FFFFu : 0u) | (tok0 + 2 * w + 1 < nvalid ? 0xFFFF0000u : 0u);
-#pragma unroll
-      for (int jb = 0; jb < JB; ++jb) vr[jb] &= mask;
-    }
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) {
-      o[jb] *= alpha;
-      o[jb] = mfma_bf16(vr[jb], phi, o[jb]);
-      o[jb] = mfma_bf16(vr[jb], plo, o[jb]);
-    }
+  // Two register blocks alternate: block i+1 is in flight while block i is used.
+  for (int pg = pb; pg < pe; pg += 4) {
+    if (pg + 2 < pe) load_block(c, pg + 2, blk[1]);
+    consume_block(blk[0], qf, min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage), grp, a.scale_log2, st);
+    if (pg + 2 >= pe) break;
+    if (pg + 4 < pe) load_block(c, pg + 4, blk[0]);
+    consume_block(blk[1], qf, min(len - (pg + 2) * kPage, pg + 3 < pe ? 2 * kPage : kPage), grp,
+                  a.scale_log2, st);
   }
 
-  float lt = lsum + __shfl_xor(lsum, 16);
+  float lt = st.lsum + __shfl_xor(st.lsum, 16);
   lt += __shfl_xor(lt, 32);
-  if (!head_ok) return;
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
   // Lane holds O[head col][16*jb + 4*grp + i], i = 0..3.
   if (slot < 0) {
+    if (!head_ok) return;
     float* dst = a.out + (size_t(seq) * a.num_q_heads + head) * D + 4 * grp;
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = o[jb] * inv;
+    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
     if (a.lse && grp == 0)
-      a.lse[size_t(seq) * a.num_q_heads + head] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -__builtin_inff();
-  } else {
+      a.lse[size_t(seq) * a.num_q_heads + head] = lt > 0.f ? (st.m + __log2f(lt)) * kLn2 : -__builtin_inff();
+    return;
+  }
+  if (head_ok) {
     float* dst = a.part_o + (size_t(slot) * g + col) * D + 4 * grp;
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = o[jb] * inv;
-    if (grp == 0) a.part_lse[size_t(slot) * g + col] = m + __log2f(lt);
+    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
+    if (grp == 0) a.part_lse[size_t(slot) * g + col] = st.m + __log2f(lt);
   }
 }
 
@@ -221,14 +283,19 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   for (int idx = threadIdx.x; idx < g * d4n; idx += blockDim.x) {
     const int h = idx / d4n;
     const int d4 = idx - h * d4n;
+    const float* lse_h = a.part_lse + size_t(base) * g + h;           // stride g per chunk
+    const float* o_h = a.part_o + (size_t(base) * g + h) * a.head_dim + 4 * d4;
+    const size_t o_stride = size_t(g) * a.head_dim;
     float mx = -__builtin_inff();
-    for (int c = 0; c < n; ++c) mx = fmaxf(mx, a.part_lse[size_t(base + c) * g + h]);
+#pragma unroll 8
+    for (int c = 0; c < n; ++c) mx = fmaxf(mx, lse_h[size_t(c) * g]);
     float wsum = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
     for (int c = 0; c < n; ++c) {
-      const float w = fast_exp2(a.part_lse[size_t(base + c) * g + h] - mx);
+      const float w = fast_exp2(lse_h[size_t(c) * g] - mx);
       wsum += w;
-      acc += w * *reinterpret_cast<const f32x4*>(a.part_o + (size_t(base + c) * g + h) * a.head_dim + 4 * d4);
+      acc += w * *reinterpret_cast<const f32x4*>(o_h + c * o_stride);
     }
     const int head = kvh * g + h;
     *reinterpret_cast<f32x4*>(a.out + (size_t(seq) * a.num_q_heads + head) * a.head_dim + 4 * d4) =

@@ -33,8 +33,8 @@ sf_status validate_desc(const sf_attn_desc* d) {
 
 uint64_t desc_key(const sf_attn_desc* d) {
   // FNV-1a over the shape fields a plan depends on.
-  const int32_t f[7] = {0x5f440001, d->num_seqs, d->num_q_heads, d->num_kv_heads,
-                        d->head_dim, d->page_size, d->block_table_stride};
+  const int32_t f[8] = {0x5f440001, d->num_seqs, d->num_q_heads, d->num_kv_heads,
+                        d->head_dim, d->page_size, d->block_table_stride, d->num_pages};
   uint64_t h = 1469598103934665603ull;
   const unsigned char* p = reinterpret_cast<const unsigned char*>(f);
   for (size_t i = 0; i < sizeof f; ++i) {
@@ -78,14 +78,14 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   }
   if (mn > mx) return SF_ERR_INVALID_ARG;
 
-  std::vector<int64_t> pages(B);
-  int64_t total = 0;
+  int64_t total = 0, max_pages = 0;
   for (int32_t s = 0; s < B; ++s) {
     const int32_t L = seq_lens_host[s];
-    if (L < 0) return SF_ERR_INVALID_ARG;
-    pages[s] = (int64_t(L) + kPage - 1) / kPage;
-    if (pages[s] > desc->block_table_stride) return SF_ERR_INVALID_ARG;
-    total += pages[s] * hkv;
+    if (L < 0 || (L > 0 && desc->num_pages == 0)) return SF_ERR_INVALID_ARG;
+    const int64_t npg = (int64_t(L) + kPage - 1) / kPage;
+    if (npg > desc->block_table_stride) return SF_ERR_INVALID_ARG;
+    total += npg * hkv;
+    max_pages = std::max(max_pages, npg);
   }
   int64_t chunk;
   if (forced > 0) {
@@ -95,18 +95,20 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
     chunk = (total + units - 1) / units;
     chunk = std::min<int64_t>(std::max<int64_t>(chunk, mn), mx);
   }
+  auto pages_of = [&](int32_t s) { return (int64_t(seq_lens_host[s]) + kPage - 1) / kPage; };
+  auto chunks_of = [&](int64_t npg) { return npg ? (npg + chunk - 1) / chunk : int64_t(1); };
 
   // Sizes first: items, combine rows, partial slots.
   int64_t n_work = 0, n_comb = 0, n_part = 0;
   for (int32_t s = 0; s < B; ++s) {
-    const int64_t n = pages[s] ? (pages[s] + chunk - 1) / chunk : 1;
+    const int64_t n = chunks_of(pages_of(s));
     n_work += n * hkv;
     if (n > 1) {
       n_comb += hkv;
       n_part += n * hkv;
     }
   }
-  if (n_work > INT32_MAX / kItemInts || n_part > INT32_MAX) return SF_ERR_INVALID_ARG;
+  if (n_work + n_comb > INT32_MAX / kItemInts || n_part > INT32_MAX) return SF_ERR_INVALID_ARG;
   const int32_t g = desc->num_q_heads / hkv;
   info->num_work = int32_t(n_work);
   info->num_combine = int32_t(n_comb);
@@ -119,39 +121,81 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   if (!work_host) return SF_OK;
   if (work_capacity_bytes < info->work_bytes) return SF_ERR_CAPACITY;
 
-  // Rows in (s, kvh, c) order, then a stable sort by page count (descending)
-  // keeps that order among equal sizes.
-  struct Row {
-    int32_t size;
-    int32_t f[kItemInts];
-  };
-  std::vector<Row> rows;
-  rows.reserve(size_t(n_work));
-  int32_t* comb = work_host + n_work * kItemInts;
-  int32_t slot = 0;
-  for (int32_t s = 0; s < B; ++s) {
-    const int64_t npg = pages[s];
-    const int32_t L = seq_lens_host[s];
-    for (int32_t kvh = 0; kvh < hkv; ++kvh) {
-      if (npg == 0) {
-        rows.push_back(Row{0, {s, kvh, 0, 0, L, -1, 0, 1}});
-        continue;
+  // Items are generated in (s, kvh, c) order and placed by a stable counting
+  // sort on page count, largest first. Chunk c of a pair spans
+  // floor((c+1)*npg/n) - floor(c*npg/n) <= chunk pages.
+  const int64_t max_size = std::min<int64_t>(chunk, max_pages);
+  // Scratch reused across calls on this thread; raw pointers keep the loops
+  // free of per-access thread-local lookups.
+  thread_local std::vector<int64_t> pos_buf;
+  thread_local std::vector<int32_t> bounds_buf;
+  pos_buf.assign(size_t(max_size) + 2, 0);
+  int64_t* pos = pos_buf.data();
+  // Chunk sizes of a pair are q = floor(npg/n) or q + 1; the bounds
+  // floor(c*npg/n) follow by stepping a remainder (one division per sequence).
+  int32_t* bounds = nullptr;
+  auto fill_bounds = [&](int64_t npg, int64_t n) {
+    if (bounds_buf.size() < size_t(n) + 1) bounds_buf.resize(size_t(n) + 1);
+    bounds = bounds_buf.data();
+    const int64_t q = npg / n, r = npg % n;
+    int64_t e = 0, rem = 0;
+    bounds[0] = 0;
+    for (int64_t c = 1; c <= n; ++c) {
+      e += q;
+      rem += r;
+      if (rem >= n) {
+        rem -= n;
+        ++e;
       }
-      const int64_t n = (npg + chunk - 1) / chunk;
+      bounds[c] = int32_t(e);
+    }
+  };
+  for (int32_t s = 0; s < B; ++s) {
+    const int64_t npg = pages_of(s);
+    const int64_t n = chunks_of(npg);
+    if (n == 1) {
+      pos[npg] += hkv;
+      continue;
+    }
+    const int64_t q = npg / n, r = npg % n;  // r chunks of q + 1 pages, n - r of q
+    pos[q + 1] += r * hkv;
+    pos[q] += (n - r) * hkv;
+  }
+  int64_t start = 0;  // descending sizes: the largest size starts at row 0
+  for (int64_t sz = max_size; sz >= 0; --sz) {
+    const int64_t cnt = pos[sz];
+    pos[sz] = start;
+    start += cnt;
+  }
+  int32_t* comb = work_host + n_work * kItemInts;
+  int32_t slot = 0, comb_idx = 0;
+  for (int32_t s = 0; s < B; ++s) {
+    const int64_t npg = pages_of(s);
+    const int64_t n = chunks_of(npg);
+    const int32_t L = seq_lens_host[s];
+    fill_bounds(npg, n);
+    for (int32_t kvh = 0; kvh < hkv; ++kvh) {
       for (int64_t c = 0; c < n; ++c) {
-        const int32_t b = int32_t(c * npg / n);
-        const int32_t e = int32_t((c + 1) * npg / n);
-        rows.push_back(Row{e - b, {s, kvh, b, e, L, n > 1 ? slot + int32_t(c) : -1, int32_t(c), int32_t(n)}});
+        const int32_t b = bounds[c];
+        const int32_t e = bounds[c + 1];
+        int32_t* row = work_host + pos[e - b]++ * kItemInts;
+        row[0] = s;
+        row[1] = kvh;
+        row[2] = b;
+        row[3] = e;
+        row[4] = L;
+        row[5] = n > 1 ? slot + int32_t(c) : -1;
+        row[6] = n > 1 ? comb_idx : -1;
+        row[7] = int32_t(n);
       }
       if (n > 1) {
         const int32_t c8[kItemInts] = {s, kvh, slot, int32_t(n), 0, 0, 0, 0};
         std::memcpy(comb, c8, sizeof c8);
         comb += kItemInts;
         slot += int32_t(n);
+        ++comb_idx;
       }
     }
   }
-  std::stable_sort(rows.begin(), rows.end(), [](const Row& a, const Row& b) { return a.size > b.size; });
-  for (size_t i = 0; i < rows.size(); ++i) std::memcpy(work_host + i * kItemInts, rows[i].f, sizeof rows[i].f);
   return SF_OK;
 }

@@ -60,8 +60,9 @@ def _assert_same(info, work, ref):
     assert info.num_partials == ref["num_partials"]
     assert info.workspace_bytes == ref["workspace_bytes"]
     assert info.work_bytes == ref["work_bytes"]
-    assert np.array_equal(work[: info.num_work], ref["items"])
-    assert np.array_equal(work[info.num_work:], ref["combine"])
+    w = info.num_work
+    assert np.array_equal(work[:w], ref["items"])
+    assert np.array_equal(work[w:], ref["combine"])
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -97,11 +98,11 @@ def test_tiny_plan_by_hand():
     info, work, _ = _plan_both([17, 64, 130, 300], 4, 1, 64)
     assert info.chunk_pages == 16 and info.num_work == 5 and info.num_combine == 1
     assert info.num_partials == 2
-    expect = [[3, 0, 9, 19, 300, 1, 1, 2],
-              [2, 0, 0, 9, 130, -1, 0, 1],
+    expect = [[3, 0, 9, 19, 300, 1, 0, 2],
+              [2, 0, 0, 9, 130, -1, -1, 1],
               [3, 0, 0, 9, 300, 0, 0, 2],
-              [1, 0, 0, 4, 64, -1, 0, 1],
-              [0, 0, 0, 2, 17, -1, 0, 1],
+              [1, 0, 0, 4, 64, -1, -1, 1],
+              [0, 0, 0, 2, 17, -1, -1, 1],
               [3, 0, 0, 2, 0, 0, 0, 0]]
     assert np.array_equal(work, np.array(expect, dtype=np.int32))
     assert info.workspace_bytes == 2 * 4 * 64 * 4 + 256
@@ -127,20 +128,22 @@ def test_plan_invariants(seed):
         for kvh in range(hkv):
             mine = items[(items[:, 0] == s) & (items[:, 1] == kvh)]
             assert np.all(mine[:, 4] == L)
-            mine = mine[np.argsort(mine[:, 6])]
+            mine = mine[np.argsort(mine[:, 2])]
             n = mine.shape[0]
-            assert np.array_equal(mine[:, 6], np.arange(n)) and np.all(mine[:, 7] == n)
+            assert np.all(mine[:, 7] == n)
             if npg == 0:
-                assert n == 1 and mine[0, 2] == mine[0, 3] == 0
+                assert n == 1 and mine[0, 2] == mine[0, 3] == 0 and mine[0, 5] == mine[0, 6] == -1
                 continue
             assert mine[0, 2] == 0 and mine[-1, 3] == npg
             assert np.all(mine[1:, 2] == mine[:-1, 3]) and np.all(mine[:, 3] > mine[:, 2])
             if n > 1:
-                row = comb[(comb[:, 0] == s) & (comb[:, 1] == kvh)]
-                assert row.shape[0] == 1 and row[0, 3] == n
-                assert np.array_equal(mine[:, 5], row[0, 2] + np.arange(n))
+                ci = mine[0, 6]
+                assert np.all(mine[:, 6] == ci)
+                row = comb[ci]
+                assert row[0] == s and row[1] == kvh and row[3] == n
+                assert np.array_equal(mine[:, 5], row[2] + np.arange(n))
             else:
-                assert mine[0, 5] == -1
+                assert mine[0, 5] == -1 and mine[0, 6] == -1
 
 
 def test_plan_size_query_and_capacity(lib):
@@ -229,6 +232,11 @@ def test_combine_rejects_bad_arguments(lib):
     assert c(ctypes.byref(desc), ctypes.byref(info), FAKE, FAKE, 0, FAKE, None, None) == 3
     assert c(ctypes.byref(desc), ctypes.byref(info), None, FAKE, 1 << 30, FAKE, None, None) == 1
     assert c(ctypes.byref(desc), ctypes.byref(info), FAKE, FAKE, 1 << 30, FAKE + 4, None, None) == 1
+    # a plan without split pairs makes the combine call a no-op
+    lens1 = np.array((40, 200), np.int32)
+    one, _ = B.sf_decode_attn_plan(desc, lens1, B.make_opts(num_cus=4))
+    assert one.num_combine == 0
+    assert c(ctypes.byref(desc), ctypes.byref(one), None, None, 0, None, None, None) == 0
 
 
 def test_gather_rejects_bad_arguments(lib):
@@ -238,3 +246,27 @@ def test_gather_rejects_bad_arguments(lib):
     assert g(ctypes.byref(desc), FAKE, FAKE, FAKE, 0, 2, 5, FAKE, FAKE, None) == 1   # kv head
     assert g(ctypes.byref(desc), FAKE, FAKE, FAKE, 0, 0, 65, FAKE, FAKE, None) == 1  # > stride pages
     assert g(ctypes.byref(desc), FAKE, FAKE, FAKE, 0, 0, 5, FAKE + 8, FAKE, None) == 1
+
+
+def test_empty_pool_only_for_empty_batches(lib):
+    info = B.sf_plan_info()
+    desc = B.make_desc(2, 8, 2, 128, 1, 0, 0.1)
+    zero = np.zeros(2, np.int32)
+    assert lib.sf_decode_attn_plan(ctypes.byref(desc), zero.ctypes.data, None, None, 0,
+                                   ctypes.byref(info)) == 0
+    one = np.array([0, 1], np.int32)
+    assert lib.sf_decode_attn_plan(ctypes.byref(desc), one.ctypes.data, None, None, 0,
+                                   ctypes.byref(info)) == 1
+    # pools may be NULL only with num_pages == 0
+    d2 = B.make_desc(2, 8, 2, 128, 1, 5, 0.1)
+    info2, _ = B.sf_decode_attn_plan(d2, zero)
+    assert _call(lib, d2, info2, k=None) == 1
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    desc, info, work = _planned()
+    q = torch.zeros((2, 8, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        B.sf_decode_attn(desc, info, work, torch.zeros(16, dtype=torch.int32), q, q, q,
+                         torch.zeros((2, 200), dtype=torch.int32), torch.zeros((2, 8, 128)))

@@ -73,8 +73,9 @@ def assert_close(gpu, ref, what=""):
 def check_batch(batch, ref=None, chunk_pages=None, dev=None):
     ref = ref or run_oracle(batch)
     out, lse, runner = run_gpu(batch, dev=dev, chunk_pages=chunk_pages)
-    assert_close(out, ref[0], f"{batch.name} out chunk={chunk_pages}")
-    assert_close(lse, ref[1], f"{batch.name} lse chunk={chunk_pages}")
+    tag = f"{batch.name} chunk={chunk_pages}"
+    assert_close(out, ref[0], f"{tag} out")
+    assert_close(lse, ref[1], f"{tag} lse")
     return out, lse, runner.last_info
 
 
@@ -119,6 +120,32 @@ def test_gather_is_bit_exact(which):
 def test_tiny_parity(chunk):
     _say(f"tiny chunk={chunk}")
     check_batch(named("tiny"), named_ref("tiny"), chunk_pages=chunk)
+
+
+def test_uploaded_plan_is_reusable():
+    """Rerunning a plan already on the device (work_host = NULL) gives the same bits."""
+    b = build_batch([5, 700, 3000, 9000], 28, 4, 128, 43)
+    dev = to_dev(b)
+    desc = B.make_desc(b.num_seqs, 28, 4, 128, b.block_table.shape[1], b.num_pages, b.scale)
+    info, work = B.sf_decode_attn_plan(desc, b.seq_lens, B.make_opts(num_cus=256, chunk_pages=5))
+    assert info.num_combine > 0
+    pinned = torch.from_numpy(work[: info.work_bytes // 4].copy()).pin_memory()
+    work_dev = torch.empty(info.work_bytes // 4, dtype=torch.int32, device="cuda")
+    ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device="cuda")
+    outs = []
+    for rep in range(3):
+        out = torch.empty((b.num_seqs, 28, 128), dtype=torch.float32, device="cuda")
+        lse = torch.empty((b.num_seqs, 28), dtype=torch.float32, device="cuda")
+        B.sf_decode_attn(desc, info, pinned if rep == 0 else None, work_dev, dev["q"], dev["k"], dev["v"],
+                         dev["bt"], out, lse, ws)
+        B.sf_decode_attn_combine(desc, info, work_dev, ws, out, lse)
+        torch.cuda.synchronize()
+        outs.append((out.cpu().numpy(), lse.cpu().numpy()))
+    ref = run_oracle(b)
+    assert_close(outs[0][0], ref[0], "reused plan")
+    assert_close(outs[0][1], ref[1], "reused plan lse")
+    for o, l in outs[1:]:
+        assert np.array_equal(o, outs[0][0]) and np.array_equal(l, outs[0][1])
 
 
 def test_chunk_count_invariance():
