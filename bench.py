@@ -40,7 +40,7 @@ def kernel_source_hash() -> str:
 class Stepper:
     """Runs plan -> upload -> attention (+ merge) for a fixed batch on one stream."""
 
-    def __init__(self, batch, chunk_pages=0, units_per_cu=0):
+    def __init__(self, batch, chunk_pages=0, workers_per_cu=0):
         import torch
         from paper_2601_12784_amd import binding as B
         self.torch = torch
@@ -51,7 +51,7 @@ class Stepper:
         self.chunk = chunk_pages or None
         cus = torch.cuda.get_device_properties(0).multi_processor_count
         self.runner = B.DecodeAttention(batch.num_q_heads, batch.num_kv_heads, batch.head_dim,
-                                        opts=B.make_opts(num_cus=cus, units_per_cu=units_per_cu))
+                                        opts=B.make_opts(num_cus=cus, workers_per_cu=workers_per_cu))
         self.stream = torch.cuda.Stream()  # default priority
         self.out = torch.empty((batch.num_seqs, batch.num_q_heads, batch.head_dim), dtype=torch.float32,
                                device="cuda")
@@ -123,19 +123,115 @@ def stored_traffic(kv_bytes_per_launch):
     return doc.get("traffic_bytes_per_launch")
 
 
+ATTN_KERNEL = "attn_chunk_kernel<128>"
+COMBINE_KERNEL = "combine_kernel"
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def _csv_rows(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTERS_FILE):
+    """Per-launch HBM traffic of the attention kernel from two rocprofv3 --pmc
+    runs (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what
+    the same counter reads for a plain device copy of copy_mib MiB."""
+    def per_kernel(path, counter):
+        vals = {}
+        for r in _csv_rows(path):
+            if r["Counter_Name"] != counter:
+                continue
+            vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
+        return vals
+
+    def pick(vals, name):
+        hits = [v for k, v in vals.items() if name in k]
+        if not hits:
+            raise SystemExit(f"no dispatch of {name} in the counter file")
+        return float(np.mean(hits[0])), len(hits[0])
+
+    fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    write = per_kernel(write_csv, "WRITE_SIZE")
+    copy_bytes = float(copy_mib) * (1 << 20)
+    f_copy, _ = pick(fetch, COPY_KERNEL)
+    w_copy, _ = pick(write, COPY_KERNEL)
+    f_scale, w_scale = copy_bytes / f_copy, copy_bytes / w_copy
+    f_attn, nf = pick(fetch, ATTN_KERNEL)
+    w_attn, nw = pick(write, ATTN_KERNEL)
+    doc = {
+        "kernel": ATTN_KERNEL,
+        "workload": "long-tail rollout batch (bench.py default)",
+        "kernel_source_sha256_16": kernel_source_hash(),
+        "copy_probe_bytes": copy_bytes,
+        "fetch_scale": round(f_scale, 5), "write_scale": round(w_scale, 5),
+        "fetch_bytes_per_launch": round(f_attn * f_scale), "write_bytes_per_launch": round(w_attn * w_scale),
+        "traffic_bytes_per_launch": round(f_attn * f_scale + w_attn * w_scale),
+        "algorithmic_kv_bytes_per_launch": kv_bytes,
+        "traffic_over_algorithmic": round((f_attn * f_scale + w_attn * w_scale) / kv_bytes, 4),
+        "dispatches": {"fetch": nf, "write": nw},
+        "raw_counter_bytes_per_launch": {"FETCH_SIZE": round(f_attn), "WRITE_SIZE": round(w_attn),
+                                         "copy_FETCH_SIZE": round(f_copy), "copy_WRITE_SIZE": round(w_copy)},
+    }
+    for name in (COMBINE_KERNEL,):
+        try:
+            fc, _ = pick(fetch, name)
+            wc, _ = pick(write, name)
+            doc[name + "_traffic_bytes_per_launch"] = round(fc * f_scale + wc * w_scale)
+        except SystemExit:
+            pass
+    with open(out_path, "w") as f:
+        json.dump(doc, f, indent=1)
+    return doc
+
+
+def summarize_trace(stats_csv, command, out_md, bench_json=None):
+    """Markdown summary of a rocprofv3 --kernel-trace --stats run."""
+    rows = _csv_rows(stats_csv)
+    lines = [f"# Kernel trace: {ATTN_KERNEL} on the long-tail batch", "",
+             "Command (from the repository root):", "", "```", command, "```", "",
+             f"Kernel source sha256[:16]: `{kernel_source_hash()}`", "",
+             "| kernel | calls | average us | min us | max us | share % |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    if bench_json:
+        b = json.load(open(bench_json))
+        lines += ["", "bench.py line of the same run (HIP events on the kernel's stream):", "",
+                  f"- attention kernel mean: {b['attn_kernel_us']} us",
+                  f"- step: {b['ms_per_step'] * 1e3:.1f} us; value {b['value']} GB/s",
+                  f"- roofline achieved: {b['roofline']['achieved']} GB/s ({100 * b['roofline']['frac']:.1f}% of 8000)"]
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=1000,
                     help="untimed steps first (the GPU leaves its idle clocks during these)")
-    ap.add_argument("--chunk-pages", type=int, default=0, help="force the chunk size (pages)")
-    ap.add_argument("--units-per-cu", type=int, default=0, help="planner target items per CU")
+    ap.add_argument("--chunk-pages", type=int, default=0, help="force the pages per worker")
+    ap.add_argument("--workers-per-cu", type=int, default=0, help="planner workers (waves) per CU")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-skew", action="store_true", help="skip the equal-bytes uniform batch")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the counters summary from two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("STATS_CSV", "COMMAND", "OUT_MD"),
+                    help="write a markdown summary of a --kernel-trace --stats run and exit")
+    ap.add_argument("--bench-json", default=None, help="bench.py output of the traced run")
     args = ap.parse_args()
+    if args.summarize_counters:
+        from paper_2601_12784_amd.workloads import make_batch
+        kv = make_batch("longtail").kv_bytes()
+        print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_probe or 1024, kv), indent=1))
+        return
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace, bench_json=args.bench_json)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU; --gpus must be 1"}))
         log("bench.py runs on exactly one GPU: the decode-attention path here is single-GPU "
@@ -164,11 +260,12 @@ def main():
     batch = make_batch("longtail")
     kv = batch.kv_bytes()
     log(f"  {batch.num_seqs} seqs, {int(batch.seq_lens.sum())} tokens, {kv / 1e9:.3f} GB KV/step")
-    st = Stepper(batch, chunk_pages=args.chunk_pages, units_per_cu=args.units_per_cu)
+    st = Stepper(batch, chunk_pages=args.chunk_pages, workers_per_cu=args.workers_per_cu)
     ms_step, attn_ms_mean, attn_ms_med = time_steps(st, args.steps, args.warmup)
     info = st.info0
     log(f"  step {ms_step * 1e3:.1f} us, attention kernel {attn_ms_mean * 1e3:.1f} us (median "
-        f"{attn_ms_med * 1e3:.1f}), {info.num_work} items, chunk {info.chunk_pages}")
+        f"{attn_ms_med * 1e3:.1f}), {info.num_workers} workers x {info.chunk_pages} pages, "
+        f"{info.num_work} segments, {info.num_combine} cut pairs")
 
     desc = B.make_desc(batch.num_seqs, batch.num_q_heads, batch.num_kv_heads, batch.head_dim,
                        batch.block_table.shape[1], batch.num_pages, batch.scale)
@@ -197,8 +294,8 @@ def main():
                                "page 16, KV lengths lognormal(median 2048, sigma 1.0) clipped to [256, 16384], "
                                "bf16 N(0,1), one decode step",
                    "seed": batch.seed, "kv_bytes_per_step": kv, "tokens": int(batch.seq_lens.sum()),
-                   "chunk_pages": info.chunk_pages, "work_items": info.num_work,
-                   "split_pairs": info.num_combine},
+                   "workers": info.num_workers, "pages_per_worker": info.chunk_pages,
+                   "segments": info.num_work, "cut_pairs": info.num_combine},
         "seq_steps_per_s": round(batch.num_seqs / (ms_step * 1e-3), 1),
         "pct_of_peak_hbm": round(100.0 * kv / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2),
         "attn_kernel_us": round(attn_ms_mean * 1e3, 2),
@@ -214,7 +311,7 @@ def main():
         lens_u = uniform_lengths_like(batch.seq_lens.astype(np.int64))
         log("generating equal-token uniform batch")
         ub = build_batch(lens_u, 28, 4, 128, batch.seed + 100, name="uniform")
-        su = Stepper(ub, chunk_pages=args.chunk_pages, units_per_cu=args.units_per_cu)
+        su = Stepper(ub, chunk_pages=args.chunk_pages, workers_per_cu=args.workers_per_cu)
         ms_u, attn_u, _ = time_steps(su, args.steps, args.warmup)
         result["skew"] = {"uniform_ms_per_step": round(ms_u, 5), "uniform_kv_bytes": ub.kv_bytes(),
                           "skewed_over_uniform": round(ms_step / ms_u, 4),

@@ -23,12 +23,15 @@
  *
  * Memory layouts (row-major, every device pointer 16-byte aligned):
  *   q            bf16  [B][Hq][D]
- *   k_pool       bf16  [num_pages][Hkv][16][D]   a page tile is token-major
- *   v_pool       bf16  [num_pages][Hkv][D][16]   a page tile is dim-major
- *   block_table  int32 [B][block_table_stride]   entries 0 .. ceil(L_s/16)-1 are read
+ *   k_pool       bf16  [num_pages][Hkv][D/8][16][8]  key of slot t, dim d at [..][d/8][t][d%8]
+ *   v_pool       bf16  [num_pages][Hkv][D][16]       value of slot t, dim d at [..][d][t]
+ *   block_table  int32 [B][block_table_stride]       entries 0 .. ceil(L_s/16)-1 are read
  *   out          fp32  [B][Hq][D]
- *   lse          fp32  [B][Hq]                   optional (NULL = not written)
- * A (page, KV head) tile is 16*D*2 bytes (4 KiB at D = 128) and contiguous.
+ *   lse          fp32  [B][Hq]                       optional (NULL = not written)
+ * A (page, KV head) tile is 16*D*2 bytes (4 KiB at D = 128) and contiguous in
+ * both pools. Inside a K tile each group of 8 dims holds the 16 tokens' 8-dim
+ * pieces back to back; a V tile is dim-major. (Both are what the gfx950
+ * matrix-core operands of one page read as contiguous runs.)
  * Supported: D in {64, 128}, page_size 16, 1 <= g <= 16. The pools may be NULL
  * only when num_pages == 0, and then every sequence length must be 0.
  *
@@ -77,19 +80,22 @@ typedef struct sf_attn_desc {
 /* Planner knobs; a zero field takes its default. */
 typedef struct sf_plan_opts {
   int32_t num_cus;          /* compute units of the target GPU (default 256) */
-  int32_t chunk_pages;      /* > 0 forces this chunk size (pages) */
-  int32_t units_per_cu;     /* default 8 */
-  int32_t min_chunk_pages;  /* default 16 */
-  int32_t max_chunk_pages;  /* default 4096 */
+  int32_t chunk_pages;      /* > 0 forces the pages per worker: workers = ceil(T / chunk_pages) */
+  int32_t workers_per_cu;   /* default 4: attention waves per CU (one per SIMD) */
+  int32_t min_chunk_pages;  /* default 8: fewer workers rather than slices thinner than this */
+  int32_t reserved;         /* must be 0 */
 } sf_plan_opts;
 
 /* Filled by the planner; passed back unchanged to the other calls. */
 typedef struct sf_plan_info {
-  int32_t num_work;          /* attention work items */
-  int32_t num_combine;       /* (seq, KV head) pairs cut into more than one chunk */
-  int32_t num_partials;      /* partial-result slots = sum of their chunk counts */
-  int32_t chunk_pages;       /* chunk size the plan used */
-  uint64_t work_bytes;       /* bytes of the work list: (num_work + num_combine) * 32 */
+  int32_t num_workers;       /* attention waves to launch (one per worker) */
+  int32_t num_work;          /* segments (work items) */
+  int32_t num_combine;       /* (seq, KV head) pairs cut into more than one segment */
+  int32_t num_partials;      /* partial-result slots = sum of their segment counts */
+  int32_t chunk_pages;       /* pages per worker, ceil(T / num_workers) (0 if T = 0) */
+  int32_t reserved;          /* 0 */
+  uint64_t work_bytes;       /* bytes of the work list:
+                                (ceil(num_workers / 4) + num_work + num_combine) * 32 */
   uint64_t workspace_bytes;  /* device scratch sf_decode_attn needs (0 if no partials) */
   uint64_t desc_key;         /* fingerprint of the descriptor's shape and pool-size fields */
 } sf_plan_info;
@@ -97,22 +103,30 @@ typedef struct sf_plan_info {
 /*
  * Builds the work list on the host (no device calls).
  *
- * Rule (the length-aware split-K partition; the paper balances skewed
- * trajectory lengths across rollout instances, Sec. 5.2, and this balances
- * them across the compute units of one GPU):
- *   pages_s = ceil(L_s / 16);  T = sum_s pages_s * Hkv
- *   C   = opts.chunk_pages if > 0, else
- *         clamp(ceil(T / (units_per_cu * num_cus)), min_chunk_pages, max_chunk_pages)
- *   n_s = ceil(pages_s / C); chunk c of (s, kvh) covers pages
- *         [floor(c * pages_s / n_s), floor((c + 1) * pages_s / n_s))
- *   A sequence with L_s = 0 gets one item per KV head with an empty range.
- *   Items are ordered by page count, largest first, ties by (s, kvh, c).
- *   Pairs with n_s > 1 get consecutive partial slots in (s, kvh) order
- *   (chunk c -> slot_base + c) and one combine item each, in (s, kvh) order.
- * Work list, int32 rows of 8: attention items, then combine items:
- *   attention: seq, kv_head, page_begin, page_end, seq_len,
- *              slot (-1 = write out directly), combine index (-1 if n_s = 1), n_s
- *   combine:   seq, kv_head, slot_base, n_s, 0, 0, 0, 0
+ * Rule (the length-aware partition; the paper balances skewed trajectory
+ * lengths across rollout instances, Sec. 5.2, and this balances them across
+ * the compute units of one GPU). The pairs p = (s, kvh), in order s-major,
+ * kvh-minor, have pages_p = ceil(L_s / 16); laid end to end they form
+ * T = sum_p pages_p global pages. With
+ *   W = ceil(T / chunk_pages)                                   if chunk_pages > 0
+ *   W = min(workers_per_cu * num_cus, ceil(T / min_chunk_pages)) otherwise
+ * (W = 1 if T = 0 but B * Hkv > 0), worker w owns the global pages
+ * [floor(w T / W), floor((w + 1) T / W)): every worker reads the same number
+ * of pages (within one), however skewed the lengths are. A worker's range is
+ * cut at pair boundaries into segments, each a work item on one pair; a pair
+ * crossing k worker boundaries has n_p = k + 1 segments. Empty pairs
+ * (L_s = 0) get one item each, handed to worker e mod W for the e-th empty
+ * pair, after that worker's segments; their rows are written as zeros.
+ * Pairs with n_p > 1 get consecutive partial slots in pair order (segment c,
+ * counted in page order, -> slot_base + c) and one combine item each.
+ *
+ * Work list, int32 rows of 8:
+ *   ceil(W / 4) rows of worker table: worker w at ints 2w, 2w+1 =
+ *     (first item, item count); the worker's items are consecutive
+ *   num_work item rows, worker by worker:
+ *     seq, kv_head, page_begin, page_end (pages of the pair), seq_len,
+ *     slot (-1 = write out directly), combine index (-1 if n_p = 1), n_p
+ *   num_combine rows: seq, kv_head, slot_base, n_p, 0, 0, 0, 0
  *
  * seq_lens_host: B lengths on the host. opts may be NULL (all defaults).
  * work_host: host buffer of work_capacity_bytes; NULL only reports the sizes
@@ -127,10 +141,11 @@ sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t* seq_lens_
  *
  * If work_host is not NULL its info->work_bytes are first copied to work_dev
  * on the stream (work_host should be pinned memory for an asynchronous copy);
- * if it is NULL, work_dev must already hold this plan. Items whose sequence
- * fits in one chunk write out (and lse) directly; the others write partial
- * results into workspace, which sf_decode_attn_combine then merges. Calls
- * that share a work_dev or workspace must not overlap on the device.
+ * if it is NULL, work_dev must already hold this plan. One wave runs per
+ * worker and walks its segments in order. A pair with a single segment
+ * writes out (and lse) directly; segments of cut pairs write partial results
+ * into workspace, which sf_decode_attn_combine then merges. Calls that share
+ * a work_dev or workspace must not overlap on the device.
  * workspace: device buffer of workspace_bytes >= info->workspace_bytes
  * (may be NULL when that is 0). q, k_pool, v_pool, block_table, out: device
  * pointers in the layouts above. lse: device pointer or NULL.

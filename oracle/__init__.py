@@ -63,16 +63,18 @@ def _u16(a) -> np.ndarray:
 
 
 def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale, nthreads: int = 0):
-    """fp64 reference. q/k_pool/v_pool are uint16 bf16 bit arrays in the
-    documented layouts; returns (out [B,Hq,D] float64, lse [B,Hq] float64)."""
+    """fp64 reference. q [B,Hq,D], k_pool [N,Hkv,D/8,16,8] and v_pool
+    [N,Hkv,D,16] are uint16 bf16 bit arrays; returns (out [B,Hq,D] float64,
+    lse [B,Hq] float64)."""
     q = _u16(q)
     k_pool = _u16(k_pool)
     v_pool = _u16(v_pool)
     bt = np.ascontiguousarray(block_table, dtype=np.int32)
     lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
     b, hq, d = q.shape
-    n, hkv, p, d2 = k_pool.shape
-    assert d2 == d and v_pool.shape == (n, hkv, d, p) and bt.shape[0] == b and lens.shape == (b,)
+    n, hkv, groups, p, eight = k_pool.shape
+    assert groups * eight == d and eight == 8
+    assert v_pool.shape == (n, hkv, d, p) and bt.shape[0] == b and lens.shape == (b,)
     out = np.empty((b, hq, d), dtype=np.float64)
     lse = np.empty((b, hq), dtype=np.float64)
     rc = lib().sf_oracle_decode_attn(b, hq, hkv, d, p, bt.shape[1], n, _ptr(q), _ptr(k_pool),
@@ -88,7 +90,8 @@ def gather(k_pool, v_pool, block_table, seq: int, kvh: int, length: int):
     k_pool = _u16(k_pool)
     v_pool = _u16(v_pool)
     bt = np.ascontiguousarray(block_table, dtype=np.int32)
-    n, hkv, p, d = k_pool.shape
+    n, hkv, groups, p, eight = k_pool.shape
+    d = groups * eight
     kd = np.empty((length, d), dtype=np.uint16)
     vd = np.empty((length, d), dtype=np.uint16)
     rc = lib().sf_oracle_gather(hkv, d, p, bt.shape[1], n, _ptr(k_pool), _ptr(v_pool), _ptr(bt),

@@ -18,16 +18,16 @@ def widen(bits) -> np.ndarray:
 
 def gather_dense(k_pool, v_pool, block_table, seq, kvh, length):
     """[L, D] float64 keys and values of one (sequence, KV head)."""
-    k_pool = np.asarray(k_pool)
-    v_pool = np.asarray(v_pool)
-    page = k_pool.shape[2]
+    k_pool = np.asarray(k_pool)          # [N, Hkv, D/8, P, 8]
+    v_pool = np.asarray(v_pool)          # [N, Hkv, D, P]
+    page = k_pool.shape[3]
     rows_k, rows_v = [], []
     for t in range(length):
         pg = int(block_table[seq][t // page])
         slot = t % page
-        rows_k.append(widen(k_pool[pg, kvh, slot, :]))
+        rows_k.append(widen(k_pool[pg, kvh, :, slot, :].reshape(-1)))
         rows_v.append(widen(v_pool[pg, kvh, :, slot]))
-    d = k_pool.shape[3]
+    d = v_pool.shape[2]
     if not rows_k:
         return np.zeros((0, d)), np.zeros((0, d))
     return np.stack(rows_k), np.stack(rows_v)

@@ -52,8 +52,8 @@ def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale):
     k_pool = np.asarray(k_pool)
     v_pool = np.asarray(v_pool)
     b, hq, d = q.shape
-    hkv = k_pool.shape[1]
-    page = k_pool.shape[2]
+    hkv = k_pool.shape[1]                 # k_pool [N, Hkv, D/8, P, 8]
+    page = k_pool.shape[3]
     g = hq // hkv
     with localcontext() as ctx:
         ctx.prec = PREC
@@ -70,7 +70,7 @@ def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale):
             krows, vrows = [], []
             for t in range(n):
                 pg = int(block_table[s][t // page])
-                krows.append([int(x) for x in k_pool[pg, kvh, t % page, :]])
+                krows.append([int(x) for x in k_pool[pg, kvh, :, t % page, :].reshape(-1)])
                 vrows.append([int(x) for x in v_pool[pg, kvh, :, t % page]])
             o, l = attention_one([int(x) for x in q[s, h, :]], krows, vrows, sc)
             dec[(s, h)] = (o, l)

@@ -1,32 +1,30 @@
-"""Re-derivation of the split-K work plan from its written rule.
+"""Re-derivation of the work plan (length-balanced worker slices) from its written rule.
 
 TEST INFRASTRUCTURE ONLY. The paper balances skewed trajectory lengths across
 rollout instances (routing and migration, Sec. 5.2); inside one GPU the same
-skew is balanced by cutting long (sequence, KV head) ranges into page-aligned
-chunks. This module restates that rule in plain Python so the C planner can be
-checked against it bit for bit:
+skew is balanced by giving every resident wave the same number of KV pages.
+This module restates that rule in plain Python, independently of the C
+planner, so the two can be compared bit for bit:
 
-  pages_s = ceil(L_s / 16)
-  T       = sum_s pages_s * Hkv                       (page-heads in the batch)
-  C       = chunk_pages if given (> 0), else
-            clamp(ceil(T / (units_per_cu * num_cus)), min_chunk, max_chunk)
-  n_s     = ceil(pages_s / C)                         (0 pages -> one empty item)
-  chunk c of (s, kvh) covers pages [floor(c*pages_s/n_s), floor((c+1)*pages_s/n_s))
-  items   sorted by page count descending, ties by (s, kvh, c) ascending
-  partial slots: pairs with n_s > 1, in (s, kvh) order, chunk c -> base + c
-  combine items: one per such pair, in (s, kvh) order
+  pairs p = (s, kvh), s-major; pages_p = ceil(L_s / 16); T = sum_p pages_p
+  W = ceil(T / chunk_pages) if chunk_pages > 0
+      else min(workers_per_cu * num_cus, ceil(T / min_chunk))   (1 if T = 0 < #pairs)
+  worker w owns global pages [floor(w*T/W), floor((w+1)*T/W)), cut at pair
+  boundaries into segments (items); empty pairs go to worker e mod W after
+  its segments; n_p = segments of pair p
+  partial slots for pairs with n_p > 1 in pair order, segment c -> base + c
 
-Item rows (int32 x 8):
-  attention: seq, kv_head, page_begin, page_end, seq_len, slot (-1 = direct),
-             combine index (-1 if n_s = 1), n_s
-  combine:   seq, kv_head, slot_base, n_s, 0, 0, 0, 0
+Work list rows (int32 x 8): ceil(W/4) worker-table rows (first item, count
+per worker), then the items worker by worker
+  (seq, kv_head, page_begin, page_end, seq_len, slot or -1, combine index or -1, n_p),
+then one combine row per cut pair (seq, kv_head, slot_base, n_p, 0, 0, 0, 0).
 """
 from __future__ import annotations
 
 import numpy as np
 
 PAGE = 16
-DEFAULTS = dict(units_per_cu=8, min_chunk=16, max_chunk=4096)
+DEFAULTS = dict(workers_per_cu=4, min_chunk=8)
 
 
 def _ceil(a, b):
@@ -38,45 +36,70 @@ def _align(x, a=256):
 
 
 def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
-         units_per_cu=None, min_chunk=None, max_chunk=None):
-    upc = DEFAULTS["units_per_cu"] if not units_per_cu else units_per_cu
-    mn = DEFAULTS["min_chunk"] if not min_chunk else min_chunk
-    mx = DEFAULTS["max_chunk"] if not max_chunk else max_chunk
+         workers_per_cu=None, min_chunk=None):
+    wpc = workers_per_cu or DEFAULTS["workers_per_cu"]
+    mn = min_chunk or DEFAULTS["min_chunk"]
     lens = [int(x) for x in seq_lens]
-    pages = [_ceil(L, PAGE) for L in lens]
-    total = sum(pages) * num_kv_heads
-    if chunk_pages > 0:
-        c_pages = chunk_pages
+    pairs = [(s, kvh) for s in range(len(lens)) for kvh in range(num_kv_heads)]
+    pages = [_ceil(lens[s], PAGE) for s, _ in pairs]
+    total = sum(pages)
+    if not pairs:
+        workers = 0
+    elif total == 0:
+        workers = 1
+    elif chunk_pages > 0:
+        workers = _ceil(total, chunk_pages)
     else:
-        c_pages = min(max(_ceil(total, upc * num_cus), mn), mx)
+        workers = min(wpc * num_cus, _ceil(total, mn))
 
-    rows = []      # (size, s, kvh, c, row)
-    combine = []
-    slot = 0
-    for s, (L, npg) in enumerate(zip(lens, pages)):
-        for kvh in range(num_kv_heads):
+    # every (worker, pair) overlap is a segment
+    starts = np.cumsum([0] + pages)
+    bounds = [w * total // workers for w in range(workers + 1)] if workers else [0]
+    per_worker = [[] for _ in range(workers)]
+    seg_of_pair = {p: [] for p in range(len(pairs))}
+    for w in range(workers):
+        lo, hi = bounds[w], bounds[w + 1]
+        for p, npg in enumerate(pages):
             if npg == 0:
-                rows.append((0, s, kvh, 0, [s, kvh, 0, 0, L, -1, -1, 1]))
                 continue
-            n = _ceil(npg, c_pages)
-            for c in range(n):
-                b = c * npg // n
-                e = (c + 1) * npg // n
-                if n > 1:
-                    row = [s, kvh, b, e, L, slot + c, len(combine), n]
-                else:
-                    row = [s, kvh, b, e, L, -1, -1, 1]
-                rows.append((e - b, s, kvh, c, row))
-            if n > 1:
-                combine.append([s, kvh, slot, n, 0, 0, 0, 0])
-                slot += n
-    rows.sort(key=lambda r: (-r[0], r[1], r[2], r[3]))
-    items = np.array([r[4] for r in rows], dtype=np.int32).reshape(-1, 8)
+            a, b = max(lo, starts[p]), min(hi, starts[p] + npg)
+            if a < b:
+                seg = [p, int(a - starts[p]), int(b - starts[p])]
+                per_worker[w].append(seg)
+                seg_of_pair[p].append(seg)
+    empties = [p for p, npg in enumerate(pages) if npg == 0]
+    for e, p in enumerate(empties):
+        seg = [p, 0, 0]
+        per_worker[e % workers].append(seg)
+        seg_of_pair[p].append(seg)
+
+    slot, combine, meta = 0, [], {}
+    for p in range(len(pairs)):
+        n = len(seg_of_pair[p])
+        if n > 1:
+            meta[p] = (slot, len(combine), n)
+            s, kvh = pairs[p]
+            combine.append([s, kvh, slot, n, 0, 0, 0, 0])
+            slot += n
+
+    table = np.zeros((_ceil(workers, 4), 8), dtype=np.int32)
+    rows = []
+    for w in range(workers):
+        table.reshape(-1)[2 * w] = len(rows)
+        table.reshape(-1)[2 * w + 1] = len(per_worker[w])
+        for p, b, e in per_worker[w]:
+            s, kvh = pairs[p]
+            if p in meta:
+                base, ci, n = meta[p]
+                c = [tuple(x) for x in seg_of_pair[p]].index((p, b, e))
+                rows.append([s, kvh, b, e, lens[s], base + c, ci, n])
+            else:
+                rows.append([s, kvh, b, e, lens[s] if e > b else 0, -1, -1, 1])
+    items = np.array(rows, dtype=np.int32).reshape(-1, 8)
     comb = np.array(combine, dtype=np.int32).reshape(-1, 8)
     g = num_q_heads // num_kv_heads
-    if slot:
-        ws = _align(slot * g * head_dim * 4) + _align(slot * g * 4)
-    else:
-        ws = 0
-    return dict(items=items, combine=comb, chunk_pages=c_pages, num_partials=slot,
-                workspace_bytes=ws, work_bytes=(items.shape[0] + comb.shape[0]) * 8 * 4)
+    ws = _align(slot * g * head_dim * 4) + _align(slot * g * 4) if slot else 0
+    return dict(table=table, items=items, combine=comb, num_workers=workers,
+                chunk_pages=_ceil(total, workers) if workers and total else 0,
+                num_partials=slot, workspace_bytes=ws,
+                work_bytes=(table.shape[0] + items.shape[0] + comb.shape[0]) * 8 * 4)

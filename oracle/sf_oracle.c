@@ -13,8 +13,8 @@
  *
  *   for sequence s with L = seq_lens[s] cached tokens and query head h,
  *   with g = Hq / Hkv query heads sharing KV head kvh = h / g:
- *     K_s[t] = k_pool[bt[s][t / P], kvh, t % P, :]          t = 0 .. L-1
- *     V_s[t] = v_pool[bt[s][t / P], kvh, :, t % P]
+ *     K_s[t][d] = k_pool[bt[s][t / P]][kvh][d / 8][t % P][d % 8]   t = 0 .. L-1
+ *     V_s[t][d] = v_pool[bt[s][t / P]][kvh][d][t % P]
  *     z_t    = scale * sum_d q[s,h,d] * K_s[t][d]
  *     m      = max_t z_t,  w_t = exp(z_t - m)
  *     out    = sum_t w_t V_s[t] / sum_t w_t
@@ -26,7 +26,7 @@
  * rescaling and no split: subtracting the max is the textbook way to keep
  * exp() in range and does not change the mathematical value.
  *
- * Layouts: q [B][Hq][D]; k_pool [N][Hkv][P][D]; v_pool [N][Hkv][D][P];
+ * Layouts: q [B][Hq][D]; k_pool [N][Hkv][D/8][P][8]; v_pool [N][Hkv][D][P];
  * bt [B][stride] int32; all bf16 stored as uint16 bit patterns.
  */
 #include <math.h>
@@ -37,6 +37,14 @@
 #include <omp.h>
 #endif
 
+/* Element offsets of key and value (page pg, KV head kvh, slot, dim d). */
+static int64_t k_index(int64_t pg, int Hkv, int kvh, int D, int P, int slot, int d) {
+  return ((((pg * Hkv + kvh) * (D / 8) + d / 8) * P) + slot) * 8 + d % 8;
+}
+static int64_t v_index(int64_t pg, int Hkv, int kvh, int D, int P, int slot, int d) {
+  return ((pg * Hkv + kvh) * D + d) * P + slot;
+}
+
 /* bf16 is the upper half of an IEEE binary32; widening is exact. */
 static double bf16_to_double(uint16_t bits) {
   uint32_t u = (uint32_t)bits << 16;
@@ -45,7 +53,7 @@ static double bf16_to_double(uint16_t bits) {
   return (double)f;
 }
 
-int sf_oracle_version(void) { return 1; }
+int sf_oracle_version(void) { return 2; }
 
 int sf_oracle_max_threads(void) {
 #ifdef _OPENMP
@@ -83,10 +91,8 @@ int sf_oracle_gather(int Hkv, int D, int P, int stride, int num_pages,
     if (pg < 0 || pg >= num_pages) return 1;
     int slot = t % P;
     for (int d = 0; d < D; ++d) {
-      int64_t kidx = (((int64_t)pg * Hkv + kvh) * P + slot) * D + d;
-      int64_t vidx = (((int64_t)pg * Hkv + kvh) * D + d) * P + slot;
-      k_out[(int64_t)t * D + d] = k_pool[kidx];
-      v_out[(int64_t)t * D + d] = v_pool[vidx];
+      k_out[(int64_t)t * D + d] = k_pool[k_index(pg, Hkv, kvh, D, P, slot, d)];
+      v_out[(int64_t)t * D + d] = v_pool[v_index(pg, Hkv, kvh, D, P, slot, d)];
     }
   }
   return 0;
@@ -137,9 +143,9 @@ int sf_oracle_decode_attn(int B, int Hq, int Hkv, int D, int P, int stride, int 
       for (int t = 0; t < L; ++t) {
         int32_t pg = bt[(int64_t)s * stride + t / P];
         int slot = t % P;
-        const uint16_t* krow = k_pool + (((int64_t)pg * Hkv + kvh) * P + slot) * D;
         double dot = 0.0;
-        for (int d = 0; d < D; ++d) dot += bf16_to_double(qv[d]) * bf16_to_double(krow[d]);
+        for (int d = 0; d < D; ++d)
+          dot += bf16_to_double(qv[d]) * bf16_to_double(k_pool[k_index(pg, Hkv, kvh, D, P, slot, d)]);
         z[t] = scale * dot;
         if (z[t] > m) m = z[t];
       }
@@ -149,10 +155,9 @@ int sf_oracle_decode_attn(int B, int Hq, int Hkv, int D, int P, int stride, int 
       for (int t = 0; t < L; ++t) {
         int32_t pg = bt[(int64_t)s * stride + t / P];
         int slot = t % P;
-        const uint16_t* vtile = v_pool + ((int64_t)pg * Hkv + kvh) * (int64_t)D * P;
         double w = exp(z[t] - m);
         wsum += w;
-        for (int d = 0; d < D; ++d) acc[d] += w * bf16_to_double(vtile[(int64_t)d * P + slot]);
+        for (int d = 0; d < D; ++d) acc[d] += w * bf16_to_double(v_pool[v_index(pg, Hkv, kvh, D, P, slot, d)]);
       }
       for (int d = 0; d < D; ++d) o[d] = acc[d] / wsum;
       if (lse) lse[sh] = m + log(wsum);

@@ -39,13 +39,14 @@ class sf_attn_desc(ctypes.Structure):
 
 class sf_plan_opts(ctypes.Structure):
     _fields_ = [("num_cus", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
-                ("units_per_cu", ctypes.c_int32), ("min_chunk_pages", ctypes.c_int32),
-                ("max_chunk_pages", ctypes.c_int32)]
+                ("workers_per_cu", ctypes.c_int32), ("min_chunk_pages", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class sf_plan_info(ctypes.Structure):
-    _fields_ = [("num_work", ctypes.c_int32), ("num_combine", ctypes.c_int32),
-                ("num_partials", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
+    _fields_ = [("num_workers", ctypes.c_int32), ("num_work", ctypes.c_int32),
+                ("num_combine", ctypes.c_int32), ("num_partials", ctypes.c_int32),
+                ("chunk_pages", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("work_bytes", ctypes.c_uint64), ("workspace_bytes", ctypes.c_uint64),
                 ("desc_key", ctypes.c_uint64)]
 
@@ -101,9 +102,8 @@ def make_desc(num_seqs, num_q_heads, num_kv_heads, head_dim, block_table_stride,
                         int(page_size), int(block_table_stride), int(num_pages), float(softmax_scale))
 
 
-def make_opts(num_cus=0, chunk_pages=0, units_per_cu=0, min_chunk_pages=0, max_chunk_pages=0):
-    return sf_plan_opts(int(num_cus), int(chunk_pages), int(units_per_cu), int(min_chunk_pages),
-                        int(max_chunk_pages))
+def make_opts(num_cus=0, chunk_pages=0, workers_per_cu=0, min_chunk_pages=0):
+    return sf_plan_opts(int(num_cus), int(chunk_pages), int(workers_per_cu), int(min_chunk_pages), 0)
 
 
 def _addr(x) -> int | None:
@@ -178,7 +178,7 @@ def sf_decode_attn(desc, info, work_host, work_dev, q, k_pool, v_pool, block_tab
     """Enqueues the attention kernel (and the work-list upload if work_host is given)."""
     b, hq, hkv, d = desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
     _dev(q, "q", torch.bfloat16, (b, hq, d))
-    _dev(k_pool, "k_pool", torch.bfloat16, (desc.num_pages, hkv, PAGE, d))
+    _dev(k_pool, "k_pool", torch.bfloat16, (desc.num_pages, hkv, d // 8, PAGE, 8))
     _dev(v_pool, "v_pool", torch.bfloat16, (desc.num_pages, hkv, d, PAGE))
     _dev(block_table, "block_table", torch.int32, (b, desc.block_table_stride))
     _dev(out, "out", torch.float32, (b, hq, d))
@@ -321,8 +321,7 @@ class DecodeAttention:
         o = self.opts
         if chunk_pages is None:
             return o
-        return sf_plan_opts(o.num_cus, int(chunk_pages), o.units_per_cu, o.min_chunk_pages,
-                            o.max_chunk_pages)
+        return sf_plan_opts(o.num_cus, int(chunk_pages), o.workers_per_cu, o.min_chunk_pages, 0)
 
     def _check_tensors(self, q, k_pool, v_pool, block_table, out, lse):
         key = (q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
@@ -332,7 +331,7 @@ class DecodeAttention:
             return
         b, hkv, d = q.shape[0], self.hkv, self.d
         _dev(q, "q", torch.bfloat16, (b, self.hq, d))
-        _dev(k_pool, "k_pool", torch.bfloat16, (k_pool.shape[0], hkv, PAGE, d))
+        _dev(k_pool, "k_pool", torch.bfloat16, (k_pool.shape[0], hkv, d // 8, PAGE, 8))
         _dev(v_pool, "v_pool", torch.bfloat16, (k_pool.shape[0], hkv, d, PAGE))
         _dev(block_table, "block_table", torch.int32, (b, block_table.shape[1]))
         _dev(out, "out", torch.float32, (b, self.hq, d))

@@ -15,8 +15,10 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 sf_status check_plan(const sf_attn_desc* d, const sf_plan_info* info) {
   if (!info) return SF_ERR_INVALID_ARG;
   if (info->desc_key != desc_key(d)) return SF_ERR_PLAN_MISMATCH;
-  if (info->num_work < 0 || info->num_combine < 0 || info->num_partials < 0) return SF_ERR_INVALID_ARG;
-  if (info->work_bytes != uint64_t(info->num_work + info->num_combine) * kItemInts * 4)
+  if (info->num_workers < 0 || info->num_work < 0 || info->num_combine < 0 || info->num_partials < 0)
+    return SF_ERR_INVALID_ARG;
+  if (info->reserved != 0 || info->work_bytes != uint64_t(table_rows(info->num_workers) + info->num_work +
+                                                          info->num_combine) * kItemInts * 4)
     return SF_ERR_PLAN_MISMATCH;
   return SF_OK;
 }
@@ -33,7 +35,7 @@ extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info
   sf_status st = validate_desc(desc);
   if (st != SF_OK) return st;
   if ((st = check_plan(desc, info)) != SF_OK) return st;
-  if (info->num_work == 0) return SF_OK;
+  if (info->num_workers == 0) return SF_OK;
   if (!work_dev || !q || !block_table || !out) return SF_ERR_INVALID_ARG;
   // An empty pool (num_pages == 0) only backs plans whose sequences are all empty.
   if (desc->num_pages > 0 && (!k_pool || !v_pool)) return SF_ERR_INVALID_ARG;
@@ -51,8 +53,9 @@ extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info
   const int32_t g = desc->num_q_heads / desc->num_kv_heads;
   Workspace ws = carve_workspace(workspace, info->num_partials, g, desc->head_dim);
   AttnArgs a;
-  a.work = work_dev;
-  a.num_work = info->num_work;
+  a.worker_table = work_dev;
+  a.items = work_dev + table_rows(info->num_workers) * kItemInts;
+  a.num_workers = info->num_workers;
   a.q = static_cast<const uint16_t*>(q);
   a.k_pool = static_cast<const uint16_t*>(k_pool);
   a.v_pool = static_cast<const uint16_t*>(v_pool);
@@ -85,7 +88,7 @@ extern "C" sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_p
   const int32_t g = desc->num_q_heads / desc->num_kv_heads;
   Workspace ws = carve_workspace(const_cast<void*>(workspace), info->num_partials, g, desc->head_dim);
   CombineArgs a;
-  a.items = work_dev + int64_t(info->num_work) * kItemInts;
+  a.items = work_dev + (table_rows(info->num_workers) + info->num_work) * kItemInts;
   a.num_items = info->num_combine;
   a.part_o = ws.part_o;
   a.part_lse = ws.part_lse;

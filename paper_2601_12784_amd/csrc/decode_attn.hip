@@ -2,23 +2,25 @@
 //
 // One decode step lets each running trajectory's new query attend over its
 // whole cached K/V (App. B.1 of the paper, attention-latency term); the step is
-// bound by reading that cache from HBM. A work item is one page-aligned chunk
-// of one (sequence, KV head) pair; one wave64 owns one item and walks it two
-// pages (32 tokens) at a time:
+// bound by reading that cache from HBM. A work item is one page-aligned
+// segment of one (sequence, KV head) pair; one wave64 runs per worker, walks
+// its segments in order and each segment two pages (32 tokens) at a time:
 //
-//   S^T[32 tok][16 heads] = K_blk Q^T      2 x (D/32) v_mfma_f32_16x16x32_bf16
+//   S^T[16 tok][16 heads] = K_page Q^T per page, (D/32) v_mfma_f32_16x16x32_bf16 each
 //   online softmax in base 2 (wave64 max across the four 16-lane groups)
 //   O^T[D][16 heads]     += V_blk^T P^T    (D/16) x 2 MFMAs, P split bf16 hi + lo
 //
 // The GQA group's g <= 16 query heads fill the 16 MFMA columns (zero padded),
-// so K and V bytes are read exactly once per KV head. K page tiles are
-// token-major and V page tiles dim-major, so both MFMA A operands are single
-// 128-bit global loads straight into registers: no LDS staging is needed.
-// The contraction index order inside an MFMA is free as long as both operands
-// agree; the kernel assigns tokens to MFMA rows so that each lane's eight
-// score values are tokens 8*grp .. 8*grp+7 of the block, which are exactly the
-// eight P^T values its PV operand needs and the eight V^T values of one
-// contiguous 16-byte load.
+// so K and V bytes are read exactly once per KV head. The page-tile layouts
+// make every MFMA A operand a plain global load straight into registers (no
+// LDS staging): a K tile stores, for each group of 8 dims, the 16 tokens'
+// 8-dim pieces back to back, so the QK operand of one page (row = token slot,
+// k-group = dim group) is one contiguous 1 KiB load per MFMA; a V tile is
+// dim-major, so the PV operand (row = dim, k = tokens) is two 8-byte loads,
+// 4 tokens from each page of the block. Each lane's eight scores are tokens
+// 4*grp .. 4*grp+3 of both pages, exactly the eight P^T values its PV operand
+// needs (the contraction order inside an MFMA is free as long as both
+// operands agree).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -41,11 +43,26 @@ __device__ __forceinline__ size_t tile_offset(int32_t page, int32_t num_kv_heads
                                               int32_t d) {
   return (size_t(page) * num_kv_heads + kv_head) * size_t(kPage * d);
 }
-__device__ __forceinline__ int k_elem(int slot, int dim, int d) { return slot * d + dim; }
+// K tile: D/8 groups of 8 dims; inside a group the 16 slots' 8-dim pieces are
+// consecutive (16 bytes each). V tile: dim-major, 16 slots per dim.
+__device__ __forceinline__ int k_elem(int slot, int dim, int d) {
+  (void)d;
+  return ((dim >> 3) * kPage + slot) * 8 + (dim & 7);
+}
 __device__ __forceinline__ int v_elem(int slot, int dim) { return dim * kPage + slot; }
 
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
+}
+
+// The work list and the block table are never written while a kernel runs.
+// Reading them through the constant address space lets the compiler use
+// scalar loads, whose completion is counted apart from the K/V vector loads
+// (a vector load of a page id would make the wave wait for every K/V load
+// issued before it).
+typedef __attribute__((address_space(4))) const int32_t* const_i32_ptr;
+__device__ __forceinline__ const_i32_ptr as_constant(const int32_t* p) {
+  return (const_i32_ptr)(p);
 }
 
 __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
@@ -66,133 +83,183 @@ __device__ __forceinline__ float bf16_value(uint32_t bits) {
 // attention over one chunk per wave
 // ---------------------------------------------------------------------------
 // K and V are streamed once and never reused, so they are read with
-// nontemporal loads; the next two-page block is fetched while the current one
-// is multiplied, which keeps 32 KiB in flight per wave.
+// nontemporal loads. Each two-page block is fetched in two halves: the next
+// block's K is issued before this block's scores are formed and its V before
+// this block's P.V product, so 16 loads (16 KiB) stay in flight behind every
+// wait while only three half-blocks occupy registers.
 __device__ __forceinline__ u32x4 stream16(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 
 template <int D>
-struct KvBlock {
+struct Shape {
   static constexpr int KB = D / 32;  // QK MFMA steps over the head dimension
   static constexpr int JB = D / 16;  // PV output blocks of 16 dims
-  u32x4 k[2][KB];
-  u32x4 v[JB];
+};
+
+template <int D>
+struct KHalf {
+  u32x4 k[2][Shape<D>::KB];
+};
+
+template <int D>
+struct VHalf {
+  u32x4 v[Shape<D>::JB];
 };
 
 template <int D>
 struct ChunkCtx {
   const uint16_t* k_pool;
   const uint16_t* v_pool;
-  const int32_t* bt;  // this sequence's block-table row
+  const_i32_ptr bt;   // this sequence's block-table row
   int num_kv_heads;
   int kvh;
-  int pe;             // end of this chunk (pages)
-  int k_page_sel;     // which page of the block this lane's K rows come from
-  int k_off;          // element offset of this lane's K row piece inside a tile
-  int v_page_sel;
-  int v_off;
+  int pe;             // end of this segment (pages)
+  int k_off;          // element offset of this lane's K piece inside a tile
+  int v_off;          // element offset of this lane's V^T piece inside a tile
 };
 
-// Loads the two-page block that starts at logical page pg (a single page if
+// Physical pages of the two-page block at logical page pg (a single page if
 // pg + 1 == pe; the missing page then aliases the first and is masked later).
+struct PagePair {
+  int p0, p1;
+};
 template <int D>
-__device__ __forceinline__ void load_block(const ChunkCtx<D>& c, int pg, KvBlock<D>& b) {
-  const int pid0 = c.bt[pg];
-  int pid1 = pid0;
-  if (pg + 1 < c.pe) pid1 = c.bt[pg + 1];
-  const uint16_t* kp = c.k_pool + tile_offset(c.k_page_sel ? pid1 : pid0, c.num_kv_heads, c.kvh, D) + c.k_off;
-  const uint16_t* vp = c.v_pool + tile_offset(c.v_page_sel ? pid1 : pid0, c.num_kv_heads, c.kvh, D) + c.v_off;
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int kb = 0; kb < KvBlock<D>::KB; ++kb) b.k[h][kb] = stream16(kp + k_elem(4 * h, kb * 32, D));
-#pragma unroll
-  for (int jb = 0; jb < KvBlock<D>::JB; ++jb) b.v[jb] = stream16(vp + v_elem(0, 16 * jb));
+__device__ __forceinline__ PagePair block_pages(const ChunkCtx<D>& c, int pg) {
+  PagePair pp;
+  pp.p0 = c.bt[pg];
+  pp.p1 = pp.p0;
+  if (pg + 1 < c.pe) pp.p1 = c.bt[pg + 1];
+  return pp;
 }
+
+// K operand of page h for MFMA step kb: row = token slot col, k-group = dims
+// 32*kb + 8*grp .. +8; the wave reads one contiguous 1 KiB per step.
+template <int D>
+__device__ __forceinline__ void load_k(const ChunkCtx<D>& c, PagePair pp, KHalf<D>& b) {
+  const uint16_t* k0 = c.k_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.k_off;
+  const uint16_t* k1 = c.k_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.k_off;
+#pragma unroll
+  for (int kb = 0; kb < Shape<D>::KB; ++kb) {
+    b.k[0][kb] = stream16(k0 + k_elem(0, 32 * kb, D));
+    b.k[1][kb] = stream16(k1 + k_elem(0, 32 * kb, D));
+  }
+}
+
+// V^T operand for dims 16*jb + col: tokens 4*grp .. +3 of each page (8 bytes
+// each); the wave reads 512 contiguous bytes per page and step.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x2 stream8(const uint16_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+}
+template <int D>
+__device__ __forceinline__ void load_v(const ChunkCtx<D>& c, PagePair pp, VHalf<D>& b) {
+  const uint16_t* v0 = c.v_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.v_off;
+  const uint16_t* v1 = c.v_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.v_off;
+#pragma unroll
+  for (int jb = 0; jb < Shape<D>::JB; ++jb) {
+    const u32x2 x = stream8(v0 + v_elem(0, 16 * jb));
+    const u32x2 y = stream8(v1 + v_elem(0, 16 * jb));
+    b.v[jb] = u32x4{x[0], x[1], y[0], y[1]};
+  }
+}
+
+// Block token (counted from the block's first token) of a lane's item e:
+// items 0..3 are slots 4*grp + e of the first page, 4..7 of the second.
+__device__ __forceinline__ int item_token(int grp, int e) { return (e < 4 ? 0 : kPage - 4) + 4 * grp + e; }
 
 template <int D>
 struct SoftmaxState {
-  f32x4 o[KvBlock<D>::JB];  // O^T block jb: O[head col][16*jb + 4*grp + i]
-  float m;                  // running max of this lane's head, log2 units
-  float lsum;               // this lane's share of sum_t 2^(z_t - m)
+  f32x4 o[Shape<D>::JB];  // O^T block jb: O[head col][16*jb + 4*grp + i]
+  float m;                // running max of this lane's head, log2 units
+  float lsum;             // this lane's share of sum_t 2^(z_t - m)
 };
 
-// Scores, online-softmax update and P.V accumulation for one block.
+// Weights of one block as the P^T operand (bf16 hi + lo parts, about 16 bits
+// of each weight) and the factor that rescales earlier accumulations.
+struct BlockWeights {
+  u32x4 phi, plo;
+  float alpha;
+};
+
+// Scores and online-softmax update for one block.
 // nvalid = tokens of the block (from its first token) inside the sequence.
 template <int D>
-__device__ __forceinline__ void consume_block(KvBlock<D>& b, const u32x4* qf, int nvalid, int grp,
-                                              float scale_log2, SoftmaxState<D>& st) {
-  constexpr int KB = KvBlock<D>::KB;
-  constexpr int JB = KvBlock<D>::JB;
+__device__ __forceinline__ BlockWeights score_block(const KHalf<D>& b, const u32x4* qf, int nvalid, int grp,
+                                                    float scale_log2, SoftmaxState<D>& st) {
   f32x4 s0 = {0.f, 0.f, 0.f, 0.f};
   f32x4 s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int kb = 0; kb < KB; ++kb) {
+  for (int kb = 0; kb < Shape<D>::KB; ++kb) {
     s0 = mfma_bf16(b.k[0][kb], qf[kb], s0);
     s1 = mfma_bf16(b.k[1][kb], qf[kb], s1);
   }
-  // This lane now holds head `col`, block tokens 8*grp + e (e < 4 from s0).
-  const int tok0 = 8 * grp;
+  // This lane now holds head `col`: s0[e] = slot 4*grp + e of the first page,
+  // s1[e] = the same slot of the second page.
   float sc[8];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    sc[e] = (tok0 + e < nvalid) ? s0[e] * scale_log2 : -__builtin_inff();
-    sc[4 + e] = (tok0 + 4 + e < nvalid) ? s1[e] * scale_log2 : -__builtin_inff();
+    sc[e] = (item_token(grp, e) < nvalid) ? s0[e] * scale_log2 : -__builtin_inff();
+    sc[4 + e] = (item_token(grp, 4 + e) < nvalid) ? s1[e] * scale_log2 : -__builtin_inff();
   }
   float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
                    fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
   const float mnew = fmaxf(st.m, mx);
-  const float alpha = fast_exp2(st.m - mnew);
+  BlockWeights w;
+  w.alpha = fast_exp2(st.m - mnew);
   st.m = mnew;
-
-  // P^T operand: the lane's eight weights as bf16 hi + lo parts, so the
-  // PV product keeps about 16 bits of each weight.
   float ps = 0.f;
   uint32_t hi[4], lo[4];
 #pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const float p0 = fast_exp2(sc[2 * w] - mnew);
-    const float p1 = fast_exp2(sc[2 * w + 1] - mnew);
+  for (int i = 0; i < 4; ++i) {
+    const float p0 = fast_exp2(sc[2 * i] - mnew);
+    const float p1 = fast_exp2(sc[2 * i + 1] - mnew);
     ps += p0 + p1;
     const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
     const uint32_t l0 = bf16_bits(p0 - bf16_value(h0)), l1 = bf16_bits(p1 - bf16_value(h1));
-    hi[w] = h0 | (h1 << 16);
-    lo[w] = l0 | (l1 << 16);
+    hi[i] = h0 | (h1 << 16);
+    lo[i] = l0 | (l1 << 16);
   }
-  st.lsum = st.lsum * alpha + ps;
-  const u32x4 phi = {hi[0], hi[1], hi[2], hi[3]};
-  const u32x4 plo = {lo[0], lo[1], lo[2], lo[3]};
+  st.lsum = st.lsum * w.alpha + ps;
+  w.phi = u32x4{hi[0], hi[1], hi[2], hi[3]};
+  w.plo = u32x4{lo[0], lo[1], lo[2], lo[3]};
+  return w;
+}
 
+// P.V accumulation for one block.
+template <int D>
+__device__ __forceinline__ void accumulate_block(VHalf<D>& b, const BlockWeights& w, int nvalid, int grp,
+                                                 SoftmaxState<D>& st) {
   if (nvalid < 2 * kPage) {
     // Slots past the sequence end may hold anything (even NaN): zero them,
     // since a zero weight times NaN would still be NaN.
     u32x4 mask;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
-      mask[w] = (tok0 + 2 * w < nvalid ? 0x0000FFFFu : 0u) | (tok0 + 2 * w + 1 < nvalid ? 0xFFFF0000u : 0u);
+    for (int i = 0; i < 4; ++i)
+      mask[i] = (item_token(grp, 2 * i) < nvalid ? 0x0000FFFFu : 0u) |
+                (item_token(grp, 2 * i + 1) < nvalid ? 0xFFFF0000u : 0u);
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) b.v[jb] &= mask;
+    for (int jb = 0; jb < Shape<D>::JB; ++jb) b.v[jb] &= mask;
   }
 #pragma unroll
-  for (int jb = 0; jb < JB; ++jb) {
-    st.o[jb] *= alpha;
-    st.o[jb] = mfma_bf16(b.v[jb], phi, st.o[jb]);
-    st.o[jb] = mfma_bf16(b.v[jb], plo, st.o[jb]);
+  for (int jb = 0; jb < Shape<D>::JB; ++jb) {
+    st.o[jb] *= w.alpha;
+    st.o[jb] = mfma_bf16(b.v[jb], w.phi, st.o[jb]);
+    st.o[jb] = mfma_bf16(b.v[jb], w.plo, st.o[jb]);
   }
 }
 
+// One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
 template <int D>
-__global__ __launch_bounds__(64) void attn_chunk_kernel(AttnArgs a) {
-  constexpr int KB = KvBlock<D>::KB;
-  constexpr int JB = KvBlock<D>::JB;
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr item) {
+  constexpr int KB = Shape<D>::KB;
+  constexpr int JB = Shape<D>::JB;
   const int lane = threadIdx.x;
   const int col = lane & 15;   // MFMA column (query head in group) and A-operand row
   const int grp = lane >> 4;   // MFMA k-group
 
-  const int32_t* item = a.work + size_t(blockIdx.x) * kItemInts;
   const int seq = item[0];
   const int kvh = item[1];
   const int pb = item[2];
@@ -206,20 +273,22 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(AttnArgs a) {
   ChunkCtx<D> c;
   c.k_pool = a.k_pool;
   c.v_pool = a.v_pool;
-  c.bt = a.block_table + size_t(seq) * a.bt_stride;
+  c.bt = as_constant(a.block_table) + size_t(seq) * a.bt_stride;
   c.num_kv_heads = a.num_kv_heads;
   c.kvh = kvh;
   c.pe = pe;
-  // K operand: A-row r = col holds block token 8*(r/4) + r%4 (+4 for the
-  // second MFMA): page r/8 of the block, slot 8*((r/4)%2) + r%4.
-  c.k_page_sel = col >> 3;
-  c.k_off = k_elem(8 * ((col >> 2) & 1) + (col & 3), grp * 8, D);
-  // V operand: A-row = dim 16*jb + col, k-group grp = block tokens 8*grp .. +7.
-  c.v_page_sel = grp >> 1;
-  c.v_off = v_elem(8 * (grp & 1), col);
+  // K operand: A-row = token slot col, k-group grp = dims 8*grp .. +8 (+32*kb).
+  c.k_off = k_elem(col, 8 * grp, D);
+  // V operand: A-row = dim col (+16*jb), k-group grp = slots 4*grp .. +3.
+  c.v_off = v_elem(4 * grp, col);
 
-  KvBlock<D> blk[2];
-  if (pb < pe) load_block(c, pb, blk[0]);
+  KHalf<D> kb_[2];
+  VHalf<D> vb_[2];
+  if (pb < pe) {
+    const PagePair pp = block_pages(c, pb);
+    load_k(c, pp, kb_[0]);
+    load_v(c, pp, vb_[0]);
+  }
 
   // Q as the B operand of S^T = K Q^T: column = head, k = 8 dims per group.
   u32x4 qf[KB];
@@ -238,14 +307,23 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(AttnArgs a) {
   st.m = -__builtin_inff();
   st.lsum = 0.f;
 
-  // Two register blocks alternate: block i+1 is in flight while block i is used.
+  // Register halves alternate between even and odd blocks.
+  auto step = [&](int pg, KHalf<D>& kc, VHalf<D>& vc, KHalf<D>& kn, VHalf<D>& vn) {
+    const bool more = pg + 2 < pe;
+    PagePair nxt = {0, 0};
+    if (more) {
+      nxt = block_pages(c, pg + 2);
+      load_k(c, nxt, kn);
+    }
+    const int nvalid = min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage);
+    const BlockWeights w = score_block(kc, qf, nvalid, grp, a.scale_log2, st);
+    if (more) load_v(c, nxt, vn);
+    accumulate_block(vc, w, nvalid, grp, st);
+  };
   for (int pg = pb; pg < pe; pg += 4) {
-    if (pg + 2 < pe) load_block(c, pg + 2, blk[1]);
-    consume_block(blk[0], qf, min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage), grp, a.scale_log2, st);
+    step(pg, kb_[0], vb_[0], kb_[1], vb_[1]);
     if (pg + 2 >= pe) break;
-    if (pg + 4 < pe) load_block(c, pg + 4, blk[0]);
-    consume_block(blk[1], qf, min(len - (pg + 2) * kPage, pg + 3 < pe ? 2 * kPage : kPage), grp,
-                  a.scale_log2, st);
+    step(pg + 2, kb_[1], vb_[1], kb_[0], vb_[0]);
   }
 
   float lt = st.lsum + __shfl_xor(st.lsum, 16);
@@ -269,11 +347,22 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(AttnArgs a) {
   }
 }
 
+// One wave per worker: its segments are consecutive in the work list and
+// together cover the same number of KV pages as every other worker's.
+// Two waves per SIMD (at most 256 registers) keep 2048 workers resident.
+template <int D>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_kernel(AttnArgs a) {
+  const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
+  const int first = wt[0];
+  const int count = wt[1];
+  for (int i = 0; i < count; ++i) attend_segment<D>(a, as_constant(a.items) + size_t(first + i) * kItemInts);
+}
+
 // ---------------------------------------------------------------------------
 // log-sum-exp merge of the chunks of split (sequence, KV head) pairs
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
-  const int32_t* it = a.items + size_t(blockIdx.x) * kItemInts;
+  const_i32_ptr it = as_constant(a.items) + size_t(blockIdx.x) * kItemInts;
   const int seq = it[0];
   const int kvh = it[1];
   const int base = it[2];
@@ -326,12 +415,12 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
-  if (a.num_work == 0) return hipSuccess;
-  const dim3 grid(a.num_work), block(64);
+  if (a.num_workers == 0) return hipSuccess;
+  const dim3 grid(a.num_workers), block(64);
   if (a.head_dim == 128)
-    hipLaunchKernelGGL(attn_chunk_kernel<128>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(attn_worker_kernel<128>, grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(attn_chunk_kernel<64>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(attn_worker_kernel<64>, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

@@ -3,11 +3,12 @@
 // Rollout batches mix a few very long trajectories with many short ones
 // (Sec. 2.3 of the paper); the paper balances that skew across rollout
 // instances by routing and migration (Sec. 5.2). Inside one GPU the same job
-// falls to this planner: it cuts every (sequence, KV head) range of pages into
-// balanced page-aligned chunks no longer than a target derived from the
-// batch's total KV pages and the number of compute units, so that long
-// sequences are read by many workgroups at once. The exact rule is stated in
-// sf_decode_attn.h next to sf_decode_attn_plan.
+// falls to this planner: it lays every (sequence, KV head) page range end to
+// end and gives each resident attention wave (a worker) an equal slice of the
+// pages, cut at pair boundaries into segments. Long sequences are then read
+// by many waves at once and every wave finishes at about the same time,
+// whatever the skew. The exact rule is stated in sf_decode_attn.h next to
+// sf_decode_attn_plan.
 #include <algorithm>
 #include <cstring>
 #include <vector>
@@ -65,137 +66,159 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
 
   const int32_t B = desc->num_seqs;
   const int32_t hkv = desc->num_kv_heads;
-  int32_t num_cus = kDefaultNumCus, forced = 0, upc = kDefaultUnitsPerCu;
-  int32_t mn = kDefaultMinChunk, mx = kDefaultMaxChunk;
+  int32_t num_cus = kDefaultNumCus, forced = 0, wpc = kDefaultWorkersPerCu, mn = kDefaultMinChunk;
   if (opts) {
-    if (opts->num_cus < 0 || opts->chunk_pages < 0 || opts->units_per_cu < 0 ||
-        opts->min_chunk_pages < 0 || opts->max_chunk_pages < 0) return SF_ERR_INVALID_ARG;
+    if (opts->num_cus < 0 || opts->chunk_pages < 0 || opts->workers_per_cu < 0 ||
+        opts->min_chunk_pages < 0 || opts->reserved != 0) return SF_ERR_INVALID_ARG;
     if (opts->num_cus) num_cus = opts->num_cus;
     forced = opts->chunk_pages;
-    if (opts->units_per_cu) upc = opts->units_per_cu;
+    if (opts->workers_per_cu) wpc = opts->workers_per_cu;
     if (opts->min_chunk_pages) mn = opts->min_chunk_pages;
-    if (opts->max_chunk_pages) mx = opts->max_chunk_pages;
   }
-  if (mn > mx) return SF_ERR_INVALID_ARG;
 
-  int64_t total = 0, max_pages = 0;
+  int64_t total = 0;
   for (int32_t s = 0; s < B; ++s) {
     const int32_t L = seq_lens_host[s];
     if (L < 0 || (L > 0 && desc->num_pages == 0)) return SF_ERR_INVALID_ARG;
     const int64_t npg = (int64_t(L) + kPage - 1) / kPage;
     if (npg > desc->block_table_stride) return SF_ERR_INVALID_ARG;
     total += npg * hkv;
-    max_pages = std::max(max_pages, npg);
   }
-  int64_t chunk;
-  if (forced > 0) {
-    chunk = forced;
+  if (total > (int64_t(1) << 40)) return SF_ERR_INVALID_ARG;
+  const int64_t num_pairs = int64_t(B) * hkv;
+  int64_t workers;
+  if (num_pairs == 0) {
+    workers = 0;
+  } else if (total == 0) {
+    workers = 1;  // only empty pairs: one worker writes their zero rows
+  } else if (forced > 0) {
+    workers = (total + forced - 1) / forced;
   } else {
-    const int64_t units = int64_t(upc) * num_cus;
-    chunk = (total + units - 1) / units;
-    chunk = std::min<int64_t>(std::max<int64_t>(chunk, mn), mx);
+    workers = std::min<int64_t>(int64_t(wpc) * num_cus, (total + mn - 1) / mn);
   }
-  auto pages_of = [&](int32_t s) { return (int64_t(seq_lens_host[s]) + kPage - 1) / kPage; };
-  auto chunks_of = [&](int64_t npg) { return npg ? (npg + chunk - 1) / chunk : int64_t(1); };
+  if (workers > INT32_MAX / 2) return SF_ERR_INVALID_ARG;
+  auto pages_of = [&](int64_t pair) { return (int64_t(seq_lens_host[pair / hkv]) + kPage - 1) / kPage; };
+  auto lo_of = [&](int64_t w) { return w * total / workers; };
 
-  // Sizes first: items, combine rows, partial slots.
-  int64_t n_work = 0, n_comb = 0, n_part = 0;
-  for (int32_t s = 0; s < B; ++s) {
-    const int64_t n = chunks_of(pages_of(s));
-    n_work += n * hkv;
-    if (n > 1) {
-      n_comb += hkv;
-      n_part += n * hkv;
+  // Pass 1: segments per pair. Worker ranges are cut at pair boundaries; a
+  // pair spanning k worker boundaries has k + 1 segments.
+  thread_local std::vector<int32_t> nseg_buf;
+  nseg_buf.assign(size_t(num_pairs), 0);
+  int32_t* nseg = nseg_buf.data();
+  int64_t n_work = 0;
+  {
+    int64_t start = 0;  // global page where the current pair starts
+    for (int64_t p = 0; p < num_pairs; ++p) {
+      const int64_t npg = pages_of(p);
+      if (npg == 0) {
+        nseg[p] = 1;
+        continue;
+      }
+      // workers whose range intersects [start, start + npg)
+      const int64_t w_first = (start * workers) / total;          // lo_of(w) <= start
+      int64_t wf = w_first;
+      while (wf + 1 < workers && lo_of(wf + 1) <= start) ++wf;
+      while (lo_of(wf) > start) --wf;
+      int64_t wl = wf;
+      while (wl + 1 < workers && lo_of(wl + 1) < start + npg) ++wl;
+      nseg[p] = int32_t(wl - wf + 1);
+      start += npg;
     }
   }
-  if (n_work + n_comb > INT32_MAX / kItemInts || n_part > INT32_MAX) return SF_ERR_INVALID_ARG;
+  int64_t n_comb = 0, n_part = 0;
+  for (int64_t p = 0; p < num_pairs; ++p) {
+    n_work += nseg[p];
+    if (nseg[p] > 1) {
+      ++n_comb;
+      n_part += nseg[p];
+    }
+  }
+  const int64_t table_rows = (workers + 3) / 4;
+  if (table_rows + n_work + n_comb > INT32_MAX / kItemInts || n_part > INT32_MAX) return SF_ERR_INVALID_ARG;
   const int32_t g = desc->num_q_heads / hkv;
+  info->num_workers = int32_t(workers);
   info->num_work = int32_t(n_work);
   info->num_combine = int32_t(n_comb);
   info->num_partials = int32_t(n_part);
-  info->chunk_pages = int32_t(std::min<int64_t>(chunk, INT32_MAX));
-  info->work_bytes = uint64_t(n_work + n_comb) * kItemInts * 4;
+  info->chunk_pages = workers && total ? int32_t((total + workers - 1) / workers) : 0;
+  info->reserved = 0;
+  info->work_bytes = uint64_t(table_rows + n_work + n_comb) * kItemInts * 4;
   info->workspace_bytes =
       n_part ? align256(uint64_t(n_part) * g * desc->head_dim * 4) + align256(uint64_t(n_part) * g * 4) : 0;
   info->desc_key = desc_key(desc);
   if (!work_host) return SF_OK;
   if (work_capacity_bytes < info->work_bytes) return SF_ERR_CAPACITY;
 
-  // Items are generated in (s, kvh, c) order and placed by a stable counting
-  // sort on page count, largest first. Chunk c of a pair spans
-  // floor((c+1)*npg/n) - floor(c*npg/n) <= chunk pages.
-  const int64_t max_size = std::min<int64_t>(chunk, max_pages);
-  // Scratch reused across calls on this thread; raw pointers keep the loops
-  // free of per-access thread-local lookups.
-  thread_local std::vector<int64_t> pos_buf;
-  thread_local std::vector<int32_t> bounds_buf;
-  pos_buf.assign(size_t(max_size) + 2, 0);
-  int64_t* pos = pos_buf.data();
-  // Chunk sizes of a pair are q = floor(npg/n) or q + 1; the bounds
-  // floor(c*npg/n) follow by stepping a remainder (one division per sequence).
-  int32_t* bounds = nullptr;
-  auto fill_bounds = [&](int64_t npg, int64_t n) {
-    if (bounds_buf.size() < size_t(n) + 1) bounds_buf.resize(size_t(n) + 1);
-    bounds = bounds_buf.data();
-    const int64_t q = npg / n, r = npg % n;
-    int64_t e = 0, rem = 0;
-    bounds[0] = 0;
-    for (int64_t c = 1; c <= n; ++c) {
-      e += q;
-      rem += r;
-      if (rem >= n) {
-        rem -= n;
-        ++e;
-      }
-      bounds[c] = int32_t(e);
-    }
-  };
-  for (int32_t s = 0; s < B; ++s) {
-    const int64_t npg = pages_of(s);
-    const int64_t n = chunks_of(npg);
-    if (n == 1) {
-      pos[npg] += hkv;
-      continue;
-    }
-    const int64_t q = npg / n, r = npg % n;  // r chunks of q + 1 pages, n - r of q
-    pos[q + 1] += r * hkv;
-    pos[q] += (n - r) * hkv;
-  }
-  int64_t start = 0;  // descending sizes: the largest size starts at row 0
-  for (int64_t sz = max_size; sz >= 0; --sz) {
-    const int64_t cnt = pos[sz];
-    pos[sz] = start;
-    start += cnt;
-  }
-  int32_t* comb = work_host + n_work * kItemInts;
-  int32_t slot = 0, comb_idx = 0;
-  for (int32_t s = 0; s < B; ++s) {
-    const int64_t npg = pages_of(s);
-    const int64_t n = chunks_of(npg);
-    const int32_t L = seq_lens_host[s];
-    fill_bounds(npg, n);
-    for (int32_t kvh = 0; kvh < hkv; ++kvh) {
-      for (int64_t c = 0; c < n; ++c) {
-        const int32_t b = bounds[c];
-        const int32_t e = bounds[c + 1];
-        int32_t* row = work_host + pos[e - b]++ * kItemInts;
-        row[0] = s;
-        row[1] = kvh;
-        row[2] = b;
-        row[3] = e;
-        row[4] = L;
-        row[5] = n > 1 ? slot + int32_t(c) : -1;
-        row[6] = n > 1 ? comb_idx : -1;
-        row[7] = int32_t(n);
-      }
-      if (n > 1) {
-        const int32_t c8[kItemInts] = {s, kvh, slot, int32_t(n), 0, 0, 0, 0};
-        std::memcpy(comb, c8, sizeof c8);
-        comb += kItemInts;
-        slot += int32_t(n);
-        ++comb_idx;
-      }
+  // Pass 2: partial slots and combine rows (pairs with several segments, in pair order).
+  int32_t* table = work_host;
+  int32_t* items = work_host + table_rows * kItemInts;
+  int32_t* comb = items + n_work * kItemInts;
+  std::memset(table, 0, size_t(table_rows) * kItemInts * 4);
+  thread_local std::vector<int32_t> base_buf, cidx_buf;
+  base_buf.assign(size_t(num_pairs), -1);
+  cidx_buf.assign(size_t(num_pairs), -1);
+  {
+    int32_t slot = 0, ci = 0;
+    for (int64_t p = 0; p < num_pairs; ++p) {
+      if (nseg[p] <= 1) continue;
+      base_buf[size_t(p)] = slot;
+      cidx_buf[size_t(p)] = ci;
+      const int32_t c8[kItemInts] = {int32_t(p / hkv), int32_t(p % hkv), slot, nseg[p], 0, 0, 0, 0};
+      std::memcpy(comb + int64_t(ci) * kItemInts, c8, sizeof c8);
+      slot += nseg[p];
+      ++ci;
     }
   }
-  return SF_OK;
+  const int32_t* base = base_buf.data();
+  const int32_t* cidx = cidx_buf.data();
+
+  // Pass 3: items, worker by worker; a worker's segments in pair order, then
+  // the empty pairs e with e mod workers == w.
+  thread_local std::vector<int64_t> empty_buf;
+  empty_buf.clear();
+  for (int64_t p = 0; p < num_pairs; ++p)
+    if (pages_of(p) == 0) empty_buf.push_back(p);
+  int64_t row = 0, p = 0, pstart = 0;
+  int32_t seg_c = 0;  // segment index within the current pair
+  while (p < num_pairs && pages_of(p) == 0) ++p;
+  for (int64_t w = 0; w < workers; ++w) {
+    const int64_t lo = lo_of(w), hi = lo_of(w + 1);
+    table[2 * w] = int32_t(row);
+    int64_t cnt = 0;
+    while (p < num_pairs && pstart < hi) {
+      const int64_t npg = pages_of(p);
+      const int64_t b = std::max(lo, pstart) - pstart, e = std::min(hi, pstart + npg) - pstart;
+      int32_t* r = items + row * kItemInts;
+      const int32_t L = seq_lens_host[p / hkv];
+      r[0] = int32_t(p / hkv);
+      r[1] = int32_t(p % hkv);
+      r[2] = int32_t(b);
+      r[3] = int32_t(e);
+      r[4] = L;
+      r[5] = nseg[p] > 1 ? base[p] + seg_c : -1;
+      r[6] = cidx[p];
+      r[7] = nseg[p];
+      ++row;
+      ++cnt;
+      if (pstart + npg <= hi) {  // pair finished inside this worker
+        pstart += npg;
+        seg_c = 0;
+        ++p;
+        while (p < num_pairs && pages_of(p) == 0) ++p;
+      } else {
+        ++seg_c;
+        break;
+      }
+    }
+    for (size_t e = size_t(w); e < empty_buf.size(); e += size_t(workers)) {
+      const int64_t q = empty_buf[e];
+      int32_t* r = items + row * kItemInts;
+      const int32_t r8[kItemInts] = {int32_t(q / hkv), int32_t(q % hkv), 0, 0, 0, -1, -1, 1};
+      std::memcpy(r, r8, sizeof r8);
+      ++row;
+      ++cnt;
+    }
+    table[2 * w + 1] = int32_t(cnt);
+  }
+  return row == n_work ? SF_OK : SF_ERR_INVALID_ARG;
 }

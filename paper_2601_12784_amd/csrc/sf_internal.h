@@ -16,11 +16,11 @@ constexpr int kMaxGroup = 16;   // query heads per KV head handled by one MFMA c
 
 // Defaults of the length-aware chunk rule (see sf_decode_attn_plan).
 constexpr int kDefaultNumCus = 256;
-constexpr int kDefaultUnitsPerCu = 8;
-constexpr int kDefaultMinChunk = 16;
-constexpr int kDefaultMaxChunk = 4096;
+constexpr int kDefaultWorkersPerCu = 4;  // attention waves per CU (one per SIMD)
+constexpr int kDefaultMinChunk = 8;      // pages: fewer workers rather than thinner slices
 
 sf_status validate_desc(const sf_attn_desc* d);
+inline int64_t table_rows(int64_t workers) { return (workers + 3) / 4; }
 uint64_t desc_key(const sf_attn_desc* d);
 uint64_t align256(uint64_t x);
 
@@ -32,8 +32,9 @@ struct Workspace {
 Workspace carve_workspace(void* base, int32_t slots, int32_t g, int32_t d);
 
 struct AttnArgs {
-  const int32_t* work;
-  int32_t num_work;
+  const int32_t* worker_table;  // (first item, item count) per worker
+  const int32_t* items;         // segment rows
+  int32_t num_workers;
   const uint16_t* q;
   const uint16_t* k_pool;
   const uint16_t* v_pool;

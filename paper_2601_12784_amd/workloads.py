@@ -12,8 +12,8 @@ None of the paper's datasets or weights are used: every value is drawn here.
 
 Layouts (all row-major, bf16 stored as torch.bfloat16 on the CPU):
   q        [B, Hq, D]
-  k_pool   [N_pages, Hkv, P, D]   token-major inside a page tile
-  v_pool   [N_pages, Hkv, D, P]   dim-major inside a page tile
+  k_pool   [N_pages, Hkv, D/8, P, 8]   key of slot t, dim d at [.., d/8, t, d%8]
+  v_pool   [N_pages, Hkv, D, P]        value of slot t, dim d at [.., d, t]
   block_table int32 [B, stride]   physical page of logical page j, -1 = unused
   seq_lens int32 [B]              cached tokens per sequence (incl. the current one)
 
@@ -137,7 +137,7 @@ class Batch:
     seq_lens: np.ndarray          # int32 [B]
     block_table: np.ndarray       # int32 [B, stride]
     q: torch.Tensor               # bf16 [B, Hq, D]
-    k_pool: torch.Tensor          # bf16 [N, Hkv, P, D]
+    k_pool: torch.Tensor          # bf16 [N, Hkv, D/8, P, 8]
     v_pool: torch.Tensor          # bf16 [N, Hkv, D, P]
     scale: float
     alloc_lens: np.ndarray = field(default=None)  # int64 [B] tokens backed by pages
@@ -189,7 +189,7 @@ def build_batch(lens, num_q_heads, num_kv_heads, head_dim, seed, *, name="custom
     hq, hkv, d = num_q_heads, num_kv_heads, head_dim
     qshape = (b, hq, d) if num_queries == 1 else (num_queries, b, hq, d)
     q = _fill_normal(ss_q, int(np.prod(qshape)), 1.0).view(*qshape)
-    k_pool = _fill_normal(ss_k, n_pool * hkv * PAGE * d, k_mult).view(n_pool, hkv, PAGE, d)
+    k_pool = _fill_normal(ss_k, n_pool * hkv * PAGE * d, k_mult).view(n_pool, hkv, d // 8, PAGE, 8)
     v_pool = _fill_normal(ss_v, n_pool * hkv * d * PAGE, 1.0).view(n_pool, hkv, d, PAGE)
 
     if poison:
@@ -203,7 +203,7 @@ def build_batch(lens, num_q_heads, num_kv_heads, head_dim, seed, *, name="custom
             tail = int(alloc[i] % PAGE)
             if pages[i] and tail:
                 last = bt[i, pages[i] - 1]
-                kb[last, :, tail:, :] = NAN_BF16
+                kb[last, :, :, tail:, :] = NAN_BF16
                 vb[last, :, :, tail:] = NAN_BF16
 
     return Batch(name=name, seed=seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,

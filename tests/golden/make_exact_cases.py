@@ -31,7 +31,7 @@ def grid_bits(vals):
 def case(name, lens, hq, hkv, d, n_pages, bt, scale, seed, q_mult=1.0):
     rng = np.random.default_rng(seed)
     q = grid_bits(rng.integers(-32, 33, size=(len(lens), hq, d)) / 16.0 * q_mult)
-    k = grid_bits(rng.integers(-32, 33, size=(n_pages, hkv, PAGE, d)) / 16.0)
+    k = grid_bits(rng.integers(-32, 33, size=(n_pages, hkv, d // 8, PAGE, 8)) / 16.0)
     v = grid_bits(rng.integers(-32, 33, size=(n_pages, hkv, d, PAGE)) / 16.0)
     bt = np.array(bt, dtype=np.int32)
     out, lse, dec = exact_ref.decode_attn(q, k, v, bt, np.array(lens), scale)
@@ -54,7 +54,7 @@ def main():
     doc = {
         "about": "Decode attention (App. B.1 decode step: one query per sequence over its "
                  "paged cache) evaluated at 60 significant digits by oracle/exact_ref.py. "
-                 "Layouts: q [B][Hq][D], k_pool [N][Hkv][16][D], v_pool [N][Hkv][D][16], "
+                 "Layouts: q [B][Hq][D], k_pool [N][Hkv][D/8][16][8], v_pool [N][Hkv][D][16], "
                  "bf16 bit patterns; out/lse keyed by 'seq,head'.",
         "generator": "tests/golden/make_exact_cases.py",
         "cases": cases,

@@ -35,34 +35,40 @@ def test_version_and_status_strings(lib):
 def test_struct_sizes_match_header():
     assert ctypes.sizeof(B.sf_attn_desc) == 32
     assert ctypes.sizeof(B.sf_plan_opts) == 20
-    assert ctypes.sizeof(B.sf_plan_info) == 40
+    assert ctypes.sizeof(B.sf_plan_info) == 48
 
 
 # ---------------------------------------------------------------------------
 # planner parity
 # ---------------------------------------------------------------------------
-def _plan_both(lens, hq, hkv, d, num_cus=256, chunk=0, upc=0, mn=0, mx=0, stride=None):
+def _plan_both(lens, hq, hkv, d, num_cus=256, chunk=0, wpc=0, mn=0, stride=None):
     lens = np.asarray(lens, dtype=np.int32)
     if stride is None:
         stride = max(1, int(((lens.astype(np.int64) + PAGE - 1) // PAGE).max(initial=1)))
     desc = B.make_desc(lens.size, hq, hkv, d, stride, 1, 0.1)
-    opts = B.make_opts(num_cus=num_cus, chunk_pages=chunk, units_per_cu=upc,
-                       min_chunk_pages=mn, max_chunk_pages=mx)
+    opts = B.make_opts(num_cus=num_cus, chunk_pages=chunk, workers_per_cu=wpc, min_chunk_pages=mn)
     info, work = B.sf_decode_attn_plan(desc, lens, opts)
-    ref = plan_ref.plan(lens, hkv, hq, d, num_cus, chunk, upc or None, mn or None, mx or None)
+    ref = plan_ref.plan(lens, hkv, hq, d, num_cus, chunk, wpc or None, mn or None)
     return info, work[: info.work_bytes // 4].reshape(-1, 8), ref
 
 
+def _split(info, work):
+    t = (info.num_workers + 3) // 4
+    return work[:t], work[t:t + info.num_work], work[t + info.num_work:]
+
+
 def _assert_same(info, work, ref):
+    assert info.num_workers == ref["num_workers"]
     assert info.chunk_pages == ref["chunk_pages"]
     assert info.num_work == ref["items"].shape[0]
     assert info.num_combine == ref["combine"].shape[0]
     assert info.num_partials == ref["num_partials"]
     assert info.workspace_bytes == ref["workspace_bytes"]
     assert info.work_bytes == ref["work_bytes"]
-    w = info.num_work
-    assert np.array_equal(work[:w], ref["items"])
-    assert np.array_equal(work[w:], ref["combine"])
+    table, items, comb = _split(info, work)
+    assert np.array_equal(table, ref["table"])
+    assert np.array_equal(items, ref["items"])
+    assert np.array_equal(comb, ref["combine"])
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -86,64 +92,81 @@ def test_plan_matches_rederivation_forced_chunk(chunk):
 
 def test_plan_matches_rederivation_knobs():
     lens = np.arange(0, 5000, 37)
-    info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=32, upc=3, mn=5, mx=40)
+    info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=32, wpc=3, mn=5)
     _assert_same(info, work, ref)
-    assert info.chunk_pages == 40
+    assert info.num_workers == 96
+
+
+def test_plan_all_empty_and_no_sequences():
+    info, work, ref = _plan_both([0, 0, 0], 8, 2, 128)
+    _assert_same(info, work, ref)
+    assert info.num_workers == 1 and info.num_work == 6 and info.num_combine == 0
+    desc = B.make_desc(0, 8, 2, 128, 1, 1, 0.1)
+    info0, _ = B.sf_decode_attn_plan(desc, np.zeros(0, np.int32))
+    assert info0.num_workers == 0 and info0.num_work == 0
 
 
 def test_tiny_plan_by_hand():
-    """L = {17, 64, 130, 300}: pages {2, 4, 9, 19}, T = 34 page-heads -> chunk 16
-    (clamped up); only the 19-page sequence splits, into pages [0,9) and [9,19).
-    The two 9-page items tie and go in sequence order."""
+    """L = {17, 64, 130, 300}, one KV head: pages {2, 4, 9, 19} laid end to end
+    give T = 34 global pages. W = min(8 * 256, ceil(34 / 8)) = 5 workers own
+    [0,6) [6,13) [13,20) [20,27) [27,34); pair 2 ([6,15)) is cut once and
+    pair 3 ([15,34)) twice."""
     info, work, _ = _plan_both([17, 64, 130, 300], 4, 1, 64)
-    assert info.chunk_pages == 16 and info.num_work == 5 and info.num_combine == 1
-    assert info.num_partials == 2
-    expect = [[3, 0, 9, 19, 300, 1, 0, 2],
-              [2, 0, 0, 9, 130, -1, -1, 1],
-              [3, 0, 0, 9, 300, 0, 0, 2],
+    assert (info.num_workers, info.num_work, info.num_combine, info.num_partials, info.chunk_pages) == \
+        (5, 7, 2, 5, 7)
+    table, items, comb = _split(info, work)
+    assert np.array_equal(table, np.array([[0, 2, 2, 1, 3, 2, 5, 1], [6, 1, 0, 0, 0, 0, 0, 0]], np.int32))
+    expect = [[0, 0, 0, 2, 17, -1, -1, 1],
               [1, 0, 0, 4, 64, -1, -1, 1],
-              [0, 0, 0, 2, 17, -1, -1, 1],
-              [3, 0, 0, 2, 0, 0, 0, 0]]
-    assert np.array_equal(work, np.array(expect, dtype=np.int32))
-    assert info.workspace_bytes == 2 * 4 * 64 * 4 + 256
+              [2, 0, 0, 7, 130, 0, 0, 2],
+              [2, 0, 7, 9, 130, 1, 0, 2],
+              [3, 0, 0, 5, 300, 2, 1, 3],
+              [3, 0, 5, 12, 300, 3, 1, 3],
+              [3, 0, 12, 19, 300, 4, 1, 3]]
+    assert np.array_equal(items, np.array(expect, np.int32))
+    assert np.array_equal(comb, np.array([[2, 0, 0, 2, 0, 0, 0, 0], [3, 0, 2, 3, 0, 0, 0, 0]], np.int32))
+    assert info.workspace_bytes == 5 * 4 * 64 * 4 + 256
 
 
 @pytest.mark.parametrize("seed", range(4))
 def test_plan_invariants(seed):
-    """Chunks tile [0, pages) exactly; none exceeds the chunk size; slots are
-    a permutation of [0, num_partials); order is by size, largest first."""
+    """Every worker owns floor or ceil of T / W pages; each pair's segments tile
+    [0, pages) in worker order; slots of cut pairs are consecutive; every
+    pair appears; empty pairs have one empty item."""
     rng = np.random.default_rng(100 + seed)
     lens = rng.integers(0, 20000, size=int(rng.integers(1, 200)))
+    lens[rng.random(lens.size) < 0.1] = 0
     hkv = 4
     info, work, _ = _plan_both(lens, 28, hkv, 128, num_cus=int(rng.integers(1, 300)))
-    items = work[: info.num_work]
-    comb = work[info.num_work:]
-    sizes = items[:, 3] - items[:, 2]
-    assert np.all(np.diff(sizes) <= 0)
-    assert np.all(sizes <= info.chunk_pages)
-    slots = items[items[:, 5] >= 0, 5]
-    assert np.array_equal(np.sort(slots), np.arange(info.num_partials))
+    table, items, comb = _split(info, work)
+    tab = table.reshape(-1)[: 2 * info.num_workers].reshape(-1, 2)
+    pages = (lens.astype(np.int64) + PAGE - 1) // PAGE
+    total = int(pages.sum()) * hkv
+    W = info.num_workers
+    assert np.array_equal(tab[:, 0], np.concatenate([[0], np.cumsum(tab[:, 1])[:-1]]))
+    assert tab[:, 1].sum() == info.num_work
+    for w in range(W):
+        seg = items[tab[w, 0]: tab[w, 0] + tab[w, 1]]
+        assert (seg[:, 3] - seg[:, 2]).sum() in (total // W, -(-total // W))
     for s, L in enumerate(lens):
-        npg = (int(L) + PAGE - 1) // PAGE
+        npg = int(pages[s])
         for kvh in range(hkv):
-            mine = items[(items[:, 0] == s) & (items[:, 1] == kvh)]
-            assert np.all(mine[:, 4] == L)
-            mine = mine[np.argsort(mine[:, 2])]
+            mine = items[(items[:, 0] == s) & (items[:, 1] == kvh)]  # in worker order
             n = mine.shape[0]
-            assert np.all(mine[:, 7] == n)
+            assert n >= 1 and np.all(mine[:, 7] == n) and np.all(mine[:, 4] == (L if npg else 0))
             if npg == 0:
-                assert n == 1 and mine[0, 2] == mine[0, 3] == 0 and mine[0, 5] == mine[0, 6] == -1
+                assert n == 1 and mine[0, 2] == mine[0, 3] == 0 and mine[0, 5] == -1
                 continue
             assert mine[0, 2] == 0 and mine[-1, 3] == npg
             assert np.all(mine[1:, 2] == mine[:-1, 3]) and np.all(mine[:, 3] > mine[:, 2])
             if n > 1:
-                ci = mine[0, 6]
-                assert np.all(mine[:, 6] == ci)
-                row = comb[ci]
+                row = comb[mine[0, 6]]
                 assert row[0] == s and row[1] == kvh and row[3] == n
                 assert np.array_equal(mine[:, 5], row[2] + np.arange(n))
             else:
                 assert mine[0, 5] == -1 and mine[0, 6] == -1
+    slots = items[items[:, 5] >= 0, 5]
+    assert np.array_equal(np.sort(slots), np.arange(info.num_partials))
 
 
 def test_plan_size_query_and_capacity(lib):
@@ -232,9 +255,9 @@ def test_combine_rejects_bad_arguments(lib):
     assert c(ctypes.byref(desc), ctypes.byref(info), FAKE, FAKE, 0, FAKE, None, None) == 3
     assert c(ctypes.byref(desc), ctypes.byref(info), None, FAKE, 1 << 30, FAKE, None, None) == 1
     assert c(ctypes.byref(desc), ctypes.byref(info), FAKE, FAKE, 1 << 30, FAKE + 4, None, None) == 1
-    # a plan without split pairs makes the combine call a no-op
+    # a plan without cut pairs makes the combine call a no-op
     lens1 = np.array((40, 200), np.int32)
-    one, _ = B.sf_decode_attn_plan(desc, lens1, B.make_opts(num_cus=4))
+    one, _ = B.sf_decode_attn_plan(desc, lens1, B.make_opts(num_cus=4, chunk_pages=1 << 20))
     assert one.num_combine == 0
     assert c(ctypes.byref(desc), ctypes.byref(one), None, None, 0, None, None, None) == 0
 

@@ -183,9 +183,9 @@ def test_dominant_key_returns_its_v_row_bitwise():
     q = np.zeros(d, np.float32)
     q[0] = 64.0
     bf16_bits(b.q)[0, :] = (q.view(np.uint32) >> 16).astype(np.uint16)
-    kb = bf16_bits(b.k_pool)
+    kb = bf16_bits(b.k_pool)  # [N, Hkv, D/8, 16, 8]: dim 0 of slot t at [.., 0, t, 0]
     for t in range(length):
-        kb[b.block_table[0, t // PAGE], 0, t % PAGE, 0] = 0x4280 if t == hot else 0  # 64.0 / 0.0
+        kb[b.block_table[0, t // PAGE], 0, 0, t % PAGE, 0] = 0x4280 if t == hot else 0  # 64.0 / 0.0
     out, _, _ = run_gpu(b)
     pg = b.block_table[0, hot // PAGE]
     v = (bf16_bits(b.v_pool)[pg, 0, :, hot % PAGE].astype(np.uint32) << 16).view(np.float32)

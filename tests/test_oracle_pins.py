@@ -32,9 +32,15 @@ def _widen(bits):
     return dense_ref.widen(bits)
 
 
+def _k_row(batch, s, kvh, t):
+    """uint16 key row of token t (the K tile stores 8-dim pieces per slot)."""
+    pg = batch.block_table[s, t // PAGE]
+    return bf16_bits(batch.k_pool)[pg, kvh, :, t % PAGE, :].reshape(-1)
+
+
 def _set_k_row(batch, s, kvh, t, row_bits):
     pg = batch.block_table[s, t // PAGE]
-    bf16_bits(batch.k_pool)[pg, kvh, t % PAGE, :] = row_bits
+    bf16_bits(batch.k_pool)[pg, kvh, :, t % PAGE, :] = np.asarray(row_bits).reshape(-1, 8)
 
 
 def _set_v_row(batch, s, kvh, t, row_bits):
@@ -88,7 +94,7 @@ def test_length_one_returns_v_row_exactly():
             assert np.array_equal(out[s, h], v)
             # lse of one token is its own score
             qv = _widen(bf16_bits(b.q)[s, h])
-            kv = _widen(bf16_bits(b.k_pool)[pg, h // g, 0, :])
+            kv = _widen(_k_row(b, s, h // g, 0))
             assert lse[s, h] == pytest.approx(b.scale * float(qv @ kv), rel=1e-14, abs=1e-15)
 
 
@@ -147,7 +153,7 @@ def test_dominant_key_returns_its_value_row():
     q[0] = 64.0
     bf16_bits(b.q)[0, 0] = f32_to_bf16_exact(q)
     for t in range(length):
-        row = _widen(bf16_bits(b.k_pool)[b.block_table[0, t // PAGE], 0, t % PAGE]).astype(np.float32)
+        row = _widen(_k_row(b, 0, 0, t)).astype(np.float32)
         row[0] = 64.0 if t == hot else 0.0
         _set_k_row(b, 0, 0, t, f32_to_bf16_exact(row))
     out, lse = _run(b, scale=1.0)
@@ -301,7 +307,9 @@ def test_gather_matches_layout_definition():
             kd, vd = oracle.gather(bf16_bits(b.k_pool), bf16_bits(b.v_pool), b.block_table, s, kvh, L)
             for t in range(L):
                 pg = b.block_table[s, t // PAGE]
-                assert np.array_equal(kd[t], bf16_bits(b.k_pool)[pg, kvh, t % PAGE, :])
+                # key dim d of slot t sits at [d // 8, t, d % 8] of its tile
+                kt = bf16_bits(b.k_pool)[pg, kvh]
+                assert all(kd[t, d] == kt[d // 8, t % PAGE, d % 8] for d in range(32))
                 assert np.array_equal(vd[t], bf16_bits(b.v_pool)[pg, kvh, :, t % PAGE])
 
 
