@@ -123,7 +123,7 @@ def stored_traffic(kv_bytes_per_launch):
     return doc.get("traffic_bytes_per_launch")
 
 
-ATTN_KERNEL = "attn_chunk_kernel<128>"
+ATTN_KERNEL = "attn_worker_kernel<128>"
 COMBINE_KERNEL = "combine_kernel"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
@@ -183,6 +183,30 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
             pass
     with open(out_path, "w") as f:
         json.dump(doc, f, indent=1)
+    md = out_path[:-len(".json")] + ".md"
+    cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
+           "-d $REPO/gpurun_out/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
+           "--no-skew --copy-probe " + str(int(copy_mib)))
+    lines = [f"# HBM traffic of {ATTN_KERNEL} on the long-tail batch (rocprofv3 counters)", "",
+             "Two counter passes (one counter each), then the summary:", "", "```",
+             cmd.format(c="FETCH_SIZE", d="pmc_fetch", o="f"), cmd.format(c="WRITE_SIZE", d="pmc_write", o="w"),
+             "python bench.py --summarize-counters gpurun_out/pmc_fetch/f_counter_collection.csv "
+             f"gpurun_out/pmc_write/w_counter_collection.csv --copy-probe {int(copy_mib)}", "```", "",
+             f"Kernel source sha256[:16]: `{doc['kernel_source_sha256_16']}`", "",
+             "Calibration: a plain device copy (`__amd_rocclr_copyBuffer`) of "
+             f"{int(copy_mib)} MiB reads FETCH_SIZE = {doc['raw_counter_bytes_per_launch']['copy_FETCH_SIZE']} B "
+             f"and WRITE_SIZE = {doc['raw_counter_bytes_per_launch']['copy_WRITE_SIZE']} B, so the counters are "
+             f"scaled by {doc['fetch_scale']} (reads) and {doc['write_scale']} (writes).", "",
+             "| per attention launch | bytes |", "|---|---|",
+             f"| FETCH_SIZE x scale | {doc['fetch_bytes_per_launch']} |",
+             f"| WRITE_SIZE x scale | {doc['write_bytes_per_launch']} |",
+             f"| traffic | {doc['traffic_bytes_per_launch']} |",
+             f"| algorithmic K+V bytes | {doc['algorithmic_kv_bytes_per_launch']} |",
+             f"| traffic / algorithmic | {doc['traffic_over_algorithmic']} |"]
+    if COMBINE_KERNEL + "_traffic_bytes_per_launch" in doc:
+        lines.append(f"| combine kernel traffic | {doc[COMBINE_KERNEL + '_traffic_bytes_per_launch']} |")
+    with open(md, "w") as f:
+        f.write("\n".join(lines) + "\n")
     return doc
 
 
@@ -225,8 +249,9 @@ def main():
     ap.add_argument("--bench-json", default=None, help="bench.py output of the traced run")
     args = ap.parse_args()
     if args.summarize_counters:
-        from paper_2601_12784_amd.workloads import make_batch
-        kv = make_batch("longtail").kv_bytes()
+        from paper_2601_12784_amd.workloads import config_seed, sample_lengths
+        lens = sample_lengths("longtail", np.random.Generator(np.random.PCG64(config_seed("longtail"))))
+        kv = int(lens.sum()) * 4 * 128 * 2 * 2  # 4 KV heads, head_dim 128, K and V, bf16
         print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_probe or 1024, kv), indent=1))
         return
     if args.summarize_trace:
