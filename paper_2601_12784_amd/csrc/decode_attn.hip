@@ -375,16 +375,21 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
     const float* lse_h = a.part_lse + size_t(base) * g + h;           // stride g per chunk
     const float* o_h = a.part_o + (size_t(base) * g + h) * a.head_dim + 4 * d4;
     const size_t o_stride = size_t(g) * a.head_dim;
+    // One pass in chunk order with a running maximum (log2 units): the
+    // loads of several chunks are independent and issue together.
     float mx = -__builtin_inff();
-#pragma unroll 8
-    for (int c = 0; c < n; ++c) mx = fmaxf(mx, lse_h[size_t(c) * g]);
     float wsum = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
+#pragma unroll 4
     for (int c = 0; c < n; ++c) {
-      const float w = fast_exp2(lse_h[size_t(c) * g] - mx);
-      wsum += w;
-      acc += w * *reinterpret_cast<const f32x4*>(o_h + c * o_stride);
+      const float l = lse_h[size_t(c) * g];
+      const f32x4 o = *reinterpret_cast<const f32x4*>(o_h + c * o_stride);
+      const float mnew = fmaxf(mx, l);
+      const float keep = fast_exp2(mx - mnew);
+      const float w = fast_exp2(l - mnew);
+      acc = acc * keep + o * w;
+      wsum = wsum * keep + w;
+      mx = mnew;
     }
     const int head = kvh * g + h;
     *reinterpret_cast<f32x4*>(a.out + (size_t(seq) * a.num_q_heads + head) * a.head_dim + 4 * d4) =

@@ -15,6 +15,10 @@
 
 #include "sf_internal.h"
 
+static_assert(sizeof(sf_attn_desc) == 32, "sf_attn_desc layout is part of the ABI");
+static_assert(sizeof(sf_plan_opts) == 20, "sf_plan_opts layout is part of the ABI");
+static_assert(sizeof(sf_plan_info) == 48, "sf_plan_info layout is part of the ABI");
+
 namespace sf {
 
 uint64_t align256(uint64_t x) { return (x + 255u) & ~uint64_t(255u); }

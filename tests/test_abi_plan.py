@@ -169,6 +169,18 @@ def test_plan_invariants(seed):
     assert np.array_equal(np.sort(slots), np.arange(info.num_partials))
 
 
+def test_plan_rejects_bad_knobs(lib):
+    desc = B.make_desc(2, 8, 2, 128, 10, 4, 0.1)
+    lens = np.array([10, 20], np.int32)
+    info = B.sf_plan_info()
+    for field, value in (("num_cus", -1), ("chunk_pages", -1), ("workers_per_cu", -1),
+                         ("min_chunk_pages", -1), ("reserved", 1)):
+        opts = B.make_opts()
+        setattr(opts, field, value)
+        assert lib.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts), None, 0,
+                                       ctypes.byref(info)) == 1, field
+
+
 def test_plan_size_query_and_capacity(lib):
     lens = np.array([100, 5000, 3], np.int32)
     desc = B.make_desc(3, 8, 2, 128, 400, 1, 0.1)

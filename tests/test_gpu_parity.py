@@ -141,11 +141,37 @@ def test_uploaded_plan_is_reusable():
         B.sf_decode_attn_combine(desc, info, work_dev, ws, out, lse)
         torch.cuda.synchronize()
         outs.append((out.cpu().numpy(), lse.cpu().numpy()))
+        # the pass leaves the whole work list, queue row included, as planned
+        assert np.array_equal(work_dev.cpu().numpy(), pinned.numpy()), f"work list changed (rep {rep})"
     ref = run_oracle(b)
     assert_close(outs[0][0], ref[0], "reused plan")
     assert_close(outs[0][1], ref[1], "reused plan lse")
     for o, l in outs[1:]:
         assert np.array_equal(o, outs[0][0]) and np.array_equal(l, outs[0][1])
+
+
+def test_few_workers_walk_many_segments():
+    """Four workers (one CU) each walk several segments, most of them cut."""
+    _say("few workers, many segments")
+    b = build_batch([3, 17, 250, 1000, 4096, 0, 777], 28, 4, 128, 44)
+    dev = to_dev(b)
+    desc = B.make_desc(b.num_seqs, 28, 4, 128, b.block_table.shape[1], b.num_pages, b.scale)
+    info, work = B.sf_decode_attn_plan(desc, b.seq_lens, B.make_opts(num_cus=1))
+    assert info.num_workers == 4 and info.num_work >= 28 and info.num_combine > 0
+    pinned = torch.from_numpy(work[: info.work_bytes // 4].copy()).pin_memory()
+    work_dev = torch.empty(info.work_bytes // 4, dtype=torch.int32, device="cuda")
+    ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty((b.num_seqs, 28, 128), dtype=torch.float32, device="cuda")
+    lse = torch.empty((b.num_seqs, 28), dtype=torch.float32, device="cuda")
+    for rep in range(2):
+        B.sf_decode_attn(desc, info, pinned if rep == 0 else None, work_dev, dev["q"], dev["k"], dev["v"],
+                         dev["bt"], out, lse, ws)
+        B.sf_decode_attn_combine(desc, info, work_dev, ws, out, lse)
+        torch.cuda.synchronize()
+        assert np.array_equal(work_dev.cpu().numpy(), pinned.numpy())
+        ref = run_oracle(b)
+        assert_close(out.cpu().numpy(), ref[0], f"few workers rep {rep}")
+        assert_close(lse.cpu().numpy(), ref[1], f"few workers lse rep {rep}")
 
 
 def test_chunk_count_invariance():
