@@ -104,7 +104,7 @@ typedef struct sf_plan_info {
  * Builds the work list on the host (no device calls).
  *
  * Rule (the length-aware partition; the paper balances skewed trajectory
- * lengths across rollout instances, Sec. 5.2, and this balances them across
+ * lengths across rollout instances, Sec. 5.3, and this balances them across
  * the compute units of one GPU). The pairs p = (s, kvh), in order s-major,
  * kvh-minor, have pages_p = ceil(L_s / 16); laid end to end they form
  * T = sum_p pages_p global pages. With

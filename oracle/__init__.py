@@ -10,6 +10,7 @@ Modules:
   exact_ref    high-precision decimal attention for a handful of tokens
   merge_ref    fp64 log-sum-exp merge of partial attention results
   plan_ref     re-derivation of the split-K chunk plan from its stated rule
+  append_ref   page allocator, KV append and the growing-cache decode loop
 """
 from __future__ import annotations
 

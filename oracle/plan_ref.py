@@ -1,7 +1,7 @@
 """Re-derivation of the work plan (length-balanced worker slices) from its written rule.
 
 TEST INFRASTRUCTURE ONLY. The paper balances skewed trajectory lengths across
-rollout instances (routing and migration, Sec. 5.2); inside one GPU the same
+rollout instances (routing and migration, Sec. 5.3); inside one GPU the same
 skew is balanced by giving every resident wave the same number of KV pages.
 This module restates that rule in plain Python, independently of the C
 planner, so the two can be compared bit for bit:

@@ -2,7 +2,7 @@
 //
 // Rollout batches mix a few very long trajectories with many short ones
 // (Sec. 2.3 of the paper); the paper balances that skew across rollout
-// instances by routing and migration (Sec. 5.2). Inside one GPU the same job
+// instances by routing and migration (Sec. 5.3). Inside one GPU the same job
 // falls to this planner: it lays every (sequence, KV head) page range end to
 // end and gives each resident attention wave (a worker) an equal slice of the
 // pages, cut at pair boundaries into segments. Long sequences are then read

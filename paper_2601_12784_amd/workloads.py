@@ -285,3 +285,61 @@ def make_straggler(seed: int | None = None, steps: int = STRAGGLER_STEPS, poison
     q_all = base.q
     base.q = q_all[0]
     return StragglerRun(base=base, caps=caps, steps=steps, q_all=q_all)
+
+
+@dataclass
+class DecodeLoop:
+    """Multi-step decode that grows its own cache (same lengths and caps as the
+    extreme-straggler schedule).
+
+    The pool starts with only each sequence's first L_i tokens (its pages
+    scattered over a pool of sum_i ceil(cap_i / 16) pages, every other page
+    free and NaN-filled). Sequence i is active at step t iff L_i + t <= cap_i,
+    with KV length L_i + t; at every step t >= 1 each active sequence appends
+    one token, position L_i + t - 1, whose key and value are k_new[t, i] and
+    v_new[t, i]. Inactive sequences keep their batch row with length 0.
+    """
+    base: Batch                   # lengths L_i; block table widened to the caps' stride
+    caps: np.ndarray              # int64 [B0]
+    steps: int
+    q_all: torch.Tensor           # bf16 [steps, B0, Hq, D]
+    k_new: torch.Tensor           # bf16 [steps, B0, Hkv, D] (row t = 0 unused)
+    v_new: torch.Tensor           # bf16 [steps, B0, Hkv, D]
+
+    def active(self, t: int) -> np.ndarray:
+        return self.base.seq_lens.astype(np.int64) + t <= self.caps
+
+    def lengths(self, t: int) -> np.ndarray:
+        """int32 [B0]: KV length at step t (0 once a sequence has finished)."""
+        return np.where(self.active(t), self.base.seq_lens.astype(np.int64) + t, 0).astype(np.int32)
+
+    def seq_steps(self) -> int:
+        return int(sum(int(self.active(t).sum()) for t in range(self.steps)))
+
+
+def make_decode_loop(seed: int | None = None, steps: int = STRAGGLER_STEPS, poison: bool = True,
+                     lens=None, cap_extra_max: int = 64, num_q_heads=28, num_kv_heads=4,
+                     head_dim=128) -> DecodeLoop:
+    """The growing-cache version of make_straggler(): same seed, lengths and caps;
+    new-token keys and values come from SeedSequence(seed).spawn(5)[3] and [4]."""
+    seed = config_seed("straggler") if seed is None else seed
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if lens is None:
+        lens = sample_lengths("straggler", rng)
+    lens = np.asarray(lens, dtype=np.int64)
+    caps = lens + rng.integers(0, cap_extra_max, size=lens.size, endpoint=True)
+    n_pool = int(((caps + PAGE - 1) // PAGE).sum())
+    base = build_batch(lens, num_q_heads, num_kv_heads, head_dim, seed, name="decode-loop",
+                       pool_pages=n_pool, poison=poison, rng=rng, num_queries=steps)
+    stride = max(1, int(((caps + PAGE - 1) // PAGE).max()))
+    bt = np.full((lens.size, stride), -1, dtype=np.int32)
+    bt[:, : base.block_table.shape[1]] = base.block_table
+    base.block_table = bt
+    q_all = base.q
+    base.q = q_all[0]
+    ss = np.random.SeedSequence(seed).spawn(5)
+    shape = (steps, lens.size, num_kv_heads, head_dim)
+    n = int(np.prod(shape))
+    k_new = _fill_normal(ss[3], n, 1.0).view(*shape)
+    v_new = _fill_normal(ss[4], n, 1.0).view(*shape)
+    return DecodeLoop(base=base, caps=caps, steps=steps, q_all=q_all, k_new=k_new, v_new=v_new)
