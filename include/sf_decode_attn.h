@@ -60,7 +60,7 @@ typedef enum sf_status {
   SF_OK = 0,
   SF_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad shape or length */
   SF_ERR_UNSUPPORTED = 2,   /* valid but not built: D, page size or g out of range */
-  SF_ERR_CAPACITY = 3,      /* work-list buffer or workspace smaller than the plan needs */
+  SF_ERR_CAPACITY = 3,      /* work-list buffer or workspace smaller than the plan needs, or too few free pages */
   SF_ERR_PLAN_MISMATCH = 4, /* plan was built for a different descriptor */
   SF_ERR_HIP = 5            /* the HIP runtime reported an error */
 } sf_status;
@@ -166,6 +166,59 @@ sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info* info,
 sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_plan_info* info,
                                  const int32_t* work_dev, const void* workspace,
                                  uint64_t workspace_bytes, float* out, float* lse, void* stream);
+
+/*
+ * Append, then attend: the decode step of a growing cache. Each step of a
+ * batched decode produces one new token per running trajectory (App. B.1),
+ * whose key and value join the trajectory's cache before its query attends.
+ *
+ * Same as sf_decode_attn over the plan's lengths L_s, after, for every
+ * sequence with L_s >= 1, storing its newest token (index t = L_s - 1):
+ *   key k_new[s][kvh][:] and value v_new[s][kvh][:] (bf16 [B][Hkv][D], device)
+ *   go to slot t % 16 of page P = new_pages[s] if new_pages is not NULL and
+ *   new_pages[s] >= 0 (P is then also written to block_table[s][t / 16]),
+ *   else of page P = block_table[s][t / 16].
+ * new_pages: device int32 [B] or NULL; the caller allocates the pages (see
+ * sf_page_pool_*) and passes -1 where the token lands in a page the sequence
+ * already holds. Sequences with L_s = 0 store nothing. The store and the
+ * attention over all L_s tokens happen in the same launch; the pools and the
+ * block table are written, so they must not be read by other work on the
+ * device until the call's stream has passed it. Errors as sf_decode_attn,
+ * plus SF_ERR_INVALID_ARG for NULL or misaligned (16 bytes) k_new / v_new.
+ */
+sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* info,
+                                const int32_t* work_host, int32_t* work_dev, const void* q,
+                                const void* k_new, const void* v_new, const int32_t* new_pages,
+                                void* k_pool, void* v_pool, int32_t* block_table, float* out,
+                                float* lse, void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * Host page allocator for the KV pool. A trajectory's cache grows by one
+ * 16-token page at a time and is released when it leaves, within a pool of
+ * fixed size (the KV-cache budget of Sec. 5.2). Pages are ids 0 .. N-1 of
+ * the pool's first dimension. The free list is last in, first out: a new
+ * pool hands out pages in increasing id order, and a released page is handed
+ * out again before any page released earlier. Host memory only, no device
+ * calls; calls on one pool must not overlap. Every call checks all of its
+ * arguments before it changes anything.
+ */
+typedef struct sf_page_pool sf_page_pool;
+
+/* *pool = a pool of num_pages >= 0 free pages; free with sf_page_pool_destroy. */
+sf_status sf_page_pool_create(int32_t num_pages, sf_page_pool** pool);
+void sf_page_pool_destroy(sf_page_pool* pool);
+/* Free pages, or -1 for a NULL pool. */
+int32_t sf_page_pool_available(const sf_page_pool* pool);
+/* Marks the n given free pages as in use (e.g. a prompt's pages), keeping the
+ * order of the rest. SF_ERR_INVALID_ARG if one is out of range, repeated or
+ * already in use. */
+sf_status sf_page_pool_claim(sf_page_pool* pool, const int32_t* pages, int32_t n);
+/* Takes n pages into pages[0..n) (host), in hand-out order; SF_ERR_CAPACITY
+ * if fewer than n are free. */
+sf_status sf_page_pool_alloc(sf_page_pool* pool, int32_t n, int32_t* pages);
+/* Returns n pages in use, in the given order (the last one is handed out
+ * next). SF_ERR_INVALID_ARG if one is out of range, repeated or not in use. */
+sf_status sf_page_pool_release(sf_page_pool* pool, const int32_t* pages, int32_t n);
 
 /*
  * Test support: copies the cached keys and values of tokens 0 .. len-1 of

@@ -72,7 +72,19 @@ def lib():
                                          vp, vp, vp]
     L.sf_debug_gather_kv.argtypes = [P(sf_attn_desc), vp, vp, vp, ctypes.c_int32, ctypes.c_int32,
                                      ctypes.c_int32, vp, vp, vp]
-    for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv"):
+    L.sf_decode_attn_append.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp,
+                                        vp, vp, vp, vp, ctypes.c_uint64, vp]
+    L.sf_page_pool_create.argtypes = [ctypes.c_int32, P(vp)]
+    L.sf_page_pool_destroy.argtypes = [vp]
+    L.sf_page_pool_destroy.restype = None
+    L.sf_page_pool_available.argtypes = [vp]
+    L.sf_page_pool_available.restype = ctypes.c_int32
+    for fn in ("sf_page_pool_claim", "sf_page_pool_release"):
+        getattr(L, fn).argtypes = [vp, vp, ctypes.c_int32]
+    L.sf_page_pool_alloc.argtypes = [vp, ctypes.c_int32, vp]
+    for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv",
+               "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
+               "sf_page_pool_release"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -195,6 +207,68 @@ def sf_decode_attn(desc, info, work_host, work_dev, q, k_pool, v_pool, block_tab
         ctypes.byref(desc), ctypes.byref(info), _addr(work_host), _addr(work_dev), _addr(q),
         _addr(k_pool), _addr(v_pool), _addr(block_table), _addr(out), _addr(lse),
         _addr(workspace), ws_bytes, _stream(stream)))
+
+
+def sf_decode_attn_append(desc, info, work_host, work_dev, q, k_new, v_new, new_pages, k_pool, v_pool,
+                          block_table, out, lse=None, workspace=None, stream=None):
+    """Enqueues append-then-attend: stores each sequence's newest token
+    (k_new, v_new: bf16 [B, Hkv, D]) into its page, then attends as
+    sf_decode_attn. new_pages: device int32 [B] (-1 = no new page) or None."""
+    b, hq, hkv, d = desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
+    _dev(q, "q", torch.bfloat16, (b, hq, d))
+    _dev(k_new, "k_new", torch.bfloat16, (b, hkv, d))
+    _dev(v_new, "v_new", torch.bfloat16, (b, hkv, d))
+    if new_pages is not None:
+        _dev(new_pages, "new_pages", torch.int32, (b,))
+    _dev(k_pool, "k_pool", torch.bfloat16, (desc.num_pages, hkv, d // 8, PAGE, 8))
+    _dev(v_pool, "v_pool", torch.bfloat16, (desc.num_pages, hkv, d, PAGE))
+    _dev(block_table, "block_table", torch.int32, (b, desc.block_table_stride))
+    _dev(out, "out", torch.float32, (b, hq, d))
+    _dev(work_dev, "work_dev", torch.int32)
+    if work_dev.numel() * 4 < info.work_bytes:
+        raise ValueError("work_dev is smaller than the plan")
+    if lse is not None:
+        _dev(lse, "lse", torch.float32, (b, hq))
+    ws_bytes = 0
+    if workspace is not None:
+        _dev(workspace, "workspace", workspace.dtype)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check("sf_decode_attn_append", lib().sf_decode_attn_append(
+        ctypes.byref(desc), ctypes.byref(info), _addr(work_host), _addr(work_dev), _addr(q), _addr(k_new),
+        _addr(v_new), _addr(new_pages), _addr(k_pool), _addr(v_pool), _addr(block_table), _addr(out),
+        _addr(lse), _addr(workspace), ws_bytes, _stream(stream)))
+
+
+class PagePool:
+    """The library's host page allocator (LIFO free list over page ids)."""
+
+    def __init__(self, num_pages: int):
+        self._p = ctypes.c_void_p()
+        self._L = lib()
+        _check("sf_page_pool_create", self._L.sf_page_pool_create(int(num_pages), ctypes.byref(self._p)))
+        self.num_pages = int(num_pages)
+
+    def available(self) -> int:
+        return int(self._L.sf_page_pool_available(self._p))
+
+    def claim(self, pages) -> None:
+        a = np.ascontiguousarray(pages, dtype=np.int32)
+        _check("sf_page_pool_claim", self._L.sf_page_pool_claim(self._p, a.ctypes.data, a.size))
+
+    def alloc(self, n: int) -> np.ndarray:
+        out = np.empty(max(0, int(n)), dtype=np.int32)
+        _check("sf_page_pool_alloc", self._L.sf_page_pool_alloc(self._p, int(n), out.ctypes.data))
+        return out
+
+    def release(self, pages) -> None:
+        a = np.ascontiguousarray(pages, dtype=np.int32)
+        _check("sf_page_pool_release", self._L.sf_page_pool_release(self._p, a.ctypes.data, a.size))
+
+    def __del__(self):
+        p = getattr(self, "_p", None)
+        if p is not None and p.value:
+            self._L.sf_page_pool_destroy(p)
+        self._p = None
 
 
 def sf_decode_attn_combine(desc, info, work_dev, workspace, out, lse=None, stream=None):
@@ -355,10 +429,14 @@ class DecodeAttention:
         return slot, buf
 
     def __call__(self, q, k_pool, v_pool, block_table, seq_lens, scale, out=None, lse=None,
-                 chunk_pages=None, stream: torch.cuda.Stream | None = None, attn_events=None):
+                 chunk_pages=None, stream: torch.cuda.Stream | None = None, attn_events=None,
+                 append=None):
         """One decode step on `stream` (default: the current stream). attn_events,
         if given, is a (start, end) pair of torch events recorded around the
-        attention kernel."""
+        attention kernel. append = (k_new, v_new, new_pages) makes it an
+        append-then-attend step: k_new, v_new are device bf16 [B, Hkv, D] and
+        new_pages a host int32 [B] array (-1 = the token's page is already
+        held), uploaded together with the work list."""
         b = q.shape[0]
         main = stream or torch.cuda.current_stream(self.device)
         main_h = main.cuda_stream
@@ -385,6 +463,19 @@ class DecodeAttention:
                                          device=self.device)
         j = self._n % 2
         nbytes = info.work_bytes
+        if append is not None:
+            k_new, v_new, new_pages = append
+            _dev(k_new, "k_new", torch.bfloat16, (b, self.hkv, self.d))
+            _dev(v_new, "v_new", torch.bfloat16, (b, self.hkv, self.d))
+            pages = np.ascontiguousarray(new_pages, dtype=np.int32)
+            if pages.shape != (b,):
+                raise ValueError("new_pages must have one entry per sequence")
+            if buf.numel() < nbytes // 4 + b:
+                grown = torch.empty(nbytes // 4 + b + 1024, dtype=torch.int32, pin_memory=True)
+                grown[: nbytes // 4].copy_(buf[: nbytes // 4])
+                self._ring[slot] = buf = grown
+            buf[nbytes // 4: nbytes // 4 + b].numpy()[:] = pages
+            nbytes += 4 * b
         if self._work[j].numel() * 4 < nbytes:
             torch.cuda.synchronize(self.device)
             self._work[j] = torch.empty(nbytes // 4 * 5 // 4 + 1024, dtype=torch.int32, device=self.device)
@@ -400,10 +491,17 @@ class DecodeAttention:
         if attn_events is not None:
             attn_events[0].record(main)
         ws = self.workspace
-        _check("sf_decode_attn", self.L.sf_decode_attn(
-            ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
-            k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),
-            None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
+        if append is None:
+            _check("sf_decode_attn", self.L.sf_decode_attn(
+                ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
+                k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),
+                None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
+        else:
+            _check("sf_decode_attn_append", self.L.sf_decode_attn_append(
+                ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
+                k_new.data_ptr(), v_new.data_ptr(), work.data_ptr() + info.work_bytes, k_pool.data_ptr(),
+                v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),
+                None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
         if attn_events is not None:
             attn_events[1].record(main)
         if info.num_combine:
@@ -414,4 +512,80 @@ class DecodeAttention:
         self._n += 1
         self.last_info = sf_plan_info.from_buffer_copy(info)
         self.last_work_dev = work
+        return out
+
+
+class PageTable:
+    """Host bookkeeping of a growing paged cache: the page pool and a host copy
+    of the block table.
+
+    Each decode step generates one token per running trajectory (App. B.1).
+    advance(lens) moves to the next step's lengths (0 for a sequence that has
+    left) and
+      1. returns to the pool every page of the sequences that have left since
+         the previous step (ascending sequence order, each in block-table order);
+      2. if appending, takes one page for every newest token that opens a page
+         (index L - 1 a multiple of 16), in ascending sequence order, and
+         records it in the host block table.
+    It returns the int32 [B] new-page array the append kernel takes (-1 where
+    the token lands in a page the sequence already holds).
+    """
+
+    def __init__(self, num_pages, bt_host, lens0):
+        self.bt = np.array(bt_host, dtype=np.int32, copy=True)
+        lens0 = np.asarray(lens0, dtype=np.int64)
+        self.pool = PagePool(num_pages)
+        npg = (lens0 + PAGE - 1) // PAGE
+        held = [self.bt[s, : npg[s]] for s in range(lens0.size)]
+        self.pool.claim(np.concatenate(held) if held else np.zeros(0, np.int32))
+        self.prev = lens0.copy()
+
+    def advance(self, lens, appending=True) -> np.ndarray:
+        lens = np.asarray(lens, dtype=np.int64)
+        gone = np.nonzero((self.prev > 0) & (lens == 0))[0]
+        if gone.size:
+            npg = (self.prev[gone] + PAGE - 1) // PAGE
+            self.pool.release(np.concatenate([self.bt[s, :n] for s, n in zip(gone, npg)]))
+        new_pages = np.full(lens.size, -1, dtype=np.int32)
+        if appending:
+            opens = np.nonzero((lens > 0) & ((lens - 1) % PAGE == 0))[0]
+            if opens.size:
+                pages = self.pool.alloc(opens.size)
+                new_pages[opens] = pages
+                self.bt[opens, (lens[opens] - 1) // PAGE] = pages
+        self.prev = lens
+        return new_pages
+
+
+class DecodeLoopRunner:
+    """Multi-step decode over a growing paged cache: per step, PageTable
+    bookkeeping on the host, then append-then-attend and the merge of split
+    sequences on the GPU. The first step (the prompt) only attends.
+    block_table is the device table the kernels read and extend."""
+
+    def __init__(self, num_q_heads, num_kv_heads, head_dim, k_pool, v_pool, block_table, bt_host, lens0,
+                 scale, device=None, num_cus=None):
+        self.attn = DecodeAttention(num_q_heads, num_kv_heads, head_dim, device=device, num_cus=num_cus)
+        self.k_pool, self.v_pool, self.block_table, self.scale = k_pool, v_pool, block_table, float(scale)
+        self.table = PageTable(k_pool.shape[0], bt_host, lens0)
+        self.steps = 0
+
+    @property
+    def bt_host(self):
+        return self.table.bt
+
+    @property
+    def pool(self):
+        return self.table.pool
+
+    def step(self, q, lens, k_new=None, v_new=None, out=None, lse=None, stream=None, attn_events=None):
+        lens = np.asarray(lens, dtype=np.int64)
+        appending = self.steps > 0
+        if appending and (k_new is None or v_new is None):
+            raise ValueError("every step after the first appends a token: pass k_new and v_new")
+        new_pages = self.table.advance(lens, appending)
+        append = (k_new, v_new, new_pages) if appending else None
+        out = self.attn(q, self.k_pool, self.v_pool, self.block_table, lens.astype(np.int32), self.scale,
+                        out=out, lse=lse, stream=stream, attn_events=attn_events, append=append)
+        self.steps += 1
         return out

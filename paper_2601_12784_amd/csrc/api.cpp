@@ -27,11 +27,20 @@ sf_status from_hip(hipError_t e) { return e == hipSuccess ? SF_OK : SF_ERR_HIP; 
 
 }  // namespace
 
-extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info* info,
-                                    const int32_t* work_host, int32_t* work_dev, const void* q,
-                                    const void* k_pool, const void* v_pool,
-                                    const int32_t* block_table, float* out, float* lse,
-                                    void* workspace, uint64_t workspace_bytes, void* stream) {
+namespace {
+
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  const int32_t* new_pages;
+};
+
+// Shared by sf_decode_attn and sf_decode_attn_append: checks, optional
+// work-list upload, one attention launch.
+sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_host,
+                 int32_t* work_dev, const void* q, const void* k_pool, const void* v_pool,
+                 const int32_t* block_table, float* out, float* lse, void* workspace,
+                 uint64_t workspace_bytes, void* stream, const AppendArgs* app) {
   sf_status st = validate_desc(desc);
   if (st != SF_OK) return st;
   if ((st = check_plan(desc, info)) != SF_OK) return st;
@@ -41,6 +50,9 @@ extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info
   if (desc->num_pages > 0 && (!k_pool || !v_pool)) return SF_ERR_INVALID_ARG;
   if (!aligned16(work_dev) || !aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) ||
       !aligned16(out) || !aligned4(block_table) || (lse && !aligned4(lse)))
+    return SF_ERR_INVALID_ARG;
+  if (app && (!app->k_new || !app->v_new || !aligned16(app->k_new) || !aligned16(app->v_new) ||
+              (app->new_pages && !aligned4(app->new_pages))))
     return SF_ERR_INVALID_ARG;
   if (workspace_bytes < info->workspace_bytes) return SF_ERR_CAPACITY;
   if (info->workspace_bytes && (!workspace || !aligned16(workspace))) return SF_ERR_INVALID_ARG;
@@ -70,7 +82,35 @@ extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info
   a.head_dim = desc->head_dim;
   a.bt_stride = desc->block_table_stride;
   a.scale_log2 = float(double(desc->softmax_scale) * 1.4426950408889634074);
+  a.k_new = app ? static_cast<const uint16_t*>(app->k_new) : nullptr;
+  a.v_new = app ? static_cast<const uint16_t*>(app->v_new) : nullptr;
+  a.new_pages = app ? app->new_pages : nullptr;
+  a.k_dst = app ? const_cast<uint16_t*>(a.k_pool) : nullptr;
+  a.v_dst = app ? const_cast<uint16_t*>(a.v_pool) : nullptr;
+  a.bt_dst = app ? const_cast<int32_t*>(block_table) : nullptr;
   return from_hip(launch_attention(a, s));
+}
+
+}  // namespace
+
+extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info* info,
+                                    const int32_t* work_host, int32_t* work_dev, const void* q,
+                                    const void* k_pool, const void* v_pool,
+                                    const int32_t* block_table, float* out, float* lse,
+                                    void* workspace, uint64_t workspace_bytes, void* stream) {
+  return attend(desc, info, work_host, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
+                workspace_bytes, stream, nullptr);
+}
+
+extern "C" sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* info,
+                                           const int32_t* work_host, int32_t* work_dev, const void* q,
+                                           const void* k_new, const void* v_new, const int32_t* new_pages,
+                                           void* k_pool, void* v_pool, int32_t* block_table, float* out,
+                                           float* lse, void* workspace, uint64_t workspace_bytes,
+                                           void* stream) {
+  const AppendArgs app = {k_new, v_new, new_pages};
+  return attend(desc, info, work_host, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
+                workspace_bytes, stream, &app);
 }
 
 extern "C" sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_plan_info* info,
@@ -134,7 +174,7 @@ extern "C" const char* sf_status_string(sf_status s) {
     case SF_OK: return "ok";
     case SF_ERR_INVALID_ARG: return "invalid argument";
     case SF_ERR_UNSUPPORTED: return "unsupported shape (head_dim must be 64 or 128, page_size 16, Hq/Hkv <= 16)";
-    case SF_ERR_CAPACITY: return "buffer smaller than the plan requires";
+    case SF_ERR_CAPACITY: return "buffer, workspace or page pool too small";
     case SF_ERR_PLAN_MISMATCH: return "plan was built for a different descriptor";
     case SF_ERR_HIP: return "HIP runtime error";
   }

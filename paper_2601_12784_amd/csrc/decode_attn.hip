@@ -117,6 +117,8 @@ struct ChunkCtx {
   int pe;             // end of this segment (pages)
   int k_off;          // element offset of this lane's K piece inside a tile
   int v_off;          // element offset of this lane's V^T piece inside a tile
+  int last_idx;       // appending: logical page of the newest token (-1: none)
+  int last_page;      // appending: its physical page
 };
 
 // Physical pages of the two-page block at logical page pg (a single page if
@@ -124,12 +126,21 @@ struct ChunkCtx {
 struct PagePair {
   int p0, p1;
 };
-template <int D>
+// When appending, the newest token's page may be new in this very launch:
+// it is taken from the launch's arguments, not from the block table.
+template <int D, bool kAppend>
+__device__ __forceinline__ int page_of(const ChunkCtx<D>& c, int pg) {
+  if constexpr (kAppend) {
+    if (pg == c.last_idx) return c.last_page;
+  }
+  return c.bt[pg];
+}
+template <int D, bool kAppend>
 __device__ __forceinline__ PagePair block_pages(const ChunkCtx<D>& c, int pg) {
   PagePair pp;
-  pp.p0 = c.bt[pg];
+  pp.p0 = page_of<D, kAppend>(c, pg);
   pp.p1 = pp.p0;
-  if (pg + 1 < c.pe) pp.p1 = c.bt[pg + 1];
+  if (pg + 1 < c.pe) pp.p1 = page_of<D, kAppend>(c, pg + 1);
   return pp;
 }
 
@@ -252,7 +263,22 @@ __device__ __forceinline__ void accumulate_block(VHalf<D>& b, const BlockWeights
 }
 
 // One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
+// Stores the newest token of (seq, kvh) into its page slot: lane l < D/8
+// writes key dims 8l .. 8l+7 (one 16-byte piece of the K tile), and every
+// lane writes the value dims l, l + 64 (two bytes each, 32 bytes apart).
 template <int D>
+__device__ __forceinline__ void store_token(const AttnArgs& a, int seq, int kvh, int page, int slot) {
+  const int lane = threadIdx.x;
+  const size_t row = (size_t(seq) * a.num_kv_heads + kvh) * D;
+  const size_t tile = tile_offset(page, a.num_kv_heads, kvh, D);
+  if (lane < D / 8)
+    *reinterpret_cast<u32x4*>(a.k_dst + tile + k_elem(slot, 8 * lane, D)) =
+        *reinterpret_cast<const u32x4*>(a.k_new + row + 8 * lane);
+#pragma unroll
+  for (int dim = lane; dim < D; dim += 64) a.v_dst[tile + v_elem(slot, dim)] = a.v_new[row + dim];
+}
+
+template <int D, bool kAppend>
 __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr item) {
   constexpr int KB = Shape<D>::KB;
   constexpr int JB = Shape<D>::JB;
@@ -281,11 +307,25 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr 
   c.k_off = k_elem(col, 8 * grp, D);
   // V operand: A-row = dim col (+16*jb), k-group grp = slots 4*grp .. +3.
   c.v_off = v_elem(4 * grp, col);
+  c.last_idx = -1;
+  c.last_page = 0;
+  if constexpr (kAppend) {
+    // The segment that ends the sequence also stores its newest token
+    // (index len - 1) before reading: no other segment touches that page.
+    if (len > 0 && pe == (len + kPage - 1) / kPage) {
+      const int t = len - 1;
+      const int fresh = a.new_pages ? as_constant(a.new_pages)[seq] : -1;
+      c.last_idx = t / kPage;
+      c.last_page = fresh >= 0 ? fresh : c.bt[c.last_idx];
+      store_token<D>(a, seq, kvh, c.last_page, t % kPage);
+      if (fresh >= 0 && kvh == 0 && lane == 0) a.bt_dst[size_t(seq) * a.bt_stride + c.last_idx] = fresh;
+    }
+  }
 
   KHalf<D> kb_[2];
   VHalf<D> vb_[2];
   if (pb < pe) {
-    const PagePair pp = block_pages(c, pb);
+    const PagePair pp = block_pages<D, kAppend>(c, pb);
     load_k(c, pp, kb_[0]);
     load_v(c, pp, vb_[0]);
   }
@@ -312,7 +352,7 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr 
     const bool more = pg + 2 < pe;
     PagePair nxt = {0, 0};
     if (more) {
-      nxt = block_pages(c, pg + 2);
+      nxt = block_pages<D, kAppend>(c, pg + 2);
       load_k(c, nxt, kn);
     }
     const int nvalid = min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage);
@@ -350,12 +390,13 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr 
 // One wave per worker: its segments are consecutive in the work list and
 // together cover the same number of KV pages as every other worker's.
 // Two waves per SIMD (at most 256 registers) keep 2048 workers resident.
-template <int D>
+template <int D, bool kAppend>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_kernel(AttnArgs a) {
   const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
   const int first = wt[0];
   const int count = wt[1];
-  for (int i = 0; i < count; ++i) attend_segment<D>(a, as_constant(a.items) + size_t(first + i) * kItemInts);
+  for (int i = 0; i < count; ++i)
+    attend_segment<D, kAppend>(a, as_constant(a.items) + size_t(first + i) * kItemInts);
 }
 
 // ---------------------------------------------------------------------------
@@ -422,10 +463,18 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
   if (a.num_workers == 0) return hipSuccess;
   const dim3 grid(a.num_workers), block(64);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(attn_worker_kernel<128>, grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL(attn_worker_kernel<64>, grid, block, 0, stream, a);
+  const bool append = a.k_new != nullptr;
+  if (a.head_dim == 128) {
+    if (append)
+      hipLaunchKernelGGL((attn_worker_kernel<128, true>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((attn_worker_kernel<128, false>), grid, block, 0, stream, a);
+  } else {
+    if (append)
+      hipLaunchKernelGGL((attn_worker_kernel<64, true>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((attn_worker_kernel<64, false>), grid, block, 0, stream, a);
+  }
   return hipGetLastError();
 }
 

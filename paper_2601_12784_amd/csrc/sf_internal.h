@@ -49,6 +49,13 @@ struct AttnArgs {
   int32_t head_dim;
   int32_t bt_stride;
   float scale_log2;   // softmax_scale * log2(e)
+  // Token append (sf_decode_attn_append only; k_new is NULL otherwise).
+  const uint16_t* k_new;      // [B][Hkv][D] newest token's keys
+  const uint16_t* v_new;      // [B][Hkv][D] and values
+  const int32_t* new_pages;   // [B] page newly given to that token, -1 = none; may be NULL
+  uint16_t* k_dst;            // the pools and block table, writable
+  uint16_t* v_dst;
+  int32_t* bt_dst;
 };
 
 struct CombineArgs {
