@@ -90,6 +90,53 @@ def time_steps(stepper, steps, warmup, every=EVENT_EVERY):
     return wall / steps * 1e3, float(np.mean(attn_ms)), float(np.median(attn_ms))
 
 
+def decode_loop_bench(reps=5):
+    """The extreme-straggler lengths and caps as a growing-cache decode loop:
+    512 sequences, 64 steps, one appended token per active sequence per step.
+    Returns seq-steps/s over whole loops, host bookkeeping, planning and
+    uploads included (median of `reps` timed loops after one untimed loop).
+    Each loop starts from the same prompt-time pools and block table."""
+    import torch
+    from paper_2601_12784_amd import binding as B
+    from paper_2601_12784_amd.workloads import make_decode_loop
+    run = make_decode_loop()
+    b = run.base
+    k0, v0 = b.k_pool.cuda(), b.v_pool.cuda()
+    bt0 = torch.from_numpy(b.block_table).cuda()
+    k, v, bt = k0.clone(), v0.clone(), bt0.clone()
+    q_all, k_new, v_new = run.q_all.cuda(), run.k_new.cuda(), run.v_new.cuda()
+    lens = [run.lengths(t) for t in range(run.steps)]
+    kv_read = sum(b.kv_bytes(L) for L in lens)
+    out = torch.empty((b.num_seqs, b.num_q_heads, b.head_dim), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.Stream()
+    times, issue = [], []
+    for rep in range(reps + 1):
+        k.copy_(k0)
+        v.copy_(v0)
+        bt.copy_(bt0)
+        runner = B.DecodeLoopRunner(b.num_q_heads, b.num_kv_heads, b.head_dim, k, v, bt, b.block_table,
+                                    b.seq_lens, b.scale)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(run.steps):
+            runner.step(q_all[t], lens[t], k_new[t] if t else None, v_new[t] if t else None, out=out,
+                        stream=stream)
+        t1 = time.perf_counter()
+        torch.cuda.synchronize()
+        if rep:
+            times.append(time.perf_counter() - t0)
+            issue.append(t1 - t0)
+    wall = float(np.median(times))
+    seq_steps = run.seq_steps()
+    return {"workload": f"growing-cache decode loop: {b.num_seqs} sequences (502 x U[1,2048] + 10 x 32768 "
+                        f"tokens at step 0), caps +U[0,64], {run.steps} steps, 28 q / 4 kv heads, "
+                        "head_dim 128; each step appends one token per active sequence",
+            "seq_steps": seq_steps, "loop_ms": round(wall * 1e3, 3),
+            "seq_steps_per_s": round(seq_steps / wall, 1),
+            "kv_gb_per_s": round(kv_read / wall / 1e9, 2), "kv_bytes_read": int(kv_read),
+            "host_issue_ms": round(float(np.median(issue)) * 1e3, 3), "timed_loops": reps}
+
+
 def cpu_baseline(batch, min_s=10.0, max_s=30.0):
     """The fp64 oracle, timed on the host cores over repeated passes of the
     batch (or of a prefix of it, if one pass would exceed max_s)."""
@@ -130,7 +177,7 @@ def stored_traffic(kv_bytes_per_launch):
     return doc.get("traffic_bytes_per_launch")
 
 
-ATTN_KERNEL = "attn_worker_kernel<128>"
+ATTN_KERNEL = "attn_worker_kernel<128, false>"
 COMBINE_KERNEL = "combine_kernel"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
@@ -193,7 +240,7 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
     md = out_path[:-len(".json")] + ".md"
     cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
            "-d $REPO/gpurun_out/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
-           "--no-skew --copy-probe " + str(int(copy_mib)))
+           "--no-skew --no-loop --copy-probe " + str(int(copy_mib)))
     lines = [f"# HBM traffic of {ATTN_KERNEL} on the long-tail batch (rocprofv3 counters)", "",
              "Two counter passes (one counter each), then the summary:", "", "```",
              cmd.format(c="FETCH_SIZE", d="pmc_fetch", o="f"), cmd.format(c="WRITE_SIZE", d="pmc_write", o="w"),
@@ -247,6 +294,7 @@ def main():
     ap.add_argument("--workers-per-cu", type=int, default=0, help="planner workers (waves) per CU")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-skew", action="store_true", help="skip the equal-bytes uniform batch")
+    ap.add_argument("--no-loop", action="store_true", help="skip the growing-cache decode loop")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -349,6 +397,12 @@ def main():
                           "skewed_over_uniform": round(ms_step / ms_u, 4),
                           "uniform_attn_kernel_us": round(attn_u * 1e3, 2)}
         del su
+
+    if not args.no_loop:
+        log("growing-cache decode loop (straggler lengths, 64 steps)")
+        result["decode_loop"] = decode_loop_bench()
+        log(f"  {result['decode_loop']['seq_steps_per_s']} seq-steps/s, "
+            f"{result['decode_loop']['loop_ms']} ms per loop")
 
     if not args.no_cpu_baseline:
         log("timing the oracle on the host")

@@ -126,7 +126,7 @@ typedef struct sf_plan_info {
  *   num_work item rows, worker by worker:
  *     seq, kv_head, page_begin, page_end (pages of the pair), seq_len,
  *     slot (-1 = write out directly), combine index (-1 if n_p = 1), n_p
- *   num_combine rows: seq, kv_head, slot_base, n_p, 0, 0, 0, 0
+ *   num_combine rows: seq, kv_head, slot_base, n_p, seq_len, 0, 0, 0
  *
  * seq_lens_host: B lengths on the host. opts may be NULL (all defaults).
  * work_host: host buffer of work_capacity_bytes; NULL only reports the sizes
@@ -172,19 +172,25 @@ sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_plan_info* i
  * batched decode produces one new token per running trajectory (App. B.1),
  * whose key and value join the trajectory's cache before its query attends.
  *
- * Same as sf_decode_attn over the plan's lengths L_s, after, for every
- * sequence with L_s >= 1, storing its newest token (index t = L_s - 1):
- *   key k_new[s][kvh][:] and value v_new[s][kvh][:] (bf16 [B][Hkv][D], device)
- *   go to slot t % 16 of page P = new_pages[s] if new_pages is not NULL and
- *   new_pages[s] >= 0 (P is then also written to block_table[s][t / 16]),
- *   else of page P = block_table[s][t / 16].
+ * Same as sf_decode_attn over the plan's lengths L_s, where for every
+ * sequence with L_s >= 1 the newest token (index t = L_s - 1) is not yet in
+ * the pool: its key and value are k_new[s][kvh][:] and v_new[s][kvh][:]
+ * (bf16 [B][Hkv][D], device). The call also stores them into the pool, at
+ * slot t % 16 of page P = new_pages[s] if new_pages is not NULL and
+ * new_pages[s] >= 0 (P is then also written to block_table[s][t / 16]),
+ * else of page P = block_table[s][t / 16].
  * new_pages: device int32 [B] or NULL; the caller allocates the pages (see
- * sf_page_pool_*) and passes -1 where the token lands in a page the sequence
- * already holds. Sequences with L_s = 0 store nothing. The store and the
- * attention over all L_s tokens happen in the same launch; the pools and the
- * block table are written, so they must not be read by other work on the
- * device until the call's stream has passed it. Errors as sf_decode_attn,
- * plus SF_ERR_INVALID_ARG for NULL or misaligned (16 bytes) k_new / v_new.
+ * sf_page_pool_* and sf_page_table_step) and passes -1 where the token lands
+ * in a page the sequence already holds. Sequences with L_s = 0 store nothing.
+ * Two launches on the stream: the attention pass over the L_s - 1 cached
+ * tokens, then a merge pass that adds the newest token as one more softmax
+ * term, merges split sequences and stores the tokens. The call thus also
+ * does sf_decode_attn_combine's work: do not call that for this step. lse is
+ * required (not NULL): the merge reads it back. The pools and the block
+ * table are written, so they must not be read by other work on the device
+ * until the call's stream has passed it. Errors as sf_decode_attn, plus
+ * SF_ERR_INVALID_ARG for NULL or misaligned (16 bytes) k_new / v_new or a
+ * NULL lse.
  */
 sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* info,
                                 const int32_t* work_host, int32_t* work_dev, const void* q,
@@ -219,6 +225,26 @@ sf_status sf_page_pool_alloc(sf_page_pool* pool, int32_t n, int32_t* pages);
 /* Returns n pages in use, in the given order (the last one is handed out
  * next). SF_ERR_INVALID_ARG if one is out of range, repeated or not in use. */
 sf_status sf_page_pool_release(sf_page_pool* pool, const int32_t* pages, int32_t n);
+
+/*
+ * Host bookkeeping of one decode step over a growing cache, on a host copy of
+ * the block table (int32 [num_seqs][stride]). Moving from lengths prev_lens
+ * to lens (host int32 [num_seqs]; 0 for a sequence that is not running):
+ *   1. every sequence with prev_lens > 0 and lens == 0 returns its
+ *      ceil(prev_lens / 16) pages to the pool (ascending sequence order, each
+ *      in block-table order);
+ *   2. if appending != 0, every sequence whose newest token (index lens - 1)
+ *      opens a page, i.e. lens > 0 and (lens - 1) % 16 == 0, takes one page,
+ *      in ascending sequence order, recorded in the block table;
+ *   3. new_pages[s] = that page, or -1: the array sf_decode_attn_append takes.
+ * Appending steps expect lens = prev_lens + 1 for every running sequence.
+ * All or nothing: SF_ERR_INVALID_ARG for a length outside [0, 16 * stride]
+ * or a page to return that is not in use, SF_ERR_CAPACITY if the pool cannot
+ * supply the pages; nothing changes then.
+ */
+sf_status sf_page_table_step(sf_page_pool* pool, int32_t* block_table, int32_t stride,
+                             int32_t num_seqs, const int32_t* prev_lens, const int32_t* lens,
+                             int32_t appending, int32_t* new_pages);
 
 /*
  * Test support: copies the cached keys and values of tokens 0 .. len-1 of

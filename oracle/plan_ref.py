@@ -17,7 +17,7 @@ planner, so the two can be compared bit for bit:
 Work list rows (int32 x 8): ceil(W/4) worker-table rows (first item, count
 per worker), then the items worker by worker
   (seq, kv_head, page_begin, page_end, seq_len, slot or -1, combine index or -1, n_p),
-then one combine row per cut pair (seq, kv_head, slot_base, n_p, 0, 0, 0, 0).
+then one combine row per cut pair (seq, kv_head, slot_base, n_p, seq_len, 0, 0, 0).
 """
 from __future__ import annotations
 
@@ -79,7 +79,7 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
         if n > 1:
             meta[p] = (slot, len(combine), n)
             s, kvh = pairs[p]
-            combine.append([s, kvh, slot, n, 0, 0, 0, 0])
+            combine.append([s, kvh, slot, n, lens[s], 0, 0, 0])
             slot += n
 
     table = np.zeros((_ceil(workers, 4), 8), dtype=np.int32)

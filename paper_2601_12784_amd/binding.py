@@ -82,9 +82,10 @@ def lib():
     for fn in ("sf_page_pool_claim", "sf_page_pool_release"):
         getattr(L, fn).argtypes = [vp, vp, ctypes.c_int32]
     L.sf_page_pool_alloc.argtypes = [vp, ctypes.c_int32, vp]
+    L.sf_page_table_step.argtypes = [vp, vp, ctypes.c_int32, ctypes.c_int32, vp, vp, ctypes.c_int32, vp]
     for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv",
                "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
-               "sf_page_pool_release"):
+               "sf_page_pool_release", "sf_page_table_step"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -210,10 +211,12 @@ def sf_decode_attn(desc, info, work_host, work_dev, q, k_pool, v_pool, block_tab
 
 
 def sf_decode_attn_append(desc, info, work_host, work_dev, q, k_new, v_new, new_pages, k_pool, v_pool,
-                          block_table, out, lse=None, workspace=None, stream=None):
-    """Enqueues append-then-attend: stores each sequence's newest token
-    (k_new, v_new: bf16 [B, Hkv, D]) into its page, then attends as
-    sf_decode_attn. new_pages: device int32 [B] (-1 = no new page) or None."""
+                          block_table, out, lse, workspace=None, stream=None):
+    """Enqueues an appending decode pass: attention over every sequence
+    including its newest token (k_new, v_new: bf16 [B, Hkv, D]), then the
+    merge of split sequences and the token stores into the pools and the
+    block table (so no separate combine call). new_pages: device int32 [B]
+    (-1 = no new page) or None."""
     b, hq, hkv, d = desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
     _dev(q, "q", torch.bfloat16, (b, hq, d))
     _dev(k_new, "k_new", torch.bfloat16, (b, hkv, d))
@@ -227,8 +230,9 @@ def sf_decode_attn_append(desc, info, work_host, work_dev, q, k_new, v_new, new_
     _dev(work_dev, "work_dev", torch.int32)
     if work_dev.numel() * 4 < info.work_bytes:
         raise ValueError("work_dev is smaller than the plan")
-    if lse is not None:
-        _dev(lse, "lse", torch.float32, (b, hq))
+    if lse is None:
+        raise ValueError("sf_decode_attn_append needs an lse buffer (the merge reads it back)")
+    _dev(lse, "lse", torch.float32, (b, hq))
     ws_bytes = 0
     if workspace is not None:
         _dev(workspace, "workspace", workspace.dtype)
@@ -390,6 +394,7 @@ class DecodeAttention:
         self._desc = None
         self.last_info = None
         self.last_work_dev = None
+        self._lse = None
 
     def _opts(self, chunk_pages):
         o = self.opts
@@ -497,6 +502,10 @@ class DecodeAttention:
                 k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),
                 None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
         else:
+            if lse is None:  # the merge reads lse back: keep one of our own
+                if self._lse is None or self._lse.numel() < b * self.hq:
+                    self._lse = torch.empty(b * self.hq * 5 // 4 + 64, dtype=torch.float32, device=self.device)
+                lse = self._lse[: b * self.hq].view(b, self.hq)
             _check("sf_decode_attn_append", self.L.sf_decode_attn_append(
                 ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
                 k_new.data_ptr(), v_new.data_ptr(), work.data_ptr() + info.work_bytes, k_pool.data_ptr(),
@@ -504,7 +513,7 @@ class DecodeAttention:
                 None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
         if attn_events is not None:
             attn_events[1].record(main)
-        if info.num_combine:
+        if info.num_combine and append is None:  # an appending pass merges by itself
             _check("sf_decode_attn_combine", self.L.sf_decode_attn_combine(
                 ctypes.byref(desc), ctypes.byref(info), work.data_ptr(), ws.data_ptr(), ws.numel(),
                 out.data_ptr(), None if lse is None else lse.data_ptr(), main_h))
@@ -532,29 +541,25 @@ class PageTable:
     """
 
     def __init__(self, num_pages, bt_host, lens0):
-        self.bt = np.array(bt_host, dtype=np.int32, copy=True)
+        self.bt = np.array(bt_host, dtype=np.int32, order="C", copy=True)
         lens0 = np.asarray(lens0, dtype=np.int64)
         self.pool = PagePool(num_pages)
         npg = (lens0 + PAGE - 1) // PAGE
         held = [self.bt[s, : npg[s]] for s in range(lens0.size)]
         self.pool.claim(np.concatenate(held) if held else np.zeros(0, np.int32))
-        self.prev = lens0.copy()
+        self.prev = np.ascontiguousarray(lens0, dtype=np.int32)
+        self.new_pages = np.empty(lens0.size, dtype=np.int32)
 
     def advance(self, lens, appending=True) -> np.ndarray:
-        lens = np.asarray(lens, dtype=np.int64)
-        gone = np.nonzero((self.prev > 0) & (lens == 0))[0]
-        if gone.size:
-            npg = (self.prev[gone] + PAGE - 1) // PAGE
-            self.pool.release(np.concatenate([self.bt[s, :n] for s, n in zip(gone, npg)]))
-        new_pages = np.full(lens.size, -1, dtype=np.int32)
-        if appending:
-            opens = np.nonzero((lens > 0) & ((lens - 1) % PAGE == 0))[0]
-            if opens.size:
-                pages = self.pool.alloc(opens.size)
-                new_pages[opens] = pages
-                self.bt[opens, (lens[opens] - 1) // PAGE] = pages
+        """The library's sf_page_table_step on the host table; returns new_pages."""
+        lens = np.ascontiguousarray(lens, dtype=np.int32)
+        if lens.shape != self.prev.shape:
+            raise ValueError("lens must have one entry per sequence")
+        _check("sf_page_table_step", self.pool._L.sf_page_table_step(
+            self.pool._p, self.bt.ctypes.data, self.bt.shape[1], lens.size, self.prev.ctypes.data,
+            lens.ctypes.data, int(bool(appending)), self.new_pages.ctypes.data))
         self.prev = lens
-        return new_pages
+        return self.new_pages
 
 
 class DecodeLoopRunner:

@@ -30,13 +30,49 @@ sf_status from_hip(hipError_t e) { return e == hipSuccess ? SF_OK : SF_ERR_HIP; 
 namespace {
 
 struct AppendArgs {
+  const void* q;
   const void* k_new;
   const void* v_new;
   const int32_t* new_pages;
 };
 
+// Merge rows of a plan; with `app`, also the newest-token stores.
+CombineArgs combine_args(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,
+                         void* workspace, float* out, float* lse, const AppendArgs* app, void* k_pool,
+                         void* v_pool, int32_t* block_table) {
+  const int32_t g = desc->num_q_heads / desc->num_kv_heads;
+  Workspace ws = carve_workspace(workspace, info->num_partials, g, desc->head_dim);
+  CombineArgs a = {};
+  a.items = work_dev + (table_rows(info->num_workers) + info->num_work) * kItemInts;
+  a.num_items = info->num_combine;
+  a.part_o = info->num_partials ? ws.part_o : nullptr;
+  a.part_lse = info->num_partials ? ws.part_lse : nullptr;
+  a.out = out;
+  a.lse = lse;
+  a.num_q_heads = desc->num_q_heads;
+  a.group = g;
+  a.head_dim = desc->head_dim;
+  if (app) {
+    a.work_items = work_dev + table_rows(info->num_workers) * kItemInts;
+    a.num_work = info->num_work;
+    a.q = static_cast<const uint16_t*>(app->q);
+    a.scale_log2 = float(double(desc->softmax_scale) * 1.4426950408889634074);
+    a.k_new = static_cast<const uint16_t*>(app->k_new);
+    a.v_new = static_cast<const uint16_t*>(app->v_new);
+    a.new_pages = app->new_pages;
+    a.block_table = block_table;
+    a.bt_dst = block_table;
+    a.k_dst = static_cast<uint16_t*>(k_pool);
+    a.v_dst = static_cast<uint16_t*>(v_pool);
+    a.num_kv_heads = desc->num_kv_heads;
+    a.bt_stride = desc->block_table_stride;
+  }
+  return a;
+}
+
 // Shared by sf_decode_attn and sf_decode_attn_append: checks, optional
-// work-list upload, one attention launch.
+// work-list upload, the attention launch; when appending, also the merge
+// launch that stores the newest tokens.
 sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_host,
                  int32_t* work_dev, const void* q, const void* k_pool, const void* v_pool,
                  const int32_t* block_table, float* out, float* lse, void* workspace,
@@ -52,7 +88,7 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
       !aligned16(out) || !aligned4(block_table) || (lse && !aligned4(lse)))
     return SF_ERR_INVALID_ARG;
   if (app && (!app->k_new || !app->v_new || !aligned16(app->k_new) || !aligned16(app->v_new) ||
-              (app->new_pages && !aligned4(app->new_pages))))
+              (app->new_pages && !aligned4(app->new_pages)) || !lse))
     return SF_ERR_INVALID_ARG;
   if (workspace_bytes < info->workspace_bytes) return SF_ERR_CAPACITY;
   if (info->workspace_bytes && (!workspace || !aligned16(workspace))) return SF_ERR_INVALID_ARG;
@@ -85,10 +121,10 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
   a.k_new = app ? static_cast<const uint16_t*>(app->k_new) : nullptr;
   a.v_new = app ? static_cast<const uint16_t*>(app->v_new) : nullptr;
   a.new_pages = app ? app->new_pages : nullptr;
-  a.k_dst = app ? const_cast<uint16_t*>(a.k_pool) : nullptr;
-  a.v_dst = app ? const_cast<uint16_t*>(a.v_pool) : nullptr;
-  a.bt_dst = app ? const_cast<int32_t*>(block_table) : nullptr;
-  return from_hip(launch_attention(a, s));
+  if ((st = from_hip(launch_attention(a, s))) != SF_OK || !app) return st;
+  const CombineArgs m = combine_args(desc, info, work_dev, workspace, out, lse, app, const_cast<void*>(k_pool),
+                                     const_cast<void*>(v_pool), const_cast<int32_t*>(block_table));
+  return from_hip(launch_combine(m, s));
 }
 
 }  // namespace
@@ -108,7 +144,7 @@ extern "C" sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_pl
                                            void* k_pool, void* v_pool, int32_t* block_table, float* out,
                                            float* lse, void* workspace, uint64_t workspace_bytes,
                                            void* stream) {
-  const AppendArgs app = {k_new, v_new, new_pages};
+  const AppendArgs app = {q, k_new, v_new, new_pages};
   return attend(desc, info, work_host, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
                 workspace_bytes, stream, &app);
 }
@@ -125,18 +161,8 @@ extern "C" sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_p
   if (!aligned16(work_dev) || !aligned16(workspace) || !aligned16(out) || (lse && !aligned4(lse)))
     return SF_ERR_INVALID_ARG;
   if (workspace_bytes < info->workspace_bytes) return SF_ERR_CAPACITY;
-  const int32_t g = desc->num_q_heads / desc->num_kv_heads;
-  Workspace ws = carve_workspace(const_cast<void*>(workspace), info->num_partials, g, desc->head_dim);
-  CombineArgs a;
-  a.items = work_dev + (table_rows(info->num_workers) + info->num_work) * kItemInts;
-  a.num_items = info->num_combine;
-  a.part_o = ws.part_o;
-  a.part_lse = ws.part_lse;
-  a.out = out;
-  a.lse = lse;
-  a.num_q_heads = desc->num_q_heads;
-  a.group = g;
-  a.head_dim = desc->head_dim;
+  const CombineArgs a = combine_args(desc, info, work_dev, const_cast<void*>(workspace), out, lse, nullptr,
+                                     nullptr, nullptr, nullptr);
   return from_hip(launch_combine(a, static_cast<hipStream_t>(stream)));
 }
 

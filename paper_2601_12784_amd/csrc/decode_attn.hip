@@ -34,6 +34,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kLog2e = 1.44269504088896340736f;
 
 // ---------------------------------------------------------------------------
 // Block-table address translation, shared by the attention and gather kernels.
@@ -118,7 +119,7 @@ struct ChunkCtx {
   int k_off;          // element offset of this lane's K piece inside a tile
   int v_off;          // element offset of this lane's V^T piece inside a tile
   int last_idx;       // appending: logical page of the newest token (-1: none)
-  int last_page;      // appending: its physical page
+  const_i32_ptr fresh;  // appending: that token's entry of new_pages (or NULL)
 };
 
 // Physical pages of the two-page block at logical page pg (a single page if
@@ -126,12 +127,17 @@ struct ChunkCtx {
 struct PagePair {
   int p0, p1;
 };
-// When appending, the newest token's page may be new in this very launch:
-// it is taken from the launch's arguments, not from the block table.
+// When appending, the newest token's page may be new in this very step and
+// not yet in the block table: it comes from the launch's arguments.
+// Looked up only when that block is prefetched, so the extra load overlaps
+// the previous block's work.
 template <int D, bool kAppend>
 __device__ __forceinline__ int page_of(const ChunkCtx<D>& c, int pg) {
   if constexpr (kAppend) {
-    if (pg == c.last_idx) return c.last_page;
+    if (pg == c.last_idx && c.fresh) {
+      const int p = *c.fresh;
+      if (p >= 0) return p;
+    }
   }
   return c.bt[pg];
 }
@@ -195,7 +201,9 @@ struct BlockWeights {
 
 // Scores and online-softmax update for one block.
 // nvalid = tokens of the block (from its first token) inside the sequence.
-template <int D>
+// kMayBeEmpty: the block may hold no valid token (then nothing changes);
+// without it every block holds at least one, as in a plain decode step.
+template <int D, bool kMayBeEmpty = false>
 __device__ __forceinline__ BlockWeights score_block(const KHalf<D>& b, const u32x4* qf, int nvalid, int grp,
                                                     float scale_log2, SoftmaxState<D>& st) {
   f32x4 s0 = {0.f, 0.f, 0.f, 0.f};
@@ -218,15 +226,18 @@ __device__ __forceinline__ BlockWeights score_block(const KHalf<D>& b, const u32
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
   const float mnew = fmaxf(st.m, mx);
+  // With no token seen yet mnew is -inf: subtract 0 instead, so that
+  // 2^(-inf - 0) = 0 rather than 2^(-inf + inf).
+  const float mref = (kMayBeEmpty && mnew == -__builtin_inff()) ? 0.f : mnew;
   BlockWeights w;
-  w.alpha = fast_exp2(st.m - mnew);
+  w.alpha = fast_exp2(st.m - mref);
   st.m = mnew;
   float ps = 0.f;
   uint32_t hi[4], lo[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float p0 = fast_exp2(sc[2 * i] - mnew);
-    const float p1 = fast_exp2(sc[2 * i + 1] - mnew);
+    const float p0 = fast_exp2(sc[2 * i] - mref);
+    const float p1 = fast_exp2(sc[2 * i + 1] - mref);
     ps += p0 + p1;
     const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
     const uint32_t l0 = bf16_bits(p0 - bf16_value(h0)), l1 = bf16_bits(p1 - bf16_value(h1));
@@ -262,22 +273,26 @@ __device__ __forceinline__ void accumulate_block(VHalf<D>& b, const BlockWeights
   }
 }
 
-// One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
 // Stores the newest token of (seq, kvh) into its page slot: lane l < D/8
 // writes key dims 8l .. 8l+7 (one 16-byte piece of the K tile), and every
 // lane writes the value dims l, l + 64 (two bytes each, 32 bytes apart).
+// Nontemporal stores: these scattered small writes, if left as ordinary
+// dirty cache lines, slow the next attention pass by several percent.
 template <int D>
-__device__ __forceinline__ void store_token(const AttnArgs& a, int seq, int kvh, int page, int slot) {
-  const int lane = threadIdx.x;
-  const size_t row = (size_t(seq) * a.num_kv_heads + kvh) * D;
-  const size_t tile = tile_offset(page, a.num_kv_heads, kvh, D);
+__device__ __forceinline__ void store_token(uint16_t* k_dst, uint16_t* v_dst, const uint16_t* k_new,
+                                            const uint16_t* v_new, int num_kv_heads, int seq, int kvh,
+                                            int page, int slot, int lane) {
+  const size_t row = (size_t(seq) * num_kv_heads + kvh) * D;
+  const size_t tile = tile_offset(page, num_kv_heads, kvh, D);
   if (lane < D / 8)
-    *reinterpret_cast<u32x4*>(a.k_dst + tile + k_elem(slot, 8 * lane, D)) =
-        *reinterpret_cast<const u32x4*>(a.k_new + row + 8 * lane);
+    __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(k_new + row + 8 * lane),
+                                reinterpret_cast<u32x4*>(k_dst + tile + k_elem(slot, 8 * lane, D)));
 #pragma unroll
-  for (int dim = lane; dim < D; dim += 64) a.v_dst[tile + v_elem(slot, dim)] = a.v_new[row + dim];
+  for (int dim = lane; dim < D; dim += 64)
+    __builtin_nontemporal_store(v_new[row + dim], v_dst + tile + v_elem(slot, dim));
 }
 
+// One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
 template <int D, bool kAppend>
 __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr item) {
   constexpr int KB = Shape<D>::KB;
@@ -308,17 +323,17 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr 
   // V operand: A-row = dim col (+16*jb), k-group grp = slots 4*grp .. +3.
   c.v_off = v_elem(4 * grp, col);
   c.last_idx = -1;
-  c.last_page = 0;
+  c.fresh = nullptr;
+  // When appending, the segment that ends the sequence leaves the newest
+  // token (index len - 1, not yet in the pool) out: its pages hold tokens
+  // [0, len_pages), and the merge launch that follows adds the newest one.
+  // Its page may be new in this step, so the page comes from new_pages.
+  int len_pages = len;
   if constexpr (kAppend) {
-    // The segment that ends the sequence also stores its newest token
-    // (index len - 1) before reading: no other segment touches that page.
     if (len > 0 && pe == (len + kPage - 1) / kPage) {
-      const int t = len - 1;
-      const int fresh = a.new_pages ? as_constant(a.new_pages)[seq] : -1;
-      c.last_idx = t / kPage;
-      c.last_page = fresh >= 0 ? fresh : c.bt[c.last_idx];
-      store_token<D>(a, seq, kvh, c.last_page, t % kPage);
-      if (fresh >= 0 && kvh == 0 && lane == 0) a.bt_dst[size_t(seq) * a.bt_stride + c.last_idx] = fresh;
+      c.last_idx = (len - 1) / kPage;
+      c.fresh = a.new_pages ? as_constant(a.new_pages) + seq : nullptr;
+      len_pages = len - 1;
     }
   }
 
@@ -355,8 +370,10 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr 
       nxt = block_pages<D, kAppend>(c, pg + 2);
       load_k(c, nxt, kn);
     }
-    const int nvalid = min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage);
-    const BlockWeights w = score_block(kc, qf, nvalid, grp, a.scale_log2, st);
+    // (appending: a last page that holds only the newest token has none,
+    // nvalid <= 0, and leaves the state as it was)
+    const int nvalid = min(len_pages - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage);
+    const BlockWeights w = score_block<D, kAppend>(kc, qf, nvalid, grp, a.scale_log2, st);
     if (more) load_v(c, nxt, vn);
     accumulate_block(vc, w, nvalid, grp, st);
   };
@@ -390,6 +407,8 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr 
 // One wave per worker: its segments are consecutive in the work list and
 // together cover the same number of KV pages as every other worker's.
 // Two waves per SIMD (at most 256 registers) keep 2048 workers resident.
+// The appending variant reads the newest tokens from k_new / v_new and
+// stores nothing: the stores come in the merge launch that follows.
 template <int D, bool kAppend>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_kernel(AttnArgs a) {
   const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
@@ -402,8 +421,34 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 // ---------------------------------------------------------------------------
 // log-sum-exp merge of the chunks of split (sequence, KV head) pairs
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
-  const_i32_ptr it = as_constant(a.items) + size_t(blockIdx.x) * kItemInts;
+// Merges the n partial results of a split pair for head h, dims 4*d4 .. +3:
+// one pass in chunk order with a running maximum (log2 units); the loads of
+// several chunks are independent and issue together. Returns the maximum,
+// the weight sum relative to it and the weighted sum of the partial outputs.
+__device__ __forceinline__ void merge_partials(const CombineArgs& a, int base, int n, int h, int d4, float& mx,
+                                               float& wsum, f32x4& acc) {
+  const int g = a.group;
+  const float* lse_h = a.part_lse + size_t(base) * g + h;           // stride g per chunk
+  const float* o_h = a.part_o + (size_t(base) * g + h) * a.head_dim + 4 * d4;
+  const size_t o_stride = size_t(g) * a.head_dim;
+  mx = -__builtin_inff();
+  wsum = 0.f;
+  acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int c = 0; c < n; ++c) {
+    const float l = lse_h[size_t(c) * g];
+    const f32x4 o = *reinterpret_cast<const f32x4*>(o_h + c * o_stride);
+    const float mnew = fmaxf(mx, l);
+    const float keep = fast_exp2(mx - mnew);
+    const float w = fast_exp2(l - mnew);
+    acc = acc * keep + o * w;
+    wsum = wsum * keep + w;
+    mx = mnew;
+  }
+}
+
+__device__ __forceinline__ void merge_row(const CombineArgs& a, int row) {
+  const_i32_ptr it = as_constant(a.items) + size_t(row) * kItemInts;
   const int seq = it[0];
   const int kvh = it[1];
   const int base = it[2];
@@ -413,29 +458,102 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   for (int idx = threadIdx.x; idx < g * d4n; idx += blockDim.x) {
     const int h = idx / d4n;
     const int d4 = idx - h * d4n;
-    const float* lse_h = a.part_lse + size_t(base) * g + h;           // stride g per chunk
-    const float* o_h = a.part_o + (size_t(base) * g + h) * a.head_dim + 4 * d4;
-    const size_t o_stride = size_t(g) * a.head_dim;
-    // One pass in chunk order with a running maximum (log2 units): the
-    // loads of several chunks are independent and issue together.
-    float mx = -__builtin_inff();
-    float wsum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-    for (int c = 0; c < n; ++c) {
-      const float l = lse_h[size_t(c) * g];
-      const f32x4 o = *reinterpret_cast<const f32x4*>(o_h + c * o_stride);
-      const float mnew = fmaxf(mx, l);
-      const float keep = fast_exp2(mx - mnew);
-      const float w = fast_exp2(l - mnew);
-      acc = acc * keep + o * w;
-      wsum = wsum * keep + w;
-      mx = mnew;
-    }
+    float mx, wsum;
+    f32x4 acc;
+    merge_partials(a, base, n, h, d4, mx, wsum, acc);
     const int head = kvh * g + h;
     *reinterpret_cast<f32x4*>(a.out + (size_t(seq) * a.num_q_heads + head) * a.head_dim + 4 * d4) =
         acc * (1.f / wsum);
     if (a.lse && d4 == 0) a.lse[size_t(seq) * a.num_q_heads + head] = (mx + __log2f(wsum)) * kLn2;
+  }
+}
+
+__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) { merge_row(a, blockIdx.x); }
+
+// The merge launch of an appending step. The attention pass left each
+// sequence's newest token (index len - 1, not yet in the pool) out; here it
+// joins every (sequence, KV head) pair as one more term of the softmax:
+//   z = scale * q . k_new (log2 units), and with the pages' result (o, l)
+//   M = max(l, z); out = (o 2^(l-M) W + v_new 2^(z-M)) / (W 2^(l-M) + 2^(z-M))
+//   lse = M + log2(W 2^(l-M) + 2^(z-M))
+// where (o, l, W) is the merged partial sum of a split pair (its weight sum
+// W relative to l = its maximum), or out, lse and W = 1 of a pair the
+// attention pass finished. Then the token is stored into its page slot, and
+// a page newly given to it is recorded in the block table (KV head 0).
+// Blocks [0, num_items) take the split pairs' merge rows; the rest take one
+// work item each, acting on the single-segment pairs.
+template <int D>
+__global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
+  __shared__ float z_new[kMaxGroup];
+  const bool split = int(blockIdx.x) < a.num_items;
+  const_i32_ptr row = split ? as_constant(a.items) + size_t(blockIdx.x) * kItemInts
+                            : as_constant(a.work_items) + size_t(int(blockIdx.x) - a.num_items) * kItemInts;
+  const int seq = row[0];
+  const int kvh = row[1];
+  const int base = row[2];
+  const int n = row[3];
+  const int len = row[4];
+  if (!split && (row[7] != 1 || len <= 0)) return;   // split pairs come through their merge row
+  const int g = a.group;
+  const size_t new_row = (size_t(seq) * a.num_kv_heads + kvh) * D;
+
+  // z for each query head of the group: 16 lanes per head, 8 dims each.
+  {
+    const int h = threadIdx.x >> 4;
+    const int part = threadIdx.x & 15;
+    float acc = 0.f;
+    if (h < g && part < D / 8) {
+      const u32x4 qv = load16(a.q + (size_t(seq) * a.num_q_heads + kvh * g + h) * D + 8 * part);
+      const u32x4 kv = load16(a.k_new + new_row + 8 * part);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc += bf16_value(qv[e] & 0xFFFFu) * bf16_value(kv[e] & 0xFFFFu);
+        acc += bf16_value(qv[e] >> 16) * bf16_value(kv[e] >> 16);
+      }
+    }
+    acc += __shfl_xor(acc, 8);
+    acc += __shfl_xor(acc, 4);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 1);
+    if (part == 0 && h < g) z_new[h] = acc * a.scale_log2;
+  }
+  __syncthreads();
+
+  const int d4n = D / 4;
+  for (int idx = threadIdx.x; idx < g * d4n; idx += blockDim.x) {
+    const int h = idx / d4n;
+    const int d4 = idx - h * d4n;
+    const int head = kvh * g + h;
+    float* out = a.out + (size_t(seq) * a.num_q_heads + head) * D + 4 * d4;
+    float mx, wsum;
+    f32x4 acc;
+    if (split) {
+      merge_partials(a, base, n, h, d4, mx, wsum, acc);
+    } else {
+      acc = *reinterpret_cast<const f32x4*>(out);
+      mx = a.lse[size_t(seq) * a.num_q_heads + head] * kLog2e;   // -inf if the pages held no token
+      wsum = 1.f;
+    }
+    const u32x2 vv = *reinterpret_cast<const u32x2*>(a.v_new + new_row + 4 * d4);
+    const f32x4 v = {bf16_value(vv[0] & 0xFFFFu), bf16_value(vv[0] >> 16), bf16_value(vv[1] & 0xFFFFu),
+                     bf16_value(vv[1] >> 16)};
+    const float z = z_new[h];
+    const float m = fmaxf(mx, z);
+    const float a1 = fast_exp2(mx - m);
+    const float a2 = fast_exp2(z - m);
+    const float den = wsum * a1 + a2;
+    *reinterpret_cast<f32x4*>(out) = (acc * a1 + v * a2) * (1.f / den);
+    if (d4 == 0) a.lse[size_t(seq) * a.num_q_heads + head] = (m + __log2f(den)) * kLn2;
+  }
+
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const int t = len - 1;
+    const int fresh = a.new_pages ? as_constant(a.new_pages)[seq] : -1;
+    const size_t entry = size_t(seq) * a.bt_stride + t / kPage;
+    const int page = fresh >= 0 ? fresh : as_constant(a.block_table)[entry];
+    store_token<D>(a.k_dst, a.v_dst, a.k_new, a.v_new, a.num_kv_heads, seq, kvh, page, t % kPage, lane);
+    if (fresh >= 0 && kvh == 0 && lane == 0) a.bt_dst[entry] = fresh;
   }
 }
 
@@ -479,6 +597,15 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
+  if (a.k_new) {
+    const int blocks = a.num_items + a.num_work;
+    if (blocks == 0) return hipSuccess;
+    if (a.head_dim == 128)
+      hipLaunchKernelGGL(merge_append_kernel<128>, dim3(blocks), dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL(merge_append_kernel<64>, dim3(blocks), dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
   if (a.num_items == 0) return hipSuccess;
   hipLaunchKernelGGL(combine_kernel, dim3(a.num_items), dim3(256), 0, stream, a);
   return hipGetLastError();

@@ -98,3 +98,43 @@ extern "C" sf_status sf_page_pool_release(sf_page_pool* pool, const int32_t* pag
   }
   return SF_OK;
 }
+
+using sf::kPage;
+
+extern "C" sf_status sf_page_table_step(sf_page_pool* pool, int32_t* block_table, int32_t stride,
+                                        int32_t num_seqs, const int32_t* prev_lens, const int32_t* lens,
+                                        int32_t appending, int32_t* new_pages) {
+  if (!pool || !block_table || stride < 1 || num_seqs < 0) return SF_ERR_INVALID_ARG;
+  if (num_seqs > 0 && (!prev_lens || !lens || !new_pages)) return SF_ERR_INVALID_ARG;
+  const int64_t max_len = int64_t(stride) * kPage;
+  thread_local std::vector<int32_t> gone;
+  gone.clear();
+  int64_t opens = 0;
+  for (int32_t s = 0; s < num_seqs; ++s) {
+    const int32_t prev = prev_lens[s], len = lens[s];
+    if (prev < 0 || len < 0 || prev > max_len || len > max_len) return SF_ERR_INVALID_ARG;
+    if (prev > 0 && len == 0) {
+      const int32_t* row = block_table + int64_t(s) * stride;
+      for (int32_t j = 0; j < (prev + kPage - 1) / kPage; ++j) gone.push_back(row[j]);
+    }
+    if (appending && len > 0 && (len - 1) % kPage == 0) ++opens;
+  }
+  if (!check_pages(pool, gone.data(), int32_t(gone.size()), 1)) return SF_ERR_INVALID_ARG;
+  if (opens > int64_t(pool->stack.size() + gone.size())) return SF_ERR_CAPACITY;
+  for (int32_t pg : gone) {
+    pool->in_use[size_t(pg)] = 0;
+    pool->stack.push_back(pg);
+  }
+  for (int32_t s = 0; s < num_seqs; ++s) {
+    const int32_t len = lens[s];
+    int32_t page = -1;
+    if (appending && len > 0 && (len - 1) % kPage == 0) {
+      page = pool->stack.back();
+      pool->stack.pop_back();
+      pool->in_use[size_t(page)] = 1;
+      block_table[int64_t(s) * stride + (len - 1) / kPage] = page;
+    }
+    new_pages[s] = page;
+  }
+  return SF_OK;
+}

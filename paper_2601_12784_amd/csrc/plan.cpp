@@ -167,7 +167,8 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
       if (nseg[p] <= 1) continue;
       base_buf[size_t(p)] = slot;
       cidx_buf[size_t(p)] = ci;
-      const int32_t c8[kItemInts] = {int32_t(p / hkv), int32_t(p % hkv), slot, nseg[p], 0, 0, 0, 0};
+      const int32_t c8[kItemInts] = {int32_t(p / hkv), int32_t(p % hkv), slot, nseg[p], seq_lens_host[p / hkv],
+                                     0, 0, 0};
       std::memcpy(comb + int64_t(ci) * kItemInts, c8, sizeof c8);
       slot += nseg[p];
       ++ci;

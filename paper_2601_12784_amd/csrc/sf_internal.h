@@ -49,17 +49,15 @@ struct AttnArgs {
   int32_t head_dim;
   int32_t bt_stride;
   float scale_log2;   // softmax_scale * log2(e)
-  // Token append (sf_decode_attn_append only; k_new is NULL otherwise).
+  // Appending step (sf_decode_attn_append only; k_new is NULL otherwise):
+  // the newest tokens, read straight into registers.
   const uint16_t* k_new;      // [B][Hkv][D] newest token's keys
   const uint16_t* v_new;      // [B][Hkv][D] and values
   const int32_t* new_pages;   // [B] page newly given to that token, -1 = none; may be NULL
-  uint16_t* k_dst;            // the pools and block table, writable
-  uint16_t* v_dst;
-  int32_t* bt_dst;
 };
 
 struct CombineArgs {
-  const int32_t* items;
+  const int32_t* items;       // merge rows
   int32_t num_items;
   const float* part_o;
   const float* part_lse;
@@ -68,6 +66,21 @@ struct CombineArgs {
   int32_t num_q_heads;
   int32_t group;
   int32_t head_dim;
+  // Appending step (k_new NULL otherwise): the newest tokens join the
+  // softmax and go to the pool.
+  const int32_t* work_items;  // segment rows
+  int32_t num_work;
+  const uint16_t* q;
+  float scale_log2;
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  const int32_t* new_pages;
+  const int32_t* block_table;
+  int32_t* bt_dst;            // the block table, writable
+  uint16_t* k_dst;            // the pools, writable
+  uint16_t* v_dst;
+  int32_t num_kv_heads;
+  int32_t bt_stride;
 };
 
 struct GatherArgs {

@@ -124,7 +124,7 @@ def test_tiny_plan_by_hand():
               [3, 0, 5, 12, 300, 3, 1, 3],
               [3, 0, 12, 19, 300, 4, 1, 3]]
     assert np.array_equal(items, np.array(expect, np.int32))
-    assert np.array_equal(comb, np.array([[2, 0, 0, 2, 0, 0, 0, 0], [3, 0, 2, 3, 0, 0, 0, 0]], np.int32))
+    assert np.array_equal(comb, np.array([[2, 0, 0, 2, 130, 0, 0, 0], [3, 0, 2, 3, 300, 0, 0, 0]], np.int32))
     assert info.workspace_bytes == 5 * 4 * 64 * 4 + 256
 
 
@@ -161,7 +161,7 @@ def test_plan_invariants(seed):
             assert np.all(mine[1:, 2] == mine[:-1, 3]) and np.all(mine[:, 3] > mine[:, 2])
             if n > 1:
                 row = comb[mine[0, 6]]
-                assert row[0] == s and row[1] == kvh and row[3] == n
+                assert row[0] == s and row[1] == kvh and row[3] == n and row[4] == L
                 assert np.array_equal(mine[:, 5], row[2] + np.arange(n))
             else:
                 assert mine[0, 5] == -1 and mine[0, 6] == -1

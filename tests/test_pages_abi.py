@@ -79,13 +79,14 @@ def _planned():
 
 
 @pytest.mark.parametrize("kw", [dict(k_new=None), dict(v_new=None), dict(k_new=FAKE + 8),
-                                dict(v_new=FAKE + 2), dict(pages=FAKE + 2), dict(bt=None), dict(k=None)])
+                                dict(v_new=FAKE + 2), dict(pages=FAKE + 2), dict(bt=None), dict(k=None),
+                                dict(lse=None), dict(lse=FAKE + 2)])
 def test_append_rejects_bad_arguments(kw):
     desc, info = _planned()
-    a = dict(k_new=FAKE, v_new=FAKE, pages=None, k=FAKE, v=FAKE, bt=FAKE)
+    a = dict(k_new=FAKE, v_new=FAKE, pages=None, k=FAKE, v=FAKE, bt=FAKE, lse=FAKE)
     a.update(kw)
     st = B.lib().sf_decode_attn_append(ctypes.byref(desc), ctypes.byref(info), None, FAKE, FAKE, a["k_new"],
-                                        a["v_new"], a["pages"], a["k"], a["v"], a["bt"], FAKE, None, FAKE,
+                                        a["v_new"], a["pages"], a["k"], a["v"], a["bt"], FAKE, a["lse"], FAKE,
                                         1 << 30, None)
     assert st == 1
 
