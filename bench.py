@@ -137,6 +137,82 @@ def decode_loop_bench(reps=5):
             "host_issue_ms": round(float(np.median(issue)) * 1e3, 3), "timed_loops": reps}
 
 
+# KV bytes per token of one decode step over all layers of the paper's
+# cost-model example model (48 layers x 4 KV heads x head_dim 128, K and V, bf16).
+QWEN3_30B_A3B_KV_BYTES_PER_TOKEN = 48 * 4 * 128 * 2 * 2
+PAPER_K1_H20 = 7.28e-8   # App. B, coefficient table (seconds per token, reading)
+
+
+def calibrate_k1(batch_sizes=(64, 96, 128, 192, 256), reps=60):
+    """Fits the cost model's attention term, latency = k1 * kv_bytes + c, to
+    this library's decode step (plan, upload, attention, merge) on long-tail
+    batches of several sizes (every one above the 256 MB last-level cache).
+    Each point is the GPU time per step over `reps` back-to-back steps."""
+    import torch
+    from paper_2601_12784_amd.workloads import build_batch, sample_lengths, config_seed
+    points = []
+    for bsz in batch_sizes:
+        seed = config_seed("longtail") + 50 + bsz
+        rng = np.random.Generator(np.random.PCG64(seed))
+        lens = sample_lengths("longtail", rng)[:bsz]
+        b = build_batch(lens, 28, 4, 128, seed, rng=rng, poison=False)
+        st = Stepper(b)
+        for _ in range(50):
+            st.step()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        with torch.cuda.stream(st.stream):
+            ev[0].record()
+            for _ in range(reps):
+                st.step()
+            ev[1].record()
+        ev[1].synchronize()
+        points.append((b.kv_bytes(), ev[0].elapsed_time(ev[1]) / reps * 1e-3))
+        del st, b
+        torch.cuda.empty_cache()
+    x = np.array([p[0] for p in points], dtype=np.float64)
+    y = np.array([p[1] for p in points], dtype=np.float64)
+    k1, c = np.polyfit(x, y, 1)
+    r2 = 1.0 - float(((y - (k1 * x + c)) ** 2).sum() / ((y - y.mean()) ** 2).sum())
+    return {"fit": "decode-step latency = k1 * kv_bytes + c (App. B.1 attention term)",
+            "k1_s_per_byte": float(k1), "c_us": round(float(c) * 1e6, 2), "r2": round(r2, 5),
+            "points_bytes_us": [[int(a), round(float(t) * 1e6, 2)] for a, t in points],
+            "effective_gb_s": round(1e-9 / float(k1), 1),
+            "k1_s_per_token_qwen3_30b_a3b": float(k1) * QWEN3_30B_A3B_KV_BYTES_PER_TOKEN,
+            "paper_k1_h20_s_per_token": PAPER_K1_H20}
+
+
+def routing_demo(k1_per_token, mu=0.3, seed=0):
+    """The routing strategy (sf_route) on a synthetic 16-instance snapshot and
+    600 waiting trajectories, with the fitted k1 and the paper's k2..k4."""
+    from paper_2601_12784_amd import binding as B
+    rng = np.random.default_rng(seed)
+
+    class I:  # noqa: E742
+        def __init__(self, v, n, w, kv):
+            self.version, self.running, self.waiting, self.kv = v, n, w, kv
+
+    class T:
+        def __init__(self, v, length):
+            self.version, self.length = v, length
+
+    budget = 250_000.0   # tokens of KV per instance
+    model = B.sf_cost_model(k1_per_token, 1.72e-3, 1.25e-4, 1.07e-2, 1.0, budget)
+    insts = [I(int(rng.integers(3, 6)), int(rng.integers(0, 120)), 0, float(rng.uniform(0, 200_000)))
+             for _ in range(16)]
+    trajs = [T(None if rng.random() < 0.5 else int(rng.integers(3, 6)), float(rng.integers(200, 20_000)))
+             for _ in range(600)]
+    t0 = time.perf_counter()
+    for _ in range(20):
+        target, after = B.route(model, mu, 4, insts, trajs)
+    us = (time.perf_counter() - t0) / 20 * 1e6
+    before = sum(B.cost_throughput(model, B.sf_instance_state(s.version, s.running, s.waiting, 0, s.kv)) for s in insts)
+    after_t = sum(B.cost_throughput(model, B.sf_instance_state(s.version, s.running, s.waiting, 0, s.kv)) for s in after)
+    return {"instances": 16, "trajectories": 600, "mu": mu, "routed": int(sum(t >= 0 for t in target)),
+            "tokens_per_s_before": round(before, 1), "tokens_per_s_after": round(after_t, 1),
+            "sf_route_us": round(us, 1)}
+
+
 def cpu_baseline(batch, min_s=10.0, max_s=30.0):
     """The fp64 oracle, timed on the host cores over repeated passes of the
     batch (or of a prefix of it, if one pass would exceed max_s)."""
@@ -240,7 +316,7 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
     md = out_path[:-len(".json")] + ".md"
     cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
            "-d $REPO/gpurun_out/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
-           "--no-skew --no-loop --copy-probe " + str(int(copy_mib)))
+           "--no-skew --no-loop --no-cost --copy-probe " + str(int(copy_mib)))
     lines = [f"# HBM traffic of {ATTN_KERNEL} on the long-tail batch (rocprofv3 counters)", "",
              "Two counter passes (one counter each), then the summary:", "", "```",
              cmd.format(c="FETCH_SIZE", d="pmc_fetch", o="f"), cmd.format(c="WRITE_SIZE", d="pmc_write", o="w"),
@@ -295,6 +371,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-skew", action="store_true", help="skip the equal-bytes uniform batch")
     ap.add_argument("--no-loop", action="store_true", help="skip the growing-cache decode loop")
+    ap.add_argument("--no-cost", action="store_true", help="skip the cost-model k1 fit")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -397,6 +474,14 @@ def main():
                           "skewed_over_uniform": round(ms_step / ms_u, 4),
                           "uniform_attn_kernel_us": round(attn_u * 1e3, 2)}
         del su
+
+    if not args.no_cost:
+        log("cost model: fitting k1 to the decode step on five batch sizes")
+        cm = calibrate_k1()
+        cm["routing_demo"] = routing_demo(cm["k1_s_per_token_qwen3_30b_a3b"])
+        result["cost_model"] = cm
+        log(f"  k1 = {cm['k1_s_per_byte']:.3e} s/byte ({cm['effective_gb_s']} GB/s), c = {cm['c_us']} us, "
+            f"r2 = {cm['r2']}")
 
     if not args.no_loop:
         log("growing-cache decode loop (straggler lengths, 64 steps)")

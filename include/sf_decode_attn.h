@@ -247,6 +247,70 @@ sf_status sf_page_table_step(sf_page_pool* pool, int32_t* block_table, int32_t s
                              int32_t appending, int32_t* new_pages);
 
 /*
+ * Throughput cost model and trajectory routing (host only, no device calls).
+ *
+ * The paper's coordinator charges a rollout instance's decode step as
+ * attention linear in its KV-cache size, plus a matrix-multiplication term
+ * that is memory bound for few running trajectories and compute bound for
+ * many, plus a constant, and takes throughput as running trajectories over
+ * that latency (App. B.1, final throughput equation):
+ *   T_i = n / (k1 * kv + max(k2, k3 * n) + k4),  n = num_running (T_i = 0 if n = 0)
+ * Routing a trajectory of length l to instance i (Sec. 5.3, marginal gain):
+ *   it runs there iff kv + k5 * l <= kv_budget and num_waiting == 0 (then
+ *   kv += k5 * l, n += 1), else it waits (num_waiting += 1);
+ *   gain = T_i(after) - T_i(before);  ideal gain = 1 / (k1 * k5 * l + max(k2, k3) + k4).
+ * kv_cache, kv_budget and k5 * l share one unit (bytes or tokens); k1 is
+ * seconds per that unit, k2 and k4 seconds, k3 seconds per trajectory.
+ */
+typedef struct sf_cost_model {
+  double k1, k2, k3, k4;     /* >= 0 */
+  double k5;                 /* KV footprint per token, >= 0 */
+  double kv_budget;          /* M */
+} sf_cost_model;
+
+typedef struct sf_instance_state {  /* one instance of a snapshot */
+  int32_t version;           /* model version the instance runs */
+  int32_t num_running;       /* |run_trajs| */
+  int32_t num_waiting;       /* |wait_trajs| */
+  int32_t reserved;          /* 0 */
+  double kv_cache;           /* KV-cache size */
+} sf_instance_state;
+
+typedef struct sf_trajectory {
+  int32_t version;           /* version it was generated with; < 0: initial (none yet) */
+  int32_t reserved;          /* 0 */
+  double length;             /* tokens, >= 0 */
+} sf_trajectory;
+
+/* T_i of one instance; NaN for an invalid model or state. */
+double sf_cost_throughput(const sf_cost_model* model, const sf_instance_state* state);
+/* Marginal gain of routing a trajectory of this length to the instance; NaN if invalid. */
+double sf_cost_marginal_gain(const sf_cost_model* model, const sf_instance_state* state, double length);
+/* Gain of routing it to an idle instance; NaN if invalid. */
+double sf_cost_ideal_gain(const sf_cost_model* model, double length);
+
+/*
+ * Routing strategy (Sec. 5.3; App. D, check-routable and routing algorithms).
+ * Trajectories form queues by version, oldest first, initial ones last,
+ * arrival order inside a queue. For the head of the current queue:
+ *   candidates = instances it may run on: initial trajectories on instances
+ *   with version >= min_initial_version (the staleness manager's admission,
+ *   given as this bound), others on instances with version >= its version;
+ *   no candidate: stop. Candidates are grouped by increasing version; in the
+ *   first group whose largest gain (first maximum in instance order) is
+ *   >= mu * ideal gain, the trajectory goes to that instance, whose state is
+ *   updated as above, and the walk goes on; if no group qualifies: stop.
+ * inst (host, in/out): the snapshot, updated with every routed trajectory.
+ * target[j] (host, out): instance of trajectory j, or -1 if it stays.
+ * *num_routed: trajectories routed. SF_ERR_INVALID_ARG for a bad model (any
+ * coefficient negative or not finite), mu not finite, negative counts or
+ * lengths, or a NULL pointer where data is expected.
+ */
+sf_status sf_route(const sf_cost_model* model, double mu, int32_t min_initial_version,
+                   sf_instance_state* inst, int32_t num_inst, const sf_trajectory* trajs,
+                   int32_t num_trajs, int32_t* target, int32_t* num_routed);
+
+/*
  * Test support: copies the cached keys and values of tokens 0 .. len-1 of
  * (seq, kv_head) through the same address translation the attention kernel
  * uses, into device buffers k_dense and v_dense, bf16 [len][D] token-major.

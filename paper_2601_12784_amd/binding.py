@@ -51,6 +51,20 @@ class sf_plan_info(ctypes.Structure):
                 ("desc_key", ctypes.c_uint64)]
 
 
+class sf_cost_model(ctypes.Structure):
+    _fields_ = [("k1", ctypes.c_double), ("k2", ctypes.c_double), ("k3", ctypes.c_double),
+                ("k4", ctypes.c_double), ("k5", ctypes.c_double), ("kv_budget", ctypes.c_double)]
+
+
+class sf_instance_state(ctypes.Structure):
+    _fields_ = [("version", ctypes.c_int32), ("num_running", ctypes.c_int32),
+                ("num_waiting", ctypes.c_int32), ("reserved", ctypes.c_int32), ("kv_cache", ctypes.c_double)]
+
+
+class sf_trajectory(ctypes.Structure):
+    _fields_ = [("version", ctypes.c_int32), ("reserved", ctypes.c_int32), ("length", ctypes.c_double)]
+
+
 _lib = None
 
 
@@ -83,9 +97,16 @@ def lib():
         getattr(L, fn).argtypes = [vp, vp, ctypes.c_int32]
     L.sf_page_pool_alloc.argtypes = [vp, ctypes.c_int32, vp]
     L.sf_page_table_step.argtypes = [vp, vp, ctypes.c_int32, ctypes.c_int32, vp, vp, ctypes.c_int32, vp]
+    L.sf_cost_throughput.argtypes = [P(sf_cost_model), P(sf_instance_state)]
+    L.sf_cost_marginal_gain.argtypes = [P(sf_cost_model), P(sf_instance_state), ctypes.c_double]
+    L.sf_cost_ideal_gain.argtypes = [P(sf_cost_model), ctypes.c_double]
+    for fn in ("sf_cost_throughput", "sf_cost_marginal_gain", "sf_cost_ideal_gain"):
+        getattr(L, fn).restype = ctypes.c_double
+    L.sf_route.argtypes = [P(sf_cost_model), ctypes.c_double, ctypes.c_int32, vp, ctypes.c_int32, vp,
+                           ctypes.c_int32, vp, P(ctypes.c_int32)]
     for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv",
                "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
-               "sf_page_pool_release", "sf_page_table_step"):
+               "sf_page_pool_release", "sf_page_table_step", "sf_route"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -273,6 +294,42 @@ class PagePool:
         if p is not None and p.value:
             self._L.sf_page_pool_destroy(p)
         self._p = None
+
+
+def cost_throughput(model: sf_cost_model, state: sf_instance_state) -> float:
+    return float(lib().sf_cost_throughput(ctypes.byref(model), ctypes.byref(state)))
+
+
+def cost_marginal_gain(model: sf_cost_model, state: sf_instance_state, length: float) -> float:
+    return float(lib().sf_cost_marginal_gain(ctypes.byref(model), ctypes.byref(state), float(length)))
+
+
+def cost_ideal_gain(model: sf_cost_model, length: float) -> float:
+    return float(lib().sf_cost_ideal_gain(ctypes.byref(model), float(length)))
+
+
+def route(model: sf_cost_model, mu: float, min_initial_version: int, instances, trajectories):
+    """sf_route on objects with version/running/waiting/kv (instances) and
+    version (None = initial)/length (trajectories). Returns (targets, the
+    updated instances as sf_instance_state)."""
+    ni, nt = len(instances), len(trajectories)
+    inst = (sf_instance_state * max(1, ni))()
+    for i, s in enumerate(instances):
+        inst[i] = sf_instance_state(int(s.version), int(s.running), int(s.waiting), 0, float(s.kv))
+    tr = (sf_trajectory * max(1, nt))()
+    for j, t in enumerate(trajectories):
+        tr[j] = sf_trajectory(-1 if t.version is None else int(t.version), 0, float(t.length))
+    target = np.full(max(1, nt), -1, dtype=np.int32)
+    routed = ctypes.c_int32()
+    _check("sf_route", lib().sf_route(ctypes.byref(model), float(mu), int(min_initial_version), inst, ni, tr, nt,
+                                      target.ctypes.data, ctypes.byref(routed)))
+    after = [_InstanceView(inst[i]) for i in range(ni)]
+    return target[:nt].tolist(), after
+
+
+class _InstanceView:
+    def __init__(self, s: sf_instance_state):
+        self.version, self.running, self.waiting, self.kv = s.version, s.num_running, s.num_waiting, s.kv_cache
 
 
 def sf_decode_attn_combine(desc, info, work_dev, workspace, out, lse=None, stream=None):

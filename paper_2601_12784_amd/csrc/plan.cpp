@@ -18,6 +18,8 @@
 static_assert(sizeof(sf_attn_desc) == 32, "sf_attn_desc layout is part of the ABI");
 static_assert(sizeof(sf_plan_opts) == 20, "sf_plan_opts layout is part of the ABI");
 static_assert(sizeof(sf_plan_info) == 48, "sf_plan_info layout is part of the ABI");
+static_assert(sizeof(sf_cost_model) == 48 && sizeof(sf_instance_state) == 24 && sizeof(sf_trajectory) == 16,
+              "cost-model structs are part of the ABI");
 
 namespace sf {
 
