@@ -174,8 +174,10 @@ def calibrate_k1(batch_sizes=(64, 96, 128, 192, 256), reps=60):
     y = np.array([p[1] for p in points], dtype=np.float64)
     k1, c = np.polyfit(x, y, 1)
     r2 = 1.0 - float(((y - (k1 * x + c)) ** 2).sum() / ((y - y.mean()) ** 2).sum())
+    max_rel = float(np.max(np.abs(k1 * x + c - y) / y))
     return {"fit": "decode-step latency = k1 * kv_bytes + c (App. B.1 attention term)",
             "k1_s_per_byte": float(k1), "c_us": round(float(c) * 1e6, 2), "r2": round(r2, 5),
+            "max_rel_err": round(max_rel, 4),
             "points_bytes_us": [[int(a), round(float(t) * 1e6, 2)] for a, t in points],
             "effective_gb_s": round(1e-9 / float(k1), 1),
             "k1_s_per_token_qwen3_30b_a3b": float(k1) * QWEN3_30B_A3B_KV_BYTES_PER_TOKEN,
