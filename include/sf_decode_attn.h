@@ -199,6 +199,71 @@ sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* in
                                 float* lse, void* workspace, uint64_t workspace_bytes, void* stream);
 
 /*
+ * Extend (re-prefill) attention. A trajectory interrupted for a model update
+ * or migrated to another instance has its KV cache recomputed before its
+ * generation resumes (partial rollout and migration, Sec. 2.3; prefill and
+ * re-prefill are the second largest share of rollout time, Table
+ * "time_breakdown"). Such a pass appends E_s = q_lens[s] new tokens to
+ * sequence s, which then holds L_s = seq_lens[s] tokens in the pool: a prefix
+ * of P_s = L_s - E_s tokens cached before (0 for a full re-prefill) and the
+ * new tokens at positions P_s .. L_s - 1. New token j of sequence s has query
+ * row r = cu_s + j, cu_s = E_0 + ... + E_{s-1}, and attends causally:
+ *
+ *   z_t      = softmax_scale * sum_d q[r,h,d] * K_s[t,d]     t = 0 .. P_s + j
+ *   out[r,h] = sum_t exp(z_t) V_s[t] / sum_t exp(z_t)
+ *   lse[r,h] = ln sum_t exp(z_t)
+ *
+ * Layouts: q bf16 [T][Hq][D], out fp32 [T][Hq][D], lse fp32 [T][Hq] (optional),
+ * T = sum_s E_s; k_new and v_new bf16 [T][Hkv][D] (the new tokens' keys and
+ * values, optional); pools and block table as for a decode step. Block-table
+ * entries 0 .. ceil(L_s / 16) - 1 of every sequence with E_s > 0 are read.
+ */
+typedef struct sf_extend_info {
+  int32_t num_items;        /* work items (thread blocks of 256) */
+  int32_t tokens_per_item;  /* new tokens per item: floor(256 / g) */
+  int32_t num_q_rows;       /* T */
+  int32_t reserved;         /* 0 */
+  uint64_t work_bytes;      /* num_items * 32 */
+  uint64_t desc_key;        /* fingerprint of the descriptor */
+} sf_extend_info;
+
+/*
+ * Builds the extend work list on the host (no device calls).
+ *
+ * Rule: each sequence's new tokens are cut into blocks of n = floor(256 / g)
+ * (the last block shorter), and each (sequence, KV head, block) is one item,
+ * whose rows are the block's tokens times the group's g query heads. An item
+ * whose block starts at new token t0 with nt tokens reads the keys
+ * [0, P_s + t0 + nt), i.e. steps = ceil((P_s + t0 + nt) / 32) blocks of 32
+ * keys. Items are ordered by steps, largest first; equal steps keep the
+ * order (sequence, KV head, t0) ascending.
+ * Work list, int32 rows of 8: seq, kv_head, t0, nt, P_s, cu_s, steps, 0.
+ * Lengths must satisfy 0 <= E_s <= L_s <= 16 * block_table_stride.
+ * work_host NULL only reports the sizes in *info; SF_ERR_CAPACITY if
+ * work_capacity_bytes < info->work_bytes.
+ */
+sf_status sf_extend_attn_plan(const sf_attn_desc* desc, const int32_t* seq_lens_host,
+                              const int32_t* q_lens_host, int32_t* work_host,
+                              uint64_t work_capacity_bytes, sf_extend_info* info);
+
+/*
+ * Enqueues extend attention on the stream. If work_host is not NULL its
+ * info->work_bytes are first copied to work_dev (as for sf_decode_attn). If
+ * k_new and v_new are not NULL, a first launch stores every new token's keys
+ * and values into the pool, at slot p % 16 of page block_table[s][p / 16]
+ * for position p = P_s + j, before the attention reads them; the pools are
+ * then written, and the block table must already hold every page the new
+ * tokens land in. With both NULL the pool must already hold them. One
+ * launch of the attention kernel follows (one 256-thread block per item).
+ * Errors as sf_decode_attn; SF_ERR_INVALID_ARG also if only one of k_new and
+ * v_new is given, or either is not 16-byte aligned.
+ */
+sf_status sf_extend_attn(const sf_attn_desc* desc, const sf_extend_info* info, const int32_t* work_host,
+                         int32_t* work_dev, const void* q, const void* k_new, const void* v_new,
+                         void* k_pool, void* v_pool, const int32_t* block_table, float* out,
+                         float* lse, void* stream);
+
+/*
  * Host page allocator for the KV pool. A trajectory's cache grows by one
  * 16-token page at a time and is released when it leaves, within a pool of
  * fixed size (the KV-cache budget of Sec. 5.2). Pages are ids 0 .. N-1 of

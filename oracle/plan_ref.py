@@ -103,3 +103,26 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
                 chunk_pages=_ceil(total, workers) if workers and total else 0,
                 num_partials=slot, workspace_bytes=ws,
                 work_bytes=(table.shape[0] + items.shape[0] + comb.shape[0]) * 8 * 4)
+
+
+def extend_plan(seq_lens, q_lens, num_kv_heads, num_q_heads, rows_per_item=256):
+    """The extend work list, re-derived from its rule: new tokens cut into
+    blocks of floor(256 / g) per (sequence, KV head); an item starting at new
+    token t0 with nt tokens reads ceil((P_s + t0 + nt) / 32) blocks of 32
+    keys; items by that count, largest first, ties in (s, kvh, t0) order.
+    Rows: (seq, kv_head, t0, nt, P_s, cu_s, steps, 0)."""
+    g = num_q_heads // num_kv_heads
+    n = rows_per_item // g
+    items = []
+    cu = 0
+    for s, (L, e) in enumerate(zip(seq_lens, q_lens)):
+        L, e = int(L), int(e)
+        prefix = L - e
+        for kvh in range(num_kv_heads):
+            for t0 in range(0, e, n):
+                nt = min(n, e - t0)
+                steps = _ceil(prefix + t0 + nt, 2 * PAGE)
+                items.append((-steps, s, kvh, t0, (s, kvh, t0, nt, prefix, cu, steps, 0)))
+        cu += e
+    items.sort(key=lambda x: x[:4])
+    return np.array([it[4] for it in items], dtype=np.int32).reshape(-1, 8), n

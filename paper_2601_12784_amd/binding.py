@@ -51,6 +51,12 @@ class sf_plan_info(ctypes.Structure):
                 ("desc_key", ctypes.c_uint64)]
 
 
+class sf_extend_info(ctypes.Structure):
+    _fields_ = [("num_items", ctypes.c_int32), ("tokens_per_item", ctypes.c_int32),
+                ("num_q_rows", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("work_bytes", ctypes.c_uint64), ("desc_key", ctypes.c_uint64)]
+
+
 class sf_cost_model(ctypes.Structure):
     _fields_ = [("k1", ctypes.c_double), ("k2", ctypes.c_double), ("k3", ctypes.c_double),
                 ("k4", ctypes.c_double), ("k5", ctypes.c_double), ("kv_budget", ctypes.c_double)]
@@ -88,6 +94,8 @@ def lib():
                                      ctypes.c_int32, vp, vp, vp]
     L.sf_decode_attn_append.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp,
                                         vp, vp, vp, vp, ctypes.c_uint64, vp]
+    L.sf_extend_attn_plan.argtypes = [P(sf_attn_desc), vp, vp, vp, ctypes.c_uint64, P(sf_extend_info)]
+    L.sf_extend_attn.argtypes = [P(sf_attn_desc), P(sf_extend_info), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sf_page_pool_create.argtypes = [ctypes.c_int32, P(vp)]
     L.sf_page_pool_destroy.argtypes = [vp]
     L.sf_page_pool_destroy.restype = None
@@ -106,7 +114,8 @@ def lib():
                            ctypes.c_int32, vp, P(ctypes.c_int32)]
     for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv",
                "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
-               "sf_page_pool_release", "sf_page_table_step", "sf_route"):
+               "sf_page_pool_release", "sf_page_table_step", "sf_route", "sf_extend_attn_plan",
+               "sf_extend_attn"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -262,6 +271,94 @@ def sf_decode_attn_append(desc, info, work_host, work_dev, q, k_new, v_new, new_
         ctypes.byref(desc), ctypes.byref(info), _addr(work_host), _addr(work_dev), _addr(q), _addr(k_new),
         _addr(v_new), _addr(new_pages), _addr(k_pool), _addr(v_pool), _addr(block_table), _addr(out),
         _addr(lse), _addr(workspace), ws_bytes, _stream(stream)))
+
+
+def sf_extend_attn_plan(desc: sf_attn_desc, seq_lens, q_lens, work_host=None):
+    """Plans extend attention on the host. seq_lens (L_s, new tokens
+    included) and q_lens (E_s): int32 host arrays. Returns (info, work_host)."""
+    lens = np.ascontiguousarray(np.asarray(seq_lens), dtype=np.int32)
+    qls = np.ascontiguousarray(np.asarray(q_lens), dtype=np.int32)
+    if lens.shape != (desc.num_seqs,) or qls.shape != (desc.num_seqs,):
+        raise ValueError("seq_lens and q_lens must have num_seqs entries")
+    info = sf_extend_info()
+    L = lib()
+    if work_host is None:
+        _check("sf_extend_attn_plan", L.sf_extend_attn_plan(ctypes.byref(desc), lens.ctypes.data, qls.ctypes.data,
+                                                            None, 0, ctypes.byref(info)))
+        work_host = np.empty(max(1, info.work_bytes // 4), dtype=np.int32)
+    cap = work_host.numel() * 4 if isinstance(work_host, torch.Tensor) else work_host.nbytes
+    _check("sf_extend_attn_plan", L.sf_extend_attn_plan(ctypes.byref(desc), lens.ctypes.data, qls.ctypes.data,
+                                                        _addr(work_host), cap, ctypes.byref(info)))
+    return info, work_host
+
+
+def sf_extend_attn(desc, info, work_host, work_dev, q, k_pool, v_pool, block_table, out, lse=None,
+                   k_new=None, v_new=None, stream=None):
+    """Enqueues extend attention (after the store of k_new / v_new into the
+    pools when both are given). q, out: [T, Hq, D]; k_new, v_new: [T, Hkv, D]."""
+    t, hq, hkv, d = info.num_q_rows, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
+    _dev(q, "q", torch.bfloat16, (t, hq, d))
+    _dev(k_pool, "k_pool", torch.bfloat16, (desc.num_pages, hkv, d // 8, PAGE, 8))
+    _dev(v_pool, "v_pool", torch.bfloat16, (desc.num_pages, hkv, d, PAGE))
+    _dev(block_table, "block_table", torch.int32, (desc.num_seqs, desc.block_table_stride))
+    _dev(out, "out", torch.float32, (t, hq, d))
+    _dev(work_dev, "work_dev", torch.int32)
+    if work_dev.numel() * 4 < info.work_bytes:
+        raise ValueError("work_dev is smaller than the plan")
+    if lse is not None:
+        _dev(lse, "lse", torch.float32, (t, hq))
+    if (k_new is None) != (v_new is None):
+        raise ValueError("give both k_new and v_new, or neither")
+    if k_new is not None:
+        _dev(k_new, "k_new", torch.bfloat16, (t, hkv, d))
+        _dev(v_new, "v_new", torch.bfloat16, (t, hkv, d))
+    _check("sf_extend_attn", lib().sf_extend_attn(
+        ctypes.byref(desc), ctypes.byref(info), _addr(work_host), _addr(work_dev), _addr(q), _addr(k_new),
+        _addr(v_new), _addr(k_pool), _addr(v_pool), _addr(block_table), _addr(out), _addr(lse),
+        _stream(stream)))
+
+
+class ExtendAttention:
+    """Plans and launches extend attention for one batch of re-prefills.
+
+    The work list is planned on the host at each call, written into a pinned
+    buffer and uploaded with the launch; everything else runs in the
+    library's kernels. Before the pinned buffer is rewritten, the call waits
+    for the event recorded after the previous upload, so a queued copy never
+    reads a half-written list."""
+
+    def __init__(self, num_q_heads, num_kv_heads, head_dim, device=None):
+        self.hq, self.hkv, self.d = int(num_q_heads), int(num_kv_heads), int(head_dim)
+        self.device = torch.device("cuda") if device is None else torch.device(device)
+        self._work_host = None
+        self._work_dev = None
+        self._uploaded = None
+        self.last_info = None
+
+    def __call__(self, q, k_pool, v_pool, block_table, seq_lens, q_lens, scale, out=None, lse=None,
+                 k_new=None, v_new=None, stream=None):
+        lens = np.ascontiguousarray(np.asarray(seq_lens), dtype=np.int32)
+        qls = np.ascontiguousarray(np.asarray(q_lens), dtype=np.int32)
+        desc = make_desc(lens.size, self.hq, self.hkv, self.d, block_table.shape[1], k_pool.shape[0], scale)
+        info = sf_extend_info()
+        _check("sf_extend_attn_plan", lib().sf_extend_attn_plan(ctypes.byref(desc), lens.ctypes.data,
+                                                                qls.ctypes.data, None, 0, ctypes.byref(info)))
+        need = max(8, int(info.work_bytes) // 4)
+        if self._uploaded is not None:
+            self._uploaded.synchronize()
+        if self._work_host is None or self._work_host.numel() < need:
+            self._work_host = torch.empty(need, dtype=torch.int32, pin_memory=True)
+            self._work_dev = torch.empty(need, dtype=torch.int32, device=self.device)
+        info, _ = sf_extend_attn_plan(desc, lens, qls, work_host=self._work_host)
+        if out is None:
+            out = torch.empty((info.num_q_rows, self.hq, self.d), dtype=torch.float32, device=self.device)
+        sf_extend_attn(desc, info, self._work_host, self._work_dev, q, k_pool, v_pool, block_table, out, lse,
+                       k_new=k_new, v_new=v_new, stream=stream)
+        ev = torch.cuda.Event()
+        ev.record(stream if isinstance(stream, torch.cuda.Stream) else torch.cuda.current_stream())
+        self._uploaded = ev
+        self.last_info = info
+        return out
 
 
 class PagePool:

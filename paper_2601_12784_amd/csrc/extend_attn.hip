@@ -1,0 +1,346 @@
+// gfx950 kernels for extend (re-prefill) attention over the paged KV cache.
+//
+// A trajectory resumed on an instance after an interrupt or a migration has
+// its KV cache recomputed before decoding goes on (partial rollout and
+// migration, Sec. 2.3; the prefill share of rollout time is in Table
+// "time_breakdown"). Such a pass appends E new tokens to a sequence whose
+// cache already holds P tokens (P = 0 for a full re-prefill); new token j, at
+// position P + j, attends causally to positions 0 .. P + j.
+//
+// Unlike a decode step this is a dense contraction: every key tile is used by
+// all new tokens after it, so the work runs on the matrix cores. A work item
+// is one (sequence, KV head, block of new tokens); its rows are the block's
+// tokens times the g query heads of the group (token-major), at most 256 rows,
+// 64 per wave. The item walks the keys 32 at a time (two pages): the four
+// waves stage the two K tiles and two V tiles (16 KiB at D = 128) through LDS,
+// double buffered, and each wave computes, per 16-row tile,
+//
+//   S^T[32 keys][16 rows] = K Q^T        2 x (D/32) v_mfma_f32_16x16x32_bf16
+//   online softmax in base 2             (row = lane column; max over the four 16-lane groups)
+//   O^T[D][16 rows]      += V^T P^T      (D/16) MFMAs, P rounded to bf16
+//
+// with each K and V operand read from LDS once per wave and used for all
+// four row tiles. The operand mapping is the decode kernel's: each lane's
+// eight scores are keys 4*grp .. 4*grp+3 of both pages, the eight P^T values
+// its P.V operand needs.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sf_internal.h"
+
+namespace sf {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(4))) const int32_t* const_i32_ptr;
+
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr int kThreads = 256;     // four waves
+constexpr int kRowTiles = 4;      // 16-row MFMA tiles per wave
+constexpr int kStepKeys = 2 * kPage;
+
+__device__ __forceinline__ const_i32_ptr as_constant(const int32_t* p) { return (const_i32_ptr)(p); }
+
+__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return uint32_t(__builtin_bit_cast(uint16_t, static_cast<__bf16>(lo))) |
+         (uint32_t(__builtin_bit_cast(uint16_t, static_cast<__bf16>(hi))) << 16);
+}
+
+// Element offset of a (page, KV head) tile in either pool.
+__device__ __forceinline__ size_t tile_base(int32_t page, int32_t num_kv_heads, int32_t kvh, int d) {
+  return (size_t(page) * num_kv_heads + kvh) * size_t(kPage * d);
+}
+
+template <int D>
+struct Tiles {
+  static constexpr int kElems = kPage * D;            // bf16 per (page, KV head) tile
+  static constexpr int kChunks = kElems / 8;          // 16-byte pieces per tile
+  static constexpr int kLoads = 4 * kChunks / kThreads;  // pieces per thread per step
+};
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
+  constexpr int KB = D / 32;
+  constexpr int JB = D / 16;
+  constexpr int TE = Tiles<D>::kElems;
+  constexpr int TC = Tiles<D>::kChunks;
+  constexpr int NL = Tiles<D>::kLoads;
+  // [buffer][K page 0, K page 1, V page 0, V page 1][tile]
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2][4][TE];
+
+  const const_i32_ptr item = as_constant(a.items) + size_t(blockIdx.x) * kItemInts;
+  const int seq = item[0];
+  const int kvh = item[1];
+  const int t0 = item[2];
+  const int nt = item[3];
+  const int prefix = item[4];
+  const int qrow0 = item[5];
+  const int nsteps = item[6];
+  const int g = a.group;
+  const int rows = nt * g;
+  const int kend = prefix + t0 + nt;          // keys [0, kend) are read
+  const int npages = (kend + kPage - 1) / kPage;
+  const const_i32_ptr bt = as_constant(a.block_table) + size_t(seq) * a.bt_stride;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int col = lane & 15;
+  const int grp = lane >> 4;
+
+  // Rows of this lane (one per row tile): token-major over (token, head).
+  int limit[kRowTiles];
+  u32x4 qf[kRowTiles][KB];
+#pragma unroll
+  for (int rt = 0; rt < kRowTiles; ++rt) {
+    const int r = wave * 64 + rt * 16 + col;
+    const bool valid = r < rows;
+    const int tok = valid ? r / g : 0;
+    const int hh = valid ? r - tok * g : 0;
+    // Padding rows see every key with a zero query: finite, never stored.
+    limit[rt] = valid ? prefix + t0 + tok : kend - 1;
+    const uint16_t* qrow = a.q + (size_t(qrow0 + t0 + tok) * a.num_q_heads + kvh * g + hh) * D + 8 * grp;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(qrow + 32 * kb) ^ a.q_sign;
+      qf[rt][kb] = valid ? v : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  const int wrow0 = wave * 64;
+  const int wrow1 = min(rows, wrow0 + 64) - 1;       // last valid row of the wave
+  const int wave_kmin = prefix + t0 + wrow0 / g;     // every row of the wave sees keys <= this
+  const int wave_kmax = wrow1 >= wrow0 ? prefix + t0 + wrow1 / g : -1;
+
+  f32x4 o[kRowTiles][JB];
+  float m[kRowTiles], lsum[kRowTiles];
+#pragma unroll
+  for (int rt = 0; rt < kRowTiles; ++rt) {
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) o[rt][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m[rt] = -__builtin_inff();
+    lsum[rt] = 0.f;
+  }
+
+  // Staging: thread tid moves pieces tid, tid + 256, ... of the step's four
+  // tiles. A page past the item's last is replaced by its first page (always
+  // in range); its keys lie past kend and are masked.
+  u32x4 pre[NL];
+  auto fetch = [&](int j) {
+    const int pg0 = 2 * j;
+    const int p0 = bt[pg0];
+    const int p1 = pg0 + 1 < npages ? bt[pg0 + 1] : p0;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int piece = tid + i * kThreads;
+      const int tile = piece / TC;
+      const int off = (piece % TC) * 8;
+      const uint16_t* pool = tile < 2 ? a.k_pool : a.v_pool;
+      const int page = (tile & 1) ? p1 : p0;
+      pre[i] = *reinterpret_cast<const u32x4*>(pool + tile_base(page, a.num_kv_heads, kvh, D) + off);
+    }
+  };
+  auto stage = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int piece = tid + i * kThreads;
+      *reinterpret_cast<u32x4*>(&lds[buf][piece / TC][(piece % TC) * 8]) = pre[i];
+    }
+  };
+
+  fetch(0);
+  stage(0);
+  __syncthreads();
+
+  for (int j = 0; j < nsteps; ++j) {
+    const int buf = j & 1;
+    if (j + 1 < nsteps) fetch(j + 1);
+    const int key0 = j * kStepKeys;
+    if (key0 <= wave_kmax) {
+      // Scores S^T: lane holds row `col`, keys key0 + 4*grp + e (page 0) and +16 (page 1).
+      f32x4 s[2][kRowTiles];
+#pragma unroll
+      for (int rt = 0; rt < kRowTiles; ++rt) {
+        s[0][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        s[1][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const int ko = ((4 * kb + grp) * kPage + col) * 8;
+        const u32x4 k0 = *reinterpret_cast<const u32x4*>(&lds[buf][0][ko]);
+        const u32x4 k1 = *reinterpret_cast<const u32x4*>(&lds[buf][1][ko]);
+#pragma unroll
+        for (int rt = 0; rt < kRowTiles; ++rt) {
+          s[0][rt] = mfma_bf16(k0, qf[rt][kb], s[0][rt]);
+          s[1][rt] = mfma_bf16(k1, qf[rt][kb], s[1][rt]);
+        }
+      }
+      const bool masked = key0 + kStepKeys - 1 > wave_kmin;
+      u32x4 pf[kRowTiles];
+#pragma unroll
+      for (int rt = 0; rt < kRowTiles; ++rt) {
+        float sc[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          sc[e] = s[0][rt][e];
+          sc[4 + e] = s[1][rt][e];
+        }
+        bool ok[8];
+        if (masked) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            ok[e] = key0 + (e < 4 ? 0 : kPage) + 4 * grp + (e & 3) <= limit[rt];
+            sc[e] = ok[e] ? sc[e] : -__builtin_inff();
+          }
+        }
+        // The scale is >= 0 here (the host flips the query's sign for a
+        // negative one), so the row max of the raw scores gives the max of
+        // the scaled ones.
+        float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                         fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        // Key 0 is in every row's first step, so mnew is finite from then on
+        // (fmaxf drops the NaN of -inf * 0 for a zero scale).
+        const float mnew = fmaxf(m[rt], mx * a.scale_log2);
+        const float alpha = __builtin_amdgcn_exp2f(m[rt] - mnew);
+        m[rt] = mnew;
+        float p[8];
+        float ps = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], a.scale_log2, -mnew));
+          if (masked) p[e] = ok[e] ? p[e] : 0.f;
+          ps += p[e];
+        }
+        lsum[rt] = lsum[rt] * alpha + ps;
+        pf[rt] = u32x4{pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3]), pack_bf16(p[4], p[5]),
+                       pack_bf16(p[6], p[7])};
+        if (__any(alpha != 1.f)) {
+#pragma unroll
+          for (int jb = 0; jb < JB; ++jb) o[rt][jb] *= alpha;
+        }
+      }
+      // Keys at or past kend may be stale or NaN in V: zero them (a zero
+      // weight times NaN would still be NaN).
+      u32x4 vmask = u32x4{~0u, ~0u, ~0u, ~0u};
+      if (key0 + kStepKeys > kend) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kl = key0 + (i < 2 ? 0 : kPage) + 4 * grp + 2 * (i & 1);
+          vmask[i] = (kl < kend ? 0x0000FFFFu : 0u) | (kl + 1 < kend ? 0xFFFF0000u : 0u);
+        }
+      }
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb) {
+        const int vo = (16 * jb + col) * kPage + 4 * grp;
+        const u32x2 v0 = *reinterpret_cast<const u32x2*>(&lds[buf][2][vo]);
+        const u32x2 v1 = *reinterpret_cast<const u32x2*>(&lds[buf][3][vo]);
+        const u32x4 vf = u32x4{v0[0], v0[1], v1[0], v1[1]} & vmask;
+#pragma unroll
+        for (int rt = 0; rt < kRowTiles; ++rt) o[rt][jb] = mfma_bf16(vf, pf[rt], o[rt][jb]);
+      }
+    }
+    if (j + 1 < nsteps) stage(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Lane holds O[row col][16*jb + 4*grp + i] of each row tile.
+#pragma unroll
+  for (int rt = 0; rt < kRowTiles; ++rt) {
+    float lt = lsum[rt] + __shfl_xor(lsum[rt], 16);
+    lt += __shfl_xor(lt, 32);
+    const int r = wave * 64 + rt * 16 + col;
+    if (r >= rows) continue;
+    const int tok = r / g;
+    const int head = kvh * g + (r - tok * g);
+    const size_t orow = size_t(qrow0 + t0 + tok) * a.num_q_heads + head;
+    const float inv = 1.f / lt;
+    float* dst = a.out + orow * D + 4 * grp;
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = o[rt][jb] * inv;
+    if (a.lse && grp == 0) a.lse[orow] = (m[rt] + __log2f(lt)) * kLn2;
+  }
+}
+
+// Stores the new tokens' keys and values of one item (one sequence and KV
+// head, tokens t0 .. t0 + nt - 1) into their page slots. Keys: one 16-byte
+// piece per (token, 8 dims). Values: one thread per (page, dim) writes the
+// 16 slots of a page it fills completely as two 16-byte stores, else slot by
+// slot.
+template <int D>
+__global__ __launch_bounds__(kThreads) void kv_store_kernel(ExtendArgs a) {
+  const const_i32_ptr item = as_constant(a.items) + size_t(blockIdx.x) * kItemInts;
+  const int seq = item[0];
+  const int kvh = item[1];
+  const int t0 = item[2];
+  const int nt = item[3];
+  const int prefix = item[4];
+  const int qrow0 = item[5];
+  const const_i32_ptr bt = as_constant(a.block_table) + size_t(seq) * a.bt_stride;
+  const int first = prefix + t0;   // position of the item's first token
+  const size_t row_stride = size_t(a.num_kv_heads) * D;
+  const uint16_t* kn = a.k_new + size_t(qrow0 + t0) * row_stride + size_t(kvh) * D;
+  const uint16_t* vn = a.v_new + size_t(qrow0 + t0) * row_stride + size_t(kvh) * D;
+
+  for (int i = threadIdx.x; i < nt * (D / 8); i += kThreads) {
+    const int t = i / (D / 8);
+    const int c = i - t * (D / 8);
+    const int pos = first + t;
+    const int page = bt[pos / kPage];
+    uint16_t* dst = a.k_dst + tile_base(page, a.num_kv_heads, kvh, D) + ((c * kPage) + pos % kPage) * 8;
+    *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(kn + size_t(t) * row_stride + 8 * c);
+  }
+
+  const int pg_a = first / kPage;
+  const int pg_b = (first + nt - 1) / kPage;
+  for (int i = threadIdx.x; i < (pg_b - pg_a + 1) * D; i += kThreads) {
+    const int pg = pg_a + i / D;
+    const int dim = i % D;
+    const int lo = max(first, pg * kPage);
+    const int hi = min(first + nt, (pg + 1) * kPage);
+    uint16_t* dst = a.v_dst + tile_base(bt[pg], a.num_kv_heads, kvh, D) + dim * kPage;
+    if (hi - lo == kPage) {
+      uint32_t w[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const uint32_t x = vn[size_t(lo + 2 * s - first) * row_stride + dim];
+        const uint32_t y = vn[size_t(lo + 2 * s + 1 - first) * row_stride + dim];
+        w[s] = x | (y << 16);
+      }
+      reinterpret_cast<u32x4*>(dst)[0] = u32x4{w[0], w[1], w[2], w[3]};
+      reinterpret_cast<u32x4*>(dst)[1] = u32x4{w[4], w[5], w[6], w[7]};
+    } else {
+      for (int pos = lo; pos < hi; ++pos) dst[pos % kPage] = vn[size_t(pos - first) * row_stride + dim];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream) {
+  if (a.num_items == 0) return hipSuccess;
+  const dim3 grid(a.num_items), block(kThreads);
+  if (a.k_new) {
+    if (a.head_dim == 128)
+      hipLaunchKernelGGL(kv_store_kernel<128>, grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL(kv_store_kernel<64>, grid, block, 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL(extend_attn_kernel<128>, grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(extend_attn_kernel<64>, grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace sf

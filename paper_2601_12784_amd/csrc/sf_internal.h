@@ -97,7 +97,35 @@ struct GatherArgs {
   int32_t bt_stride;
 };
 
+// Extend (re-prefill) attention and the store of the new tokens.
+struct ExtendArgs {
+  const int32_t* items;       // rows: seq, kv_head, t0, nt, prefix, q_row0, key steps, 0
+  int32_t num_items;
+  const uint16_t* q;          // [T][Hq][D]
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_table;
+  float* out;                 // [T][Hq][D]
+  float* lse;                 // [T][Hq] or NULL
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;
+  int32_t head_dim;
+  int32_t bt_stride;
+  float scale_log2;           // |softmax_scale| * log2(e)
+  uint32_t q_sign;            // 0x80008000 for a negative scale: query bf16 sign flips
+  // Store launch first when k_new is not NULL.
+  const uint16_t* k_new;      // [T][Hkv][D]
+  const uint16_t* v_new;
+  uint16_t* k_dst;            // the pools, writable
+  uint16_t* v_dst;
+};
+
+// Rows (tokens x query heads of a group) of one extend work item.
+constexpr int kExtendRows = 256;
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
 

@@ -343,3 +343,82 @@ def make_decode_loop(seed: int | None = None, steps: int = STRAGGLER_STEPS, pois
     k_new = _fill_normal(ss[3], n, 1.0).view(*shape)
     v_new = _fill_normal(ss[4], n, 1.0).view(*shape)
     return DecodeLoop(base=base, caps=caps, steps=steps, q_all=q_all, k_new=k_new, v_new=v_new)
+
+
+# ----------------------------------------------------------------------------
+# extend (re-prefill) batches
+# ----------------------------------------------------------------------------
+@dataclass
+class ExtendBatch:
+    """Extend attention input: every sequence's cache holds L_s tokens, the
+    last E_s of which are new (positions L_s - E_s .. L_s - 1; query rows in
+    sequence order). The pools already hold the new tokens; k_new and v_new
+    are those same keys and values ([T, Hkv, D]) for the store path."""
+    batch: Batch
+    q_lens: np.ndarray            # int32 [B]
+    q: torch.Tensor               # bf16 [T, Hq, D]
+    k_new: torch.Tensor           # bf16 [T, Hkv, D]
+    v_new: torch.Tensor
+
+    @property
+    def num_rows(self) -> int:
+        return int(self.q_lens.sum())
+
+    def slots(self):
+        """(page, slot) of every new token, in row order."""
+        pages, slots = [], []
+        for s, (L, e) in enumerate(zip(self.batch.seq_lens, self.q_lens)):
+            pos = np.arange(int(L) - int(e), int(L))
+            pages.append(self.batch.block_table[s, pos // PAGE])
+            slots.append(pos % PAGE)
+        if not pages:
+            return np.zeros(0, np.int64), np.zeros(0, np.int64)
+        return np.concatenate(pages).astype(np.int64), np.concatenate(slots).astype(np.int64)
+
+    def causal_flops(self) -> int:
+        """Multiply-adds x 2 of the causal QK^T and PV products: each new
+        token at position p pairs with p + 1 keys, 4*D flops per pair and head."""
+        tot = 0
+        for L, e in zip(self.batch.seq_lens.astype(np.int64), self.q_lens.astype(np.int64)):
+            p0 = L - e
+            tot += int(e * (p0 + 1) + e * (e - 1) // 2)
+        return tot * self.batch.num_q_heads * 4 * self.batch.head_dim
+
+
+def build_extend(lens, q_lens, num_q_heads, num_kv_heads, head_dim, seed, *, name="extend",
+                 poison=True, rng=None, pool_pages=None, k_mult=1.0) -> ExtendBatch:
+    """Pools as build_batch() for the full lengths, queries for every new
+    token from SeedSequence(seed).spawn(6)[5], and the new tokens' keys and
+    values copied out of the pools."""
+    lens = np.asarray(lens, dtype=np.int64)
+    q_lens = np.asarray(q_lens, dtype=np.int64)
+    assert q_lens.shape == lens.shape and np.all(q_lens >= 0) and np.all(q_lens <= lens)
+    b = build_batch(lens, num_q_heads, num_kv_heads, head_dim, seed, name=name, poison=poison, rng=rng,
+                    pool_pages=pool_pages, k_mult=k_mult)
+    t = int(q_lens.sum())
+    ss = np.random.SeedSequence(seed).spawn(6)[5]
+    q = _fill_normal(ss, t * num_q_heads * head_dim, 1.0).view(t, num_q_heads, head_dim)
+    eb = ExtendBatch(batch=b, q_lens=q_lens.astype(np.int32), q=q, k_new=None, v_new=None)
+    pages, slots = eb.slots()
+    kp = b.k_pool.view(torch.int16).numpy()
+    vp = b.v_pool.view(torch.int16).numpy()
+    kn = kp[pages, :, :, slots, :].reshape(t, num_kv_heads, head_dim)   # [T, Hkv, D/8, 8] -> [T, Hkv, D]
+    vn = vp[pages, :, :, slots].reshape(t, num_kv_heads, head_dim)
+    eb.k_new = torch.from_numpy(np.ascontiguousarray(kn)).view(torch.bfloat16)
+    eb.v_new = torch.from_numpy(np.ascontiguousarray(vn)).view(torch.bfloat16)
+    return eb
+
+
+REPREFILL = dict(num_seqs=32, num_q_heads=28, num_kv_heads=4, head_dim=128)
+
+
+def make_reprefill(seed: int | None = None, poison: bool = True, num_seqs=None) -> ExtendBatch:
+    """Full re-prefill of resumed trajectories: 32 sequences with the long-tail
+    lengths (lognormal, median 2048, sigma 1.0, clipped to [256, 16384]), every
+    token new (E_s = L_s), 28 query / 4 KV heads, head_dim 128."""
+    seed = 1000 + 5 if seed is None else seed
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n = REPREFILL["num_seqs"] if num_seqs is None else num_seqs
+    lens = _lognormal_lengths(rng, n, 2048, 1.0, 256, 16384)
+    return build_extend(lens, lens, REPREFILL["num_q_heads"], REPREFILL["num_kv_heads"], REPREFILL["head_dim"],
+                        seed, name="reprefill", poison=poison, rng=rng)
