@@ -215,6 +215,54 @@ def routing_demo(k1_per_token, mu=0.3, seed=0):
             "sf_route_us": round(us, 1)}
 
 
+EXTEND_KERNEL = "extend_attn_kernel<128>"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
+
+
+def reprefill_bench(reps=20, warmup=5):
+    """Extend attention on the 32-sequence full re-prefill: the work list is
+    planned and uploaded once, then `reps` attention launches are timed with
+    HIP events on their stream. Algorithmic flops count the causal pairs only
+    (4 * D per query head and pair)."""
+    import torch
+    from paper_2601_12784_amd import binding as B
+    from paper_2601_12784_amd.workloads import make_reprefill
+    eb = make_reprefill(poison=False)
+    b = eb.batch
+    desc = B.make_desc(b.num_seqs, b.num_q_heads, b.num_kv_heads, b.head_dim, b.block_table.shape[1],
+                       b.num_pages, b.scale)
+    t0 = time.perf_counter()
+    info, work = B.sf_extend_attn_plan(desc, b.seq_lens, eb.q_lens)
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    work_dev = torch.from_numpy(np.ascontiguousarray(work)).cuda()
+    q, kp, vp = eb.q.cuda(), b.k_pool.cuda(), b.v_pool.cuda()
+    bt = torch.from_numpy(b.block_table).cuda()
+    out = torch.empty((eb.num_rows, b.num_q_heads, b.head_dim), dtype=torch.float32, device="cuda")
+    lse = torch.empty((eb.num_rows, b.num_q_heads), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for _ in range(warmup):
+            B.sf_extend_attn(desc, info, None, work_dev, q, kp, vp, bt, out, lse, stream=stream)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, z in evs:
+            a.record(stream)
+            B.sf_extend_attn(desc, info, None, work_dev, q, kp, vp, bt, out, lse, stream=stream)
+            z.record(stream)
+    torch.cuda.synchronize()
+    ms = [a.elapsed_time(z) for a, z in evs]
+    mean_ms = float(np.mean(ms))
+    flops = eb.causal_flops()
+    tflops = flops / (mean_ms * 1e-3) / 1e12
+    return {"workload": "full re-prefill of 32 resumed trajectories: long-tail lengths (lognormal median 2048, "
+                        "sigma 1.0, clipped to [256, 16384]), every token new, 28 q / 4 kv heads, head_dim 128, "
+                        "page 16, bf16",
+            "new_tokens": eb.num_rows, "items": int(info.num_items), "causal_flops": int(flops),
+            "kernel_ms": round(mean_ms, 4), "kernel_ms_median": round(float(np.median(ms)), 4),
+            "tokens_per_s": round(eb.num_rows / (mean_ms * 1e-3), 1), "host_plan_ms": round(plan_ms, 3),
+            "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "kernel": EXTEND_KERNEL}}
+
+
 def cpu_baseline(batch, min_s=10.0, max_s=30.0):
     """The fp64 oracle, timed on the host cores over repeated passes of the
     batch (or of a prefix of it, if one pass would exceed max_s)."""
@@ -374,6 +422,8 @@ def main():
     ap.add_argument("--no-skew", action="store_true", help="skip the equal-bytes uniform batch")
     ap.add_argument("--no-loop", action="store_true", help="skip the growing-cache decode loop")
     ap.add_argument("--no-cost", action="store_true", help="skip the cost-model k1 fit")
+    ap.add_argument("--no-reprefill", action="store_true", help="skip the extend (re-prefill) leg")
+    ap.add_argument("--only-reprefill", action="store_true", help="run only the extend leg and print it")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -404,6 +454,10 @@ def main():
     if not torch.cuda.is_available():
         log("no GPU visible")
         sys.exit(1)
+
+    if args.only_reprefill:
+        print(json.dumps(reprefill_bench()), flush=True)
+        return
 
     if args.copy_probe:
         nbytes = args.copy_probe << 20
@@ -484,6 +538,13 @@ def main():
         result["cost_model"] = cm
         log(f"  k1 = {cm['k1_s_per_byte']:.3e} s/byte ({cm['effective_gb_s']} GB/s), c = {cm['c_us']} us, "
             f"r2 = {cm['r2']}")
+
+    if not args.no_reprefill:
+        log("extend attention: full re-prefill of 32 trajectories")
+        rp = reprefill_bench()
+        result["reprefill"] = rp
+        log(f"  {rp['kernel_ms']} ms per pass, {rp['roofline']['achieved']} TFLOP/s "
+            f"({100 * rp['roofline']['frac']:.1f} % of bf16 peak), {rp['tokens_per_s']:.0f} tokens/s")
 
     if not args.no_loop:
         log("growing-cache decode loop (straggler lengths, 64 steps)")

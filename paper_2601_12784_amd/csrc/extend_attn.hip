@@ -11,7 +11,7 @@
 // all new tokens after it, so the work runs on the matrix cores. A work item
 // is one (sequence, KV head, block of new tokens); its rows are the block's
 // tokens times the g query heads of the group (token-major), at most 256 rows,
-// 64 per wave. The item walks the keys 32 at a time (two pages): the four
+// 32 per wave. The item walks the keys 32 at a time (two pages): the eight
 // waves stage the two K tiles and two V tiles (16 KiB at D = 128) through LDS,
 // double buffered, and each wave computes, per 16-row tile,
 //
@@ -19,8 +19,10 @@
 //   online softmax in base 2             (row = lane column; max over the four 16-lane groups)
 //   O^T[D][16 rows]      += V^T P^T      (D/16) MFMAs, P rounded to bf16
 //
-// with each K and V operand read from LDS once per wave and used for all
-// four row tiles. The operand mapping is the decode kernel's: each lane's
+// with each K and V operand read from LDS once per wave and used for both
+// of its row tiles. (64 rows per wave would halve the LDS reads but does not
+// fit in the 256 architectural registers: the accumulators then shuttle
+// through AGPRs every step.) The operand mapping is the decode kernel's: each lane's
 // eight scores are keys 4*grp .. 4*grp+3 of both pages, the eight P^T values
 // its P.V operand needs.
 #include <hip/hip_runtime.h>
@@ -38,9 +40,12 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(4))) const int32_t* const_i32_ptr;
 
 constexpr float kLn2 = 0.69314718055994530942f;
-constexpr int kThreads = 256;     // four waves
-constexpr int kRowTiles = 4;      // 16-row MFMA tiles per wave
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRowTiles = 2;      // 16-row MFMA tiles per wave
 constexpr int kStepKeys = 2 * kPage;
+constexpr float kRescaleLog2 = 8.f;  // headroom of the lazily moved softmax reference
+static_assert(kWaves * kRowTiles * 16 == kExtendRows, "rows per item");
 
 __device__ __forceinline__ const_i32_ptr as_constant(const int32_t* p) { return (const_i32_ptr)(p); }
 
@@ -64,7 +69,63 @@ struct Tiles {
   static constexpr int kElems = kPage * D;            // bf16 per (page, KV head) tile
   static constexpr int kChunks = kElems / 8;          // 16-byte pieces per tile
   static constexpr int kLoads = 4 * kChunks / kThreads;  // pieces per thread per step
+  static_assert(kLoads * kThreads == 4 * kChunks, "staging split");
 };
+
+// Online-softmax update of one 16-row tile for one step of 32 keys. s0 / s1:
+// this lane's scores for keys key0 + 4*grp + e of the step's two pages.
+// Returns the bf16 weights as the P^T operand; rescales o, m, lsum when the
+// reference moves.
+template <int D, bool kMasked>
+__device__ __forceinline__ u32x4 softmax_tile(const f32x4& s0, const f32x4& s1, int key0, int grp, int limit,
+                                              float c, float& m, float& lsum, f32x4* o) {
+  float sc[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    sc[e] = s0[e];
+    sc[4 + e] = s1[e];
+  }
+  bool ok[8];
+  if constexpr (kMasked) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ok[e] = key0 + (e < 4 ? 0 : kPage) + 4 * grp + (e & 3) <= limit;
+      sc[e] = ok[e] ? sc[e] : -__builtin_inff();
+    }
+  }
+  // The scale c is >= 0 (the host flips the query's sign for a negative
+  // one), so the row max of the raw scores gives the max of the scaled ones.
+  float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])), fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  // Lazy rescaling: a row's reference max m moves only when the row max
+  // passes it by more than kRescaleLog2. Weights then stay below
+  // 2^kRescaleLog2, exact in fp32 with bf16's relative precision, and O and
+  // l share the reference, so O / l does not change; the rescale of the
+  // accumulators becomes rare. Key 0 is in every row's first step, so m is
+  // finite from then on (a zero scale gives NaN for a fully masked row,
+  // which compares false).
+  const float mx_s = mx * c;
+  const bool grow = mx_s > m + kRescaleLog2;
+  if (__any(grow)) {
+    const float mnew = grow ? mx_s : m;
+    const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+    m = mnew;
+    lsum *= alpha;
+#pragma unroll
+    for (int jb = 0; jb < D / 16; ++jb) o[jb] *= alpha;
+  }
+  float p[8];
+  float ps = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, -m));
+    if constexpr (kMasked) p[e] = ok[e] ? p[e] : 0.f;
+    ps += p[e];
+  }
+  lsum += ps;
+  return u32x4{pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3]), pack_bf16(p[4], p[5]), pack_bf16(p[6], p[7])};
+}
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
@@ -73,6 +134,7 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   constexpr int TE = Tiles<D>::kElems;
   constexpr int TC = Tiles<D>::kChunks;
   constexpr int NL = Tiles<D>::kLoads;
+  constexpr int kWaveRows = 16 * kRowTiles;
   // [buffer][K page 0, K page 1, V page 0, V page 1][tile]
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][4][TE];
 
@@ -89,6 +151,7 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   const int kend = prefix + t0 + nt;          // keys [0, kend) are read
   const int npages = (kend + kPage - 1) / kPage;
   const const_i32_ptr bt = as_constant(a.block_table) + size_t(seq) * a.bt_stride;
+  const float c = a.scale_log2;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -101,7 +164,7 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   u32x4 qf[kRowTiles][KB];
 #pragma unroll
   for (int rt = 0; rt < kRowTiles; ++rt) {
-    const int r = wave * 64 + rt * 16 + col;
+    const int r = wave * kWaveRows + rt * 16 + col;
     const bool valid = r < rows;
     const int tok = valid ? r / g : 0;
     const int hh = valid ? r - tok * g : 0;
@@ -114,9 +177,9 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
       qf[rt][kb] = valid ? v : u32x4{0u, 0u, 0u, 0u};
     }
   }
-  const int wrow0 = wave * 64;
-  const int wrow1 = min(rows, wrow0 + 64) - 1;       // last valid row of the wave
-  const int wave_kmin = prefix + t0 + wrow0 / g;     // every row of the wave sees keys <= this
+  const int wrow0 = wave * kWaveRows;
+  const int wrow1 = min(rows, wrow0 + kWaveRows) - 1;   // last valid row of the wave
+  const int wave_kmin = prefix + t0 + wrow0 / g;        // every row of the wave sees keys <= this
   const int wave_kmax = wrow1 >= wrow0 ? prefix + t0 + wrow1 / g : -1;
 
   f32x4 o[kRowTiles][JB];
@@ -129,9 +192,9 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
     lsum[rt] = 0.f;
   }
 
-  // Staging: thread tid moves pieces tid, tid + 256, ... of the step's four
-  // tiles. A page past the item's last is replaced by its first page (always
-  // in range); its keys lie past kend and are masked.
+  // Staging: thread tid moves pieces tid, tid + kThreads, ... of the step's
+  // four tiles. A page past the item's last is replaced by its first page
+  // (always in range); its keys lie past kend and are masked.
   u32x4 pre[NL];
   auto fetch = [&](int j) {
     const int pg0 = 2 * j;
@@ -182,51 +245,15 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
           s[1][rt] = mfma_bf16(k1, qf[rt][kb], s[1][rt]);
         }
       }
-      const bool masked = key0 + kStepKeys - 1 > wave_kmin;
       u32x4 pf[kRowTiles];
+      if (key0 + kStepKeys - 1 > wave_kmin) {
 #pragma unroll
-      for (int rt = 0; rt < kRowTiles; ++rt) {
-        float sc[8];
+        for (int rt = 0; rt < kRowTiles; ++rt)
+          pf[rt] = softmax_tile<D, true>(s[0][rt], s[1][rt], key0, grp, limit[rt], c, m[rt], lsum[rt], o[rt]);
+      } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          sc[e] = s[0][rt][e];
-          sc[4 + e] = s[1][rt][e];
-        }
-        bool ok[8];
-        if (masked) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            ok[e] = key0 + (e < 4 ? 0 : kPage) + 4 * grp + (e & 3) <= limit[rt];
-            sc[e] = ok[e] ? sc[e] : -__builtin_inff();
-          }
-        }
-        // The scale is >= 0 here (the host flips the query's sign for a
-        // negative one), so the row max of the raw scores gives the max of
-        // the scaled ones.
-        float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
-                         fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        // Key 0 is in every row's first step, so mnew is finite from then on
-        // (fmaxf drops the NaN of -inf * 0 for a zero scale).
-        const float mnew = fmaxf(m[rt], mx * a.scale_log2);
-        const float alpha = __builtin_amdgcn_exp2f(m[rt] - mnew);
-        m[rt] = mnew;
-        float p[8];
-        float ps = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], a.scale_log2, -mnew));
-          if (masked) p[e] = ok[e] ? p[e] : 0.f;
-          ps += p[e];
-        }
-        lsum[rt] = lsum[rt] * alpha + ps;
-        pf[rt] = u32x4{pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3]), pack_bf16(p[4], p[5]),
-                       pack_bf16(p[6], p[7])};
-        if (__any(alpha != 1.f)) {
-#pragma unroll
-          for (int jb = 0; jb < JB; ++jb) o[rt][jb] *= alpha;
-        }
+        for (int rt = 0; rt < kRowTiles; ++rt)
+          pf[rt] = softmax_tile<D, false>(s[0][rt], s[1][rt], key0, grp, limit[rt], c, m[rt], lsum[rt], o[rt]);
       }
       // Keys at or past kend may be stale or NaN in V: zero them (a zero
       // weight times NaN would still be NaN).
@@ -257,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   for (int rt = 0; rt < kRowTiles; ++rt) {
     float lt = lsum[rt] + __shfl_xor(lsum[rt], 16);
     lt += __shfl_xor(lt, 32);
-    const int r = wave * 64 + rt * 16 + col;
+    const int r = wave * kWaveRows + rt * 16 + col;
     if (r >= rows) continue;
     const int tok = r / g;
     const int head = kvh * g + (r - tok * g);
@@ -275,8 +302,10 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
 // piece per (token, 8 dims). Values: one thread per (page, dim) writes the
 // 16 slots of a page it fills completely as two 16-byte stores, else slot by
 // slot.
+constexpr int kStoreThreads = 256;
+
 template <int D>
-__global__ __launch_bounds__(kThreads) void kv_store_kernel(ExtendArgs a) {
+__global__ __launch_bounds__(kStoreThreads) void kv_store_kernel(ExtendArgs a) {
   const const_i32_ptr item = as_constant(a.items) + size_t(blockIdx.x) * kItemInts;
   const int seq = item[0];
   const int kvh = item[1];
@@ -290,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void kv_store_kernel(ExtendArgs a) {
   const uint16_t* kn = a.k_new + size_t(qrow0 + t0) * row_stride + size_t(kvh) * D;
   const uint16_t* vn = a.v_new + size_t(qrow0 + t0) * row_stride + size_t(kvh) * D;
 
-  for (int i = threadIdx.x; i < nt * (D / 8); i += kThreads) {
+  for (int i = threadIdx.x; i < nt * (D / 8); i += kStoreThreads) {
     const int t = i / (D / 8);
     const int c = i - t * (D / 8);
     const int pos = first + t;
@@ -301,7 +330,7 @@ __global__ __launch_bounds__(kThreads) void kv_store_kernel(ExtendArgs a) {
 
   const int pg_a = first / kPage;
   const int pg_b = (first + nt - 1) / kPage;
-  for (int i = threadIdx.x; i < (pg_b - pg_a + 1) * D; i += kThreads) {
+  for (int i = threadIdx.x; i < (pg_b - pg_a + 1) * D; i += kStoreThreads) {
     const int pg = pg_a + i / D;
     const int dim = i % D;
     const int lo = max(first, pg * kPage);
@@ -330,9 +359,9 @@ hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream) {
   const dim3 grid(a.num_items), block(kThreads);
   if (a.k_new) {
     if (a.head_dim == 128)
-      hipLaunchKernelGGL(kv_store_kernel<128>, grid, block, 0, stream, a);
+      hipLaunchKernelGGL(kv_store_kernel<128>, grid, dim3(kStoreThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(kv_store_kernel<64>, grid, block, 0, stream, a);
+      hipLaunchKernelGGL(kv_store_kernel<64>, grid, dim3(kStoreThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
