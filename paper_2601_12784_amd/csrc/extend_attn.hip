@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "sf_internal.h"
 
 namespace sf {
@@ -45,6 +47,7 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRowTiles = 2;      // 16-row MFMA tiles per wave
 constexpr int kStepKeys = 2 * kPage;
 constexpr float kRescaleLog2 = 8.f;  // headroom of the lazily moved softmax reference
+constexpr float kRescaleMax = 256.f; // 2^kRescaleLog2
 static_assert(kWaves * kRowTiles * 16 == kExtendRows, "rows per item");
 
 __device__ __forceinline__ const_i32_ptr as_constant(const int32_t* p) { return (const_i32_ptr)(p); }
@@ -64,6 +67,14 @@ __device__ __forceinline__ size_t tile_base(int32_t page, int32_t num_kv_heads, 
   return (size_t(page) * num_kv_heads + kvh) * size_t(kPage * d);
 }
 
+// V tiles in LDS: dim-major (32 bytes per dim, four quads of 4 tokens), with
+// token quad q of dim d stored at quad position q ^ v_swizzle(d). The P.V
+// operand has lane (col, grp) read quad grp of dim 16*jb + col; unswizzled,
+// the 16 lanes of one quad read dims whose rows share 8 of the 32 banks
+// (dims 4 apart are 128 bytes apart) and collide 4-way. With the swizzle
+// those 16 lanes cover 16 distinct 8-byte slots of a 128-byte window.
+__device__ __forceinline__ int v_swizzle(int d) { return (d >> 2) & 3; }
+
 template <int D>
 struct Tiles {
   static constexpr int kElems = kPage * D;            // bf16 per (page, KV head) tile
@@ -74,8 +85,16 @@ struct Tiles {
 
 // Online-softmax update of one 16-row tile for one step of 32 keys. s0 / s1:
 // this lane's scores for keys key0 + 4*grp + e of the step's two pages.
-// Returns the bf16 weights as the P^T operand; rescales o, m, lsum when the
-// reference moves.
+// Returns the bf16 weights as the P^T operand.
+//
+// Lazy reference: each row keeps a reference max m (log2 units) and the
+// weights are p = 2^(z - m). m moves only when some weight of the wave would
+// exceed 2^kRescaleLog2; until then the lanes of a row need not agree on the
+// row's max at all, so the common step has no cross-lane reduction. Weights
+// below 2^kRescaleLog2 are exact in fp32 and keep bf16's relative precision,
+// and O and l share the reference, so O / l does not change. When m moves,
+// the row's max over all four lane groups is formed and O and l are
+// rescaled. Key 0 is in every row's first step, so m is finite after it.
 template <int D, bool kMasked>
 __device__ __forceinline__ u32x4 softmax_tile(const f32x4& s0, const f32x4& s1, int key0, int grp, int limit,
                                               float c, float& m, float& lsum, f32x4* o) {
@@ -93,37 +112,34 @@ __device__ __forceinline__ u32x4 softmax_tile(const f32x4& s0, const f32x4& s1, 
       sc[e] = ok[e] ? sc[e] : -__builtin_inff();
     }
   }
-  // The scale c is >= 0 (the host flips the query's sign for a negative
-  // one), so the row max of the raw scores gives the max of the scaled ones.
-  float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])), fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  // Lazy rescaling: a row's reference max m moves only when the row max
-  // passes it by more than kRescaleLog2. Weights then stay below
-  // 2^kRescaleLog2, exact in fp32 with bf16's relative precision, and O and
-  // l share the reference, so O / l does not change; the rescale of the
-  // accumulators becomes rare. Key 0 is in every row's first step, so m is
-  // finite from then on (a zero scale gives NaN for a fully masked row,
-  // which compares false).
-  const float mx_s = mx * c;
-  const bool grow = mx_s > m + kRescaleLog2;
-  if (__any(grow)) {
+  float p[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, -m));
+  const float pm = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])), fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7])));
+  // Also true for inf (the first step, m = -inf) and NaN (-inf * 0 for a
+  // zero scale), which the slow path sorts out.
+  if (__any(!(pm <= kRescaleMax))) {
+    // The scale c is >= 0 (the host flips the query's sign for a negative
+    // one), so the row max of the raw scores gives the max of the scaled ones.
+    float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])), fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mx_s = mx * c;
+    const bool grow = mx_s > m + kRescaleLog2;   // NaN (fully masked, zero scale) compares false
     const float mnew = grow ? mx_s : m;
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
     lsum *= alpha;
 #pragma unroll
     for (int jb = 0; jb < D / 16; ++jb) o[jb] *= alpha;
-  }
-  float p[8];
-  float ps = 0.f;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, -m));
-    if constexpr (kMasked) p[e] = ok[e] ? p[e] : 0.f;
-    ps += p[e];
+    for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, -m));
   }
-  lsum += ps;
+  if constexpr (kMasked) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) p[e] = ok[e] ? p[e] : 0.f;
+  }
+  lsum += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
   return u32x4{pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3]), pack_bf16(p[4], p[5]), pack_bf16(p[6], p[7])};
 }
 
@@ -214,7 +230,19 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       const int piece = tid + i * kThreads;
-      *reinterpret_cast<u32x4*>(&lds[buf][piece / TC][(piece % TC) * 8]) = pre[i];
+      const int tile = piece / TC;
+      const int off = (piece % TC) * 8;
+      if (tile < 2) {
+        *reinterpret_cast<u32x4*>(&lds[buf][tile][off]) = pre[i];
+      } else {
+        // V: the piece holds token quads 2c, 2c + 1 of dim d; quad q is
+        // stored at position q ^ v_swizzle(d) (see v_swizzle).
+        const int d = off >> 4;
+        const int sw = v_swizzle(d);
+        const int chunk = ((off >> 3) & 1) ^ (sw >> 1);
+        const u32x4 x = (sw & 1) ? u32x4{pre[i][2], pre[i][3], pre[i][0], pre[i][1]} : pre[i];
+        *reinterpret_cast<u32x4*>(&lds[buf][tile][d * kPage + chunk * 8]) = x;
+      }
     }
   };
 
@@ -255,24 +283,30 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
         for (int rt = 0; rt < kRowTiles; ++rt)
           pf[rt] = softmax_tile<D, false>(s[0][rt], s[1][rt], key0, grp, limit[rt], c, m[rt], lsum[rt], o[rt]);
       }
-      // Keys at or past kend may be stale or NaN in V: zero them (a zero
-      // weight times NaN would still be NaN).
-      u32x4 vmask = u32x4{~0u, ~0u, ~0u, ~0u};
+      auto pv = [&](u32x4 vmask, auto masked) {
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) {
+          const int vo = (16 * jb + col) * kPage + 4 * (grp ^ v_swizzle(col));
+          const u32x2 v0 = *reinterpret_cast<const u32x2*>(&lds[buf][2][vo]);
+          const u32x2 v1 = *reinterpret_cast<const u32x2*>(&lds[buf][3][vo]);
+          u32x4 vf = u32x4{v0[0], v0[1], v1[0], v1[1]};
+          if constexpr (decltype(masked)::value) vf &= vmask;
+#pragma unroll
+          for (int rt = 0; rt < kRowTiles; ++rt) o[rt][jb] = mfma_bf16(vf, pf[rt], o[rt][jb]);
+        }
+      };
       if (key0 + kStepKeys > kend) {
+        // Keys at or past kend may be stale or NaN in V: zero them (a zero
+        // weight times NaN would still be NaN).
+        u32x4 vmask;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int kl = key0 + (i < 2 ? 0 : kPage) + 4 * grp + 2 * (i & 1);
           vmask[i] = (kl < kend ? 0x0000FFFFu : 0u) | (kl + 1 < kend ? 0xFFFF0000u : 0u);
         }
-      }
-#pragma unroll
-      for (int jb = 0; jb < JB; ++jb) {
-        const int vo = (16 * jb + col) * kPage + 4 * grp;
-        const u32x2 v0 = *reinterpret_cast<const u32x2*>(&lds[buf][2][vo]);
-        const u32x2 v1 = *reinterpret_cast<const u32x2*>(&lds[buf][3][vo]);
-        const u32x4 vf = u32x4{v0[0], v0[1], v1[0], v1[1]} & vmask;
-#pragma unroll
-        for (int rt = 0; rt < kRowTiles; ++rt) o[rt][jb] = mfma_bf16(vf, pf[rt], o[rt][jb]);
+        pv(vmask, std::true_type{});
+      } else {
+        pv(u32x4{}, std::false_type{});
       }
     }
     if (j + 1 < nsteps) stage(buf ^ 1);
