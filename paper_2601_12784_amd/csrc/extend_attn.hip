@@ -28,8 +28,6 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include <type_traits>
-
 #include "sf_internal.h"
 
 namespace sf {
@@ -57,9 +55,11 @@ __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+// Two floats to two bf16 (round to nearest even) in one conversion.
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  return uint32_t(__builtin_bit_cast(uint16_t, static_cast<__bf16>(lo))) |
-         (uint32_t(__builtin_bit_cast(uint16_t, static_cast<__bf16>(hi))) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // Element offset of a (page, KV head) tile in either pool.
@@ -67,13 +67,13 @@ __device__ __forceinline__ size_t tile_base(int32_t page, int32_t num_kv_heads, 
   return (size_t(page) * num_kv_heads + kvh) * size_t(kPage * d);
 }
 
-// V tiles in LDS: dim-major (32 bytes per dim, four quads of 4 tokens), with
-// token quad q of dim d stored at quad position q ^ v_swizzle(d). The P.V
-// operand has lane (col, grp) read quad grp of dim 16*jb + col; unswizzled,
-// the 16 lanes of one quad read dims whose rows share 8 of the 32 banks
-// (dims 4 apart are 128 bytes apart) and collide 4-way. With the swizzle
-// those 16 lanes cover 16 distinct 8-byte slots of a 128-byte window.
-__device__ __forceinline__ int v_swizzle(int d) { return (d >> 2) & 3; }
+// V in LDS, both pages of a step interleaved: dim d owns 64 bytes, four
+// 16-byte slots, and slot g ^ v_swizzle(d) holds [page 0 quad g | page 1
+// quad g] (quad g = tokens 4g .. 4g+3 of the page). That is exactly the P.V
+// operand of lane (col, grp) for dim 16*jb + col and quad grp, one 16-byte
+// read; the swizzle makes every 8 lanes of such a read (128 bytes) hit 8
+// distinct 16-byte bank groups.
+__device__ __forceinline__ int v_swizzle(int d) { return (d >> 1) & 3; }
 
 template <int D>
 struct Tiles {
@@ -151,8 +151,8 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   constexpr int TC = Tiles<D>::kChunks;
   constexpr int NL = Tiles<D>::kLoads;
   constexpr int kWaveRows = 16 * kRowTiles;
-  // [buffer][K page 0, K page 1, V page 0, V page 1][tile]
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][4][TE];
+  // [buffer][K page 0 | K page 1 | V of both pages, interleaved]
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2][4 * TE];
 
   const const_i32_ptr item = as_constant(a.items) + size_t(blockIdx.x) * kItemInts;
   const int seq = item[0];
@@ -170,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   const float c = a.scale_log2;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int col = lane & 15;
   const int grp = lane >> 4;
@@ -226,28 +226,41 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
       pre[i] = *reinterpret_cast<const u32x4*>(pool + tile_base(page, a.num_kv_heads, kvh, D) + off);
     }
   };
-  auto stage = [&](int buf) {
+  // Writes the fetched pieces of step j into buffer buf. V pieces are split
+  // into their two token quads (8 bytes each) at their interleaved slots;
+  // in the step that reaches kend, V tokens at or past it are zeroed here
+  // (they may be stale or NaN, and a zero weight times NaN is still NaN).
+  auto stage = [&](int buf, int j) {
+    const int key0 = j * kStepKeys;
+    const bool tail = key0 + kStepKeys > kend;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       const int piece = tid + i * kThreads;
       const int tile = piece / TC;
       const int off = (piece % TC) * 8;
       if (tile < 2) {
-        *reinterpret_cast<u32x4*>(&lds[buf][tile][off]) = pre[i];
+        *reinterpret_cast<u32x4*>(&lds[buf][tile * TE + off]) = pre[i];
       } else {
-        // V: the piece holds token quads 2c, 2c + 1 of dim d; quad q is
-        // stored at position q ^ v_swizzle(d) (see v_swizzle).
+        const int pg = tile - 2;
         const int d = off >> 4;
-        const int sw = v_swizzle(d);
-        const int chunk = ((off >> 3) & 1) ^ (sw >> 1);
-        const u32x4 x = (sw & 1) ? u32x4{pre[i][2], pre[i][3], pre[i][0], pre[i][1]} : pre[i];
-        *reinterpret_cast<u32x4*>(&lds[buf][tile][d * kPage + chunk * 8]) = x;
+        const int c = (off >> 3) & 1;   // tokens 8c .. 8c+7 of the page
+        u32x4 x = pre[i];
+        if (tail) {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const int key = key0 + pg * kPage + 8 * c + 2 * w;
+            x[w] &= (key < kend ? 0x0000FFFFu : 0u) | (key + 1 < kend ? 0xFFFF0000u : 0u);
+          }
+        }
+        uint16_t* row = &lds[buf][2 * TE + d * 32 + pg * 4];
+        *reinterpret_cast<u32x2*>(row + ((2 * c) ^ v_swizzle(d)) * 8) = u32x2{x[0], x[1]};
+        *reinterpret_cast<u32x2*>(row + ((2 * c + 1) ^ v_swizzle(d)) * 8) = u32x2{x[2], x[3]};
       }
     }
   };
 
   fetch(0);
-  stage(0);
+  stage(0, 0);
   __syncthreads();
 
   for (int j = 0; j < nsteps; ++j) {
@@ -265,8 +278,8 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         const int ko = ((4 * kb + grp) * kPage + col) * 8;
-        const u32x4 k0 = *reinterpret_cast<const u32x4*>(&lds[buf][0][ko]);
-        const u32x4 k1 = *reinterpret_cast<const u32x4*>(&lds[buf][1][ko]);
+        const u32x4 k0 = *reinterpret_cast<const u32x4*>(&lds[buf][ko]);
+        const u32x4 k1 = *reinterpret_cast<const u32x4*>(&lds[buf][TE + ko]);
 #pragma unroll
         for (int rt = 0; rt < kRowTiles; ++rt) {
           s[0][rt] = mfma_bf16(k0, qf[rt][kb], s[0][rt]);
@@ -283,33 +296,15 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
         for (int rt = 0; rt < kRowTiles; ++rt)
           pf[rt] = softmax_tile<D, false>(s[0][rt], s[1][rt], key0, grp, limit[rt], c, m[rt], lsum[rt], o[rt]);
       }
-      auto pv = [&](u32x4 vmask, auto masked) {
+      const int vo = 2 * TE + col * 32 + (grp ^ v_swizzle(col)) * 8;
 #pragma unroll
-        for (int jb = 0; jb < JB; ++jb) {
-          const int vo = (16 * jb + col) * kPage + 4 * (grp ^ v_swizzle(col));
-          const u32x2 v0 = *reinterpret_cast<const u32x2*>(&lds[buf][2][vo]);
-          const u32x2 v1 = *reinterpret_cast<const u32x2*>(&lds[buf][3][vo]);
-          u32x4 vf = u32x4{v0[0], v0[1], v1[0], v1[1]};
-          if constexpr (decltype(masked)::value) vf &= vmask;
+      for (int jb = 0; jb < JB; ++jb) {
+        const u32x4 vf = *reinterpret_cast<const u32x4*>(&lds[buf][vo + jb * 16 * 32]);
 #pragma unroll
-          for (int rt = 0; rt < kRowTiles; ++rt) o[rt][jb] = mfma_bf16(vf, pf[rt], o[rt][jb]);
-        }
-      };
-      if (key0 + kStepKeys > kend) {
-        // Keys at or past kend may be stale or NaN in V: zero them (a zero
-        // weight times NaN would still be NaN).
-        u32x4 vmask;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int kl = key0 + (i < 2 ? 0 : kPage) + 4 * grp + 2 * (i & 1);
-          vmask[i] = (kl < kend ? 0x0000FFFFu : 0u) | (kl + 1 < kend ? 0xFFFF0000u : 0u);
-        }
-        pv(vmask, std::true_type{});
-      } else {
-        pv(u32x4{}, std::false_type{});
+        for (int rt = 0; rt < kRowTiles; ++rt) o[rt][jb] = mfma_bf16(vf, pf[rt], o[rt][jb]);
       }
     }
-    if (j + 1 < nsteps) stage(buf ^ 1);
+    if (j + 1 < nsteps) stage(buf ^ 1, j + 1);
     __syncthreads();
   }
 
