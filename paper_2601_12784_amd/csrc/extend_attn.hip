@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "sf_internal.h"
 
 namespace sf {
@@ -83,9 +85,8 @@ struct Tiles {
   static_assert(kLoads * kThreads == 4 * kChunks, "staging split");
 };
 
-// Online-softmax update of one 16-row tile for one step of 32 keys. s0 / s1:
-// this lane's scores for keys key0 + 4*grp + e of the step's two pages.
-// Returns the bf16 weights as the P^T operand.
+// Online-softmax update of one 16-row tile for one step of 32 keys, in two
+// parts so that each can be interleaved with matrix-core work.
 //
 // Lazy reference: each row keeps a reference max m (log2 units) and the
 // weights are p = 2^(z - m). m moves only when some weight of the wave would
@@ -95,33 +96,50 @@ struct Tiles {
 // and O and l share the reference, so O / l does not change. When m moves,
 // the row's max over all four lane groups is formed and O and l are
 // rescaled. Key 0 is in every row's first step, so m is finite after it.
-template <int D, bool kMasked>
-__device__ __forceinline__ u32x4 softmax_tile(const f32x4& s0, const f32x4& s1, int key0, int grp, int limit,
-                                              float c, float& m, float& lsum, f32x4* o) {
-  float sc[8];
+struct TileWeights {
+  float sc[8];   // raw scores of this lane (masked ones -inf)
+  float p[8];    // 2^(sc * c - m)
+  bool ok[8];    // key inside the row's causal limit (masked steps)
+  bool need;     // some weight exceeds the headroom (or is inf / NaN)
+};
+
+// Part 1: exponentiate against the current reference. s0 / s1: this lane's
+// scores for keys key0 + 4*grp + e of the step's two pages.
+template <bool kMasked>
+__device__ __forceinline__ TileWeights exponentiate(const f32x4& s0, const f32x4& s1, int key0, int grp, int limit,
+                                                    float c, float m) {
+  TileWeights t;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    sc[e] = s0[e];
-    sc[4 + e] = s1[e];
+    t.sc[e] = s0[e];
+    t.sc[4 + e] = s1[e];
   }
-  bool ok[8];
   if constexpr (kMasked) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      ok[e] = key0 + (e < 4 ? 0 : kPage) + 4 * grp + (e & 3) <= limit;
-      sc[e] = ok[e] ? sc[e] : -__builtin_inff();
+      t.ok[e] = key0 + (e < 4 ? 0 : kPage) + 4 * grp + (e & 3) <= limit;
+      t.sc[e] = t.ok[e] ? t.sc[e] : -__builtin_inff();
     }
   }
-  float p[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, -m));
-  const float pm = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])), fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7])));
+  for (int e = 0; e < 8; ++e) t.p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(t.sc[e], c, -m));
+  const float pm = fmaxf(fmaxf(fmaxf(t.p[0], t.p[1]), fmaxf(t.p[2], t.p[3])),
+                         fmaxf(fmaxf(t.p[4], t.p[5]), fmaxf(t.p[6], t.p[7])));
   // Also true for inf (the first step, m = -inf) and NaN (-inf * 0 for a
-  // zero scale), which the slow path sorts out.
-  if (__any(!(pm <= kRescaleMax))) {
+  // zero scale), which settle() sorts out.
+  t.need = !(pm <= kRescaleMax);
+  return t;
+}
+
+// Part 2: move the reference if needed (rare), then sum and pack the
+// weights as the P^T operand.
+template <int D, bool kMasked>
+__device__ __forceinline__ u32x4 settle(TileWeights& t, float c, float& m, float& lsum, f32x4* o) {
+  if (__any(t.need)) {
     // The scale c is >= 0 (the host flips the query's sign for a negative
     // one), so the row max of the raw scores gives the max of the scaled ones.
-    float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])), fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+    float mx = fmaxf(fmaxf(fmaxf(t.sc[0], t.sc[1]), fmaxf(t.sc[2], t.sc[3])),
+                     fmaxf(fmaxf(t.sc[4], t.sc[5]), fmaxf(t.sc[6], t.sc[7])));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float mx_s = mx * c;
@@ -133,14 +151,28 @@ __device__ __forceinline__ u32x4 softmax_tile(const f32x4& s0, const f32x4& s1, 
 #pragma unroll
     for (int jb = 0; jb < D / 16; ++jb) o[jb] *= alpha;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c, -m));
+    for (int e = 0; e < 8; ++e) t.p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(t.sc[e], c, -m));
   }
   if constexpr (kMasked) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) p[e] = ok[e] ? p[e] : 0.f;
+    for (int e = 0; e < 8; ++e) t.p[e] = t.ok[e] ? t.p[e] : 0.f;
   }
-  lsum += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-  return u32x4{pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3]), pack_bf16(p[4], p[5]), pack_bf16(p[6], p[7])};
+  lsum += ((t.p[0] + t.p[1]) + (t.p[2] + t.p[3])) + ((t.p[4] + t.p[5]) + (t.p[6] + t.p[7]));
+  return u32x4{pack_bf16(t.p[0], t.p[1]), pack_bf16(t.p[2], t.p[3]), pack_bf16(t.p[4], t.p[5]),
+               pack_bf16(t.p[6], t.p[7])};
+}
+
+// Scheduling hints: n times {one MFMA, then k vector ALU ops}, so the
+// vector work of one row tile issues while the matrix core works on the
+// other (the matrix core runs an MFMA for 16 cycles; a wave issues other
+// independent work meanwhile only if it comes next in program order).
+template <int N, int K>
+__device__ __forceinline__ void interleave_mfma_valu() {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, K, 0);
+  }
 }
 
 template <int D>
@@ -268,41 +300,50 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
     if (j + 1 < nsteps) fetch(j + 1);
     const int key0 = j * kStepKeys;
     if (key0 <= wave_kmax) {
-      // Scores S^T: lane holds row `col`, keys key0 + 4*grp + e (page 0) and +16 (page 1).
-      f32x4 s[2][kRowTiles];
-#pragma unroll
-      for (int rt = 0; rt < kRowTiles; ++rt) {
-        s[0][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        s[1][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
+      static_assert(kRowTiles == 2, "the step below pipelines exactly two row tiles");
+      // K operands of both pages and V operands of the step.
+      u32x4 kf0[KB], kf1[KB], vf[JB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         const int ko = ((4 * kb + grp) * kPage + col) * 8;
-        const u32x4 k0 = *reinterpret_cast<const u32x4*>(&lds[buf][ko]);
-        const u32x4 k1 = *reinterpret_cast<const u32x4*>(&lds[buf][TE + ko]);
-#pragma unroll
-        for (int rt = 0; rt < kRowTiles; ++rt) {
-          s[0][rt] = mfma_bf16(k0, qf[rt][kb], s[0][rt]);
-          s[1][rt] = mfma_bf16(k1, qf[rt][kb], s[1][rt]);
-        }
-      }
-      u32x4 pf[kRowTiles];
-      if (key0 + kStepKeys - 1 > wave_kmin) {
-#pragma unroll
-        for (int rt = 0; rt < kRowTiles; ++rt)
-          pf[rt] = softmax_tile<D, true>(s[0][rt], s[1][rt], key0, grp, limit[rt], c, m[rt], lsum[rt], o[rt]);
-      } else {
-#pragma unroll
-        for (int rt = 0; rt < kRowTiles; ++rt)
-          pf[rt] = softmax_tile<D, false>(s[0][rt], s[1][rt], key0, grp, limit[rt], c, m[rt], lsum[rt], o[rt]);
+        kf0[kb] = *reinterpret_cast<const u32x4*>(&lds[buf][ko]);
+        kf1[kb] = *reinterpret_cast<const u32x4*>(&lds[buf][TE + ko]);
       }
       const int vo = 2 * TE + col * 32 + (grp ^ v_swizzle(col)) * 8;
 #pragma unroll
-      for (int jb = 0; jb < JB; ++jb) {
-        const u32x4 vf = *reinterpret_cast<const u32x4*>(&lds[buf][vo + jb * 16 * 32]);
+      for (int jb = 0; jb < JB; ++jb) vf[jb] = *reinterpret_cast<const u32x4*>(&lds[buf][vo + jb * 16 * 32]);
+      // Scores S^T of row tile 0: lane holds row `col`, keys key0 + 4*grp + e
+      // of page 0 (sa0) and page 1 (sa1).
+      f32x4 sa0 = {0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
 #pragma unroll
-        for (int rt = 0; rt < kRowTiles; ++rt) o[rt][jb] = mfma_bf16(vf, pf[rt], o[rt][jb]);
+      for (int kb = 0; kb < KB; ++kb) {
+        sa0 = mfma_bf16(kf0[kb], qf[0][kb], sa0);
+        sa1 = mfma_bf16(kf1[kb], qf[0][kb], sa1);
       }
+      auto pipeline = [&](auto masked_tag) {
+        constexpr bool kMasked = decltype(masked_tag)::value;
+        // Scores of row tile 1 on the matrix core while tile 0 is exponentiated.
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+          sb0 = mfma_bf16(kf0[kb], qf[1][kb], sb0);
+          sb1 = mfma_bf16(kf1[kb], qf[1][kb], sb1);
+        }
+        TileWeights ta = exponentiate<kMasked>(sa0, sa1, key0, grp, limit[0], c, m[0]);
+        interleave_mfma_valu<2 * KB, 3>();
+        const u32x4 pa = settle<D, kMasked>(ta, c, m[0], lsum[0], o[0]);
+        // P.V of row tile 0 while tile 1 is exponentiated.
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) o[0][jb] = mfma_bf16(vf[jb], pa, o[0][jb]);
+        TileWeights tb = exponentiate<kMasked>(sb0, sb1, key0, grp, limit[1], c, m[1]);
+        interleave_mfma_valu<JB, 3>();
+        const u32x4 pb = settle<D, kMasked>(tb, c, m[1], lsum[1], o[1]);
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) o[1][jb] = mfma_bf16(vf[jb], pb, o[1][jb]);
+      };
+      if (key0 + kStepKeys - 1 > wave_kmin)
+        pipeline(std::true_type{});
+      else
+        pipeline(std::false_type{});
     }
     if (j + 1 < nsteps) stage(buf ^ 1, j + 1);
     __syncthreads();
