@@ -11,20 +11,25 @@
 // all new tokens after it, so the work runs on the matrix cores. A work item
 // is one (sequence, KV head, block of new tokens); its rows are the block's
 // tokens times the g query heads of the group (token-major), at most 256 rows,
-// 32 per wave. The item walks the keys 32 at a time (two pages): the eight
-// waves stage the two K tiles and two V tiles (16 KiB at D = 128) through LDS,
-// double buffered, and each wave computes, per 16-row tile,
+// 32 per wave (8 waves). The item walks the keys in steps of 32 (two pages),
+// two steps per barrier: the waves stage the K and V tiles of both steps
+// (32 KiB at D = 128) through LDS, double buffered, and each wave computes,
+// per step and 16-row tile,
 //
 //   S^T[32 keys][16 rows] = K Q^T        2 x (D/32) v_mfma_f32_16x16x32_bf16
-//   online softmax in base 2             (row = lane column; max over the four 16-lane groups)
+//   online softmax in base 2             (row = lane column; lazily moved reference)
 //   O^T[D][16 rows]      += V^T P^T      (D/16) MFMAs, P rounded to bf16
 //
-// with each K and V operand read from LDS once per wave and used for both
-// of its row tiles. (64 rows per wave would halve the LDS reads but does not
-// fit in the 256 architectural registers: the accumulators then shuttle
-// through AGPRs every step.) The operand mapping is the decode kernel's: each lane's
-// eight scores are keys 4*grp .. 4*grp+3 of both pages, the eight P^T values
-// its P.V operand needs.
+// with each K and V operand read from LDS once per wave and used for both of
+// its row tiles, and the two tiles pipelined so that one tile's matrix-core
+// work overlaps the other's exponentials. The operand mapping is the decode
+// kernel's: each lane's eight scores are keys 4*grp .. 4*grp+3 of both
+// pages, the eight P^T values its P.V operand needs.
+//
+// Measured alternatives (full re-prefill of 32 long-tail trajectories):
+// 64 rows per wave (4 waves, one per SIMD) halves the LDS operand reads but
+// leaves no second wave per SIMD to overlap with, and is 1.5x slower; items
+// of 128 rows double the K/V staging per row and are 2x slower.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -45,7 +50,8 @@ constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowTiles = 2;      // 16-row MFMA tiles per wave
-constexpr int kStepKeys = 2 * kPage;
+constexpr int kStepKeys = 2 * kPage;   // keys per step (two pages)
+constexpr int kSub = 2;                // steps per barrier interval
 constexpr float kRescaleLog2 = 8.f;  // headroom of the lazily moved softmax reference
 constexpr float kRescaleMax = 256.f; // 2^kRescaleLog2
 static_assert(kWaves * kRowTiles * 16 == kExtendRows, "rows per item");
@@ -166,10 +172,11 @@ __device__ __forceinline__ u32x4 settle(TileWeights& t, float c, float& m, float
 // vector work of one row tile issues while the matrix core works on the
 // other (the matrix core runs an MFMA for 16 cycles; a wave issues other
 // independent work meanwhile only if it comes next in program order).
-template <int N, int K>
-__device__ __forceinline__ void interleave_mfma_valu() {
+// (n must be a compile-time constant once the caller's loops are unrolled.)
+template <int K>
+__device__ __forceinline__ void interleave_mfma_valu(int n) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
+  for (int i = 0; i < n; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x002, K, 0);
   }
@@ -183,8 +190,8 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   constexpr int TC = Tiles<D>::kChunks;
   constexpr int NL = Tiles<D>::kLoads;
   constexpr int kWaveRows = 16 * kRowTiles;
-  // [buffer][K page 0 | K page 1 | V of both pages, interleaved]
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][4 * TE];
+  // [buffer][step of the interval][K page 0 | K page 1 | V of both pages, interleaved]
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2][kSub][4 * TE];
 
   const const_i32_ptr item = as_constant(a.items) + size_t(blockIdx.x) * kItemInts;
   const int seq = item[0];
@@ -243,109 +250,130 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   // Staging: thread tid moves pieces tid, tid + kThreads, ... of the step's
   // four tiles. A page past the item's last is replaced by its first page
   // (always in range); its keys lie past kend and are masked.
-  u32x4 pre[NL];
+  // The keys are walked in intervals of kSub steps with one barrier each:
+  // a wave's work between barriers is then long enough for the two waves
+  // that share a SIMD to fall out of step (one on the matrix core while the
+  // other exponentiates).
+  u32x4 pre[kSub][NL];
   auto fetch = [&](int j) {
-    const int pg0 = 2 * j;
-    const int p0 = bt[pg0];
-    const int p1 = pg0 + 1 < npages ? bt[pg0 + 1] : p0;
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int piece = tid + i * kThreads;
-      const int tile = piece / TC;
-      const int off = (piece % TC) * 8;
-      const uint16_t* pool = tile < 2 ? a.k_pool : a.v_pool;
-      const int page = (tile & 1) ? p1 : p0;
-      pre[i] = *reinterpret_cast<const u32x4*>(pool + tile_base(page, a.num_kv_heads, kvh, D) + off);
+    for (int u = 0; u < kSub; ++u) {
+      const int js = kSub * j + u;
+      if (js >= nsteps) break;
+      const int pg0 = 2 * js;
+      const int p0 = bt[pg0];
+      const int p1 = pg0 + 1 < npages ? bt[pg0 + 1] : p0;
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        const int piece = tid + i * kThreads;
+        const int tile = piece / TC;
+        const int off = (piece % TC) * 8;
+        const uint16_t* pool = tile < 2 ? a.k_pool : a.v_pool;
+        const int page = (tile & 1) ? p1 : p0;
+        pre[u][i] = *reinterpret_cast<const u32x4*>(pool + tile_base(page, a.num_kv_heads, kvh, D) + off);
+      }
     }
   };
-  // Writes the fetched pieces of step j into buffer buf. V pieces are split
-  // into their two token quads (8 bytes each) at their interleaved slots;
-  // in the step that reaches kend, V tokens at or past it are zeroed here
-  // (they may be stale or NaN, and a zero weight times NaN is still NaN).
+  // Writes the fetched pieces of interval j into buffer buf. V pieces are
+  // split into their two token quads (8 bytes each) at their interleaved
+  // slots; in the step that reaches kend, V tokens at or past it are zeroed
+  // here (they may be stale or NaN, and a zero weight times NaN is still NaN).
   auto stage = [&](int buf, int j) {
-    const int key0 = j * kStepKeys;
-    const bool tail = key0 + kStepKeys > kend;
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int piece = tid + i * kThreads;
-      const int tile = piece / TC;
-      const int off = (piece % TC) * 8;
-      if (tile < 2) {
-        *reinterpret_cast<u32x4*>(&lds[buf][tile * TE + off]) = pre[i];
-      } else {
-        const int pg = tile - 2;
-        const int d = off >> 4;
-        const int c = (off >> 3) & 1;   // tokens 8c .. 8c+7 of the page
-        u32x4 x = pre[i];
-        if (tail) {
+    for (int u = 0; u < kSub; ++u) {
+      const int js = kSub * j + u;
+      if (js >= nsteps) break;
+      const int key0 = js * kStepKeys;
+      const bool tail = key0 + kStepKeys > kend;
+      uint16_t* base = lds[buf][u];
 #pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const int key = key0 + pg * kPage + 8 * c + 2 * w;
-            x[w] &= (key < kend ? 0x0000FFFFu : 0u) | (key + 1 < kend ? 0xFFFF0000u : 0u);
+      for (int i = 0; i < NL; ++i) {
+        const int piece = tid + i * kThreads;
+        const int tile = piece / TC;
+        const int off = (piece % TC) * 8;
+        if (tile < 2) {
+          *reinterpret_cast<u32x4*>(base + tile * TE + off) = pre[u][i];
+        } else {
+          const int pg = tile - 2;
+          const int d = off >> 4;
+          const int c = (off >> 3) & 1;   // tokens 8c .. 8c+7 of the page
+          u32x4 x = pre[u][i];
+          if (tail) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              const int key = key0 + pg * kPage + 8 * c + 2 * w;
+              x[w] &= (key < kend ? 0x0000FFFFu : 0u) | (key + 1 < kend ? 0xFFFF0000u : 0u);
+            }
           }
+          uint16_t* row = base + 2 * TE + d * 32 + pg * 4;
+          *reinterpret_cast<u32x2*>(row + ((2 * c) ^ v_swizzle(d)) * 8) = u32x2{x[0], x[1]};
+          *reinterpret_cast<u32x2*>(row + ((2 * c + 1) ^ v_swizzle(d)) * 8) = u32x2{x[2], x[3]};
         }
-        uint16_t* row = &lds[buf][2 * TE + d * 32 + pg * 4];
-        *reinterpret_cast<u32x2*>(row + ((2 * c) ^ v_swizzle(d)) * 8) = u32x2{x[0], x[1]};
-        *reinterpret_cast<u32x2*>(row + ((2 * c + 1) ^ v_swizzle(d)) * 8) = u32x2{x[2], x[3]};
       }
     }
   };
 
+  // One step: keys key0 .. key0 + 31 from the given LDS slice. The row
+  // tiles are pipelined: the scores of tile rt + 1 and the P.V product of
+  // tile rt - 1 run on the matrix core while tile rt is exponentiated.
+  auto compute = [&](const uint16_t* L, int key0) {
+    // K operands of both pages and V operands of the step.
+    u32x4 kf0[KB], kf1[KB], vf[JB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const int ko = ((4 * kb + grp) * kPage + col) * 8;
+      kf0[kb] = *reinterpret_cast<const u32x4*>(L + ko);
+      kf1[kb] = *reinterpret_cast<const u32x4*>(L + TE + ko);
+    }
+    const int vo = 2 * TE + col * 32 + (grp ^ v_swizzle(col)) * 8;
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) vf[jb] = *reinterpret_cast<const u32x4*>(L + vo + jb * 16 * 32);
+    // Scores S^T of row tile rt: lane holds row `col`, keys key0 + 4*grp + e
+    // of page 0 (s0) and page 1 (s1).
+    f32x4 s0[kRowTiles], s1[kRowTiles];
+    auto scores = [&](int rt) {
+      s0[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s1[rt] = s0[rt];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        s0[rt] = mfma_bf16(kf0[kb], qf[rt][kb], s0[rt]);
+        s1[rt] = mfma_bf16(kf1[kb], qf[rt][kb], s1[rt]);
+      }
+    };
+    scores(0);
+    auto pipeline = [&](auto masked_tag) {
+      constexpr bool kMasked = decltype(masked_tag)::value;
+#pragma unroll
+      for (int rt = 0; rt < kRowTiles; ++rt) {
+        if (rt + 1 < kRowTiles) scores(rt + 1);
+        TileWeights t = exponentiate<kMasked>(s0[rt], s1[rt], key0, grp, limit[rt], c, m[rt]);
+        interleave_mfma_valu<3>((rt + 1 < kRowTiles ? 2 * KB : 0) + (rt > 0 ? JB : 0));
+        const u32x4 pf = settle<D, kMasked>(t, c, m[rt], lsum[rt], o[rt]);
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) o[rt][jb] = mfma_bf16(vf[jb], pf, o[rt][jb]);
+      }
+    };
+    if (key0 + kStepKeys - 1 > wave_kmin)
+      pipeline(std::true_type{});
+    else
+      pipeline(std::false_type{});
+  };
+
+  const int nint = (nsteps + kSub - 1) / kSub;
   fetch(0);
   stage(0, 0);
   __syncthreads();
 
-  for (int j = 0; j < nsteps; ++j) {
+  for (int j = 0; j < nint; ++j) {
     const int buf = j & 1;
-    if (j + 1 < nsteps) fetch(j + 1);
-    const int key0 = j * kStepKeys;
-    if (key0 <= wave_kmax) {
-      static_assert(kRowTiles == 2, "the step below pipelines exactly two row tiles");
-      // K operands of both pages and V operands of the step.
-      u32x4 kf0[KB], kf1[KB], vf[JB];
+    if (j + 1 < nint) fetch(j + 1);
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        const int ko = ((4 * kb + grp) * kPage + col) * 8;
-        kf0[kb] = *reinterpret_cast<const u32x4*>(&lds[buf][ko]);
-        kf1[kb] = *reinterpret_cast<const u32x4*>(&lds[buf][TE + ko]);
-      }
-      const int vo = 2 * TE + col * 32 + (grp ^ v_swizzle(col)) * 8;
-#pragma unroll
-      for (int jb = 0; jb < JB; ++jb) vf[jb] = *reinterpret_cast<const u32x4*>(&lds[buf][vo + jb * 16 * 32]);
-      // Scores S^T of row tile 0: lane holds row `col`, keys key0 + 4*grp + e
-      // of page 0 (sa0) and page 1 (sa1).
-      f32x4 sa0 = {0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        sa0 = mfma_bf16(kf0[kb], qf[0][kb], sa0);
-        sa1 = mfma_bf16(kf1[kb], qf[0][kb], sa1);
-      }
-      auto pipeline = [&](auto masked_tag) {
-        constexpr bool kMasked = decltype(masked_tag)::value;
-        // Scores of row tile 1 on the matrix core while tile 0 is exponentiated.
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          sb0 = mfma_bf16(kf0[kb], qf[1][kb], sb0);
-          sb1 = mfma_bf16(kf1[kb], qf[1][kb], sb1);
-        }
-        TileWeights ta = exponentiate<kMasked>(sa0, sa1, key0, grp, limit[0], c, m[0]);
-        interleave_mfma_valu<2 * KB, 3>();
-        const u32x4 pa = settle<D, kMasked>(ta, c, m[0], lsum[0], o[0]);
-        // P.V of row tile 0 while tile 1 is exponentiated.
-#pragma unroll
-        for (int jb = 0; jb < JB; ++jb) o[0][jb] = mfma_bf16(vf[jb], pa, o[0][jb]);
-        TileWeights tb = exponentiate<kMasked>(sb0, sb1, key0, grp, limit[1], c, m[1]);
-        interleave_mfma_valu<JB, 3>();
-        const u32x4 pb = settle<D, kMasked>(tb, c, m[1], lsum[1], o[1]);
-#pragma unroll
-        for (int jb = 0; jb < JB; ++jb) o[1][jb] = mfma_bf16(vf[jb], pb, o[1][jb]);
-      };
-      if (key0 + kStepKeys - 1 > wave_kmin)
-        pipeline(std::true_type{});
-      else
-        pipeline(std::false_type{});
+    for (int u = 0; u < kSub; ++u) {
+      const int js = kSub * j + u;
+      const int key0 = js * kStepKeys;
+      if (js < nsteps && key0 <= wave_kmax) compute(lds[buf][u], key0);
     }
-    if (j + 1 < nsteps) stage(buf ^ 1, j + 1);
+    if (j + 1 < nint) stage(buf ^ 1, j + 1);
     __syncthreads();
   }
 
