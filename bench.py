@@ -33,8 +33,8 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def kernel_source_hash(path=None) -> str:
+    return hashlib.sha256(open(path or KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
 class Stepper:
@@ -216,6 +216,8 @@ def routing_demo(k1_per_token, mu=0.3, seed=0):
 
 
 EXTEND_KERNEL = "extend_attn_kernel<128>"
+EXTEND_SRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2601_12784_amd", "csrc",
+                          "extend_attn.hip")
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
 
 
@@ -391,17 +393,27 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
 
 
 def summarize_trace(stats_csv, command, out_md, bench_json=None):
-    """Markdown summary of a rocprofv3 --kernel-trace --stats run."""
+    """Markdown summary of a rocprofv3 --kernel-trace --stats run (the decode
+    step, or the re-prefill leg when the bench line is an --only-reprefill one)."""
     rows = _csv_rows(stats_csv)
-    lines = [f"# Kernel trace: {ATTN_KERNEL} on the long-tail batch", "",
-             "Command (from the repository root):", "", "```", command, "```", "",
-             f"Kernel source sha256[:16]: `{kernel_source_hash()}`", "",
+    b = json.load(open(bench_json)) if bench_json else None
+    reprefill = b is not None and "causal_flops" in b
+    title = (f"# Kernel trace: {EXTEND_KERNEL} on the full re-prefill batch" if reprefill
+             else f"# Kernel trace: {ATTN_KERNEL} on the long-tail batch")
+    src = EXTEND_SRC if reprefill else KERNEL_SRC
+    lines = [title, "", "Command (from the repository root):", "", "```", command, "```", "",
+             f"Kernel source sha256[:16]: `{kernel_source_hash(src)}`", "",
              "| kernel | calls | average us | min us | max us | share % |", "|---|---|---|---|---|---|"]
     for r in rows:
         lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
-    if bench_json:
-        b = json.load(open(bench_json))
+    if reprefill:
+        lines += ["", "bench.py line of the same run (HIP events on the kernel's stream):", "",
+                  f"- extend kernel mean: {b['kernel_ms'] * 1e3:.1f} us over {b['items']} work items",
+                  f"- causal flops per pass: {b['causal_flops']}",
+                  f"- roofline achieved: {b['roofline']['achieved']} TFLOP/s "
+                  f"({100 * b['roofline']['frac']:.1f}% of {b['roofline']['peak']:.0f})"]
+    elif b:
         lines += ["", "bench.py line of the same run (HIP events on the kernel's stream):", "",
                   f"- attention kernel mean: {b['attn_kernel_us']} us",
                   f"- step: {b['ms_per_step'] * 1e3:.1f} us; value {b['value']} GB/s",
