@@ -11,6 +11,9 @@ Modules:
   merge_ref    fp64 log-sum-exp merge of partial attention results
   plan_ref     re-derivation of the split-K chunk plan from its stated rule
   append_ref   page allocator, KV append and the growing-cache decode loop
+  extend_ref   extend (re-prefill) attention and the new-token store
+  cost_ref     throughput cost model and routing
+  fp8_ref      FP8 E4M3 encoding and the per-page quantizer of the KV cache
 """
 from __future__ import annotations
 
@@ -49,6 +52,10 @@ def lib():
         L.sf_oracle_gather.argtypes = [i, i, i, i, i, p, p, p, i, i, i, p, p]
         L.sf_oracle_gather.restype = i
         L.sf_oracle_max_threads.restype = i
+        L.sf_oracle_decode_attn_fp8.argtypes = [i, i, i, i, i, i, i, p, p, p, p, p, p, p, ctypes.c_double, p, p, i]
+        L.sf_oracle_decode_attn_fp8.restype = i
+        L.sf_oracle_e4m3_value.argtypes = [i]
+        L.sf_oracle_e4m3_value.restype = ctypes.c_double
         _lib = L
     return _lib
 
@@ -84,6 +91,35 @@ def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale, nthreads: int =
     if rc != 0:
         raise ValueError(f"oracle rejected its input (code {rc})")
     return out, lse
+
+
+def decode_attn_fp8(q, k8, v8, k_scale, v_scale, block_table, seq_lens, scale, nthreads: int = 0):
+    """fp64 reference over an fp8 (OCP E4M3) cache with per-(page, KV head)
+    scales. q: uint16 bf16 bits [B,Hq,D]; k8 [N,Hkv,D/8,16,8] and v8
+    [N,Hkv,D,16] uint8 codes; k_scale, v_scale float32 [N,Hkv]."""
+    q = _u16(q)
+    k8 = np.ascontiguousarray(k8, dtype=np.uint8)
+    v8 = np.ascontiguousarray(v8, dtype=np.uint8)
+    ks = np.ascontiguousarray(k_scale, dtype=np.float32)
+    vs = np.ascontiguousarray(v_scale, dtype=np.float32)
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    b, hq, d = q.shape
+    n, hkv, groups, p, eight = k8.shape
+    assert groups * eight == d and v8.shape == (n, hkv, d, p) and ks.shape == (n, hkv) and vs.shape == (n, hkv)
+    out = np.empty((b, hq, d), dtype=np.float64)
+    lse = np.empty((b, hq), dtype=np.float64)
+    rc = lib().sf_oracle_decode_attn_fp8(b, hq, hkv, d, p, bt.shape[1], n, _ptr(q), _ptr(k8), _ptr(v8), _ptr(ks),
+                                         _ptr(vs), _ptr(bt), _ptr(lens), float(scale), _ptr(out), _ptr(lse),
+                                         int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle rejected its input (code {rc})")
+    return out, lse
+
+
+def e4m3_value(code: int) -> float:
+    """The value of an OCP FP8 E4M3 code, from the format definition (C side)."""
+    return float(lib().sf_oracle_e4m3_value(int(code)))
 
 
 def gather(k_pool, v_pool, block_table, seq: int, kvh: int, length: int):

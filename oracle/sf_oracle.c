@@ -53,7 +53,7 @@ static double bf16_to_double(uint16_t bits) {
   return (double)f;
 }
 
-int sf_oracle_version(void) { return 2; }
+int sf_oracle_version(void) { return 3; }
 
 int sf_oracle_max_threads(void) {
 #ifdef _OPENMP
@@ -158,6 +158,94 @@ int sf_oracle_decode_attn(int B, int Hq, int Hkv, int D, int P, int stride, int 
         double w = exp(z[t] - m);
         wsum += w;
         for (int d = 0; d < D; ++d) acc[d] += w * bf16_to_double(v_pool[v_index(pg, Hkv, kvh, D, P, slot, d)]);
+      }
+      for (int d = 0; d < D; ++d) o[d] = acc[d] / wsum;
+      if (lse) lse[sh] = m + log(wsum);
+    }
+    free(z);
+    free(acc);
+  }
+  return 0;
+}
+
+/*
+ * fp8 KV cache (next to the bf16 one): keys and values stored as OCP FP8
+ * E4M3 codes, one fp32 scale per (page, KV head) tile for K and one for V.
+ * A code (sign s, exponent e, mantissa m) is
+ *   (-1)^s * m/8 * 2^-6            if e = 0
+ *   (-1)^s * (1 + m/8) * 2^(e - 7) otherwise, NaN for e = 15, m = 7,
+ * and the cached key of slot t, dim d is that value times k_scale[page][kvh]
+ * (values likewise with v_scale). Layouts as the bf16 pools, one byte per
+ * element: k8 [N][Hkv][D/8][P][8], v8 [N][Hkv][D][P], scales [N][Hkv].
+ * The attention itself is the bf16 oracle's: widen exactly, fp64 throughout.
+ */
+double sf_oracle_e4m3_value(int code) {
+  const int s = (code >> 7) & 1, e = (code >> 3) & 15, m = code & 7;
+  double v;
+  if (e == 15 && m == 7) return NAN;
+  if (e == 0) v = ldexp((double)m / 8.0, -6);
+  else v = ldexp(1.0 + (double)m / 8.0, e - 7);
+  return s ? -v : v;
+}
+
+int sf_oracle_decode_attn_fp8(int B, int Hq, int Hkv, int D, int P, int stride, int num_pages,
+                              const uint16_t* q, const uint8_t* k8, const uint8_t* v8,
+                              const float* k_scale, const float* v_scale,
+                              const int32_t* bt, const int32_t* lens, double scale,
+                              double* out, double* lse, int nthreads) {
+  if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || D <= 0 || P <= 0) return -1;
+  int bad = check_pages(B, P, stride, num_pages, bt, lens);
+  if (bad) return bad;
+  double table[256];
+  for (int c = 0; c < 256; ++c) table[c] = sf_oracle_e4m3_value(c);
+  const int g = Hq / Hkv;
+  const int64_t pairs = (int64_t)B * Hq;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#endif
+#pragma omp parallel
+  {
+    double* z = NULL;
+    double* acc = (double*)malloc(sizeof(double) * (size_t)D);
+    int zcap = 0;
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t sh = 0; sh < pairs; ++sh) {
+      const int s = (int)(sh / Hq);
+      const int h = (int)(sh % Hq);
+      const int kvh = h / g;
+      const int L = lens[s];
+      double* o = out + sh * D;
+      if (L == 0) {
+        for (int d = 0; d < D; ++d) o[d] = 0.0;
+        if (lse) lse[sh] = -INFINITY;
+        continue;
+      }
+      if (L > zcap) {
+        free(z);
+        z = (double*)malloc(sizeof(double) * (size_t)L);
+        zcap = L;
+      }
+      const uint16_t* qv = q + sh * D;
+      double m = -INFINITY;
+      for (int t = 0; t < L; ++t) {
+        int32_t pg = bt[(int64_t)s * stride + t / P];
+        int slot = t % P;
+        double ks = (double)k_scale[(int64_t)pg * Hkv + kvh];
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d)
+          dot += bf16_to_double(qv[d]) * (table[k8[k_index(pg, Hkv, kvh, D, P, slot, d)]] * ks);
+        z[t] = scale * dot;
+        if (z[t] > m) m = z[t];
+      }
+      double wsum = 0.0;
+      for (int d = 0; d < D; ++d) acc[d] = 0.0;
+      for (int t = 0; t < L; ++t) {
+        int32_t pg = bt[(int64_t)s * stride + t / P];
+        int slot = t % P;
+        double vs = (double)v_scale[(int64_t)pg * Hkv + kvh];
+        double w = exp(z[t] - m);
+        wsum += w;
+        for (int d = 0; d < D; ++d) acc[d] += w * (table[v8[v_index(pg, Hkv, kvh, D, P, slot, d)]] * vs);
       }
       for (int d = 0; d < D; ++d) o[d] = acc[d] / wsum;
       if (lse) lse[sh] = m + log(wsum);
