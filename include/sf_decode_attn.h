@@ -199,6 +199,42 @@ sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* in
                                 float* lse, void* workspace, uint64_t workspace_bytes, void* stream);
 
 /*
+ * fp8 KV cache. The paper lists KV-cache quantization among the
+ * optimizations its design is compatible with (Sec. 7); this variant halves
+ * the bytes a decode step reads. Keys and values are OCP FP8 E4M3 codes
+ * (sign, 4 exponent bits with bias 7, 3 mantissa bits; 0x7F / 0xFF are NaN,
+ * the largest finite magnitude is 448), one byte per element in the bf16
+ * pools' layouts: k_pool8 [num_pages][Hkv][D/8][16][8], v_pool8
+ * [num_pages][Hkv][D][16]. Each (page, KV head) tile has one fp32 scale for
+ * K and one for V: k_scale, v_scale [num_pages][Hkv]. The cached key of slot
+ * t, dim d is value(code) * k_scale[page][kvh] (values likewise), and the
+ * attention is the decode step's over those values.
+ *
+ * sf_decode_attn_fp8: as sf_decode_attn (same plan, work list and workspace;
+ * follow it with sf_decode_attn_combine for split sequences) over an fp8
+ * cache. SF_ERR_INVALID_ARG also for NULL scales when num_pages > 0.
+ */
+sf_status sf_decode_attn_fp8(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_host,
+                             int32_t* work_dev, const void* q, const void* k_pool8, const void* v_pool8,
+                             const float* k_scale, const float* v_scale, const int32_t* block_table,
+                             float* out, float* lse, void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * Quantizes pages of a bf16 cache into an fp8 one (both laid out as above).
+ * For each listed page p = pages[i] (device int32 [num_pages]) with
+ * n = valid_slots[i] valid slots (device int32, 1 .. 16), and every KV head,
+ * separately for the K tile and the V tile of the slots 0 .. n-1:
+ *   amax = max |x|;  scale = amax / 448;  inv = 448 / amax   (fp32, correctly
+ *   rounded; scale = inv = 1 for an all-zero tile)
+ *   code = E4M3 round-to-nearest-even of the fp32 product x * inv
+ * Slots n .. 15 get code 0. Writes k_pool8, v_pool8, k_scale[p][*] and
+ * v_scale[p][*]; other pages are untouched. One launch on the stream.
+ */
+sf_status sf_kv_quantize_fp8(const sf_attn_desc* desc, const void* k_pool, const void* v_pool,
+                             const int32_t* pages, const int32_t* valid_slots, int32_t num_pages,
+                             void* k_pool8, void* v_pool8, float* k_scale, float* v_scale, void* stream);
+
+/*
  * Extend (re-prefill) attention. A trajectory interrupted for a model update
  * or migrated to another instance has its KV cache recomputed before its
  * generation resumes (partial rollout and migration, Sec. 2.3; prefill and

@@ -94,6 +94,9 @@ def lib():
                                      ctypes.c_int32, vp, vp, vp]
     L.sf_decode_attn_append.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp,
                                         vp, vp, vp, vp, ctypes.c_uint64, vp]
+    L.sf_decode_attn_fp8.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                     ctypes.c_uint64, vp]
+    L.sf_kv_quantize_fp8.argtypes = [P(sf_attn_desc), vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp, vp, vp]
     L.sf_extend_attn_plan.argtypes = [P(sf_attn_desc), vp, vp, vp, ctypes.c_uint64, P(sf_extend_info)]
     L.sf_extend_attn.argtypes = [P(sf_attn_desc), P(sf_extend_info), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sf_page_pool_create.argtypes = [ctypes.c_int32, P(vp)]
@@ -115,7 +118,7 @@ def lib():
     for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv",
                "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
                "sf_page_pool_release", "sf_page_table_step", "sf_route", "sf_extend_attn_plan",
-               "sf_extend_attn"):
+               "sf_extend_attn", "sf_decode_attn_fp8", "sf_kv_quantize_fp8"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -238,6 +241,48 @@ def sf_decode_attn(desc, info, work_host, work_dev, q, k_pool, v_pool, block_tab
         ctypes.byref(desc), ctypes.byref(info), _addr(work_host), _addr(work_dev), _addr(q),
         _addr(k_pool), _addr(v_pool), _addr(block_table), _addr(out), _addr(lse),
         _addr(workspace), ws_bytes, _stream(stream)))
+
+
+def sf_decode_attn_fp8(desc, info, work_host, work_dev, q, k_pool8, v_pool8, k_scale, v_scale, block_table, out,
+                       lse=None, workspace=None, stream=None):
+    """Enqueues the attention kernel over an fp8 cache (uint8 pools, fp32 scales [N, Hkv])."""
+    b, hq, hkv, d = desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
+    _dev(q, "q", torch.bfloat16, (b, hq, d))
+    _dev(k_pool8, "k_pool8", torch.uint8, (desc.num_pages, hkv, d // 8, PAGE, 8))
+    _dev(v_pool8, "v_pool8", torch.uint8, (desc.num_pages, hkv, d, PAGE))
+    _dev(k_scale, "k_scale", torch.float32, (desc.num_pages, hkv))
+    _dev(v_scale, "v_scale", torch.float32, (desc.num_pages, hkv))
+    _dev(block_table, "block_table", torch.int32, (b, desc.block_table_stride))
+    _dev(out, "out", torch.float32, (b, hq, d))
+    _dev(work_dev, "work_dev", torch.int32)
+    if work_dev.numel() * 4 < info.work_bytes:
+        raise ValueError("work_dev is smaller than the plan")
+    if lse is not None:
+        _dev(lse, "lse", torch.float32, (b, hq))
+    ws_bytes = 0
+    if workspace is not None:
+        _dev(workspace, "workspace", workspace.dtype)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check("sf_decode_attn_fp8", lib().sf_decode_attn_fp8(
+        ctypes.byref(desc), ctypes.byref(info), _addr(work_host), _addr(work_dev), _addr(q), _addr(k_pool8),
+        _addr(v_pool8), _addr(k_scale), _addr(v_scale), _addr(block_table), _addr(out), _addr(lse),
+        _addr(workspace), ws_bytes, _stream(stream)))
+
+
+def sf_kv_quantize_fp8(desc, k_pool, v_pool, pages, valid_slots, k_pool8, v_pool8, k_scale, v_scale, stream=None):
+    """Quantizes the listed pages (device int32 pages / valid_slots) of bf16 pools into fp8 ones."""
+    hkv, d = desc.num_kv_heads, desc.head_dim
+    _dev(k_pool, "k_pool", torch.bfloat16, (desc.num_pages, hkv, d // 8, PAGE, 8))
+    _dev(v_pool, "v_pool", torch.bfloat16, (desc.num_pages, hkv, d, PAGE))
+    _dev(pages, "pages", torch.int32)
+    _dev(valid_slots, "valid_slots", torch.int32, tuple(pages.shape))
+    _dev(k_pool8, "k_pool8", torch.uint8, (desc.num_pages, hkv, d // 8, PAGE, 8))
+    _dev(v_pool8, "v_pool8", torch.uint8, (desc.num_pages, hkv, d, PAGE))
+    _dev(k_scale, "k_scale", torch.float32, (desc.num_pages, hkv))
+    _dev(v_scale, "v_scale", torch.float32, (desc.num_pages, hkv))
+    _check("sf_kv_quantize_fp8", lib().sf_kv_quantize_fp8(
+        ctypes.byref(desc), _addr(k_pool), _addr(v_pool), _addr(pages), _addr(valid_slots), int(pages.numel()),
+        _addr(k_pool8), _addr(v_pool8), _addr(k_scale), _addr(v_scale), _stream(stream)))
 
 
 def sf_decode_attn_append(desc, info, work_host, work_dev, q, k_new, v_new, new_pages, k_pool, v_pool,
@@ -556,16 +601,21 @@ class DecodeAttention:
             return o
         return sf_plan_opts(o.num_cus, int(chunk_pages), o.workers_per_cu, o.min_chunk_pages, 0)
 
-    def _check_tensors(self, q, k_pool, v_pool, block_table, out, lse):
+    def _check_tensors(self, q, k_pool, v_pool, block_table, out, lse, fp8=None):
         key = (q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
                out.data_ptr(), None if lse is None else lse.data_ptr(), tuple(q.shape),
-               tuple(k_pool.shape), tuple(v_pool.shape), tuple(block_table.shape))
+               tuple(k_pool.shape), tuple(v_pool.shape), tuple(block_table.shape),
+               None if fp8 is None else (fp8[0].data_ptr(), fp8[1].data_ptr()))
         if key == self._checked:
             return
         b, hkv, d = q.shape[0], self.hkv, self.d
+        pool_t = torch.bfloat16 if fp8 is None else torch.uint8
         _dev(q, "q", torch.bfloat16, (b, self.hq, d))
-        _dev(k_pool, "k_pool", torch.bfloat16, (k_pool.shape[0], hkv, d // 8, PAGE, 8))
-        _dev(v_pool, "v_pool", torch.bfloat16, (k_pool.shape[0], hkv, d, PAGE))
+        _dev(k_pool, "k_pool", pool_t, (k_pool.shape[0], hkv, d // 8, PAGE, 8))
+        _dev(v_pool, "v_pool", pool_t, (k_pool.shape[0], hkv, d, PAGE))
+        if fp8 is not None:
+            _dev(fp8[0], "k_scale", torch.float32, (k_pool.shape[0], hkv))
+            _dev(fp8[1], "v_scale", torch.float32, (k_pool.shape[0], hkv))
         _dev(block_table, "block_table", torch.int32, (b, block_table.shape[1]))
         _dev(out, "out", torch.float32, (b, self.hq, d))
         if lse is not None:
@@ -589,19 +639,23 @@ class DecodeAttention:
 
     def __call__(self, q, k_pool, v_pool, block_table, seq_lens, scale, out=None, lse=None,
                  chunk_pages=None, stream: torch.cuda.Stream | None = None, attn_events=None,
-                 append=None):
+                 append=None, fp8=None):
         """One decode step on `stream` (default: the current stream). attn_events,
         if given, is a (start, end) pair of torch events recorded around the
         attention kernel. append = (k_new, v_new, new_pages) makes it an
         append-then-attend step: k_new, v_new are device bf16 [B, Hkv, D] and
         new_pages a host int32 [B] array (-1 = the token's page is already
-        held), uploaded together with the work list."""
+        held), uploaded together with the work list. fp8 = (k_scale, v_scale)
+        makes k_pool / v_pool an fp8 cache (uint8 E4M3 codes, fp32 scales
+        [N, Hkv]); it cannot be combined with append."""
+        if fp8 is not None and append is not None:
+            raise ValueError("the fp8 cache has no appending step")
         b = q.shape[0]
         main = stream or torch.cuda.current_stream(self.device)
         main_h = main.cuda_stream
         if out is None:
             out = torch.empty((b, self.hq, self.d), dtype=torch.float32, device=self.device)
-        self._check_tensors(q, k_pool, v_pool, block_table, out, lse)
+        self._check_tensors(q, k_pool, v_pool, block_table, out, lse, fp8)
         dkey = (b, block_table.shape[1], k_pool.shape[0], float(scale))
         if dkey != self._desc_key:
             self._desc = make_desc(b, self.hq, self.hkv, self.d, block_table.shape[1], k_pool.shape[0], scale)
@@ -650,7 +704,12 @@ class DecodeAttention:
         if attn_events is not None:
             attn_events[0].record(main)
         ws = self.workspace
-        if append is None:
+        if fp8 is not None:
+            _check("sf_decode_attn_fp8", self.L.sf_decode_attn_fp8(
+                ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
+                k_pool.data_ptr(), v_pool.data_ptr(), fp8[0].data_ptr(), fp8[1].data_ptr(), block_table.data_ptr(),
+                out.data_ptr(), None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
+        elif append is None:
             _check("sf_decode_attn", self.L.sf_decode_attn(
                 ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
                 k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),

@@ -76,7 +76,8 @@ CombineArgs combine_args(const sf_attn_desc* desc, const sf_plan_info* info, con
 sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_host,
                  int32_t* work_dev, const void* q, const void* k_pool, const void* v_pool,
                  const int32_t* block_table, float* out, float* lse, void* workspace,
-                 uint64_t workspace_bytes, void* stream, const AppendArgs* app) {
+                 uint64_t workspace_bytes, void* stream, const AppendArgs* app,
+                 const float* k_scale = nullptr, const float* v_scale = nullptr) {
   sf_status st = validate_desc(desc);
   if (st != SF_OK) return st;
   if ((st = check_plan(desc, info)) != SF_OK) return st;
@@ -87,6 +88,8 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
   if (!aligned16(work_dev) || !aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) ||
       !aligned16(out) || !aligned4(block_table) || (lse && !aligned4(lse)))
     return SF_ERR_INVALID_ARG;
+  if ((k_scale == nullptr) != (v_scale == nullptr)) return SF_ERR_INVALID_ARG;
+  if (k_scale && desc->num_pages > 0 && (!aligned4(k_scale) || !aligned4(v_scale))) return SF_ERR_INVALID_ARG;
   if (app && (!app->k_new || !app->v_new || !aligned16(app->k_new) || !aligned16(app->v_new) ||
               (app->new_pages && !aligned4(app->new_pages)) || !lse))
     return SF_ERR_INVALID_ARG;
@@ -121,6 +124,8 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
   a.k_new = app ? static_cast<const uint16_t*>(app->k_new) : nullptr;
   a.v_new = app ? static_cast<const uint16_t*>(app->v_new) : nullptr;
   a.new_pages = app ? app->new_pages : nullptr;
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
   if ((st = from_hip(launch_attention(a, s))) != SF_OK || !app) return st;
   const CombineArgs m = combine_args(desc, info, work_dev, workspace, out, lse, app, const_cast<void*>(k_pool),
                                      const_cast<void*>(v_pool), const_cast<int32_t*>(block_table));
@@ -147,6 +152,47 @@ extern "C" sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_pl
   const AppendArgs app = {q, k_new, v_new, new_pages};
   return attend(desc, info, work_host, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
                 workspace_bytes, stream, &app);
+}
+
+extern "C" sf_status sf_decode_attn_fp8(const sf_attn_desc* desc, const sf_plan_info* info,
+                                        const int32_t* work_host, int32_t* work_dev, const void* q,
+                                        const void* k_pool8, const void* v_pool8, const float* k_scale,
+                                        const float* v_scale, const int32_t* block_table, float* out,
+                                        float* lse, void* workspace, uint64_t workspace_bytes, void* stream) {
+  if (desc && desc->num_pages > 0 && (!k_scale || !v_scale)) return SF_ERR_INVALID_ARG;
+  // With no pages there is nothing to scale; any non-NULL pointer marks the fp8 path.
+  static const float kNoScale = 1.f;
+  return attend(desc, info, work_host, work_dev, q, k_pool8, v_pool8, block_table, out, lse, workspace,
+                workspace_bytes, stream, nullptr, k_scale ? k_scale : &kNoScale, v_scale ? v_scale : &kNoScale);
+}
+
+extern "C" sf_status sf_kv_quantize_fp8(const sf_attn_desc* desc, const void* k_pool, const void* v_pool,
+                                        const int32_t* pages, const int32_t* valid_slots, int32_t num_pages,
+                                        void* k_pool8, void* v_pool8, float* k_scale, float* v_scale,
+                                        void* stream) {
+  sf_status st = validate_desc(desc);
+  if (st != SF_OK) return st;
+  if (num_pages < 0) return SF_ERR_INVALID_ARG;
+  if (num_pages == 0) return SF_OK;
+  if (desc->num_pages == 0 || !k_pool || !v_pool || !pages || !valid_slots || !k_pool8 || !v_pool8 || !k_scale ||
+      !v_scale)
+    return SF_ERR_INVALID_ARG;
+  if (!aligned16(k_pool) || !aligned16(v_pool) || !aligned16(k_pool8) || !aligned16(v_pool8) || !aligned4(pages) ||
+      !aligned4(valid_slots) || !aligned4(k_scale) || !aligned4(v_scale))
+    return SF_ERR_INVALID_ARG;
+  QuantArgs a;
+  a.k_src = static_cast<const uint16_t*>(k_pool);
+  a.v_src = static_cast<const uint16_t*>(v_pool);
+  a.pages = pages;
+  a.valid = valid_slots;
+  a.num_pages = num_pages;
+  a.k_dst = static_cast<uint8_t*>(k_pool8);
+  a.v_dst = static_cast<uint8_t*>(v_pool8);
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
+  a.num_kv_heads = desc->num_kv_heads;
+  a.head_dim = desc->head_dim;
+  return from_hip(launch_quantize_fp8(a, static_cast<hipStream_t>(stream)));
 }
 
 extern "C" sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_plan_info* info,

@@ -203,9 +203,16 @@ struct BlockWeights {
 // nvalid = tokens of the block (from its first token) inside the sequence.
 // kMayBeEmpty: the block may hold no valid token (then nothing changes);
 // without it every block holds at least one, as in a plain decode step.
-template <int D, bool kMayBeEmpty = false>
+// Per-page factors of a block for an fp8 cache: the score scale of each page
+// (softmax scale * log2(e) * the page's K scale) and each page's V scale.
+struct PageScales {
+  float c0, c1, v0, v1;
+};
+
+template <int D, bool kMayBeEmpty = false, bool kScaled = false>
 __device__ __forceinline__ BlockWeights score_block(const KHalf<D>& b, const u32x4* qf, int nvalid, int grp,
-                                                    float scale_log2, SoftmaxState<D>& st) {
+                                                    float scale_log2, SoftmaxState<D>& st,
+                                                    PageScales scl = PageScales{0.f, 0.f, 0.f, 0.f}) {
   f32x4 s0 = {0.f, 0.f, 0.f, 0.f};
   f32x4 s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -216,10 +223,12 @@ __device__ __forceinline__ BlockWeights score_block(const KHalf<D>& b, const u32
   // This lane now holds head `col`: s0[e] = slot 4*grp + e of the first page,
   // s1[e] = the same slot of the second page.
   float sc[8];
+  const float c0 = kScaled ? scl.c0 : scale_log2;
+  const float c1 = kScaled ? scl.c1 : scale_log2;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    sc[e] = (item_token(grp, e) < nvalid) ? s0[e] * scale_log2 : -__builtin_inff();
-    sc[4 + e] = (item_token(grp, 4 + e) < nvalid) ? s1[e] * scale_log2 : -__builtin_inff();
+    sc[e] = (item_token(grp, e) < nvalid) ? s0[e] * c0 : -__builtin_inff();
+    sc[4 + e] = (item_token(grp, 4 + e) < nvalid) ? s1[e] * c1 : -__builtin_inff();
   }
   float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
                    fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
@@ -236,9 +245,15 @@ __device__ __forceinline__ BlockWeights score_block(const KHalf<D>& b, const u32
   uint32_t hi[4], lo[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float p0 = fast_exp2(sc[2 * i] - mref);
-    const float p1 = fast_exp2(sc[2 * i + 1] - mref);
+    float p0 = fast_exp2(sc[2 * i] - mref);
+    float p1 = fast_exp2(sc[2 * i + 1] - mref);
     ps += p0 + p1;
+    if constexpr (kScaled) {
+      // The P.V operand carries the page's V scale (the weight sum does not).
+      const float vs = i < 2 ? scl.v0 : scl.v1;
+      p0 *= vs;
+      p1 *= vs;
+    }
     const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
     const uint32_t l0 = bf16_bits(p0 - bf16_value(h0)), l1 = bf16_bits(p1 - bf16_value(h1));
     hi[i] = h0 | (h1 << 16);
@@ -419,6 +434,269 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 }
 
 // ---------------------------------------------------------------------------
+// attention over an fp8 (OCP E4M3) cache with per-(page, KV head) scales
+// ---------------------------------------------------------------------------
+// The pools hold one-byte codes in the bf16 pools' layouts (a tile is 16*D
+// bytes), so a block moves half the bytes. The codes are widened to bf16 in
+// registers just before use; every E4M3 value is a bf16 value, so this is
+// exact and the MFMAs are the bf16 path's. The page's K scale joins the
+// score scale, its V scale the P.V operand: no per-element scaling.
+template <int D>
+struct KHalf8 {
+  u32x2 k[2][Shape<D>::KB];   // 8 codes: dims 32*kb + 8*grp .. +7 of slot col
+  float ks[2];
+};
+
+template <int D>
+struct VHalf8 {
+  uint32_t v[2][Shape<D>::JB];  // 4 codes: slots 4*grp .. +3 of dim 16*jb + col
+  float vs[2];
+};
+
+// Codes 0, 1 (kHigh false) or 2, 3 (kHigh true) of four packed codes as two bf16.
+template <bool kHigh>
+__device__ __forceinline__ uint32_t widen2(uint32_t codes4) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes4, 1.0f, kHigh));
+}
+
+template <int D>
+struct ChunkCtx8 {
+  const uint8_t* k_pool;
+  const uint8_t* v_pool;
+  const float* k_scale;
+  const float* v_scale;
+  const_i32_ptr bt;
+  int num_kv_heads;
+  int kvh;
+  int pe;
+  int k_off;
+  int v_off;
+};
+
+template <int D>
+__device__ __forceinline__ PagePair block_pages8(const ChunkCtx8<D>& c, int pg) {
+  PagePair pp;
+  pp.p0 = c.bt[pg];
+  pp.p1 = pg + 1 < c.pe ? c.bt[pg + 1] : pp.p0;
+  return pp;
+}
+
+// The scales are never written while a kernel runs: scalar loads.
+__device__ __forceinline__ float scale_of(const float* base, int page, int num_kv_heads, int kvh) {
+  typedef __attribute__((address_space(4))) const float* const_f32_ptr;
+  return ((const_f32_ptr)base)[size_t(page) * num_kv_heads + kvh];
+}
+
+template <int D>
+__device__ __forceinline__ void load_k8(const ChunkCtx8<D>& c, PagePair pp, KHalf8<D>& b) {
+  const uint8_t* k0 = c.k_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.k_off;
+  const uint8_t* k1 = c.k_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.k_off;
+#pragma unroll
+  for (int kb = 0; kb < Shape<D>::KB; ++kb) {
+    b.k[0][kb] = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(k0 + k_elem(0, 32 * kb, D)));
+    b.k[1][kb] = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(k1 + k_elem(0, 32 * kb, D)));
+  }
+  b.ks[0] = scale_of(c.k_scale, pp.p0, c.num_kv_heads, c.kvh);
+  b.ks[1] = scale_of(c.k_scale, pp.p1, c.num_kv_heads, c.kvh);
+}
+
+template <int D>
+__device__ __forceinline__ void load_v8(const ChunkCtx8<D>& c, PagePair pp, VHalf8<D>& b) {
+  const uint8_t* v0 = c.v_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.v_off;
+  const uint8_t* v1 = c.v_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.v_off;
+#pragma unroll
+  for (int jb = 0; jb < Shape<D>::JB; ++jb) {
+    b.v[0][jb] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(v0 + v_elem(0, 16 * jb)));
+    b.v[1][jb] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(v1 + v_elem(0, 16 * jb)));
+  }
+  b.vs[0] = scale_of(c.v_scale, pp.p0, c.num_kv_heads, c.kvh);
+  b.vs[1] = scale_of(c.v_scale, pp.p1, c.num_kv_heads, c.kvh);
+}
+
+template <int D>
+__device__ __forceinline__ void widen_k(const KHalf8<D>& r, KHalf<D>& b) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int kb = 0; kb < Shape<D>::KB; ++kb)
+      b.k[h][kb] = u32x4{widen2<false>(r.k[h][kb][0]), widen2<true>(r.k[h][kb][0]), widen2<false>(r.k[h][kb][1]),
+                         widen2<true>(r.k[h][kb][1])};
+}
+
+template <int D>
+__device__ __forceinline__ void widen_v(const VHalf8<D>& r, VHalf<D>& b) {
+#pragma unroll
+  for (int jb = 0; jb < Shape<D>::JB; ++jb)
+    b.v[jb] = u32x4{widen2<false>(r.v[0][jb]), widen2<true>(r.v[0][jb]), widen2<false>(r.v[1][jb]),
+                    widen2<true>(r.v[1][jb])};
+}
+
+// One segment over an fp8 cache; otherwise as attend_segment.
+template <int D>
+__device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const_i32_ptr item) {
+  constexpr int KB = Shape<D>::KB;
+  constexpr int JB = Shape<D>::JB;
+  const int lane = threadIdx.x;
+  const int col = lane & 15;
+  const int grp = lane >> 4;
+  const int seq = item[0];
+  const int kvh = item[1];
+  const int pb = item[2];
+  const int pe = item[3];
+  const int len = item[4];
+  const int slot = item[5];
+  const int g = a.group;
+  const bool head_ok = col < g;
+  const int head = kvh * g + col;
+
+  ChunkCtx8<D> c;
+  c.k_pool = reinterpret_cast<const uint8_t*>(a.k_pool);
+  c.v_pool = reinterpret_cast<const uint8_t*>(a.v_pool);
+  c.k_scale = a.k_scale;
+  c.v_scale = a.v_scale;
+  c.bt = as_constant(a.block_table) + size_t(seq) * a.bt_stride;
+  c.num_kv_heads = a.num_kv_heads;
+  c.kvh = kvh;
+  c.pe = pe;
+  c.k_off = k_elem(col, 8 * grp, D);
+  c.v_off = v_elem(4 * grp, col);
+
+  KHalf8<D> kr[2];
+  VHalf8<D> vr[2];
+  if (pb < pe) {
+    const PagePair pp = block_pages8(c, pb);
+    load_k8(c, pp, kr[0]);
+    load_v8(c, pp, vr[0]);
+  }
+  u32x4 qf[KB];
+  {
+    const uint16_t* qrow = a.q + (size_t(seq) * a.num_q_heads + (head_ok ? head : kvh * g)) * D + grp * 8;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      u32x4 v = load16(qrow + kb * 32);
+      qf[kb] = head_ok ? v : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  SoftmaxState<D> st;
+#pragma unroll
+  for (int jb = 0; jb < JB; ++jb) st.o[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.m = -__builtin_inff();
+  st.lsum = 0.f;
+
+  auto step = [&](int pg, KHalf8<D>& kc, VHalf8<D>& vc, KHalf8<D>& kn, VHalf8<D>& vn) {
+    const bool more = pg + 2 < pe;
+    PagePair nxt = {0, 0};
+    if (more) {
+      nxt = block_pages8(c, pg + 2);
+      load_k8(c, nxt, kn);
+    }
+    const int nvalid = min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage);
+    KHalf<D> kw;
+    widen_k(kc, kw);
+    const PageScales scl{a.scale_log2 * kc.ks[0], a.scale_log2 * kc.ks[1], vc.vs[0], vc.vs[1]};
+    const BlockWeights w = score_block<D, false, true>(kw, qf, nvalid, grp, a.scale_log2, st, scl);
+    if (more) load_v8(c, nxt, vn);
+    VHalf<D> vw;
+    widen_v(vc, vw);
+    accumulate_block(vw, w, nvalid, grp, st);
+  };
+  for (int pg = pb; pg < pe; pg += 4) {
+    step(pg, kr[0], vr[0], kr[1], vr[1]);
+    if (pg + 2 >= pe) break;
+    step(pg + 2, kr[1], vr[1], kr[0], vr[0]);
+  }
+
+  float lt = st.lsum + __shfl_xor(st.lsum, 16);
+  lt += __shfl_xor(lt, 32);
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+  if (slot < 0) {
+    if (!head_ok) return;
+    float* dst = a.out + (size_t(seq) * a.num_q_heads + head) * D + 4 * grp;
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
+    if (a.lse && grp == 0)
+      a.lse[size_t(seq) * a.num_q_heads + head] = lt > 0.f ? (st.m + __log2f(lt)) * kLn2 : -__builtin_inff();
+    return;
+  }
+  if (head_ok) {
+    float* dst = a.part_o + (size_t(slot) * g + col) * D + 4 * grp;
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
+    if (grp == 0) a.part_lse[size_t(slot) * g + col] = st.m + __log2f(lt);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_fp8_kernel(AttnArgs a) {
+  const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
+  const int first = wt[0];
+  const int count = wt[1];
+  for (int i = 0; i < count; ++i) attend_segment_fp8<D>(a, as_constant(a.items) + size_t(first + i) * kItemInts);
+}
+
+// ---------------------------------------------------------------------------
+// per-page fp8 quantizer
+// ---------------------------------------------------------------------------
+// One block per listed page: for every KV head, the K tile and then the V
+// tile (16 * D bf16 values each) become E4M3 codes with one scale per tile:
+//   amax = max |x| over the valid slots;  scale = amax / 448, inv = 448 / amax
+//   (correctly rounded; 1 and 1 for an all-zero tile);
+//   code = round-to-nearest-even(x * inv), 0 for slots past the valid count.
+template <int D>
+__global__ __launch_bounds__(256) void quantize_fp8_kernel(QuantArgs a) {
+  __shared__ float red[4];
+  const int page = as_constant(a.pages)[blockIdx.x];
+  const int valid = as_constant(a.valid)[blockIdx.x];
+  constexpr int kPieces = kPage * D / 8;   // 8 values per piece
+  for (int kvh = 0; kvh < a.num_kv_heads; ++kvh) {
+#pragma unroll
+    for (int which = 0; which < 2; ++which) {
+      const uint16_t* src = (which == 0 ? a.k_src : a.v_src) + tile_offset(page, a.num_kv_heads, kvh, D);
+      uint8_t* dst = (which == 0 ? a.k_dst : a.v_dst) + tile_offset(page, a.num_kv_heads, kvh, D);
+      float* scale_out = which == 0 ? a.k_scale : a.v_scale;
+      // Slot of value e of piece i: K tiles hold 8 dims of one slot per
+      // piece; V tiles 8 consecutive slots of one dim.
+      auto slot_of = [&](int piece, int e) { return which == 0 ? piece % kPage : (piece * 8 + e) % kPage; };
+      float amax = 0.f;
+      for (int i = threadIdx.x; i < kPieces; i += 256) {
+        const u32x4 x = load16(src + 8 * i);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = bf16_value((x[e / 2] >> (16 * (e & 1))) & 0xFFFFu);
+          if (slot_of(i, e) < valid) amax = fmaxf(amax, fabsf(v));
+        }
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+      if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
+      __syncthreads();
+      amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+      __syncthreads();
+      const float inv = amax > 0.f ? __fdiv_rn(448.f, amax) : 1.f;
+      if (threadIdx.x == 0) scale_out[size_t(page) * a.num_kv_heads + kvh] = amax > 0.f ? __fdiv_rn(amax, 448.f) : 1.f;
+      for (int i = threadIdx.x; i < kPieces; i += 256) {
+        const u32x4 x = load16(src + 8 * i);
+        uint32_t w[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          float f[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int idx = 4 * q + e;
+            const float v = bf16_value((x[idx / 2] >> (16 * (idx & 1))) & 0xFFFFu);
+            f[e] = slot_of(i, idx) < valid ? v * inv : 0.f;
+          }
+          int packed = __builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], 0, false);
+          packed = __builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], packed, true);
+          w[q] = uint32_t(packed);
+        }
+        *reinterpret_cast<u32x2*>(dst + 8 * i) = u32x2{w[0], w[1]};
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // log-sum-exp merge of the chunks of split (sequence, KV head) pairs
 // ---------------------------------------------------------------------------
 // Merges the n partial results of a split pair for head h, dims 4*d4 .. +3:
@@ -581,6 +859,13 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
   if (a.num_workers == 0) return hipSuccess;
   const dim3 grid(a.num_workers), block(64);
+  if (a.k_scale) {
+    if (a.head_dim == 128)
+      hipLaunchKernelGGL(attn_worker_fp8_kernel<128>, grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL(attn_worker_fp8_kernel<64>, grid, block, 0, stream, a);
+    return hipGetLastError();
+  }
   const bool append = a.k_new != nullptr;
   if (a.head_dim == 128) {
     if (append)
@@ -608,6 +893,15 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
   }
   if (a.num_items == 0) return hipSuccess;
   hipLaunchKernelGGL(combine_kernel, dim3(a.num_items), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_fp8(const QuantArgs& a, hipStream_t stream) {
+  if (a.num_pages == 0) return hipSuccess;
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL(quantize_fp8_kernel<128>, dim3(a.num_pages), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(quantize_fp8_kernel<64>, dim3(a.num_pages), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -54,6 +54,10 @@ struct AttnArgs {
   const uint16_t* k_new;      // [B][Hkv][D] newest token's keys
   const uint16_t* v_new;      // [B][Hkv][D] and values
   const int32_t* new_pages;   // [B] page newly given to that token, -1 = none; may be NULL
+  // fp8 cache (sf_decode_attn_fp8 only; NULL otherwise): k_pool / v_pool then
+  // hold E4M3 codes, and these the per-(page, KV head) scales.
+  const float* k_scale;
+  const float* v_scale;
 };
 
 struct CombineArgs {
@@ -81,6 +85,20 @@ struct CombineArgs {
   uint16_t* v_dst;
   int32_t num_kv_heads;
   int32_t bt_stride;
+};
+
+struct QuantArgs {
+  const uint16_t* k_src;      // bf16 pools
+  const uint16_t* v_src;
+  const int32_t* pages;       // [num_pages] pages to quantize
+  const int32_t* valid;       // [num_pages] valid slots of each (1 .. 16)
+  int32_t num_pages;
+  uint8_t* k_dst;             // fp8 pools
+  uint8_t* v_dst;
+  float* k_scale;             // [pool pages][Hkv]
+  float* v_scale;
+  int32_t num_kv_heads;
+  int32_t head_dim;
 };
 
 struct GatherArgs {
@@ -128,5 +146,6 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
+hipError_t launch_quantize_fp8(const QuantArgs& a, hipStream_t stream);
 
 }  // namespace sf

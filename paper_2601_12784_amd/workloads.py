@@ -422,3 +422,62 @@ def make_reprefill(seed: int | None = None, poison: bool = True, num_seqs=None) 
     lens = _lognormal_lengths(rng, n, 2048, 1.0, 256, 16384)
     return build_extend(lens, lens, REPREFILL["num_q_heads"], REPREFILL["num_kv_heads"], REPREFILL["head_dim"],
                         seed, name="reprefill", poison=poison, rng=rng)
+
+
+# ----------------------------------------------------------------------------
+# fp8 (E4M3) caches for the fp8 decode path
+# ----------------------------------------------------------------------------
+NAN_FP8 = 0x7F
+
+
+@dataclass
+class Fp8Cache:
+    """An fp8 KV cache for a Batch's block table: E4M3 codes in the bf16
+    pools' layouts (one byte per element) and fp32 scales per (page, KV head)."""
+    k8: torch.Tensor              # uint8 [N, Hkv, D/8, P, 8]
+    v8: torch.Tensor              # uint8 [N, Hkv, D, P]
+    k_scale: torch.Tensor         # float32 [N, Hkv]
+    v_scale: torch.Tensor
+
+    @property
+    def kv_bytes_per_token_head(self) -> int:
+        return 2 * int(self.v8.shape[2])
+
+
+def random_fp8_cache(batch: Batch, seed: int, poison: bool = True) -> Fp8Cache:
+    """Random finite codes for every slot of the batch's pool (sign, exponent
+    field and mantissa drawn uniformly, the NaN code excluded) and scales
+    U[2^-8, 2^-4], from PCG64(seed). Where the batch's bf16 pools are
+    poisoned (slots past each sequence's allocation, pages no sequence owns),
+    the codes are the NaN code 0x7F."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n, hkv = batch.num_pages, batch.num_kv_heads
+    d = batch.head_dim
+    def codes(shape):
+        c = rng.integers(0, 256, size=shape, dtype=np.uint16).astype(np.uint8)
+        c[(c & 0x7F) == NAN_FP8] ^= 0x01          # NaN codes -> 0x7E / 0xFE
+        return c
+    k8 = codes((n, hkv, d // 8, PAGE, 8))
+    v8 = codes((n, hkv, d, PAGE))
+    ks = rng.uniform(2.0 ** -8, 2.0 ** -4, size=(n, hkv)).astype(np.float32)
+    vs = rng.uniform(2.0 ** -8, 2.0 ** -4, size=(n, hkv)).astype(np.float32)
+    if poison:
+        kb = bf16_bits(batch.k_pool)
+        vb = bf16_bits(batch.v_pool)
+        k8[kb == NAN_BF16] = NAN_FP8
+        v8[vb == NAN_BF16] = NAN_FP8
+    return Fp8Cache(k8=torch.from_numpy(k8), v8=torch.from_numpy(v8), k_scale=torch.from_numpy(ks),
+                    v_scale=torch.from_numpy(vs))
+
+
+def page_fill(batch: Batch):
+    """(pages, valid slots) of every page some sequence holds: slots of its
+    allocation, in block-table order (int32 arrays)."""
+    pages, valid = [], []
+    alloc = batch.alloc_lens if batch.alloc_lens is not None else batch.seq_lens
+    for s in range(batch.num_seqs):
+        L = int(alloc[s])
+        for j in range(-(-L // PAGE)):
+            pages.append(int(batch.block_table[s, j]))
+            valid.append(min(PAGE, L - PAGE * j))
+    return np.array(pages, np.int32), np.array(valid, np.int32)
