@@ -40,13 +40,16 @@ def kernel_source_hash(path=None) -> str:
 class Stepper:
     """Runs plan -> upload -> attention (+ merge) for a fixed batch on one stream."""
 
-    def __init__(self, batch, chunk_pages=0, workers_per_cu=0):
+    def __init__(self, batch, chunk_pages=0, workers_per_cu=0, fp8=None):
+        """fp8 = (k8, v8, k_scale, v_scale) device tensors: step over that fp8
+        cache instead of the batch's bf16 pools."""
         import torch
         from paper_2601_12784_amd import binding as B
         self.torch = torch
         self.batch = batch
-        self.dev = dict(q=batch.q.cuda(), k=batch.k_pool.cuda(), v=batch.v_pool.cuda(),
-                        bt=torch.from_numpy(batch.block_table).cuda())
+        self.fp8 = None if fp8 is None else (fp8[2], fp8[3])
+        k, v = (batch.k_pool.cuda(), batch.v_pool.cuda()) if fp8 is None else (fp8[0], fp8[1])
+        self.dev = dict(q=batch.q.cuda(), k=k, v=v, bt=torch.from_numpy(batch.block_table).cuda())
         self.lens = np.ascontiguousarray(batch.seq_lens, dtype=np.int32)
         self.chunk = chunk_pages or None
         cus = torch.cuda.get_device_properties(0).multi_processor_count
@@ -63,7 +66,7 @@ class Stepper:
         """One decode step; ev_attn = (start, end) events bracketing the attention kernel."""
         d = self.dev
         self.runner(d["q"], d["k"], d["v"], d["bt"], self.lens, self.batch.scale, out=self.out, lse=self.lse,
-                    chunk_pages=self.chunk, stream=self.stream, attn_events=ev_attn)
+                    chunk_pages=self.chunk, stream=self.stream, attn_events=ev_attn, fp8=self.fp8)
 
 
 EVENT_EVERY = 8  # timing events bracket the attention kernel of every 8th timed step
@@ -265,6 +268,48 @@ def reprefill_bench(reps=20, warmup=5):
                          "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "kernel": EXTEND_KERNEL}}
 
 
+def fp8_bench(batch, steps, warmup, bf16_kernel_us):
+    """The same decode step over an fp8 (E4M3) copy of the batch's cache,
+    made by the library's quantizer (every page a sequence holds). Bytes per
+    step: one byte per cached element plus the K and V scale of every
+    (page, KV head) tile read."""
+    import torch
+    from paper_2601_12784_amd import binding as B
+    from paper_2601_12784_amd.workloads import page_fill
+    n, hkv, d = batch.num_pages, batch.num_kv_heads, batch.head_dim
+    desc = B.make_desc(batch.num_seqs, batch.num_q_heads, hkv, d, batch.block_table.shape[1], n, batch.scale)
+    k8 = torch.empty((n, hkv, 16 * d), dtype=torch.uint8, device="cuda")
+    v8 = torch.empty((n, hkv, 16 * d), dtype=torch.uint8, device="cuda")
+    ks = torch.ones((n, hkv), dtype=torch.float32, device="cuda")
+    vs = torch.ones((n, hkv), dtype=torch.float32, device="cuda")
+    pages, valid = page_fill(batch)
+    kq, vq = batch.k_pool.cuda(), batch.v_pool.cuda()
+    pd, vd = torch.from_numpy(pages).cuda(), torch.from_numpy(valid).cuda()
+    B.sf_kv_quantize_fp8(desc, kq, vq, pd, vd, k8, v8, ks, vs)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        B.sf_kv_quantize_fp8(desc, kq, vq, pd, vd, k8, v8, ks, vs)
+    e1.record()
+    e1.synchronize()
+    quant_ms = e0.elapsed_time(e1) / 5
+    del kq, vq
+    st = Stepper(batch, fp8=(k8, v8, ks, vs))
+    ms_step, k_mean, k_med = time_steps(st, steps, warmup)
+    tokens = int(batch.seq_lens.sum())
+    tiles = int((-(-batch.seq_lens.astype(np.int64) // 16)).sum()) * hkv
+    nbytes = tokens * hkv * d * 2 + tiles * 8
+    achieved = nbytes / (k_mean * 1e-3) / 1e9
+    return {"kv": "OCP FP8 E4M3 codes, one fp32 scale per (page, KV head) tile for K and for V",
+            "kv_bytes_per_step": nbytes, "ms_per_step": round(ms_step, 5), "attn_kernel_us": round(k_mean * 1e3, 2),
+            "seq_steps_per_s": round(batch.num_seqs / (ms_step * 1e-3), 1),
+            "kernel_speedup_vs_bf16": round(bf16_kernel_us / (k_mean * 1e3), 3),
+            "quantize_ms_whole_cache": round(quant_ms, 3),
+            "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                         "frac": round(achieved / PEAK_HBM_GBPS, 4), "kernel": "attn_worker_fp8_kernel<128>"}}
+
+
 def cpu_baseline(batch, min_s=10.0, max_s=30.0):
     """The fp64 oracle, timed on the host cores over repeated passes of the
     batch (or of a prefix of it, if one pass would exceed max_s)."""
@@ -435,6 +480,7 @@ def main():
     ap.add_argument("--no-loop", action="store_true", help="skip the growing-cache decode loop")
     ap.add_argument("--no-cost", action="store_true", help="skip the cost-model k1 fit")
     ap.add_argument("--no-reprefill", action="store_true", help="skip the extend (re-prefill) leg")
+    ap.add_argument("--no-fp8", action="store_true", help="skip the fp8-cache leg")
     ap.add_argument("--only-reprefill", action="store_true", help="run only the extend leg and print it")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
@@ -550,6 +596,13 @@ def main():
         result["cost_model"] = cm
         log(f"  k1 = {cm['k1_s_per_byte']:.3e} s/byte ({cm['effective_gb_s']} GB/s), c = {cm['c_us']} us, "
             f"r2 = {cm['r2']}")
+
+    if not args.no_fp8:
+        log("fp8 (E4M3) cache: the same step over the library-quantized cache")
+        f8 = fp8_bench(batch, max(100, args.steps // 2), max(100, args.warmup // 2), attn_ms_mean * 1e3)
+        result["fp8"] = f8
+        log(f"  step {f8['ms_per_step'] * 1e3:.1f} us, kernel {f8['attn_kernel_us']} us "
+            f"({f8['roofline']['achieved']} GB/s of fp8 codes, {f8['kernel_speedup_vs_bf16']}x the bf16 kernel)")
 
     if not args.no_reprefill:
         log("extend attention: full re-prefill of 32 trajectories")

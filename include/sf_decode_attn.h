@@ -203,9 +203,13 @@ sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* in
  * optimizations its design is compatible with (Sec. 7); this variant halves
  * the bytes a decode step reads. Keys and values are OCP FP8 E4M3 codes
  * (sign, 4 exponent bits with bias 7, 3 mantissa bits; 0x7F / 0xFF are NaN,
- * the largest finite magnitude is 448), one byte per element in the bf16
- * pools' layouts: k_pool8 [num_pages][Hkv][D/8][16][8], v_pool8
- * [num_pages][Hkv][D][16]. Each (page, KV head) tile has one fp32 scale for
+ * the largest finite magnitude is 448), one byte per element: k_pool8 and
+ * v_pool8 are [num_pages][Hkv][16*D] bytes, and inside a tile the byte of
+ * slot t, dim d sits at
+ *   K: ((d/64 * 4 + (d%32)/8) * 16 + t) * 16 + (d/32 % 2) * 8 + d%8
+ *   V: ((d/64 * 4 + t/4) * 16 + d%16) * 16 + (d/16 % 4) * 4 + t%4
+ * (the gfx950 matrix-core operands of one lane are then 16-byte pieces and
+ * each wave load a contiguous 1 KiB). Each (page, KV head) tile has one fp32 scale for
  * K and one for V: k_scale, v_scale [num_pages][Hkv]. The cached key of slot
  * t, dim d is value(code) * k_scale[page][kvh] (values likewise), and the
  * attention is the decode step's over those values.
@@ -220,7 +224,7 @@ sf_status sf_decode_attn_fp8(const sf_attn_desc* desc, const sf_plan_info* info,
                              float* out, float* lse, void* workspace, uint64_t workspace_bytes, void* stream);
 
 /*
- * Quantizes pages of a bf16 cache into an fp8 one (both laid out as above).
+ * Quantizes pages of a bf16 cache (bf16 layouts) into an fp8 one (fp8 layouts above).
  * For each listed page p = pages[i] (device int32 [num_pages]) with
  * n = valid_slots[i] valid slots (device int32, 1 .. 16), and every KV head,
  * separately for the K tile and the V tile of the slots 0 .. n-1:
@@ -228,7 +232,8 @@ sf_status sf_decode_attn_fp8(const sf_attn_desc* desc, const sf_plan_info* info,
  *   rounded; scale = inv = 1 for an all-zero tile)
  *   code = E4M3 round-to-nearest-even of the fp32 product x * inv
  * Slots n .. 15 get code 0. Writes k_pool8, v_pool8, k_scale[p][*] and
- * v_scale[p][*]; other pages are untouched. One launch on the stream.
+ * v_scale[p][*]; other pages are untouched. One launch on the stream. The
+ * valid slots must hold finite values.
  */
 sf_status sf_kv_quantize_fp8(const sf_attn_desc* desc, const void* k_pool, const void* v_pool,
                              const int32_t* pages, const int32_t* valid_slots, int32_t num_pages,

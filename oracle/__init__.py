@@ -95,8 +95,8 @@ def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale, nthreads: int =
 
 def decode_attn_fp8(q, k8, v8, k_scale, v_scale, block_table, seq_lens, scale, nthreads: int = 0):
     """fp64 reference over an fp8 (OCP E4M3) cache with per-(page, KV head)
-    scales. q: uint16 bf16 bits [B,Hq,D]; k8 [N,Hkv,D/8,16,8] and v8
-    [N,Hkv,D,16] uint8 codes; k_scale, v_scale float32 [N,Hkv]."""
+    scales. q: uint16 bf16 bits [B,Hq,D]; k8, v8: uint8 codes [N,Hkv,16*D]
+    in the fp8 tile layouts (sf_oracle.c); k_scale, v_scale float32 [N,Hkv]."""
     q = _u16(q)
     k8 = np.ascontiguousarray(k8, dtype=np.uint8)
     v8 = np.ascontiguousarray(v8, dtype=np.uint8)
@@ -105,11 +105,11 @@ def decode_attn_fp8(q, k8, v8, k_scale, v_scale, block_table, seq_lens, scale, n
     bt = np.ascontiguousarray(block_table, dtype=np.int32)
     lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
     b, hq, d = q.shape
-    n, hkv, groups, p, eight = k8.shape
-    assert groups * eight == d and v8.shape == (n, hkv, d, p) and ks.shape == (n, hkv) and vs.shape == (n, hkv)
+    n, hkv, tile = k8.shape
+    assert tile == 16 * d and v8.shape == (n, hkv, tile) and ks.shape == (n, hkv) and vs.shape == (n, hkv)
     out = np.empty((b, hq, d), dtype=np.float64)
     lse = np.empty((b, hq), dtype=np.float64)
-    rc = lib().sf_oracle_decode_attn_fp8(b, hq, hkv, d, p, bt.shape[1], n, _ptr(q), _ptr(k8), _ptr(v8), _ptr(ks),
+    rc = lib().sf_oracle_decode_attn_fp8(b, hq, hkv, d, 16, bt.shape[1], n, _ptr(q), _ptr(k8), _ptr(v8), _ptr(ks),
                                          _ptr(vs), _ptr(bt), _ptr(lens), float(scale), _ptr(out), _ptr(lse),
                                          int(nthreads))
     if rc != 0:

@@ -18,6 +18,10 @@ Quantizer of one tile (the valid slots of one page and KV head, bf16 values x):
   scale = fp32(amax / 448)          inv = fp32(448 / amax)     (both rounded once)
   code  = encode(fp32(x * inv))     (|x * inv| <= 448 up to that rounding)
 An all-zero tile gets scale = inv = 1. Slots past the valid count get code 0.
+
+fp8 tile layouts (16 * D bytes per (page, KV head) tile; byte of slot t, dim d):
+  K: ((d // 64 * 4 + d % 32 // 8) * 16 + t) * 16 + (d // 32 % 2) * 8 + d % 8
+  V: ((d // 64 * 4 + t // 4) * 16 + d % 16) * 16 + (d // 16 % 4) * 4 + t % 4
 """
 from __future__ import annotations
 
@@ -73,13 +77,33 @@ def quantize_tile(bits, valid_slots: int, slot_axis: int):
     return codes, np.float32(scale)
 
 
+def k_offset(t, d):
+    t, d = np.asarray(t), np.asarray(d)
+    return ((d // 64 * 4 + d % 32 // 8) * 16 + t) * 16 + (d // 32 % 2) * 8 + d % 8
+
+
+def v_offset(t, d):
+    t, d = np.asarray(t), np.asarray(d)
+    return ((d // 64 * 4 + t // 4) * 16 + d % 16) * 16 + (d // 16 % 4) * 4 + t % 4
+
+
+def _slot_dim(d):
+    t, dim = np.meshgrid(np.arange(PAGE), np.arange(d), indexing="ij")
+    return t.ravel(), dim.ravel()
+
+
 def quantize_pages(k_bits, v_bits, pages, valid, k8, v8, k_scale, v_scale) -> None:
     """Quantizes the listed pages of bf16 pools (k_bits [N,Hkv,D/8,16,8],
-    v_bits [N,Hkv,D,16] uint16) into fp8 pools and scales, in place.
-    valid[i]: valid slots (1..16) of page pages[i]."""
-    hkv = k_bits.shape[1]
+    v_bits [N,Hkv,D,16] uint16) into fp8 pools [N,Hkv,16*D] (fp8 tile
+    layouts) and scales [N,Hkv], in place. valid[i]: valid slots (1..16) of
+    page pages[i]."""
+    hkv, d = k_bits.shape[1], k_bits.shape[2] * 8
+    t, dim = _slot_dim(d)
+    ko, vo = k_offset(t, dim), v_offset(t, dim)
     for pg, nv in zip(pages, valid):
         pg, nv = int(pg), int(nv)
         for h in range(hkv):
-            k8[pg, h], k_scale[pg, h] = quantize_tile(k_bits[pg, h], nv, slot_axis=1)
-            v8[pg, h], v_scale[pg, h] = quantize_tile(v_bits[pg, h], nv, slot_axis=1)
+            kc, k_scale[pg, h] = quantize_tile(k_bits[pg, h], nv, slot_axis=1)   # [D/8][16][8]
+            vc, v_scale[pg, h] = quantize_tile(v_bits[pg, h], nv, slot_axis=1)   # [D][16]
+            k8[pg, h, ko] = kc[dim // 8, t, dim % 8]
+            v8[pg, h, vo] = vc[dim, t]

@@ -175,10 +175,19 @@ int sf_oracle_decode_attn(int B, int Hq, int Hkv, int D, int P, int stride, int 
  *   (-1)^s * m/8 * 2^-6            if e = 0
  *   (-1)^s * (1 + m/8) * 2^(e - 7) otherwise, NaN for e = 15, m = 7,
  * and the cached key of slot t, dim d is that value times k_scale[page][kvh]
- * (values likewise with v_scale). Layouts as the bf16 pools, one byte per
- * element: k8 [N][Hkv][D/8][P][8], v8 [N][Hkv][D][P], scales [N][Hkv].
+ * (values likewise with v_scale). Pools k8 and v8 are [N][Hkv][16*D] bytes,
+ * scales [N][Hkv]; inside a tile the byte of (slot t, dim d) is at
+ *   K: ((d/64 * 4 + (d%32)/8) * 16 + t) * 16 + (d/32 % 2) * 8 + d%8
+ *   V: ((d/64 * 4 + t/4) * 16 + d%16) * 16 + (d/16 % 4) * 4 + t%4
  * The attention itself is the bf16 oracle's: widen exactly, fp64 throughout.
  */
+static int64_t k8_index(int64_t pg, int Hkv, int kvh, int D, int t, int d) {
+  return (pg * Hkv + kvh) * 16 * D + (((d / 64) * 4 + (d % 32) / 8) * 16 + t) * 16 + ((d / 32) % 2) * 8 + d % 8;
+}
+static int64_t v8_index(int64_t pg, int Hkv, int kvh, int D, int t, int d) {
+  return (pg * Hkv + kvh) * 16 * D + (((d / 64) * 4 + t / 4) * 16 + d % 16) * 16 + ((d / 16) % 4) * 4 + t % 4;
+}
+
 double sf_oracle_e4m3_value(int code) {
   const int s = (code >> 7) & 1, e = (code >> 3) & 15, m = code & 7;
   double v;
@@ -193,7 +202,7 @@ int sf_oracle_decode_attn_fp8(int B, int Hq, int Hkv, int D, int P, int stride, 
                               const float* k_scale, const float* v_scale,
                               const int32_t* bt, const int32_t* lens, double scale,
                               double* out, double* lse, int nthreads) {
-  if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || D <= 0 || P <= 0) return -1;
+  if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || D <= 0 || D % 64 != 0 || P != 16) return -1;
   int bad = check_pages(B, P, stride, num_pages, bt, lens);
   if (bad) return bad;
   double table[256];
@@ -233,7 +242,7 @@ int sf_oracle_decode_attn_fp8(int B, int Hq, int Hkv, int D, int P, int stride, 
         double ks = (double)k_scale[(int64_t)pg * Hkv + kvh];
         double dot = 0.0;
         for (int d = 0; d < D; ++d)
-          dot += bf16_to_double(qv[d]) * (table[k8[k_index(pg, Hkv, kvh, D, P, slot, d)]] * ks);
+          dot += bf16_to_double(qv[d]) * (table[k8[k8_index(pg, Hkv, kvh, D, slot, d)]] * ks);
         z[t] = scale * dot;
         if (z[t] > m) m = z[t];
       }
@@ -245,7 +254,7 @@ int sf_oracle_decode_attn_fp8(int B, int Hq, int Hkv, int D, int P, int stride, 
         double vs = (double)v_scale[(int64_t)pg * Hkv + kvh];
         double w = exp(z[t] - m);
         wsum += w;
-        for (int d = 0; d < D; ++d) acc[d] += w * (table[v8[v_index(pg, Hkv, kvh, D, P, slot, d)]] * vs);
+        for (int d = 0; d < D; ++d) acc[d] += w * (table[v8[v8_index(pg, Hkv, kvh, D, slot, d)]] * vs);
       }
       for (int d = 0; d < D; ++d) o[d] = acc[d] / wsum;
       if (lse) lse[sh] = m + log(wsum);

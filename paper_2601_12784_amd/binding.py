@@ -248,8 +248,8 @@ def sf_decode_attn_fp8(desc, info, work_host, work_dev, q, k_pool8, v_pool8, k_s
     """Enqueues the attention kernel over an fp8 cache (uint8 pools, fp32 scales [N, Hkv])."""
     b, hq, hkv, d = desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
     _dev(q, "q", torch.bfloat16, (b, hq, d))
-    _dev(k_pool8, "k_pool8", torch.uint8, (desc.num_pages, hkv, d // 8, PAGE, 8))
-    _dev(v_pool8, "v_pool8", torch.uint8, (desc.num_pages, hkv, d, PAGE))
+    _dev(k_pool8, "k_pool8", torch.uint8, (desc.num_pages, hkv, PAGE * d))
+    _dev(v_pool8, "v_pool8", torch.uint8, (desc.num_pages, hkv, PAGE * d))
     _dev(k_scale, "k_scale", torch.float32, (desc.num_pages, hkv))
     _dev(v_scale, "v_scale", torch.float32, (desc.num_pages, hkv))
     _dev(block_table, "block_table", torch.int32, (b, desc.block_table_stride))
@@ -276,8 +276,8 @@ def sf_kv_quantize_fp8(desc, k_pool, v_pool, pages, valid_slots, k_pool8, v_pool
     _dev(v_pool, "v_pool", torch.bfloat16, (desc.num_pages, hkv, d, PAGE))
     _dev(pages, "pages", torch.int32)
     _dev(valid_slots, "valid_slots", torch.int32, tuple(pages.shape))
-    _dev(k_pool8, "k_pool8", torch.uint8, (desc.num_pages, hkv, d // 8, PAGE, 8))
-    _dev(v_pool8, "v_pool8", torch.uint8, (desc.num_pages, hkv, d, PAGE))
+    _dev(k_pool8, "k_pool8", torch.uint8, (desc.num_pages, hkv, PAGE * d))
+    _dev(v_pool8, "v_pool8", torch.uint8, (desc.num_pages, hkv, PAGE * d))
     _dev(k_scale, "k_scale", torch.float32, (desc.num_pages, hkv))
     _dev(v_scale, "v_scale", torch.float32, (desc.num_pages, hkv))
     _check("sf_kv_quantize_fp8", lib().sf_kv_quantize_fp8(
@@ -609,10 +609,13 @@ class DecodeAttention:
         if key == self._checked:
             return
         b, hkv, d = q.shape[0], self.hkv, self.d
-        pool_t = torch.bfloat16 if fp8 is None else torch.uint8
         _dev(q, "q", torch.bfloat16, (b, self.hq, d))
-        _dev(k_pool, "k_pool", pool_t, (k_pool.shape[0], hkv, d // 8, PAGE, 8))
-        _dev(v_pool, "v_pool", pool_t, (k_pool.shape[0], hkv, d, PAGE))
+        if fp8 is None:
+            _dev(k_pool, "k_pool", torch.bfloat16, (k_pool.shape[0], hkv, d // 8, PAGE, 8))
+            _dev(v_pool, "v_pool", torch.bfloat16, (k_pool.shape[0], hkv, d, PAGE))
+        else:
+            _dev(k_pool, "k_pool8", torch.uint8, (k_pool.shape[0], hkv, PAGE * d))
+            _dev(v_pool, "v_pool8", torch.uint8, (k_pool.shape[0], hkv, PAGE * d))
         if fp8 is not None:
             _dev(fp8[0], "k_scale", torch.float32, (k_pool.shape[0], hkv))
             _dev(fp8[1], "v_scale", torch.float32, (k_pool.shape[0], hkv))

@@ -436,20 +436,32 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 // ---------------------------------------------------------------------------
 // attention over an fp8 (OCP E4M3) cache with per-(page, KV head) scales
 // ---------------------------------------------------------------------------
-// The pools hold one-byte codes in the bf16 pools' layouts (a tile is 16*D
-// bytes), so a block moves half the bytes. The codes are widened to bf16 in
-// registers just before use; every E4M3 value is a bf16 value, so this is
-// exact and the MFMAs are the bf16 path's. The page's K scale joins the
-// score scale, its V scale the P.V operand: no per-element scaling.
+// The pools hold one-byte codes in tile layouts made for 16-byte loads (a
+// tile is 16*D bytes; byte of slot t, dim d):
+//   K: ((d/64 * 4 + (d%32)/8) * 16 + t) * 16 + (d/32 % 2) * 8 + d%8
+//   V: ((d/64 * 4 + t/4) * 16 + d%16) * 16 + (d/16 % 4) * 4 + t%4
+// so a lane's K operands of two 32-dim steps, and its V operands of four
+// 16-dim blocks, are one 16-byte piece, and each wave load is a contiguous
+// 1 KiB: a block moves half the bytes of bf16 in a third of the loads. The
+// codes are widened to bf16 in registers just before use; every E4M3 value is
+// a bf16 value, so this is exact and the MFMAs are the bf16 path's. The page's
+// K scale joins the score scale, its V scale the P.V operand: no per-element
+// scaling.
+template <int D>
+struct Shape8 {
+  static constexpr int KP = D / 64;   // 16-byte K pieces per page (two MFMA steps each)
+  static constexpr int JQ = D / 64;   // 16-byte V pieces per page (four 16-dim blocks each)
+};
+
 template <int D>
 struct KHalf8 {
-  u32x2 k[2][Shape<D>::KB];   // 8 codes: dims 32*kb + 8*grp .. +7 of slot col
+  u32x4 k[2][Shape8<D>::KP];   // [page][kp]: codes of dims 64*kp + 8*grp (+32) .. +7 of slot col
   float ks[2];
 };
 
 template <int D>
 struct VHalf8 {
-  uint32_t v[2][Shape<D>::JB];  // 4 codes: slots 4*grp .. +3 of dim 16*jb + col
+  u32x4 v[2][Shape8<D>::JQ];   // [page][jq]: word jr = codes of slots 4*grp .. +3, dim 64*jq + 16*jr + col
   float vs[2];
 };
 
@@ -469,8 +481,7 @@ struct ChunkCtx8 {
   int num_kv_heads;
   int kvh;
   int pe;
-  int k_off;
-  int v_off;
+  int lane_off;   // byte offset of this lane's 16-byte piece inside a 1 KiB run
 };
 
 template <int D>
@@ -489,12 +500,12 @@ __device__ __forceinline__ float scale_of(const float* base, int page, int num_k
 
 template <int D>
 __device__ __forceinline__ void load_k8(const ChunkCtx8<D>& c, PagePair pp, KHalf8<D>& b) {
-  const uint8_t* k0 = c.k_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.k_off;
-  const uint8_t* k1 = c.k_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.k_off;
+  const uint8_t* k0 = c.k_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.lane_off;
+  const uint8_t* k1 = c.k_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.lane_off;
 #pragma unroll
-  for (int kb = 0; kb < Shape<D>::KB; ++kb) {
-    b.k[0][kb] = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(k0 + k_elem(0, 32 * kb, D)));
-    b.k[1][kb] = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(k1 + k_elem(0, 32 * kb, D)));
+  for (int kp = 0; kp < Shape8<D>::KP; ++kp) {
+    b.k[0][kp] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k0 + 1024 * kp));
+    b.k[1][kp] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k1 + 1024 * kp));
   }
   b.ks[0] = scale_of(c.k_scale, pp.p0, c.num_kv_heads, c.kvh);
   b.ks[1] = scale_of(c.k_scale, pp.p1, c.num_kv_heads, c.kvh);
@@ -502,12 +513,12 @@ __device__ __forceinline__ void load_k8(const ChunkCtx8<D>& c, PagePair pp, KHal
 
 template <int D>
 __device__ __forceinline__ void load_v8(const ChunkCtx8<D>& c, PagePair pp, VHalf8<D>& b) {
-  const uint8_t* v0 = c.v_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.v_off;
-  const uint8_t* v1 = c.v_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.v_off;
+  const uint8_t* v0 = c.v_pool + tile_offset(pp.p0, c.num_kv_heads, c.kvh, D) + c.lane_off;
+  const uint8_t* v1 = c.v_pool + tile_offset(pp.p1, c.num_kv_heads, c.kvh, D) + c.lane_off;
 #pragma unroll
-  for (int jb = 0; jb < Shape<D>::JB; ++jb) {
-    b.v[0][jb] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(v0 + v_elem(0, 16 * jb)));
-    b.v[1][jb] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(v1 + v_elem(0, 16 * jb)));
+  for (int jq = 0; jq < Shape8<D>::JQ; ++jq) {
+    b.v[0][jq] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(v0 + 1024 * jq));
+    b.v[1][jq] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(v1 + 1024 * jq));
   }
   b.vs[0] = scale_of(c.v_scale, pp.p0, c.num_kv_heads, c.kvh);
   b.vs[1] = scale_of(c.v_scale, pp.p1, c.num_kv_heads, c.kvh);
@@ -518,17 +529,20 @@ __device__ __forceinline__ void widen_k(const KHalf8<D>& r, KHalf<D>& b) {
 #pragma unroll
   for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int kb = 0; kb < Shape<D>::KB; ++kb)
-      b.k[h][kb] = u32x4{widen2<false>(r.k[h][kb][0]), widen2<true>(r.k[h][kb][0]), widen2<false>(r.k[h][kb][1]),
-                         widen2<true>(r.k[h][kb][1])};
+    for (int kb = 0; kb < Shape<D>::KB; ++kb) {
+      const u32x4 w = r.k[h][kb / 2];
+      const uint32_t lo = w[2 * (kb % 2)], hi = w[2 * (kb % 2) + 1];
+      b.k[h][kb] = u32x4{widen2<false>(lo), widen2<true>(lo), widen2<false>(hi), widen2<true>(hi)};
+    }
 }
 
 template <int D>
 __device__ __forceinline__ void widen_v(const VHalf8<D>& r, VHalf<D>& b) {
 #pragma unroll
-  for (int jb = 0; jb < Shape<D>::JB; ++jb)
-    b.v[jb] = u32x4{widen2<false>(r.v[0][jb]), widen2<true>(r.v[0][jb]), widen2<false>(r.v[1][jb]),
-                    widen2<true>(r.v[1][jb])};
+  for (int jb = 0; jb < Shape<D>::JB; ++jb) {
+    const uint32_t p0 = r.v[0][jb / 4][jb % 4], p1 = r.v[1][jb / 4][jb % 4];
+    b.v[jb] = u32x4{widen2<false>(p0), widen2<true>(p0), widen2<false>(p1), widen2<true>(p1)};
+  }
 }
 
 // One segment over an fp8 cache; otherwise as attend_segment.
@@ -558,15 +572,22 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const_i32_
   c.num_kv_heads = a.num_kv_heads;
   c.kvh = kvh;
   c.pe = pe;
-  c.k_off = k_elem(col, 8 * grp, D);
-  c.v_off = v_elem(4 * grp, col);
+  c.lane_off = (grp * kPage + col) * 16;
 
-  KHalf8<D> kr[2];
-  VHalf8<D> vr[2];
+  // Codes are half the bytes of bf16, so the raw buffers go three blocks
+  // deep (two blocks of loads in flight behind the one being computed): the
+  // same bytes in flight per wave as the bf16 path keeps.
+  KHalf8<D> kr[3];
+  VHalf8<D> vr[3];
   if (pb < pe) {
     const PagePair pp = block_pages8(c, pb);
     load_k8(c, pp, kr[0]);
     load_v8(c, pp, vr[0]);
+    if (pb + 2 < pe) {
+      const PagePair pq = block_pages8(c, pb + 2);
+      load_k8(c, pq, kr[1]);
+      load_v8(c, pq, vr[1]);
+    }
   }
   u32x4 qf[KB];
   {
@@ -583,11 +604,12 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const_i32_
   st.m = -__builtin_inff();
   st.lsum = 0.f;
 
+  // Block at pg from (kc, vc); the block two ahead (pg + 4) loads into (kn, vn).
   auto step = [&](int pg, KHalf8<D>& kc, VHalf8<D>& vc, KHalf8<D>& kn, VHalf8<D>& vn) {
-    const bool more = pg + 2 < pe;
+    const bool more = pg + 4 < pe;
     PagePair nxt = {0, 0};
     if (more) {
-      nxt = block_pages8(c, pg + 2);
+      nxt = block_pages8(c, pg + 4);
       load_k8(c, nxt, kn);
     }
     const int nvalid = min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage);
@@ -600,10 +622,12 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const_i32_
     widen_v(vc, vw);
     accumulate_block(vw, w, nvalid, grp, st);
   };
-  for (int pg = pb; pg < pe; pg += 4) {
-    step(pg, kr[0], vr[0], kr[1], vr[1]);
+  for (int pg = pb; pg < pe; pg += 6) {
+    step(pg, kr[0], vr[0], kr[2], vr[2]);
     if (pg + 2 >= pe) break;
     step(pg + 2, kr[1], vr[1], kr[0], vr[0]);
+    if (pg + 4 >= pe) break;
+    step(pg + 4, kr[2], vr[2], kr[1], vr[1]);
   }
 
   float lt = st.lsum + __shfl_xor(st.lsum, 16);
@@ -690,7 +714,18 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(QuantArgs a) {
           packed = __builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], packed, true);
           w[q] = uint32_t(packed);
         }
-        *reinterpret_cast<u32x2*>(dst + 8 * i) = u32x2{w[0], w[1]};
+        if (which == 0) {
+          // K piece i: dims d0 .. d0 + 7 of slot t, contiguous in the fp8 layout
+          const int t = i % kPage, d0 = 8 * (i / kPage);
+          const int off = (((d0 / 64) * 4 + (d0 % 32) / 8) * kPage + t) * 16 + ((d0 / 32) % 2) * 8;
+          *reinterpret_cast<u32x2*>(dst + off) = u32x2{w[0], w[1]};
+        } else {
+          // V piece i: slots t0 .. t0 + 7 of dim d, two runs of four slots
+          const int d = i / 2, t0 = 8 * (i % 2);
+          const int off = (((d / 64) * 4 + t0 / 4) * kPage + d % 16) * 16 + ((d / 16) % 4) * 4;
+          *reinterpret_cast<uint32_t*>(dst + off) = w[0];
+          *reinterpret_cast<uint32_t*>(dst + off + kPage * 16) = w[1];
+        }
       }
     }
   }

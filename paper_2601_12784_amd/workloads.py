@@ -432,40 +432,55 @@ NAN_FP8 = 0x7F
 
 @dataclass
 class Fp8Cache:
-    """An fp8 KV cache for a Batch's block table: E4M3 codes in the bf16
-    pools' layouts (one byte per element) and fp32 scales per (page, KV head)."""
-    k8: torch.Tensor              # uint8 [N, Hkv, D/8, P, 8]
-    v8: torch.Tensor              # uint8 [N, Hkv, D, P]
+    """An fp8 KV cache for a Batch's block table: E4M3 codes, [N, Hkv, 16*D]
+    bytes per pool in the fp8 tile layouts (include/sf_decode_attn.h), and
+    fp32 scales per (page, KV head)."""
+    k8: torch.Tensor              # uint8 [N, Hkv, 16*D]
+    v8: torch.Tensor              # uint8 [N, Hkv, 16*D]
     k_scale: torch.Tensor         # float32 [N, Hkv]
     v_scale: torch.Tensor
 
-    @property
-    def kv_bytes_per_token_head(self) -> int:
-        return 2 * int(self.v8.shape[2])
+
+def fp8_slot_of_offset(d: int):
+    """Slot (0..15) of every byte of an fp8 K tile and V tile (int arrays [16*D]).
+    K byte ((a * 16 + t) * 16 + b) holds slot t; V byte
+    ((c * 4 + t // 4) * 16 + e) * 16 + f * 4 + t % 4 holds slot t."""
+    off = np.arange(PAGE * d)
+    return (off // 16) % 16, ((off // 256) % 4) * 4 + off % 4
 
 
 def random_fp8_cache(batch: Batch, seed: int, poison: bool = True) -> Fp8Cache:
-    """Random finite codes for every slot of the batch's pool (sign, exponent
-    field and mantissa drawn uniformly, the NaN code excluded) and scales
-    U[2^-8, 2^-4], from PCG64(seed). Where the batch's bf16 pools are
-    poisoned (slots past each sequence's allocation, pages no sequence owns),
-    the codes are the NaN code 0x7F."""
+    """Random finite codes for every byte of the batch's pool (uniform over
+    the 254 finite codes) and scales U[2^-8, 2^-4], from PCG64(seed). When
+    poisoned, pages no sequence owns and the slots past each sequence's
+    allocation in its last page hold the NaN code 0x7F."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    n, hkv = batch.num_pages, batch.num_kv_heads
-    d = batch.head_dim
+    n, hkv, d = batch.num_pages, batch.num_kv_heads, batch.head_dim
     def codes(shape):
         c = rng.integers(0, 256, size=shape, dtype=np.uint16).astype(np.uint8)
         c[(c & 0x7F) == NAN_FP8] ^= 0x01          # NaN codes -> 0x7E / 0xFE
         return c
-    k8 = codes((n, hkv, d // 8, PAGE, 8))
-    v8 = codes((n, hkv, d, PAGE))
+    k8 = codes((n, hkv, PAGE * d))
+    v8 = codes((n, hkv, PAGE * d))
     ks = rng.uniform(2.0 ** -8, 2.0 ** -4, size=(n, hkv)).astype(np.float32)
     vs = rng.uniform(2.0 ** -8, 2.0 ** -4, size=(n, hkv)).astype(np.float32)
     if poison:
-        kb = bf16_bits(batch.k_pool)
-        vb = bf16_bits(batch.v_pool)
-        k8[kb == NAN_BF16] = NAN_FP8
-        v8[vb == NAN_BF16] = NAN_FP8
+        # Owned pages are the block table's entries (a step view of a
+        # multi-step run lists only the pages its current lengths use).
+        kslot, vslot = fp8_slot_of_offset(d)
+        bt = batch.block_table
+        owned = np.zeros(n, dtype=bool)
+        owned[bt[bt >= 0]] = True
+        alloc = batch.alloc_lens if batch.alloc_lens is not None else batch.seq_lens
+        for s in range(batch.num_seqs):
+            npg = -(-int(alloc[s]) // PAGE)
+            tail = int(alloc[s]) % PAGE
+            if npg and tail and npg <= bt.shape[1] and bt[s, npg - 1] >= 0:
+                last = bt[s, npg - 1]
+                k8[last][:, kslot >= tail] = NAN_FP8
+                v8[last][:, vslot >= tail] = NAN_FP8
+        k8[~owned] = NAN_FP8
+        v8[~owned] = NAN_FP8
     return Fp8Cache(k8=torch.from_numpy(k8), v8=torch.from_numpy(v8), k_scale=torch.from_numpy(ks),
                     v_scale=torch.from_numpy(vs))
 

@@ -95,8 +95,8 @@ def _fp8_case(seed, lens, hq=4, hkv=2, d=64, pow2_scales=False):
         bt[s, : pages[s]] = perm[off: off + pages[s]]
         off += pages[s]
     finite = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], np.uint8)
-    k8 = rng.choice(finite, size=(n, hkv, d // 8, PAGE, 8))
-    v8 = rng.choice(finite, size=(n, hkv, d, PAGE))
+    k8 = rng.choice(finite, size=(n, hkv, PAGE * d))
+    v8 = rng.choice(finite, size=(n, hkv, PAGE * d))
     if pow2_scales:
         ks = np.ldexp(1.0, rng.integers(-9, -4, size=(n, hkv))).astype(np.float32)
         vs = np.ldexp(1.0, rng.integers(-9, -4, size=(n, hkv))).astype(np.float32)
@@ -108,13 +108,33 @@ def _fp8_case(seed, lens, hq=4, hkv=2, d=64, pow2_scales=False):
     return q, k8, v8, ks, vs, bt, lens, 1 / math.sqrt(d)
 
 
+def _dense_values(k8, v8, ks, vs, d):
+    """Cached values as float64 in the bf16 pools' layouts ([N,Hkv,D/8,16,8] and [N,Hkv,D,16])."""
+    vals = fp8_ref.values()
+    t, dim = np.meshgrid(np.arange(PAGE), np.arange(d), indexing="ij")
+    n, hkv = ks.shape
+    kd = np.empty((n, hkv, d // 8, PAGE, 8))
+    vd = np.empty((n, hkv, d, PAGE))
+    kd[:, :, dim // 8, t, dim % 8] = vals[k8[:, :, fp8_ref.k_offset(t, dim)]] * ks[:, :, None, None]
+    vd[:, :, dim, t] = vals[v8[:, :, fp8_ref.v_offset(t, dim)]] * vs[:, :, None, None]
+    return kd, vd
+
+
+def test_tile_layouts_are_bijections_with_contiguous_lane_pieces():
+    for d in (64, 128):
+        t, dim = np.meshgrid(np.arange(PAGE), np.arange(d), indexing="ij")
+        for f in (fp8_ref.k_offset, fp8_ref.v_offset):
+            assert np.array_equal(np.sort(f(t, dim).ravel()), np.arange(PAGE * d))
+        # a key's 8 dims 8j .. 8j+7 of one slot, and a value's 4 slots 4j .. 4j+3 of one dim, are 8 / 4 bytes in a row
+        assert np.all(np.diff(fp8_ref.k_offset(3, np.arange(8, 16))) == 1)
+        assert np.all(np.diff(fp8_ref.v_offset(np.arange(4, 8), 5)) == 1)
+
+
 def test_fp8_attention_equals_bf16_attention_on_the_same_values(oracle_lib):
     """With power-of-two scales every cached value is a bf16 value; the bf16
     oracle over those values must give the same bits."""
     q, k8, v8, ks, vs, bt, lens, scale = _fp8_case(2, [37, 16, 1, 50], pow2_scales=True)
-    vals = fp8_ref.values()
-    kd = vals[k8] * ks[:, :, None, None, None]
-    vd = vals[v8] * vs[:, :, None, None]
+    kd, vd = _dense_values(k8, v8, ks, vs, 64)
     kb = _bits(kd.astype(np.float32))
     vb = _bits(vd.astype(np.float32))
     o8, l8 = oracle.decode_attn_fp8(q, k8, v8, ks, vs, bt, lens, scale)
@@ -123,7 +143,7 @@ def test_fp8_attention_equals_bf16_attention_on_the_same_values(oracle_lib):
 
 
 def test_fp8_attention_matches_dense_numpy(oracle_lib):
-    q, k8, v8, ks, vs, bt, lens, scale = _fp8_case(3, [23, 40, 16], hq=6, hkv=3)
+    q, k8, v8, ks, vs, bt, lens, scale = _fp8_case(3, [23, 40, 16], hq=6, hkv=3, d=128)
     o8, l8 = oracle.decode_attn_fp8(q, k8, v8, ks, vs, bt, lens, scale)
     vals = fp8_ref.values()
     g = 2
@@ -133,8 +153,11 @@ def test_fp8_attention_matches_dense_numpy(oracle_lib):
             toks = np.arange(L)
             pg = bt[s, toks // PAGE]
             sl = toks % PAGE
-            K = vals[k8[pg, kvh, :, sl, :].reshape(L, -1)] * ks[pg, kvh][:, None].astype(np.float64)
-            V = vals[v8[pg, kvh][np.arange(L), :, sl]] * vs[pg, kvh][:, None].astype(np.float64)
+            dims = np.arange(128)
+            K = vals[k8[pg[:, None], kvh, fp8_ref.k_offset(sl[:, None], dims[None, :])]] * \
+                ks[pg, kvh][:, None].astype(np.float64)
+            V = vals[v8[pg[:, None], kvh, fp8_ref.v_offset(sl[:, None], dims[None, :])]] * \
+                vs[pg, kvh][:, None].astype(np.float64)
             z = scale * (K @ dense_ref.widen(q[s, h]))
             w = np.exp(z - z.max())
             np.testing.assert_allclose(o8[s, h], (w @ V) / w.sum(), rtol=1e-12, atol=1e-15)
@@ -149,3 +172,22 @@ def test_fp8_scales_act_linearly(oracle_lib):
     o3, l3 = oracle.decode_attn_fp8(q, k8, v8, ks * 2, vs, bt, lens, scale)
     o4, l4 = oracle.decode_attn_fp8(q, k8, v8, ks, vs, bt, lens, scale * 2)
     assert np.array_equal(o3, o4) and np.array_equal(l3, l4)
+
+
+def test_quantize_pages_places_codes_by_the_layouts():
+    rng = np.random.default_rng(8)
+    d, n = 64, 3
+    kb = (rng.standard_normal((n, 1, d // 8, PAGE, 8)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    vb = (rng.standard_normal((n, 1, d, PAGE)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    k8 = np.zeros((n, 1, PAGE * d), np.uint8)
+    v8 = np.zeros((n, 1, PAGE * d), np.uint8)
+    ks = np.zeros((n, 1), np.float32)
+    vs = np.zeros((n, 1), np.float32)
+    fp8_ref.quantize_pages(kb, vb, [1], [16], k8, v8, ks, vs)
+    kc, ksc = fp8_ref.quantize_tile(kb[1, 0], 16, slot_axis=1)
+    vc, vsc = fp8_ref.quantize_tile(vb[1, 0], 16, slot_axis=1)
+    assert ks[1, 0] == ksc and vs[1, 0] == vsc and not k8[0].any() and not k8[2].any()
+    for t in (0, 5, 15):
+        for dim in (0, 9, 33, 63):
+            assert k8[1, 0, fp8_ref.k_offset(t, dim)] == kc[dim // 8, t, dim % 8]
+            assert v8[1, 0, fp8_ref.v_offset(t, dim)] == vc[dim, t]

@@ -101,8 +101,8 @@ def test_fp8_attention_head_shapes(shape):
 def _quantize_gpu(batch, pages, valid):
     n, hkv, d = batch.num_pages, batch.num_kv_heads, batch.head_dim
     desc = B.make_desc(batch.num_seqs, batch.num_q_heads, hkv, d, batch.block_table.shape[1], n, batch.scale)
-    k8 = torch.full((n, hkv, d // 8, 16, 8), 0xAA, dtype=torch.uint8, device="cuda")
-    v8 = torch.full((n, hkv, d, 16), 0xAA, dtype=torch.uint8, device="cuda")
+    k8 = torch.full((n, hkv, 16 * d), 0xAA, dtype=torch.uint8, device="cuda")
+    v8 = torch.full((n, hkv, 16 * d), 0xAA, dtype=torch.uint8, device="cuda")
     ks = torch.full((n, hkv), -1.0, dtype=torch.float32, device="cuda")
     vs = torch.full((n, hkv), -1.0, dtype=torch.float32, device="cuda")
     B.sf_kv_quantize_fp8(desc, batch.k_pool.cuda(), batch.v_pool.cuda(), torch.from_numpy(pages).cuda(),
