@@ -413,7 +413,7 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
     md = out_path[:-len(".json")] + ".md"
     cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
            "-d $REPO/gpurun_out/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
-           "--no-skew --no-loop --no-cost --copy-probe " + str(int(copy_mib)))
+           "--no-skew --no-loop --no-cost --no-reprefill --no-fp8 --copy-probe " + str(int(copy_mib)))
     lines = [f"# HBM traffic of {ATTN_KERNEL} on the long-tail batch (rocprofv3 counters)", "",
              "Two counter passes (one counter each), then the summary:", "", "```",
              cmd.format(c="FETCH_SIZE", d="pmc_fetch", o="f"), cmd.format(c="WRITE_SIZE", d="pmc_write", o="w"),
