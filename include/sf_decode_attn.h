@@ -199,6 +199,49 @@ sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* in
                                 float* lse, void* workspace, uint64_t workspace_bytes, void* stream);
 
 /*
+ * Native per-step runner. A rollout instance runs one batched decode step
+ * after another (App. B.1), so host work between steps is on the critical
+ * path once the kernels are short. sf_runner_step does, in one call: plan
+ * (sf_decode_attn_plan with the runner's options) into a pinned host buffer,
+ * upload on the runner's own copy stream, then on the caller's stream the
+ * attention (plain, appending or fp8) and the merge of split sequences. The
+ * runner owns a ring of 4 pinned buffers, 2 device work-list buffers, the
+ * split-K workspace (grown on demand, after synchronizing the caller's stream
+ * and its copy stream), the copy stream (default priority) and its events: a
+ * pinned buffer is rewritten only after its upload completed, a device
+ * buffer overwritten only after the step that read it ended, and the upload
+ * of step i + 1 overlaps the kernels of step i. One runner serves one device
+ * (the current one at creation) and one caller stream at a time; steps on
+ * different streams, or calls that overlap, are not supported.
+ */
+typedef struct sf_runner sf_runner;
+
+typedef struct sf_runner_extras {
+  const void* k_new;             /* appending step (sf_decode_attn_append's arguments) */
+  const void* v_new;
+  const int32_t* new_pages_host; /* host int32 [num_seqs], copied into the upload */
+  const float* k_scale;          /* fp8 cache (sf_decode_attn_fp8's scales); not with k_new */
+  const float* v_scale;
+  void* attn_start;              /* optional hipEvent_t recorded before the attention launch */
+  void* attn_end;                /* optional hipEvent_t recorded after it (before the merge) */
+} sf_runner_extras;
+
+/* *runner = a runner for the shape's head counts, head_dim and page size
+ * (the per-step fields of shape are ignored); opts may be NULL (defaults).
+ * Allocates host and device resources; free with sf_runner_destroy. */
+sf_status sf_runner_create(const sf_attn_desc* shape, const sf_plan_opts* opts, sf_runner** runner);
+/* Waits for the runner's work to finish, then frees everything it owns. */
+void sf_runner_destroy(sf_runner* runner);
+/* One decode step: desc (its head counts, head_dim and page size as at
+ * creation), seq_lens_host (host int32 [num_seqs]) and the device tensors as
+ * for sf_decode_attn; extras may be NULL. *info (may be NULL) receives the
+ * step's plan. lse is required for an appending step. */
+sf_status sf_runner_step(sf_runner* runner, const sf_attn_desc* desc, const int32_t* seq_lens_host,
+                         const void* q, const void* k_pool, const void* v_pool, const int32_t* block_table,
+                         float* out, float* lse, const sf_runner_extras* extras, void* stream,
+                         sf_plan_info* info);
+
+/*
  * fp8 KV cache. The paper lists KV-cache quantization among the
  * optimizations its design is compatible with (Sec. 7); this variant halves
  * the bytes a decode step reads. Keys and values are OCP FP8 E4M3 codes

@@ -57,6 +57,12 @@ class sf_extend_info(ctypes.Structure):
                 ("work_bytes", ctypes.c_uint64), ("desc_key", ctypes.c_uint64)]
 
 
+class sf_runner_extras(ctypes.Structure):
+    _fields_ = [("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p), ("new_pages_host", ctypes.c_void_p),
+                ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p), ("attn_start", ctypes.c_void_p),
+                ("attn_end", ctypes.c_void_p)]
+
+
 class sf_cost_model(ctypes.Structure):
     _fields_ = [("k1", ctypes.c_double), ("k2", ctypes.c_double), ("k3", ctypes.c_double),
                 ("k4", ctypes.c_double), ("k5", ctypes.c_double), ("kv_budget", ctypes.c_double)]
@@ -94,6 +100,11 @@ def lib():
                                      ctypes.c_int32, vp, vp, vp]
     L.sf_decode_attn_append.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp,
                                         vp, vp, vp, vp, ctypes.c_uint64, vp]
+    L.sf_runner_create.argtypes = [P(sf_attn_desc), P(sf_plan_opts), P(vp)]
+    L.sf_runner_destroy.argtypes = [vp]
+    L.sf_runner_destroy.restype = None
+    L.sf_runner_step.argtypes = [vp, P(sf_attn_desc), vp, vp, vp, vp, vp, vp, vp, P(sf_runner_extras), vp,
+                                 P(sf_plan_info)]
     L.sf_decode_attn_fp8.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                      ctypes.c_uint64, vp]
     L.sf_kv_quantize_fp8.argtypes = [P(sf_attn_desc), vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp, vp, vp]
@@ -118,7 +129,8 @@ def lib():
     for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv",
                "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
                "sf_page_pool_release", "sf_page_table_step", "sf_route", "sf_extend_attn_plan",
-               "sf_extend_attn", "sf_decode_attn_fp8", "sf_kv_quantize_fp8"):
+               "sf_extend_attn", "sf_decode_attn_fp8", "sf_kv_quantize_fp8", "sf_runner_create",
+               "sf_runner_step"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -559,15 +571,11 @@ class _HipEvent:
 # convenience runner: owns the pinned work-list ring and the device buffers
 # ----------------------------------------------------------------------------
 class DecodeAttention:
-    """Plan + attention + combine for successive decode steps.
-
-    The host plans each step into a ring of pinned buffers; the work list is
-    uploaded on a side stream (default priority) into one of two device
-    buffers, so the copy for step i+1 overlaps the kernels of step i and the
-    compute stream waits on that copy only. A pinned buffer is rewritten only
-    after its upload has completed, and a device buffer only after the step
-    that read it is done. Tensor checks run once per distinct set of tensors.
-    """
+    """Plan + attention + combine for successive decode steps, through the
+    library's native runner (sf_runner_create / sf_runner_step): one call per
+    step plans into the runner's pinned ring, uploads on its copy stream and
+    launches the kernels on the caller's stream. Tensor checks run once per
+    distinct set of tensors."""
 
     def __init__(self, num_q_heads, num_kv_heads, head_dim, device=None, num_cus=None,
                  ring: int = 4, opts: sf_plan_opts | None = None):
@@ -579,27 +587,28 @@ class DecodeAttention:
         if self.opts.num_cus == 0:
             self.opts.num_cus = num_cus
         self.L = lib()
-        self._ring = [torch.empty(4096, dtype=torch.int32, pin_memory=True) for _ in range(ring)]
-        self._ring_ev = [_HipEvent() for _ in range(ring)]
-        self._n = 0
-        self.copy_stream = torch.cuda.Stream(device=self.device)
-        self._copy_h = self.copy_stream.cuda_stream
-        self._work = [torch.empty(4096, dtype=torch.int32, device=self.device) for _ in range(2)]
-        self._free_ev = [_HipEvent() for _ in range(2)]
-        self.workspace = torch.empty(0, dtype=torch.uint8, device=self.device)
+        self._runners = {}
         self._info = sf_plan_info()
+        self._extras = sf_runner_extras()
         self._checked = None
         self._desc_key = None
         self._desc = None
         self.last_info = None
-        self.last_work_dev = None
         self._lse = None
 
-    def _opts(self, chunk_pages):
+    def _runner(self, chunk_pages):
         o = self.opts
-        if chunk_pages is None:
-            return o
-        return sf_plan_opts(o.num_cus, int(chunk_pages), o.workers_per_cu, o.min_chunk_pages, 0)
+        key = (o.num_cus, int(chunk_pages or 0), o.workers_per_cu, o.min_chunk_pages)
+        r = self._runners.get(key)
+        if r is None:
+            opts = sf_plan_opts(key[0], key[1], key[2], key[3], 0)
+            shape = make_desc(0, self.hq, self.hkv, self.d, 1, 0, 1.0)
+            r = ctypes.c_void_p()
+            with torch.cuda.device(self.device):
+                _check("sf_runner_create", self.L.sf_runner_create(ctypes.byref(shape), ctypes.byref(opts),
+                                                                   ctypes.byref(r)))
+            self._runners[key] = r
+        return r
 
     def _check_tensors(self, q, k_pool, v_pool, block_table, out, lse, fp8=None):
         key = (q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
@@ -616,7 +625,6 @@ class DecodeAttention:
         else:
             _dev(k_pool, "k_pool8", torch.uint8, (k_pool.shape[0], hkv, PAGE * d))
             _dev(v_pool, "v_pool8", torch.uint8, (k_pool.shape[0], hkv, PAGE * d))
-        if fp8 is not None:
             _dev(fp8[0], "k_scale", torch.float32, (k_pool.shape[0], hkv))
             _dev(fp8[1], "v_scale", torch.float32, (k_pool.shape[0], hkv))
         _dev(block_table, "block_table", torch.int32, (b, block_table.shape[1]))
@@ -625,20 +633,11 @@ class DecodeAttention:
             _dev(lse, "lse", torch.float32, (b, self.hq))
         self._checked = key
 
-    def _plan(self, desc, lens, opts):
-        L, info = self.L, self._info
-        slot = self._n % len(self._ring)
-        self._ring_ev[slot].synchronize()  # its previous upload has finished
-        buf = self._ring[slot]
-        st = L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts),
-                                   buf.data_ptr(), buf.numel() * 4, ctypes.byref(info))
-        if st == 3:  # SF_ERR_CAPACITY: grow this ring buffer and plan again
-            buf = torch.empty(info.work_bytes // 4 * 5 // 4 + 1024, dtype=torch.int32, pin_memory=True)
-            self._ring[slot] = buf
-            st = L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts),
-                                       buf.data_ptr(), buf.numel() * 4, ctypes.byref(info))
-        _check("sf_decode_attn_plan", st)
-        return slot, buf
+    @staticmethod
+    def _event_handle(ev, stream):
+        if ev.cuda_event == 0:      # torch creates the event on its first record
+            ev.record(stream)
+        return ev.cuda_event
 
     def __call__(self, q, k_pool, v_pool, block_table, seq_lens, scale, out=None, lse=None,
                  chunk_pages=None, stream: torch.cuda.Stream | None = None, attn_events=None,
@@ -649,13 +648,12 @@ class DecodeAttention:
         append-then-attend step: k_new, v_new are device bf16 [B, Hkv, D] and
         new_pages a host int32 [B] array (-1 = the token's page is already
         held), uploaded together with the work list. fp8 = (k_scale, v_scale)
-        makes k_pool / v_pool an fp8 cache (uint8 E4M3 codes, fp32 scales
-        [N, Hkv]); it cannot be combined with append."""
+        makes k_pool / v_pool an fp8 cache (uint8 E4M3 codes [N, Hkv, 16*D],
+        fp32 scales [N, Hkv]); it cannot be combined with append."""
         if fp8 is not None and append is not None:
             raise ValueError("the fp8 cache has no appending step")
         b = q.shape[0]
         main = stream or torch.cuda.current_stream(self.device)
-        main_h = main.cuda_stream
         if out is None:
             out = torch.empty((b, self.hq, self.d), dtype=torch.float32, device=self.device)
         self._check_tensors(q, k_pool, v_pool, block_table, out, lse, fp8)
@@ -663,22 +661,15 @@ class DecodeAttention:
         if dkey != self._desc_key:
             self._desc = make_desc(b, self.hq, self.hkv, self.d, block_table.shape[1], k_pool.shape[0], scale)
             self._desc_key = dkey
-        desc = self._desc
         if isinstance(seq_lens, torch.Tensor):
             seq_lens = seq_lens.cpu().numpy()
         lens = seq_lens if (isinstance(seq_lens, np.ndarray) and seq_lens.dtype == np.int32
                             and seq_lens.flags.c_contiguous) else np.ascontiguousarray(seq_lens, np.int32)
         if lens.shape != (b,):
             raise ValueError("seq_lens must have one entry per sequence")
-        info = self._info
-        slot, buf = self._plan(desc, lens, self._opts(chunk_pages))
-
-        if self.workspace.numel() < info.workspace_bytes:
-            torch.cuda.synchronize(self.device)  # grown only while idle
-            self.workspace = torch.empty(int(info.workspace_bytes * 5 // 4) + 256, dtype=torch.uint8,
-                                         device=self.device)
-        j = self._n % 2
-        nbytes = info.work_bytes
+        ex = self._extras
+        ex.k_new = ex.v_new = ex.new_pages_host = ex.k_scale = ex.v_scale = ex.attn_start = ex.attn_end = None
+        pages = None
         if append is not None:
             k_new, v_new, new_pages = append
             _dev(k_new, "k_new", torch.bfloat16, (b, self.hkv, self.d))
@@ -686,58 +677,30 @@ class DecodeAttention:
             pages = np.ascontiguousarray(new_pages, dtype=np.int32)
             if pages.shape != (b,):
                 raise ValueError("new_pages must have one entry per sequence")
-            if buf.numel() < nbytes // 4 + b:
-                grown = torch.empty(nbytes // 4 + b + 1024, dtype=torch.int32, pin_memory=True)
-                grown[: nbytes // 4].copy_(buf[: nbytes // 4])
-                self._ring[slot] = buf = grown
-            buf[nbytes // 4: nbytes // 4 + b].numpy()[:] = pages
-            nbytes += 4 * b
-        if self._work[j].numel() * 4 < nbytes:
-            torch.cuda.synchronize(self.device)
-            self._work[j] = torch.empty(nbytes // 4 * 5 // 4 + 1024, dtype=torch.int32, device=self.device)
-        work = self._work[j]
-        # upload on the side stream once step n-2 (the last reader of work[j]) is done
-        if self._free_ev[j].used:
-            self._free_ev[j].wait_on(self._copy_h)
-        _hip_check("hipMemcpyAsync", hip().hipMemcpyAsync(work.data_ptr(), buf.data_ptr(), nbytes, 1,
-                                                          self._copy_h))
-        self._ring_ev[slot].record(self._copy_h)
-        self._ring_ev[slot].wait_on(main_h)
-
-        if attn_events is not None:
-            attn_events[0].record(main)
-        ws = self.workspace
-        if fp8 is not None:
-            _check("sf_decode_attn_fp8", self.L.sf_decode_attn_fp8(
-                ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
-                k_pool.data_ptr(), v_pool.data_ptr(), fp8[0].data_ptr(), fp8[1].data_ptr(), block_table.data_ptr(),
-                out.data_ptr(), None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
-        elif append is None:
-            _check("sf_decode_attn", self.L.sf_decode_attn(
-                ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
-                k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),
-                None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
-        else:
+            ex.k_new, ex.v_new, ex.new_pages_host = k_new.data_ptr(), v_new.data_ptr(), pages.ctypes.data
             if lse is None:  # the merge reads lse back: keep one of our own
                 if self._lse is None or self._lse.numel() < b * self.hq:
                     self._lse = torch.empty(b * self.hq * 5 // 4 + 64, dtype=torch.float32, device=self.device)
                 lse = self._lse[: b * self.hq].view(b, self.hq)
-            _check("sf_decode_attn_append", self.L.sf_decode_attn_append(
-                ctypes.byref(desc), ctypes.byref(info), None, work.data_ptr(), q.data_ptr(),
-                k_new.data_ptr(), v_new.data_ptr(), work.data_ptr() + info.work_bytes, k_pool.data_ptr(),
-                v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(),
-                None if lse is None else lse.data_ptr(), ws.data_ptr(), ws.numel(), main_h))
+        if fp8 is not None:
+            ex.k_scale, ex.v_scale = fp8[0].data_ptr(), fp8[1].data_ptr()
         if attn_events is not None:
-            attn_events[1].record(main)
-        if info.num_combine and append is None:  # an appending pass merges by itself
-            _check("sf_decode_attn_combine", self.L.sf_decode_attn_combine(
-                ctypes.byref(desc), ctypes.byref(info), work.data_ptr(), ws.data_ptr(), ws.numel(),
-                out.data_ptr(), None if lse is None else lse.data_ptr(), main_h))
-        self._free_ev[j].record(main_h)
-        self._n += 1
+            ex.attn_start = self._event_handle(attn_events[0], main)
+            ex.attn_end = self._event_handle(attn_events[1], main)
+        info = self._info
+        _check("sf_runner_step", self.L.sf_runner_step(
+            self._runner(chunk_pages), ctypes.byref(self._desc), lens.ctypes.data, q.data_ptr(), k_pool.data_ptr(),
+            v_pool.data_ptr(), block_table.data_ptr(), out.data_ptr(), None if lse is None else lse.data_ptr(),
+            ctypes.byref(ex), main.cuda_stream, ctypes.byref(info)))
         self.last_info = sf_plan_info.from_buffer_copy(info)
-        self.last_work_dev = work
         return out
+
+    def __del__(self):
+        L = getattr(self, "L", None)
+        for r in getattr(self, "_runners", {}).values():
+            if L is not None and r.value:
+                L.sf_runner_destroy(r)
+        self._runners = {}
 
 
 class PageTable:

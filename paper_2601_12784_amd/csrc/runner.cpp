@@ -1,0 +1,217 @@
+// Native per-step runner: plan -> upload -> attention (-> merge) in one call.
+//
+// A rollout instance runs one batched decode step after another (App. B.1:
+// each step generates one token per running trajectory), so the host work
+// between two steps is on the critical path once the kernels are short:
+// small batches, late steps of a long-tail batch, an fp8 cache. This object
+// keeps that work native. It owns a ring of pinned host buffers that the
+// planner writes into, two device work-list buffers, the split-K workspace,
+// a copy stream (default priority) and the events that order them:
+//   - a pinned buffer is rewritten only after its last upload completed;
+//   - a device buffer is uploaded into only after the step that read it ended;
+//   - the compute stream waits on the upload of its own step only,
+// so the upload of step i + 1 overlaps the kernels of step i.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <new>
+
+#include "sf_internal.h"
+
+static_assert(sizeof(sf_runner_extras) == 56, "sf_runner_extras layout is part of the ABI");
+
+namespace {
+
+constexpr int kRing = 4;
+
+struct Pinned {
+  int32_t* ptr = nullptr;
+  uint64_t bytes = 0;
+  hipEvent_t uploaded = nullptr;   // recorded on the copy stream after the upload that read it
+  bool used = false;
+};
+
+struct DeviceBuf {
+  int32_t* ptr = nullptr;
+  uint64_t bytes = 0;
+  hipEvent_t released = nullptr;   // recorded on the compute stream after the step that read it
+  bool used = false;
+};
+
+}  // namespace
+
+struct sf_runner {
+  sf_attn_desc shape;      // heads, head_dim, page size (per-step fields are overwritten)
+  sf_plan_opts opts;
+  int device = 0;
+  hipStream_t copy = nullptr;
+  Pinned ring[kRing];
+  DeviceBuf work[2];
+  void* workspace = nullptr;
+  uint64_t workspace_bytes = 0;
+  uint64_t steps = 0;
+  sf_plan_info last;
+};
+
+namespace {
+
+sf_status grow_pinned(Pinned& p, uint64_t bytes) {
+  if (p.bytes >= bytes) return SF_OK;
+  if (p.ptr && hipHostFree(p.ptr) != hipSuccess) return SF_ERR_HIP;
+  p.ptr = nullptr;
+  p.bytes = 0;
+  const uint64_t want = bytes + bytes / 4 + 4096;
+  if (hipHostMalloc(reinterpret_cast<void**>(&p.ptr), want, hipHostMallocDefault) != hipSuccess) return SF_ERR_HIP;
+  p.bytes = want;
+  return SF_OK;
+}
+
+// Device buffers grow only when nothing in flight can still read them.
+sf_status grow_device(void** ptr, uint64_t* have, uint64_t bytes, hipStream_t main, hipStream_t copy) {
+  if (*have >= bytes) return SF_OK;
+  if (hipStreamSynchronize(main) != hipSuccess || hipStreamSynchronize(copy) != hipSuccess) return SF_ERR_HIP;
+  if (*ptr && hipFree(*ptr) != hipSuccess) return SF_ERR_HIP;
+  *ptr = nullptr;
+  *have = 0;
+  const uint64_t want = bytes + bytes / 4 + 4096;
+  if (hipMalloc(ptr, want) != hipSuccess) return SF_ERR_HIP;
+  *have = want;
+  return SF_OK;
+}
+
+}  // namespace
+
+extern "C" sf_status sf_runner_create(const sf_attn_desc* shape, const sf_plan_opts* opts, sf_runner** out) {
+  if (!out) return SF_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!shape) return SF_ERR_INVALID_ARG;
+  sf_attn_desc probe = *shape;
+  probe.num_seqs = 0;
+  probe.block_table_stride = probe.block_table_stride > 0 ? probe.block_table_stride : 1;
+  probe.num_pages = probe.num_pages >= 0 ? probe.num_pages : 0;
+  sf_status st = sf::validate_desc(&probe);
+  if (st != SF_OK) return st;
+  if (opts && opts->reserved != 0) return SF_ERR_INVALID_ARG;
+  sf_runner* r = new (std::nothrow) sf_runner();
+  if (!r) return SF_ERR_HIP;
+  r->shape = probe;
+  if (opts) r->opts = *opts;
+  else std::memset(&r->opts, 0, sizeof r->opts);
+  if (hipGetDevice(&r->device) != hipSuccess ||
+      hipStreamCreateWithFlags(&r->copy, hipStreamNonBlocking) != hipSuccess) {
+    delete r;
+    return SF_ERR_HIP;
+  }
+  for (auto& p : r->ring)
+    if (hipEventCreateWithFlags(&p.uploaded, hipEventDisableTiming) != hipSuccess) st = SF_ERR_HIP;
+  for (auto& w : r->work)
+    if (hipEventCreateWithFlags(&w.released, hipEventDisableTiming) != hipSuccess) st = SF_ERR_HIP;
+  if (st != SF_OK) {
+    sf_runner_destroy(r);
+    return st;
+  }
+  *out = r;
+  return SF_OK;
+}
+
+// Teardown cannot report errors: every call is made, whatever the others return.
+extern "C" void sf_runner_destroy(sf_runner* r) {
+  if (!r) return;
+  if (r->copy) (void)hipStreamSynchronize(r->copy);
+  for (auto& w : r->work) {
+    if (w.released) {
+      (void)hipEventSynchronize(w.released);
+      (void)hipEventDestroy(w.released);
+    }
+    if (w.ptr) (void)hipFree(w.ptr);
+  }
+  for (auto& p : r->ring) {
+    if (p.uploaded) {
+      (void)hipEventSynchronize(p.uploaded);
+      (void)hipEventDestroy(p.uploaded);
+    }
+    if (p.ptr) (void)hipHostFree(p.ptr);
+  }
+  if (r->workspace) {
+    (void)hipDeviceSynchronize();
+    (void)hipFree(r->workspace);
+  }
+  if (r->copy) (void)hipStreamDestroy(r->copy);
+  delete r;
+}
+
+extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, const int32_t* seq_lens_host,
+                                    const void* q, const void* k_pool, const void* v_pool,
+                                    const int32_t* block_table, float* out, float* lse,
+                                    const sf_runner_extras* extras, void* stream, sf_plan_info* info_out) {
+  if (!r || !desc || (desc->num_seqs > 0 && !seq_lens_host)) return SF_ERR_INVALID_ARG;
+  if (desc->num_q_heads != r->shape.num_q_heads || desc->num_kv_heads != r->shape.num_kv_heads ||
+      desc->head_dim != r->shape.head_dim || desc->page_size != r->shape.page_size)
+    return SF_ERR_INVALID_ARG;
+  const bool append = extras && extras->k_new;
+  const bool fp8 = extras && extras->k_scale;
+  if (extras && (append && fp8)) return SF_ERR_INVALID_ARG;
+  if (append && !lse) return SF_ERR_INVALID_ARG;
+  hipStream_t main = static_cast<hipStream_t>(stream);
+
+  // 1. plan into the next pinned buffer (after its previous upload finished);
+  //    grow it and plan again only if the plan does not fit
+  Pinned& pin = r->ring[r->steps % kRing];
+  if (pin.used && hipEventSynchronize(pin.uploaded) != hipSuccess) return SF_ERR_HIP;
+  const uint64_t extra = append ? uint64_t(desc->num_seqs) * 4 : 0;
+  sf_plan_info info;
+  sf_status st = sf_decode_attn_plan(desc, seq_lens_host, &r->opts, pin.ptr, pin.bytes, &info);
+  if (st == SF_ERR_CAPACITY || (st == SF_OK && pin.bytes < info.work_bytes + extra)) {
+    if ((st = grow_pinned(pin, info.work_bytes + extra)) != SF_OK) return st;
+    st = sf_decode_attn_plan(desc, seq_lens_host, &r->opts, pin.ptr, pin.bytes, &info);
+  }
+  if (st != SF_OK) return st;
+  if (append && desc->num_seqs > 0) {
+    if (!extras->new_pages_host) return SF_ERR_INVALID_ARG;
+    std::memcpy(reinterpret_cast<char*>(pin.ptr) + info.work_bytes, extras->new_pages_host, extra);
+  }
+  if (info_out) *info_out = info;
+  r->last = info;
+  if (info.num_workers == 0) return SF_OK;
+
+  // 2. workspace and device work-list buffer (grown only while idle)
+  if ((st = grow_device(&r->workspace, &r->workspace_bytes, info.workspace_bytes, main, r->copy)) != SF_OK)
+    return st;
+  DeviceBuf& dev = r->work[r->steps % 2];
+  const uint64_t nbytes = info.work_bytes + extra;
+  void* dptr = dev.ptr;
+  if ((st = grow_device(&dptr, &dev.bytes, nbytes, main, r->copy)) != SF_OK) return st;
+  dev.ptr = static_cast<int32_t*>(dptr);
+
+  // 3. upload on the copy stream once the last reader of this buffer is done
+  if (dev.used && hipStreamWaitEvent(r->copy, dev.released, 0) != hipSuccess) return SF_ERR_HIP;
+  if (hipMemcpyAsync(dev.ptr, pin.ptr, nbytes, hipMemcpyHostToDevice, r->copy) != hipSuccess) return SF_ERR_HIP;
+  if (hipEventRecord(pin.uploaded, r->copy) != hipSuccess) return SF_ERR_HIP;
+  pin.used = true;
+  if (hipStreamWaitEvent(main, pin.uploaded, 0) != hipSuccess) return SF_ERR_HIP;
+
+  // 4. kernels on the caller's stream (optionally bracketed by the caller's events)
+  hipEvent_t ev0 = extras ? static_cast<hipEvent_t>(extras->attn_start) : nullptr;
+  hipEvent_t ev1 = extras ? static_cast<hipEvent_t>(extras->attn_end) : nullptr;
+  if (ev0 && hipEventRecord(ev0, main) != hipSuccess) return SF_ERR_HIP;
+  if (append) {
+    st = sf_decode_attn_append(desc, &info, nullptr, dev.ptr, q, extras->k_new, extras->v_new,
+                               reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(dev.ptr) + info.work_bytes),
+                               const_cast<void*>(k_pool), const_cast<void*>(v_pool),
+                               const_cast<int32_t*>(block_table), out, lse, r->workspace, r->workspace_bytes, stream);
+  } else if (fp8) {
+    st = sf_decode_attn_fp8(desc, &info, nullptr, dev.ptr, q, k_pool, v_pool, extras->k_scale, extras->v_scale,
+                            block_table, out, lse, r->workspace, r->workspace_bytes, stream);
+  } else {
+    st = sf_decode_attn(desc, &info, nullptr, dev.ptr, q, k_pool, v_pool, block_table, out, lse, r->workspace,
+                        r->workspace_bytes, stream);
+  }
+  if (st == SF_OK && ev1 && hipEventRecord(ev1, main) != hipSuccess) return SF_ERR_HIP;
+  if (st == SF_OK && !append && info.num_combine > 0)
+    st = sf_decode_attn_combine(desc, &info, dev.ptr, r->workspace, r->workspace_bytes, out, lse, stream);
+  if (st != SF_OK) return st;
+  if (hipEventRecord(dev.released, main) != hipSuccess) return SF_ERR_HIP;
+  dev.used = true;
+  ++r->steps;
+  return SF_OK;
+}
