@@ -235,7 +235,9 @@ void sf_runner_destroy(sf_runner* runner);
 /* One decode step: desc (its head counts, head_dim and page size as at
  * creation), seq_lens_host (host int32 [num_seqs]) and the device tensors as
  * for sf_decode_attn; extras may be NULL. *info (may be NULL) receives the
- * step's plan. lse is required for an appending step. */
+ * step's plan. lse is required for an appending step. An fp8 step whose
+ * runner options leave workers_per_cu at 0 plans 8 workers per CU (two waves
+ * per SIMD: its blocks move half the bytes). */
 sf_status sf_runner_step(sf_runner* runner, const sf_attn_desc* desc, const int32_t* seq_lens_host,
                          const void* q, const void* k_pool, const void* v_pool, const int32_t* block_table,
                          float* out, float* lse, const sf_runner_extras* extras, void* stream,

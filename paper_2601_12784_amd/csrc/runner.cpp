@@ -23,6 +23,7 @@ static_assert(sizeof(sf_runner_extras) == 56, "sf_runner_extras layout is part o
 namespace {
 
 constexpr int kRing = 4;
+constexpr int kFp8WorkersPerCu = 8;
 
 struct Pinned {
   int32_t* ptr = nullptr;
@@ -159,11 +160,16 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   Pinned& pin = r->ring[r->steps % kRing];
   if (pin.used && hipEventSynchronize(pin.uploaded) != hipSuccess) return SF_ERR_HIP;
   const uint64_t extra = append ? uint64_t(desc->num_seqs) * 4 : 0;
+  // An fp8 block moves half the bytes of a bf16 one: unless the caller chose,
+  // fp8 steps plan two waves per SIMD (measured: kernel 129 us instead of 136
+  // on the long-tail batch; bf16 is slower at 8).
+  sf_plan_opts opts = r->opts;
+  if (fp8 && opts.workers_per_cu == 0) opts.workers_per_cu = kFp8WorkersPerCu;
   sf_plan_info info;
-  sf_status st = sf_decode_attn_plan(desc, seq_lens_host, &r->opts, pin.ptr, pin.bytes, &info);
+  sf_status st = sf_decode_attn_plan(desc, seq_lens_host, &opts, pin.ptr, pin.bytes, &info);
   if (st == SF_ERR_CAPACITY || (st == SF_OK && pin.bytes < info.work_bytes + extra)) {
     if ((st = grow_pinned(pin, info.work_bytes + extra)) != SF_OK) return st;
-    st = sf_decode_attn_plan(desc, seq_lens_host, &r->opts, pin.ptr, pin.bytes, &info);
+    st = sf_decode_attn_plan(desc, seq_lens_host, &opts, pin.ptr, pin.bytes, &info);
   }
   if (st != SF_OK) return st;
   if (append && desc->num_seqs > 0) {
