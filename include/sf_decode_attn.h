@@ -470,6 +470,17 @@ sf_status sf_debug_gather_kv(const sf_attn_desc* desc, const void* k_pool, const
                              const int32_t* block_table, int32_t seq, int32_t kv_head,
                              int32_t len, void* k_dense, void* v_dense, void* stream);
 
+/* Measurement support: reads `bytes` of device memory at `buf` once, the way
+ * a plain streaming kernel does (`blocks` workgroups of 512 threads, each
+ * streaming its own contiguous range; every 16-byte piece loaded once,
+ * nontemporal, eight in flight per lane), so that its
+ * duration gives the bandwidth an HBM-bound kernel can reach in practice.
+ * buf and sink (16 bytes of device memory, written at most once with a
+ * meaningless value) must be 16-byte aligned; bytes a multiple of 16;
+ * 1 <= blocks <= 65536. bytes == 0 launches nothing. Asynchronous on stream.
+ * Errors: SF_ERR_INVALID_ARG for the cases above, SF_ERR_HIP on a launch error. */
+sf_status sf_debug_stream_read(const void* buf, uint64_t bytes, void* sink, int32_t blocks, void* stream);
+
 /* Static description of a status code. */
 const char* sf_status_string(sf_status status);
 

@@ -105,6 +105,7 @@ def lib():
     L.sf_runner_destroy.restype = None
     L.sf_runner_step.argtypes = [vp, P(sf_attn_desc), vp, vp, vp, vp, vp, vp, vp, P(sf_runner_extras), vp,
                                  P(sf_plan_info)]
+    L.sf_debug_stream_read.argtypes = [vp, ctypes.c_uint64, vp, ctypes.c_int32, vp]
     L.sf_decode_attn_fp8.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                      ctypes.c_uint64, vp]
     L.sf_kv_quantize_fp8.argtypes = [P(sf_attn_desc), vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp, vp, vp]
@@ -130,7 +131,7 @@ def lib():
                "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
                "sf_page_pool_release", "sf_page_table_step", "sf_route", "sf_extend_attn_plan",
                "sf_extend_attn", "sf_decode_attn_fp8", "sf_kv_quantize_fp8", "sf_runner_create",
-               "sf_runner_step"):
+               "sf_runner_step", "sf_debug_stream_read"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -498,6 +499,17 @@ def sf_decode_attn_combine(desc, info, work_dev, workspace, out, lse=None, strea
     _check("sf_decode_attn_combine", lib().sf_decode_attn_combine(
         ctypes.byref(desc), ctypes.byref(info), _addr(work_dev), _addr(workspace),
         workspace.numel() * workspace.element_size(), _addr(out), _addr(lse), _stream(stream)))
+
+
+def sf_debug_stream_read(buf, sink, blocks=16384, stream=None):
+    """Reads every byte of the uint8 device tensor buf once (measurement
+    support); sink: a uint8 device tensor of at least 16 bytes."""
+    _dev(buf, "buf", torch.uint8)
+    _dev(sink, "sink", torch.uint8)
+    if sink.numel() * sink.element_size() < 16:
+        raise ValueError("sink must hold at least 16 bytes")
+    _check("sf_debug_stream_read", lib().sf_debug_stream_read(
+        _addr(buf), buf.numel() * buf.element_size(), _addr(sink), int(blocks), _stream(stream)))
 
 
 def sf_debug_gather_kv(desc, k_pool, v_pool, block_table, seq, kv_head, length, k_dense, v_dense,

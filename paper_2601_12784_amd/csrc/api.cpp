@@ -241,6 +241,14 @@ extern "C" sf_status sf_debug_gather_kv(const sf_attn_desc* desc, const void* k_
   return from_hip(launch_gather(a, static_cast<hipStream_t>(stream)));
 }
 
+extern "C" sf_status sf_debug_stream_read(const void* buf, uint64_t bytes, void* sink, int32_t blocks,
+                                          void* stream) {
+  if (bytes == 0) return SF_OK;
+  if (!buf || !sink || !aligned16(buf) || !aligned16(sink) || bytes % 16 != 0 || blocks < 1 || blocks > 65536)
+    return SF_ERR_INVALID_ARG;
+  return from_hip(launch_stream_read(buf, bytes, sink, blocks, static_cast<hipStream_t>(stream)));
+}
+
 extern "C" const char* sf_status_string(sf_status s) {
   switch (s) {
     case SF_OK: return "ok";

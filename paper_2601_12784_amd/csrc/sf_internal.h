@@ -146,6 +146,8 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
+// Streaming-read probe: reads bytes (a multiple of 16) of buf once; sink: 16 B.
+hipError_t launch_stream_read(const void* buf, uint64_t bytes, void* sink, int blocks, hipStream_t stream);
 hipError_t launch_quantize_fp8(const QuantArgs& a, hipStream_t stream);
 
 }  // namespace sf

@@ -311,3 +311,25 @@ def test_straggler_steps():
         out, lse, _ = run_gpu(b, dev=d, runner=runner)
         assert_close(out, ref[0], f"straggler@{t}")
         assert_close(lse, ref[1], f"straggler@{t} lse")
+
+
+# ---------------------------------------------------------------------------
+# measurement support: the streaming-read probe
+# ---------------------------------------------------------------------------
+def test_stream_read_probe_runs_and_checks_its_arguments():
+    _say("stream-read probe")
+    buf = torch.full((1 << 20,), 0x5A, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    for blocks in (1, 7, 4096):
+        B.sf_debug_stream_read(buf, sink, blocks)
+    B.sf_debug_stream_read(buf[: 16 * 1000 + 16], sink, 3)          # ragged tail of the grid-stride loop
+    torch.cuda.synchronize()
+    assert not sink.any()                                             # 0x5A... XOR-reduces to 0: nothing stored
+    L = B.lib()
+    addr, sk = buf.data_ptr(), sink.data_ptr()
+    assert L.sf_debug_stream_read(addr, 0, sk, 1, None) == 0           # empty: nothing launched
+    assert L.sf_debug_stream_read(addr + 8, 1024, sk, 1, None) == 1    # misaligned buffer
+    assert L.sf_debug_stream_read(addr, 1000, sk, 1, None) == 1        # not a multiple of 16
+    assert L.sf_debug_stream_read(addr, 1024, sk, 0, None) == 1        # no blocks
+    assert L.sf_debug_stream_read(addr, 1024, sk, 65537, None) == 1    # too many blocks
+    assert L.sf_debug_stream_read(addr, 1024, None, 1, None) == 1      # no sink
