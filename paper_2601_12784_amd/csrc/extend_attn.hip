@@ -87,8 +87,10 @@ template <int D>
 struct Tiles {
   static constexpr int kElems = kPage * D;            // bf16 per (page, KV head) tile
   static constexpr int kChunks = kElems / 8;          // 16-byte pieces per tile
-  static constexpr int kLoads = 4 * kChunks / kThreads;  // pieces per thread per step
-  static_assert(kLoads * kThreads == 4 * kChunks, "staging split");
+  // A step stages four tiles (K and V of two pages); each is moved by
+  // kWaves / 4 waves, kWaveChunks wave-wide 1 KiB chunks (64 pieces) each.
+  static constexpr int kWaveChunks = kChunks / 64 / (kWaves / 4);
+  static_assert(kWaveChunks * 64 * kWaves == 4 * kChunks, "staging split");
 };
 
 // Online-softmax update of one 16-row tile for one step of 32 keys, in two
@@ -187,8 +189,7 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
   constexpr int KB = D / 32;
   constexpr int JB = D / 16;
   constexpr int TE = Tiles<D>::kElems;
-  constexpr int TC = Tiles<D>::kChunks;
-  constexpr int NL = Tiles<D>::kLoads;
+  constexpr int NC = Tiles<D>::kWaveChunks;
   constexpr int kWaveRows = 16 * kRowTiles;
   // [buffer][step of the interval][K page 0 | K page 1 | V of both pages, interleaved]
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][kSub][4 * TE];
@@ -247,14 +248,42 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
     lsum[rt] = 0.f;
   }
 
-  // Staging: thread tid moves pieces tid, tid + kThreads, ... of the step's
-  // four tiles. A page past the item's last is replaced by its first page
-  // (always in range); its keys lie past kend and are masked.
+  // Staging: wave w moves tile w / 2 of each step (0: K of the step's first
+  // page, 1: K of its second, 2 and 3: V of the two pages), in 1 KiB chunks
+  // (w % 2) * NC .. + NC - 1. The tile and its page are wave-uniform, so the
+  // global address is a scalar base plus a fixed per-lane offset, and every
+  // LDS address is fixed per lane: no per-step address arithmetic. A page past
+  // the item's last is replaced by its first page (always in range); its keys
+  // lie past kend and are masked.
   // The keys are walked in intervals of kSub steps with one barrier each:
   // a wave's work between barriers is then long enough for the two waves
   // that share a SIMD to fall out of step (one on the matrix core while the
   // other exponentiates).
-  u32x4 pre[kSub][NL];
+  const int stile = wave >> 1;
+  const uint16_t* const spool = stile < 2 ? a.k_pool : a.v_pool;
+  int soff[NC];    // element offset of this lane's piece in the tile
+  int sdst0[NC];   // LDS element offset of the piece (K) or of its first 8-byte half (V)
+  int sdst1[NC];   // V: LDS element offset of the second half
+  int skey[NC];    // V: first token of the piece within the step's 32 keys
+#pragma unroll
+  for (int q = 0; q < NC; ++q) {
+    soff[q] = (((wave & 1) * NC + q) * 64 + lane) * 8;
+    if (stile < 2) {
+      sdst0[q] = stile * TE + soff[q];
+      sdst1[q] = 0;
+      skey[q] = 0;
+    } else {
+      // V pool tile [D][16 tokens]: the piece holds tokens 8c .. 8c+7 of dim d.
+      const int pg = stile - 2;
+      const int d = soff[q] >> 4;
+      const int c = (soff[q] >> 3) & 1;
+      const int row = 2 * TE + d * 32 + pg * 4;
+      sdst0[q] = row + ((2 * c) ^ v_swizzle(d)) * 8;
+      sdst1[q] = row + ((2 * c + 1) ^ v_swizzle(d)) * 8;
+      skey[q] = pg * kPage + 8 * c;
+    }
+  }
+  u32x4 pre[kSub][NC];
   auto fetch = [&](int j) {
 #pragma unroll
     for (int u = 0; u < kSub; ++u) {
@@ -262,52 +291,41 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
       if (js >= nsteps) break;
       const int pg0 = 2 * js;
       const int p0 = bt[pg0];
-      const int p1 = pg0 + 1 < npages ? bt[pg0 + 1] : p0;
+      const int page = (stile & 1) && pg0 + 1 < npages ? bt[pg0 + 1] : p0;
+      const uint16_t* src = spool + tile_base(page, a.num_kv_heads, kvh, D);
 #pragma unroll
-      for (int i = 0; i < NL; ++i) {
-        const int piece = tid + i * kThreads;
-        const int tile = piece / TC;
-        const int off = (piece % TC) * 8;
-        const uint16_t* pool = tile < 2 ? a.k_pool : a.v_pool;
-        const int page = (tile & 1) ? p1 : p0;
-        pre[u][i] = *reinterpret_cast<const u32x4*>(pool + tile_base(page, a.num_kv_heads, kvh, D) + off);
-      }
+      for (int q = 0; q < NC; ++q) pre[u][q] = *reinterpret_cast<const u32x4*>(src + soff[q]);
     }
   };
-  // Writes the fetched pieces of interval j into buffer buf. V pieces are
-  // split into their two token quads (8 bytes each) at their interleaved
-  // slots; in the step that reaches kend, V tokens at or past it are zeroed
-  // here (they may be stale or NaN, and a zero weight times NaN is still NaN).
-  auto stage = [&](int buf, int j) {
+  // Writes the fetched pieces of interval j into LDS buffer `base` (one per
+  // step of the interval). V pieces are split into their two token quads
+  // (8 bytes each) at their interleaved slots; in the step that reaches kend,
+  // V tokens at or past it are zeroed here (they may be stale or NaN, and a
+  // zero weight times NaN is still NaN).
+  auto stage = [&](uint16_t (*base)[4 * TE], int j) {
 #pragma unroll
     for (int u = 0; u < kSub; ++u) {
       const int js = kSub * j + u;
       if (js >= nsteps) break;
-      const int key0 = js * kStepKeys;
-      const bool tail = key0 + kStepKeys > kend;
-      uint16_t* base = lds[buf][u];
+      uint16_t* L = base[u];
+      if (stile < 2) {
 #pragma unroll
-      for (int i = 0; i < NL; ++i) {
-        const int piece = tid + i * kThreads;
-        const int tile = piece / TC;
-        const int off = (piece % TC) * 8;
-        if (tile < 2) {
-          *reinterpret_cast<u32x4*>(base + tile * TE + off) = pre[u][i];
-        } else {
-          const int pg = tile - 2;
-          const int d = off >> 4;
-          const int c = (off >> 3) & 1;   // tokens 8c .. 8c+7 of the page
-          u32x4 x = pre[u][i];
+        for (int q = 0; q < NC; ++q) *reinterpret_cast<u32x4*>(L + sdst0[q]) = pre[u][q];
+      } else {
+        const int key0 = js * kStepKeys;
+        const bool tail = key0 + kStepKeys > kend;
+#pragma unroll
+        for (int q = 0; q < NC; ++q) {
+          u32x4 x = pre[u][q];
           if (tail) {
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
-              const int key = key0 + pg * kPage + 8 * c + 2 * w;
+              const int key = key0 + skey[q] + 2 * w;
               x[w] &= (key < kend ? 0x0000FFFFu : 0u) | (key + 1 < kend ? 0xFFFF0000u : 0u);
             }
           }
-          uint16_t* row = base + 2 * TE + d * 32 + pg * 4;
-          *reinterpret_cast<u32x2*>(row + ((2 * c) ^ v_swizzle(d)) * 8) = u32x2{x[0], x[1]};
-          *reinterpret_cast<u32x2*>(row + ((2 * c + 1) ^ v_swizzle(d)) * 8) = u32x2{x[2], x[3]};
+          *reinterpret_cast<u32x2*>(L + sdst0[q]) = u32x2{x[0], x[1]};
+          *reinterpret_cast<u32x2*>(L + sdst1[q]) = u32x2{x[2], x[3]};
         }
       }
     }
@@ -361,20 +379,25 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
 
   const int nint = (nsteps + kSub - 1) / kSub;
   fetch(0);
-  stage(0, 0);
+  stage(lds[0], 0);
   __syncthreads();
 
-  for (int j = 0; j < nint; ++j) {
-    const int buf = j & 1;
+  // One interval from buffer `cur` while the next is staged into `nxt`; the
+  // loop is unrolled by two so that both buffers' addresses are constants.
+  auto interval = [&](int j, uint16_t (*cur)[4 * TE], uint16_t (*nxt)[4 * TE]) {
     if (j + 1 < nint) fetch(j + 1);
 #pragma unroll
     for (int u = 0; u < kSub; ++u) {
       const int js = kSub * j + u;
       const int key0 = js * kStepKeys;
-      if (js < nsteps && key0 <= wave_kmax) compute(lds[buf][u], key0);
+      if (js < nsteps && key0 <= wave_kmax) compute(cur[u], key0);
     }
-    if (j + 1 < nint) stage(buf ^ 1, j + 1);
+    if (j + 1 < nint) stage(nxt, j + 1);
     __syncthreads();
+  };
+  for (int j = 0; j < nint; j += 2) {
+    interval(j, lds[0], lds[1]);
+    if (j + 1 < nint) interval(j + 1, lds[1], lds[0]);
   }
 
   // Lane holds O[row col][16*jb + 4*grp + i] of each row tile.
