@@ -69,63 +69,6 @@ class Stepper:
                     chunk_pages=self.chunk, stream=self.stream, attn_events=ev_attn, fp8=self.fp8)
 
 
-class ClockSampler:
-    """Samples the GPU's per-XCD graphics clocks and its memory clock (amdsmi
-    GPU metrics, in-process) every `period` seconds from a background thread.
-    Started before the warm-up steps; only samples taken between mark() and
-    the end count. Reports nothing if amdsmi or the device is unavailable."""
-
-    def __init__(self, period=0.01):
-        import threading
-        self.period, self.gfx, self.mem = period, [], []
-        self._t0 = None
-        self._stop = threading.Event()
-        self._thread = threading.Thread(target=self._run, daemon=True)
-        self._ok = False
-        try:
-            import amdsmi
-            amdsmi.amdsmi_init()
-            self._amdsmi = amdsmi
-            self._h = amdsmi.amdsmi_get_processor_handles()[0]
-            self._ok = True
-        except Exception:
-            self._amdsmi = None
-
-    def mark(self):
-        self._t0 = time.perf_counter()
-
-    def _run(self):
-        while not self._stop.wait(self.period):
-            try:
-                m = self._amdsmi.amdsmi_get_gpu_metrics_info(self._h)
-            except Exception:
-                return
-            if self._t0 is not None and time.perf_counter() >= self._t0:
-                clks = [c for c in m.get("current_gfxclks", []) if isinstance(c, (int, float))]
-                if clks:
-                    self.gfx.append(float(np.mean(clks)))
-                if isinstance(m.get("current_uclk"), (int, float)):
-                    self.mem.append(float(m["current_uclk"]))
-
-    def __enter__(self):
-        if self._ok:
-            self._thread.start()
-        return self
-
-    def __exit__(self, *exc):
-        self._stop.set()
-        if self._ok:
-            self._thread.join()
-
-    def summary(self):
-        if not self.gfx:
-            return None
-        return {"gfx_mhz_median": float(np.median(self.gfx)), "gfx_mhz_min": float(min(self.gfx)),
-                "gfx_mhz_max": float(max(self.gfx)),
-                "mem_mhz_median": float(np.median(self.mem)) if self.mem else None, "samples": len(self.gfx),
-                "source": "amdsmi GPU metrics (mean over XCDs), sampled every 10 ms during the timed steps"}
-
-
 EVENT_EVERY = 8  # timing events bracket the attention kernel of every 8th timed step
 
 
@@ -624,12 +567,7 @@ def main():
     kv = batch.kv_bytes()
     log(f"  {batch.num_seqs} seqs, {int(batch.seq_lens.sum())} tokens, {kv / 1e9:.3f} GB KV/step")
     st = Stepper(batch, chunk_pages=args.chunk_pages, workers_per_cu=args.workers_per_cu)
-    with ClockSampler() as clocks:
-        for _ in range(args.warmup):
-            st.step()
-        st.torch.cuda.synchronize()
-        clocks.mark()
-        ms_step, attn_ms_mean, attn_ms_med = time_steps(st, args.steps, 0)
+    ms_step, attn_ms_mean, attn_ms_med = time_steps(st, args.steps, args.warmup)
     info = st.info0
     log(f"  step {ms_step * 1e3:.1f} us, attention kernel {attn_ms_mean * 1e3:.1f} us (median "
         f"{attn_ms_med * 1e3:.1f}), {info.num_workers} workers x {info.chunk_pages} pages, "
@@ -668,7 +606,6 @@ def main():
         "pct_of_peak_hbm": round(100.0 * kv / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2),
         "attn_kernel_us": round(attn_ms_mean * 1e3, 2),
         "host_plan_us": round(plan_us, 2),
-        "gpu_clocks": clocks.summary(),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic},
