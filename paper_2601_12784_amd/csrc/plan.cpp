@@ -82,12 +82,17 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
     if (opts->min_chunk_pages) mn = opts->min_chunk_pages;
   }
 
+  // Pages per sequence (every KV head of a sequence has the same count).
+  thread_local std::vector<int32_t> spg_buf;
+  spg_buf.resize(size_t(B));
+  int32_t* spg = spg_buf.data();
   int64_t total = 0;
   for (int32_t s = 0; s < B; ++s) {
     const int32_t L = seq_lens_host[s];
     if (L < 0 || (L > 0 && desc->num_pages == 0)) return SF_ERR_INVALID_ARG;
     const int64_t npg = (int64_t(L) + kPage - 1) / kPage;
     if (npg > desc->block_table_stride) return SF_ERR_INVALID_ARG;
+    spg[s] = int32_t(npg);
     total += npg * hkv;
   }
   if (total > (int64_t(1) << 40)) return SF_ERR_INVALID_ARG;
@@ -103,35 +108,65 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
     workers = std::min<int64_t>(int64_t(wpc) * num_cus, (total + mn - 1) / mn);
   }
   if (workers > INT32_MAX / 2) return SF_ERR_INVALID_ARG;
-  auto pages_of = [&](int64_t pair) { return (int64_t(seq_lens_host[pair / hkv]) + kPage - 1) / kPage; };
-  auto lo_of = [&](int64_t w) { return w * total / workers; };
+
+  // Worker range starts lo(w) = floor(w T / W), walked forward without
+  // divisions: quotient and remainder advance by T / W and T mod W.
+  struct Cuts {
+    int64_t q = 0, r = 0, dq = 0, dr = 0, den = 1;
+    void init(int64_t t, int64_t w) {
+      q = r = 0;
+      den = w > 0 ? w : 1;
+      dq = t / den;
+      dr = t % den;
+    }
+    void next() {
+      q += dq;
+      r += dr;
+      if (r >= den) {
+        r -= den;
+        ++q;
+      }
+    }
+  };
 
   // Pass 1: segments per pair. Worker ranges are cut at pair boundaries; a
-  // pair spanning k worker boundaries has k + 1 segments.
+  // pair spanning k worker boundaries has k + 1 segments. Pairs are walked in
+  // order (s-major, kvh-minor) with a worker cursor that only moves forward.
   thread_local std::vector<int32_t> nseg_buf;
   nseg_buf.assign(size_t(num_pairs), 0);
   int32_t* nseg = nseg_buf.data();
-  int64_t n_work = 0;
+  int64_t n_work = 0, n_comb = 0, n_part = 0, n_empty = 0;
   {
-    int64_t start = 0;  // global page where the current pair starts
-    for (int64_t p = 0; p < num_pairs; ++p) {
-      const int64_t npg = pages_of(p);
-      if (npg == 0) {
-        nseg[p] = 1;
-        continue;
+    Cuts next_lo;           // lo(cur + 1)
+    next_lo.init(total, workers);
+    next_lo.next();
+    int64_t cur = 0;        // worker whose range holds `start`
+    int64_t start = 0;      // global page where the current pair starts
+    int64_t p = 0;
+    for (int32_t s = 0; s < B; ++s) {
+      const int64_t npg = spg[s];
+      for (int32_t h = 0; h < hkv; ++h, ++p) {
+        if (npg == 0) {
+          nseg[p] = 1;
+          ++n_empty;
+          continue;
+        }
+        while (cur + 1 < workers && next_lo.q <= start) {
+          ++cur;
+          next_lo.next();
+        }
+        // boundaries lo(w) inside (start, start + npg) each add a segment
+        int32_t k = 1;
+        while (cur + 1 < workers && next_lo.q < start + npg) {
+          ++cur;
+          next_lo.next();
+          ++k;
+        }
+        nseg[p] = k;
+        start += npg;
       }
-      // workers whose range intersects [start, start + npg)
-      const int64_t w_first = (start * workers) / total;          // lo_of(w) <= start
-      int64_t wf = w_first;
-      while (wf + 1 < workers && lo_of(wf + 1) <= start) ++wf;
-      while (lo_of(wf) > start) --wf;
-      int64_t wl = wf;
-      while (wl + 1 < workers && lo_of(wl + 1) < start + npg) ++wl;
-      nseg[p] = int32_t(wl - wf + 1);
-      start += npg;
     }
   }
-  int64_t n_comb = 0, n_part = 0;
   for (int64_t p = 0; p < num_pairs; ++p) {
     n_work += nseg[p];
     if (nseg[p] > 1) {
@@ -165,15 +200,17 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   cidx_buf.assign(size_t(num_pairs), -1);
   {
     int32_t slot = 0, ci = 0;
-    for (int64_t p = 0; p < num_pairs; ++p) {
-      if (nseg[p] <= 1) continue;
-      base_buf[size_t(p)] = slot;
-      cidx_buf[size_t(p)] = ci;
-      const int32_t c8[kItemInts] = {int32_t(p / hkv), int32_t(p % hkv), slot, nseg[p], seq_lens_host[p / hkv],
-                                     0, 0, 0};
-      std::memcpy(comb + int64_t(ci) * kItemInts, c8, sizeof c8);
-      slot += nseg[p];
-      ++ci;
+    int64_t p = 0;
+    for (int32_t s = 0; s < B; ++s) {
+      for (int32_t h = 0; h < hkv; ++h, ++p) {
+        if (nseg[p] <= 1) continue;
+        base_buf[size_t(p)] = slot;
+        cidx_buf[size_t(p)] = ci;
+        const int32_t c8[kItemInts] = {s, h, slot, nseg[p], seq_lens_host[s], 0, 0, 0};
+        std::memcpy(comb + int64_t(ci) * kItemInts, c8, sizeof c8);
+        slot += nseg[p];
+        ++ci;
+      }
     }
   }
   const int32_t* base = base_buf.data();
@@ -183,25 +220,48 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   // the empty pairs e with e mod workers == w.
   thread_local std::vector<int64_t> empty_buf;
   empty_buf.clear();
-  for (int64_t p = 0; p < num_pairs; ++p)
-    if (pages_of(p) == 0) empty_buf.push_back(p);
-  int64_t row = 0, p = 0, pstart = 0;
+  empty_buf.reserve(size_t(n_empty));
+  for (int32_t s = 0; s < B; ++s)
+    if (spg[s] == 0)
+      for (int32_t h = 0; h < hkv; ++h) empty_buf.push_back(int64_t(s) * hkv + h);
+  // Cursor over the non-empty pairs: pair p = (ps, ph).
+  int64_t p = 0;
+  int32_t ps = 0, ph = 0;
+  auto skip_empty = [&]() {
+    while (ps < B && spg[ps] == 0) {
+      ++ps;
+      p = int64_t(ps) * hkv;
+      ph = 0;
+    }
+  };
+  auto advance = [&]() {
+    ++p;
+    if (++ph == hkv) {
+      ph = 0;
+      ++ps;
+    }
+    skip_empty();
+  };
+  skip_empty();
+  int64_t row = 0, pstart = 0;
   int32_t seg_c = 0;  // segment index within the current pair
-  while (p < num_pairs && pages_of(p) == 0) ++p;
-  for (int64_t w = 0; w < workers; ++w) {
-    const int64_t lo = lo_of(w), hi = lo_of(w + 1);
+  Cuts lo_w, hi_w;
+  lo_w.init(total, workers);
+  hi_w.init(total, workers);
+  hi_w.next();
+  for (int64_t w = 0; w < workers; ++w, lo_w.next(), hi_w.next()) {
+    const int64_t lo = lo_w.q, hi = hi_w.q;
     table[2 * w] = int32_t(row);
     int64_t cnt = 0;
-    while (p < num_pairs && pstart < hi) {
-      const int64_t npg = pages_of(p);
+    while (ps < B && pstart < hi) {
+      const int64_t npg = spg[ps];
       const int64_t b = std::max(lo, pstart) - pstart, e = std::min(hi, pstart + npg) - pstart;
       int32_t* r = items + row * kItemInts;
-      const int32_t L = seq_lens_host[p / hkv];
-      r[0] = int32_t(p / hkv);
-      r[1] = int32_t(p % hkv);
+      r[0] = ps;
+      r[1] = ph;
       r[2] = int32_t(b);
       r[3] = int32_t(e);
-      r[4] = L;
+      r[4] = seq_lens_host[ps];
       r[5] = nseg[p] > 1 ? base[p] + seg_c : -1;
       r[6] = cidx[p];
       r[7] = nseg[p];
@@ -210,8 +270,7 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
       if (pstart + npg <= hi) {  // pair finished inside this worker
         pstart += npg;
         seg_c = 0;
-        ++p;
-        while (p < num_pairs && pages_of(p) == 0) ++p;
+        advance();
       } else {
         ++seg_c;
         break;
