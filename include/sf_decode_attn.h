@@ -202,24 +202,23 @@ sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* in
  * Native per-step runner. A rollout instance runs one batched decode step
  * after another (App. B.1), so host work between steps is on the critical
  * path once the kernels are short. sf_runner_step does, in one call: plan
- * (sf_decode_attn_plan with the runner's options) into a pinned host buffer,
- * upload on the runner's own copy stream, then on the caller's stream the
- * attention (plain, appending or fp8) and the merge of split sequences. The
- * runner owns a ring of 4 pinned buffers, 2 device work-list buffers, the
- * split-K workspace (grown on demand, after synchronizing the caller's stream
- * and its copy stream), the copy stream (default priority) and its events: a
- * pinned buffer is rewritten only after its upload completed, a device
- * buffer overwritten only after the step that read it ended, and the upload
- * of step i + 1 overlaps the kernels of step i. One runner serves one device
- * (the current one at creation) and one caller stream at a time; steps on
- * different streams, or calls that overlap, are not supported.
+ * (sf_decode_attn_plan with the runner's options) into a pinned, device-
+ * mapped host buffer, then on the caller's stream the attention (plain,
+ * appending or fp8) and the merge of split sequences, whose kernels read that
+ * work list in place (no separate upload). The runner owns a ring of 4 such
+ * buffers, the split-K workspace (grown on demand, after synchronizing the
+ * caller's stream) and one event per buffer: a buffer is rewritten only
+ * after the step that read it has ended, so the host plans step i + 1 while
+ * the kernels of step i run. One runner serves one device (the current one at
+ * creation) and one caller stream at a time; steps on different streams, or
+ * calls that overlap, are not supported.
  */
 typedef struct sf_runner sf_runner;
 
 typedef struct sf_runner_extras {
   const void* k_new;             /* appending step (sf_decode_attn_append's arguments) */
   const void* v_new;
-  const int32_t* new_pages_host; /* host int32 [num_seqs], copied into the upload */
+  const int32_t* new_pages_host; /* host int32 [num_seqs], copied next to the work list */
   const float* k_scale;          /* fp8 cache (sf_decode_attn_fp8's scales); not with k_new */
   const float* v_scale;
   void* attn_start;              /* optional hipEvent_t recorded before the attention launch */

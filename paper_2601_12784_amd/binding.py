@@ -585,8 +585,8 @@ class _HipEvent:
 class DecodeAttention:
     """Plan + attention + combine for successive decode steps, through the
     library's native runner (sf_runner_create / sf_runner_step): one call per
-    step plans into the runner's pinned ring, uploads on its copy stream and
-    launches the kernels on the caller's stream. Tensor checks run once per
+    step plans into the runner's pinned, device-mapped ring and launches the
+    kernels, which read that work list in place, on the caller's stream. Tensor checks run once per
     distinct set of tensors."""
 
     def __init__(self, num_q_heads, num_kv_heads, head_dim, device=None, num_cus=None,

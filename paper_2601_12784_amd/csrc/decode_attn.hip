@@ -307,21 +307,58 @@ __device__ __forceinline__ void store_token(uint16_t* k_dst, uint16_t* v_dst, co
     __builtin_nontemporal_store(v_new[row + dim], v_dst + tile + v_elem(slot, dim));
 }
 
+// The fields of a segment row that the attention pass uses.
+struct Segment {
+  int seq, kvh, pb, pe, len, slot;
+};
+
+// A worker's segment rows, kRowsPerLoad at a time: one vector load brings
+// them into the wave (lane l holds int l of the rows), so a worker pays one
+// memory round trip for its rows instead of one per segment. That matters
+// when the work list is read in place from pinned host memory.
+constexpr int kRowsPerLoad = 64 / kItemInts;
+
+__device__ __forceinline__ Segment segment_at(int v, int i) {
+  Segment sg;
+  sg.seq = __builtin_amdgcn_readlane(v, i * kItemInts + 0);
+  sg.kvh = __builtin_amdgcn_readlane(v, i * kItemInts + 1);
+  sg.pb = __builtin_amdgcn_readlane(v, i * kItemInts + 2);
+  sg.pe = __builtin_amdgcn_readlane(v, i * kItemInts + 3);
+  sg.len = __builtin_amdgcn_readlane(v, i * kItemInts + 4);
+  sg.slot = __builtin_amdgcn_readlane(v, i * kItemInts + 5);
+  return sg;
+}
+
+// Calls f(segment) for each of this wave's worker's segments, in order.
+template <class F>
+__device__ __forceinline__ void for_each_segment(const AttnArgs& a, F&& f) {
+  const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
+  const int first = wt[0];
+  const int count = wt[1];
+  const int lane = threadIdx.x;
+  for (int b = 0; b < count; b += kRowsPerLoad) {
+    const int n = min(count - b, kRowsPerLoad);
+    const int32_t* rows = a.items + size_t(first + b) * kItemInts;
+    const int v = lane < n * kItemInts ? rows[lane] : 0;
+    for (int i = 0; i < n; ++i) f(segment_at(v, i));
+  }
+}
+
 // One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
 template <int D, bool kAppend>
-__device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr item) {
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment& item) {
   constexpr int KB = Shape<D>::KB;
   constexpr int JB = Shape<D>::JB;
   const int lane = threadIdx.x;
   const int col = lane & 15;   // MFMA column (query head in group) and A-operand row
   const int grp = lane >> 4;   // MFMA k-group
 
-  const int seq = item[0];
-  const int kvh = item[1];
-  const int pb = item[2];
-  const int pe = item[3];
-  const int len = item[4];
-  const int slot = item[5];
+  const int seq = item.seq;
+  const int kvh = item.kvh;
+  const int pb = item.pb;
+  const int pe = item.pe;
+  const int len = item.len;
+  const int slot = item.slot;
   const int g = a.group;
   const bool head_ok = col < g;
   const int head = kvh * g + col;
@@ -426,11 +463,7 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const_i32_ptr 
 // stores nothing: the stores come in the merge launch that follows.
 template <int D, bool kAppend>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_kernel(AttnArgs a) {
-  const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
-  const int first = wt[0];
-  const int count = wt[1];
-  for (int i = 0; i < count; ++i)
-    attend_segment<D, kAppend>(a, as_constant(a.items) + size_t(first + i) * kItemInts);
+  for_each_segment(a, [&](const Segment& sg) { attend_segment<D, kAppend>(a, sg); });
 }
 
 // ---------------------------------------------------------------------------
@@ -547,18 +580,18 @@ __device__ __forceinline__ void widen_v(const VHalf8<D>& r, VHalf<D>& b) {
 
 // One segment over an fp8 cache; otherwise as attend_segment.
 template <int D>
-__device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const_i32_ptr item) {
+__device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segment& item) {
   constexpr int KB = Shape<D>::KB;
   constexpr int JB = Shape<D>::JB;
   const int lane = threadIdx.x;
   const int col = lane & 15;
   const int grp = lane >> 4;
-  const int seq = item[0];
-  const int kvh = item[1];
-  const int pb = item[2];
-  const int pe = item[3];
-  const int len = item[4];
-  const int slot = item[5];
+  const int seq = item.seq;
+  const int kvh = item.kvh;
+  const int pb = item.pb;
+  const int pe = item.pe;
+  const int len = item.len;
+  const int slot = item.slot;
   const int g = a.group;
   const bool head_ok = col < g;
   const int head = kvh * g + col;
@@ -652,10 +685,7 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const_i32_
 
 template <int D>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_fp8_kernel(AttnArgs a) {
-  const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
-  const int first = wt[0];
-  const int count = wt[1];
-  for (int i = 0; i < count; ++i) attend_segment_fp8<D>(a, as_constant(a.items) + size_t(first + i) * kItemInts);
+  for_each_segment(a, [&](const Segment& sg) { attend_segment_fp8<D>(a, sg); });
 }
 
 // ---------------------------------------------------------------------------

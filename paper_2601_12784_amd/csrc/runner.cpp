@@ -1,16 +1,18 @@
-// Native per-step runner: plan -> upload -> attention (-> merge) in one call.
+// Native per-step runner: plan -> attention (-> merge) in one call.
 //
 // A rollout instance runs one batched decode step after another (App. B.1:
 // each step generates one token per running trajectory), so the host work
 // between two steps is on the critical path once the kernels are short:
 // small batches, late steps of a long-tail batch, an fp8 cache. This object
 // keeps that work native. It owns a ring of pinned host buffers that the
-// planner writes into, two device work-list buffers, the split-K workspace,
-// a copy stream (default priority) and the events that order them:
-//   - a pinned buffer is rewritten only after its last upload completed;
-//   - a device buffer is uploaded into only after the step that read it ended;
-//   - the compute stream waits on the upload of its own step only,
-// so the upload of step i + 1 overlaps the kernels of step i.
+// planner writes into and the kernels read in place (mapped host memory,
+// zero-copy), the split-K workspace, and one event per ring slot:
+//   - a slot is rewritten only after the step that read it has ended;
+//   - nothing else orders the steps, so the host plans step i + 1 while the
+//     kernels of step i run.
+// A separate upload (a copy stream, a device work list and a cross-stream
+// wait) cost more per step than the kernels' in-place reads of the list, and
+// how much more depended on whether the two streams shared a hardware queue.
 #include <hip/hip_runtime.h>
 
 #include <cstring>
@@ -26,14 +28,8 @@ constexpr int kRing = 4;
 constexpr int kFp8WorkersPerCu = 8;
 
 struct Pinned {
-  int32_t* ptr = nullptr;
-  uint64_t bytes = 0;
-  hipEvent_t uploaded = nullptr;   // recorded on the copy stream after the upload that read it
-  bool used = false;
-};
-
-struct DeviceBuf {
-  int32_t* ptr = nullptr;
+  int32_t* ptr = nullptr;          // host address (the planner writes here)
+  const int32_t* dev = nullptr;    // the same memory as the kernels address it
   uint64_t bytes = 0;
   hipEvent_t released = nullptr;   // recorded on the compute stream after the step that read it
   bool used = false;
@@ -45,9 +41,7 @@ struct sf_runner {
   sf_attn_desc shape;      // heads, head_dim, page size (per-step fields are overwritten)
   sf_plan_opts opts;
   int device = 0;
-  hipStream_t copy = nullptr;
   Pinned ring[kRing];
-  DeviceBuf work[2];
   void* workspace = nullptr;
   uint64_t workspace_bytes = 0;
   uint64_t steps = 0;
@@ -56,21 +50,30 @@ struct sf_runner {
 
 namespace {
 
+// Called only when no step in flight reads the slot (its event has completed).
 sf_status grow_pinned(Pinned& p, uint64_t bytes) {
   if (p.bytes >= bytes) return SF_OK;
   if (p.ptr && hipHostFree(p.ptr) != hipSuccess) return SF_ERR_HIP;
   p.ptr = nullptr;
+  p.dev = nullptr;
   p.bytes = 0;
   const uint64_t want = bytes + bytes / 4 + 4096;
   if (hipHostMalloc(reinterpret_cast<void**>(&p.ptr), want, hipHostMallocDefault) != hipSuccess) return SF_ERR_HIP;
+  void* dev = nullptr;
+  if (hipHostGetDevicePointer(&dev, p.ptr, 0) != hipSuccess) {
+    (void)hipHostFree(p.ptr);
+    p.ptr = nullptr;
+    return SF_ERR_HIP;
+  }
+  p.dev = static_cast<const int32_t*>(dev);
   p.bytes = want;
   return SF_OK;
 }
 
-// Device buffers grow only when nothing in flight can still read them.
-sf_status grow_device(void** ptr, uint64_t* have, uint64_t bytes, hipStream_t main, hipStream_t copy) {
+// The workspace grows only when nothing in flight can still use it.
+sf_status grow_device(void** ptr, uint64_t* have, uint64_t bytes, hipStream_t main) {
   if (*have >= bytes) return SF_OK;
-  if (hipStreamSynchronize(main) != hipSuccess || hipStreamSynchronize(copy) != hipSuccess) return SF_ERR_HIP;
+  if (hipStreamSynchronize(main) != hipSuccess) return SF_ERR_HIP;
   if (*ptr && hipFree(*ptr) != hipSuccess) return SF_ERR_HIP;
   *ptr = nullptr;
   *have = 0;
@@ -98,15 +101,15 @@ extern "C" sf_status sf_runner_create(const sf_attn_desc* shape, const sf_plan_o
   r->shape = probe;
   if (opts) r->opts = *opts;
   else std::memset(&r->opts, 0, sizeof r->opts);
-  if (hipGetDevice(&r->device) != hipSuccess ||
-      hipStreamCreateWithFlags(&r->copy, hipStreamNonBlocking) != hipSuccess) {
+  if (hipGetDevice(&r->device) != hipSuccess) {
     delete r;
     return SF_ERR_HIP;
   }
+  // The events only order the host's reuse of a slot after the GPU's reads
+  // of it; they publish no GPU writes, so they skip the system-scope fence.
   for (auto& p : r->ring)
-    if (hipEventCreateWithFlags(&p.uploaded, hipEventDisableTiming) != hipSuccess) st = SF_ERR_HIP;
-  for (auto& w : r->work)
-    if (hipEventCreateWithFlags(&w.released, hipEventDisableTiming) != hipSuccess) st = SF_ERR_HIP;
+    if (hipEventCreateWithFlags(&p.released, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess)
+      st = SF_ERR_HIP;
   if (st != SF_OK) {
     sf_runner_destroy(r);
     return st;
@@ -118,18 +121,10 @@ extern "C" sf_status sf_runner_create(const sf_attn_desc* shape, const sf_plan_o
 // Teardown cannot report errors: every call is made, whatever the others return.
 extern "C" void sf_runner_destroy(sf_runner* r) {
   if (!r) return;
-  if (r->copy) (void)hipStreamSynchronize(r->copy);
-  for (auto& w : r->work) {
-    if (w.released) {
-      (void)hipEventSynchronize(w.released);
-      (void)hipEventDestroy(w.released);
-    }
-    if (w.ptr) (void)hipFree(w.ptr);
-  }
   for (auto& p : r->ring) {
-    if (p.uploaded) {
-      (void)hipEventSynchronize(p.uploaded);
-      (void)hipEventDestroy(p.uploaded);
+    if (p.released) {
+      (void)hipEventSynchronize(p.released);
+      (void)hipEventDestroy(p.released);
     }
     if (p.ptr) (void)hipHostFree(p.ptr);
   }
@@ -137,7 +132,6 @@ extern "C" void sf_runner_destroy(sf_runner* r) {
     (void)hipDeviceSynchronize();
     (void)hipFree(r->workspace);
   }
-  if (r->copy) (void)hipStreamDestroy(r->copy);
   delete r;
 }
 
@@ -155,10 +149,10 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   if (append && !lse) return SF_ERR_INVALID_ARG;
   hipStream_t main = static_cast<hipStream_t>(stream);
 
-  // 1. plan into the next pinned buffer (after its previous upload finished);
-  //    grow it and plan again only if the plan does not fit
+  // 1. plan into the next ring slot (after the step that last read it has
+  //    ended); grow it and plan again only if the plan does not fit
   Pinned& pin = r->ring[r->steps % kRing];
-  if (pin.used && hipEventSynchronize(pin.uploaded) != hipSuccess) return SF_ERR_HIP;
+  if (pin.used && hipEventSynchronize(pin.released) != hipSuccess) return SF_ERR_HIP;
   const uint64_t extra = append ? uint64_t(desc->num_seqs) * 4 : 0;
   // An fp8 block moves half the bytes of a bf16 one: unless the caller chose,
   // fp8 steps plan two waves per SIMD (measured: kernel 129 us instead of 136
@@ -180,44 +174,32 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   r->last = info;
   if (info.num_workers == 0) return SF_OK;
 
-  // 2. workspace and device work-list buffer (grown only while idle)
-  if ((st = grow_device(&r->workspace, &r->workspace_bytes, info.workspace_bytes, main, r->copy)) != SF_OK)
-    return st;
-  DeviceBuf& dev = r->work[r->steps % 2];
-  const uint64_t nbytes = info.work_bytes + extra;
-  void* dptr = dev.ptr;
-  if ((st = grow_device(&dptr, &dev.bytes, nbytes, main, r->copy)) != SF_OK) return st;
-  dev.ptr = static_cast<int32_t*>(dptr);
+  // 2. workspace (grown only while idle)
+  if ((st = grow_device(&r->workspace, &r->workspace_bytes, info.workspace_bytes, main)) != SF_OK) return st;
+  int32_t* work = const_cast<int32_t*>(pin.dev);
 
-  // 3. upload on the copy stream once the last reader of this buffer is done
-  if (dev.used && hipStreamWaitEvent(r->copy, dev.released, 0) != hipSuccess) return SF_ERR_HIP;
-  if (hipMemcpyAsync(dev.ptr, pin.ptr, nbytes, hipMemcpyHostToDevice, r->copy) != hipSuccess) return SF_ERR_HIP;
-  if (hipEventRecord(pin.uploaded, r->copy) != hipSuccess) return SF_ERR_HIP;
-  pin.used = true;
-  if (hipStreamWaitEvent(main, pin.uploaded, 0) != hipSuccess) return SF_ERR_HIP;
-
-  // 4. kernels on the caller's stream (optionally bracketed by the caller's events)
+  // 3. kernels on the caller's stream (optionally bracketed by the caller's events)
   hipEvent_t ev0 = extras ? static_cast<hipEvent_t>(extras->attn_start) : nullptr;
   hipEvent_t ev1 = extras ? static_cast<hipEvent_t>(extras->attn_end) : nullptr;
   if (ev0 && hipEventRecord(ev0, main) != hipSuccess) return SF_ERR_HIP;
   if (append) {
-    st = sf_decode_attn_append(desc, &info, nullptr, dev.ptr, q, extras->k_new, extras->v_new,
-                               reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(dev.ptr) + info.work_bytes),
+    st = sf_decode_attn_append(desc, &info, nullptr, work, q, extras->k_new, extras->v_new,
+                               reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(work) + info.work_bytes),
                                const_cast<void*>(k_pool), const_cast<void*>(v_pool),
                                const_cast<int32_t*>(block_table), out, lse, r->workspace, r->workspace_bytes, stream);
   } else if (fp8) {
-    st = sf_decode_attn_fp8(desc, &info, nullptr, dev.ptr, q, k_pool, v_pool, extras->k_scale, extras->v_scale,
+    st = sf_decode_attn_fp8(desc, &info, nullptr, work, q, k_pool, v_pool, extras->k_scale, extras->v_scale,
                             block_table, out, lse, r->workspace, r->workspace_bytes, stream);
   } else {
-    st = sf_decode_attn(desc, &info, nullptr, dev.ptr, q, k_pool, v_pool, block_table, out, lse, r->workspace,
+    st = sf_decode_attn(desc, &info, nullptr, work, q, k_pool, v_pool, block_table, out, lse, r->workspace,
                         r->workspace_bytes, stream);
   }
   if (st == SF_OK && ev1 && hipEventRecord(ev1, main) != hipSuccess) return SF_ERR_HIP;
   if (st == SF_OK && !append && info.num_combine > 0)
-    st = sf_decode_attn_combine(desc, &info, dev.ptr, r->workspace, r->workspace_bytes, out, lse, stream);
+    st = sf_decode_attn_combine(desc, &info, work, r->workspace, r->workspace_bytes, out, lse, stream);
   if (st != SF_OK) return st;
-  if (hipEventRecord(dev.released, main) != hipSuccess) return SF_ERR_HIP;
-  dev.used = true;
+  if (hipEventRecord(pin.released, main) != hipSuccess) return SF_ERR_HIP;
+  pin.used = true;
   ++r->steps;
   return SF_OK;
 }
