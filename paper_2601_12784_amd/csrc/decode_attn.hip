@@ -579,7 +579,7 @@ __device__ __forceinline__ void widen_v(const VHalf8<D>& r, VHalf<D>& b) {
 }
 
 // One segment over an fp8 cache; otherwise as attend_segment.
-template <int D>
+template <int D, int R>
 __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segment& item) {
   constexpr int KB = Shape<D>::KB;
   constexpr int JB = Shape<D>::JB;
@@ -607,20 +607,16 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
   c.pe = pe;
   c.lane_off = (grp * kPage + col) * 16;
 
-  // Codes are half the bytes of bf16, so the raw buffers go three blocks
-  // deep (two blocks of loads in flight behind the one being computed): the
-  // same bytes in flight per wave as the bf16 path keeps.
-  KHalf8<D> kr[3];
-  VHalf8<D> vr[3];
-  if (pb < pe) {
-    const PagePair pp = block_pages8(c, pb);
-    load_k8(c, pp, kr[0]);
-    load_v8(c, pp, vr[0]);
-    if (pb + 2 < pe) {
-      const PagePair pq = block_pages8(c, pb + 2);
-      load_k8(c, pq, kr[1]);
-      load_v8(c, pq, vr[1]);
-    }
+  // Codes are half the bytes of bf16, so the raw buffers go R blocks deep
+  // (R - 1 blocks of loads in flight behind the one being computed).
+  KHalf8<D> kr[R];
+  VHalf8<D> vr[R];
+#pragma unroll
+  for (int j = 0; j < R - 1; ++j) {
+    if (pb + 2 * j >= pe) break;
+    const PagePair pp = block_pages8(c, pb + 2 * j);
+    load_k8(c, pp, kr[j]);
+    load_v8(c, pp, vr[j]);
   }
   u32x4 qf[KB];
   {
@@ -637,12 +633,12 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
   st.m = -__builtin_inff();
   st.lsum = 0.f;
 
-  // Block at pg from (kc, vc); the block two ahead (pg + 4) loads into (kn, vn).
+  // Block at pg from (kc, vc); the block R - 1 ahead loads into (kn, vn).
   auto step = [&](int pg, KHalf8<D>& kc, VHalf8<D>& vc, KHalf8<D>& kn, VHalf8<D>& vn) {
-    const bool more = pg + 4 < pe;
+    const bool more = pg + 2 * (R - 1) < pe;
     PagePair nxt = {0, 0};
     if (more) {
-      nxt = block_pages8(c, pg + 4);
+      nxt = block_pages8(c, pg + 2 * (R - 1));
       load_k8(c, nxt, kn);
     }
     const int nvalid = min(len - pg * kPage, pg + 1 < pe ? 2 * kPage : kPage);
@@ -655,12 +651,12 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
     widen_v(vc, vw);
     accumulate_block(vw, w, nvalid, grp, st);
   };
-  for (int pg = pb; pg < pe; pg += 6) {
-    step(pg, kr[0], vr[0], kr[2], vr[2]);
-    if (pg + 2 >= pe) break;
-    step(pg + 2, kr[1], vr[1], kr[0], vr[0]);
-    if (pg + 4 >= pe) break;
-    step(pg + 4, kr[2], vr[2], kr[1], vr[1]);
+  for (int pg = pb; pg < pe; pg += 2 * R) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (pg + 2 * r >= pe) break;
+      step(pg + 2 * r, kr[r], vr[r], kr[(r + R - 1) % R], vr[(r + R - 1) % R]);
+    }
   }
 
   float lt = st.lsum + __shfl_xor(st.lsum, 16);
@@ -685,7 +681,7 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
 
 template <int D>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_fp8_kernel(AttnArgs a) {
-  for_each_segment(a, [&](const Segment& sg) { attend_segment_fp8<D>(a, sg); });
+  for_each_segment(a, [&](const Segment& sg) { attend_segment_fp8<D, 3>(a, sg); });
 }
 
 // ---------------------------------------------------------------------------

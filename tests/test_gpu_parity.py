@@ -333,3 +333,21 @@ def test_stream_read_probe_runs_and_checks_its_arguments():
     assert L.sf_debug_stream_read(addr, 1024, sk, 0, None) == 1        # no blocks
     assert L.sf_debug_stream_read(addr, 1024, sk, 65537, None) == 1    # too many blocks
     assert L.sf_debug_stream_read(addr, 1024, None, 1, None) == 1      # no sink
+
+
+def test_runner_ring_reuse_with_growing_and_shrinking_plans():
+    """One runner, consecutive steps whose work lists grow and shrink (its
+    pinned ring slots are rewritten, and regrown, only after the step that read
+    them ended): every step against the oracle."""
+    runner = B.DecodeAttention(28, 4, 128)
+    sizes = [3, 40, 7, 120, 1, 64, 200, 5, 90, 2, 150, 30]
+    for i, nseq in enumerate(sizes):
+        rng = np.random.default_rng(900 + i)
+        lens = np.exp(rng.normal(np.log(600), 1.0, size=nseq)).astype(np.int64).clip(0, 6000)
+        lens[rng.random(nseq) < 0.1] = 0
+        b = build_batch(lens, 28, 4, 128, 910 + i)
+        _say(f"ring reuse step {i}: {nseq} sequences, {int(lens.sum())} tokens")
+        o, l, _ = run_gpu(b, runner=runner, chunk_pages=(None if i % 3 else 5))
+        ref = run_oracle(b)
+        assert_close(o, ref[0], f"ring step {i} out")
+        assert_close(l, ref[1], f"ring step {i} lse")
