@@ -329,9 +329,11 @@ __device__ __forceinline__ Segment segment_at(int v, int i) {
   return sg;
 }
 
-// Calls f(segment) for each of this wave's worker's segments, in order.
+// Calls f(segment, next, has_next, index) for each of this wave's worker's
+// segments, in order; next is the following segment when it came in the same
+// load (has_next). Returns the worker's segment count.
 template <class F>
-__device__ __forceinline__ void for_each_segment(const AttnArgs& a, F&& f) {
+__device__ __forceinline__ int for_each_segment(const AttnArgs& a, F&& f) {
   const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
   const int first = wt[0];
   const int count = wt[1];
@@ -340,73 +342,143 @@ __device__ __forceinline__ void for_each_segment(const AttnArgs& a, F&& f) {
     const int n = min(count - b, kRowsPerLoad);
     const int32_t* rows = a.items + size_t(first + b) * kItemInts;
     const int v = lane < n * kItemInts ? rows[lane] : 0;
-    for (int i = 0; i < n; ++i) f(segment_at(v, i));
+    for (int i = 0; i < n; ++i) {
+      const bool has_next = i + 1 < n;
+      f(segment_at(v, i), segment_at(v, has_next ? i + 1 : i), has_next, b + i);
+    }
   }
+  return count;
 }
 
-// One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
+// Address context of a segment. When appending, the segment that ends the
+// sequence leaves the newest token (index len - 1, not yet in the pool) out:
+// its pages hold tokens [0, len_pages), and the merge launch that follows
+// adds the newest one. Its page may be new in this step, so the page comes
+// from new_pages.
 template <int D, bool kAppend>
-__device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment& item) {
-  constexpr int KB = Shape<D>::KB;
-  constexpr int JB = Shape<D>::JB;
+__device__ __forceinline__ ChunkCtx<D> segment_ctx(const AttnArgs& a, const Segment& sg, int& len_pages) {
   const int lane = threadIdx.x;
-  const int col = lane & 15;   // MFMA column (query head in group) and A-operand row
-  const int grp = lane >> 4;   // MFMA k-group
-
-  const int seq = item.seq;
-  const int kvh = item.kvh;
-  const int pb = item.pb;
-  const int pe = item.pe;
-  const int len = item.len;
-  const int slot = item.slot;
-  const int g = a.group;
-  const bool head_ok = col < g;
-  const int head = kvh * g + col;
-
+  const int col = lane & 15;
+  const int grp = lane >> 4;
   ChunkCtx<D> c;
   c.k_pool = a.k_pool;
   c.v_pool = a.v_pool;
-  c.bt = as_constant(a.block_table) + size_t(seq) * a.bt_stride;
+  c.bt = as_constant(a.block_table) + size_t(sg.seq) * a.bt_stride;
   c.num_kv_heads = a.num_kv_heads;
-  c.kvh = kvh;
-  c.pe = pe;
+  c.kvh = sg.kvh;
+  c.pe = sg.pe;
   // K operand: A-row = token slot col, k-group grp = dims 8*grp .. +8 (+32*kb).
   c.k_off = k_elem(col, 8 * grp, D);
   // V operand: A-row = dim col (+16*jb), k-group grp = slots 4*grp .. +3.
   c.v_off = v_elem(4 * grp, col);
   c.last_idx = -1;
   c.fresh = nullptr;
-  // When appending, the segment that ends the sequence leaves the newest
-  // token (index len - 1, not yet in the pool) out: its pages hold tokens
-  // [0, len_pages), and the merge launch that follows adds the newest one.
-  // Its page may be new in this step, so the page comes from new_pages.
-  int len_pages = len;
+  len_pages = sg.len;
   if constexpr (kAppend) {
-    if (len > 0 && pe == (len + kPage - 1) / kPage) {
-      c.last_idx = (len - 1) / kPage;
-      c.fresh = a.new_pages ? as_constant(a.new_pages) + seq : nullptr;
-      len_pages = len - 1;
+    if (sg.len > 0 && sg.pe == (sg.len + kPage - 1) / kPage) {
+      c.last_idx = (sg.len - 1) / kPage;
+      c.fresh = a.new_pages ? as_constant(a.new_pages) + sg.seq : nullptr;
+      len_pages = sg.len - 1;
     }
   }
+  return c;
+}
 
-  KHalf<D> kb_[2];
-  VHalf<D> vb_[2];
-  if (pb < pe) {
-    const PagePair pp = block_pages<D, kAppend>(c, pb);
-    load_k(c, pp, kb_[0]);
-    load_v(c, pp, vb_[0]);
+// Registers a worker's segments share: the two halves that blocks alternate
+// between, and the query operand.
+template <int D>
+struct SegmentRegs {
+  KHalf<D> k[2];
+  VHalf<D> v[2];
+  u32x4 qf[Shape<D>::KB];   // Q as the B operand of S^T = K Q^T: column = head, k = 8 dims per group
+};
+
+// First block (into half 0) and query of a segment.
+template <int D, bool kAppend>
+__device__ __forceinline__ void fetch_segment_start(const AttnArgs& a, const Segment& sg, const ChunkCtx<D>& c,
+                                                    SegmentRegs<D>& r) {
+  const int lane = threadIdx.x;
+  const int col = lane & 15;
+  const int grp = lane >> 4;
+  const int g = a.group;
+  const bool head_ok = col < g;
+  if (sg.pb < sg.pe) {
+    const PagePair pp = block_pages<D, kAppend>(c, sg.pb);
+    load_k(c, pp, r.k[0]);
+    load_v(c, pp, r.v[0]);
   }
-
-  // Q as the B operand of S^T = K Q^T: column = head, k = 8 dims per group.
-  u32x4 qf[KB];
-  {
-    const uint16_t* qrow = a.q + (size_t(seq) * a.num_q_heads + (head_ok ? head : kvh * g)) * D + grp * 8;
+  const uint16_t* qrow =
+      a.q + (size_t(sg.seq) * a.num_q_heads + (head_ok ? sg.kvh * g + col : sg.kvh * g)) * D + grp * 8;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      u32x4 v = load16(qrow + kb * 32);
-      qf[kb] = head_ok ? v : u32x4{0u, 0u, 0u, 0u};
-    }
+  for (int kb = 0; kb < Shape<D>::KB; ++kb) {
+    const u32x4 v = load16(qrow + kb * 32);
+    r.qf[kb] = head_ok ? v : u32x4{0u, 0u, 0u, 0u};
   }
+}
+
+// Stores a segment's result: its normalized output rows o (this lane: head
+// col, dims 16*jb + 4*grp .. +3) and l, the lse (natural log) of a pair
+// finished here or the log2-unit partial lse of a cut pair's segment.
+template <int D>
+__device__ __forceinline__ void write_result(const AttnArgs& a, const Segment& sg, const f32x4* o, float l) {
+  constexpr int JB = Shape<D>::JB;
+  const int lane = threadIdx.x;
+  const int col = lane & 15;
+  const int grp = lane >> 4;
+  const int g = a.group;
+  if (col >= g) return;
+  if (sg.slot < 0) {
+    const int head = sg.kvh * g + col;
+    float* dst = a.out + (size_t(sg.seq) * a.num_q_heads + head) * D + 4 * grp;
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = o[jb];
+    if (a.lse && grp == 0) a.lse[size_t(sg.seq) * a.num_q_heads + head] = l;
+    return;
+  }
+  float* dst = a.part_o + (size_t(sg.slot) * g + col) * D + 4 * grp;
+#pragma unroll
+  for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = o[jb];
+  if (grp == 0) a.part_lse[size_t(sg.slot) * g + col] = l;
+}
+
+// Stores the result a worker kept in LDS (this lane's values at
+// [j * 64 + lane], j < 4 * JB for the output rows, 4 * JB for l).
+template <int D>
+__device__ __forceinline__ void flush_stash(const AttnArgs& a, const Segment& sg, const float* stash) {
+  constexpr int JB = Shape<D>::JB;
+  const int lane = threadIdx.x;
+  f32x4 o[JB];
+#pragma unroll
+  for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[jb][i] = stash[(4 * jb + i) * 64 + lane];
+  write_result<D>(a, sg, o, stash[4 * JB * 64 + lane]);
+}
+
+// One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
+// primed: its first block and query are already in flight (fetched by the
+// previous segment). Once its last block is done, a segment fetches the next
+// one's first block and query (has_next) before it stores its own result:
+// vector memory operations complete in issue order, so loads issued after
+// the stores would wait for the stores' completion too. stash (LDS, or NULL):
+// keep the result there instead of storing it (the worker stores it last).
+template <int D, bool kAppend>
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment& item, const Segment& next,
+                                               bool has_next, SegmentRegs<D>& r, bool& primed, float* stash) {
+  constexpr int JB = Shape<D>::JB;
+  const int lane = threadIdx.x;
+  const int grp = lane >> 4;   // MFMA k-group
+
+  const int pb = item.pb;
+  const int pe = item.pe;
+  const int slot = item.slot;
+
+  int len_pages;
+  const ChunkCtx<D> c = segment_ctx<D, kAppend>(a, item, len_pages);
+  if (!primed) fetch_segment_start<D, kAppend>(a, item, c, r);
+  KHalf<D>* kb_ = r.k;
+  VHalf<D>* vb_ = r.v;
+  const u32x4* qf = r.qf;
 
   SoftmaxState<D> st;
 #pragma unroll
@@ -435,25 +507,29 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment&
     step(pg + 2, kb_[1], vb_[1], kb_[0], vb_[0]);
   }
 
+  primed = has_next && next.pb < next.pe;
+  if (primed) {
+    int unused;
+    fetch_segment_start<D, kAppend>(a, next, segment_ctx<D, kAppend>(a, next, unused), r);
+  }
+
   float lt = st.lsum + __shfl_xor(st.lsum, 16);
   lt += __shfl_xor(lt, 32);
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
   // Lane holds O[head col][16*jb + 4*grp + i], i = 0..3.
-  if (slot < 0) {
-    if (!head_ok) return;
-    float* dst = a.out + (size_t(seq) * a.num_q_heads + head) * D + 4 * grp;
+  f32x4 o[JB];
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
-    if (a.lse && grp == 0)
-      a.lse[size_t(seq) * a.num_q_heads + head] = lt > 0.f ? (st.m + __log2f(lt)) * kLn2 : -__builtin_inff();
+  for (int jb = 0; jb < JB; ++jb) o[jb] = st.o[jb] * inv;
+  const float l = slot < 0 ? (lt > 0.f ? (st.m + __log2f(lt)) * kLn2 : -__builtin_inff()) : st.m + __log2f(lt);
+  if (stash) {
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) stash[(4 * jb + i) * 64 + lane] = o[jb][i];
+    stash[4 * JB * 64 + lane] = l;
     return;
   }
-  if (head_ok) {
-    float* dst = a.part_o + (size_t(slot) * g + col) * D + 4 * grp;
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
-    if (grp == 0) a.part_lse[size_t(slot) * g + col] = st.m + __log2f(lt);
-  }
+  write_result<D>(a, item, o, l);
 }
 
 // One wave per worker: its segments are consecutive in the work list and
@@ -463,7 +539,20 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment&
 // stores nothing: the stores come in the merge launch that follows.
 template <int D, bool kAppend>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_kernel(AttnArgs a) {
-  for_each_segment(a, [&](const Segment& sg) { attend_segment<D, kAppend>(a, sg); });
+  // A worker's first segment is usually the tail of a pair cut by the
+  // previous worker, and short: its result would be written early, into the
+  // middle of the launch's read stream, which costs more than its bytes.
+  // It waits in LDS and is stored after the worker's last segment.
+  __shared__ float stash[(4 * Shape<D>::JB + 1) * 64];
+  SegmentRegs<D> regs;
+  bool primed = false;
+  Segment first = {0, 0, 0, 0, 0, -1};
+  const int count = for_each_segment(a, [&](const Segment& sg, const Segment& nx, bool has_next, int index) {
+    const bool keep = index == 0 && (has_next || int(as_constant(a.worker_table)[2 * size_t(blockIdx.x) + 1]) > 1);
+    if (index == 0) first = sg;
+    attend_segment<D, kAppend>(a, sg, nx, has_next, regs, primed, keep ? stash : nullptr);
+  });
+  if (count > 1) flush_stash<D>(a, first, stash);
 }
 
 // ---------------------------------------------------------------------------
@@ -580,7 +669,7 @@ __device__ __forceinline__ void widen_v(const VHalf8<D>& r, VHalf<D>& b) {
 
 // One segment over an fp8 cache; otherwise as attend_segment.
 template <int D, int R>
-__device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segment& item) {
+__device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segment& item, float* stash) {
   constexpr int KB = Shape<D>::KB;
   constexpr int JB = Shape<D>::JB;
   const int lane = threadIdx.x;
@@ -662,26 +751,32 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
   float lt = st.lsum + __shfl_xor(st.lsum, 16);
   lt += __shfl_xor(lt, 32);
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (slot < 0) {
-    if (!head_ok) return;
-    float* dst = a.out + (size_t(seq) * a.num_q_heads + head) * D + 4 * grp;
+  f32x4 o[JB];
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
-    if (a.lse && grp == 0)
-      a.lse[size_t(seq) * a.num_q_heads + head] = lt > 0.f ? (st.m + __log2f(lt)) * kLn2 : -__builtin_inff();
+  for (int jb = 0; jb < JB; ++jb) o[jb] = st.o[jb] * inv;
+  const float l = slot < 0 ? (lt > 0.f ? (st.m + __log2f(lt)) * kLn2 : -__builtin_inff()) : st.m + __log2f(lt);
+  if (stash) {
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) stash[(4 * jb + i) * 64 + lane] = o[jb][i];
+    stash[4 * JB * 64 + lane] = l;
     return;
   }
-  if (head_ok) {
-    float* dst = a.part_o + (size_t(slot) * g + col) * D + 4 * grp;
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(dst + 16 * jb) = st.o[jb] * inv;
-    if (grp == 0) a.part_lse[size_t(slot) * g + col] = st.m + __log2f(lt);
-  }
+  write_result<D>(a, item, o, l);
 }
 
 template <int D>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_fp8_kernel(AttnArgs a) {
-  for_each_segment(a, [&](const Segment& sg) { attend_segment_fp8<D, 3>(a, sg); });
+  // The worker's first result waits in LDS, as in attn_worker_kernel.
+  __shared__ float stash[(4 * Shape<D>::JB + 1) * 64];
+  Segment first = {0, 0, 0, 0, 0, -1};
+  const int count = for_each_segment(a, [&](const Segment& sg, const Segment& nx, bool has_next, int index) {
+    const bool keep = index == 0 && (has_next || int(as_constant(a.worker_table)[2 * size_t(blockIdx.x) + 1]) > 1);
+    if (index == 0) first = sg;
+    attend_segment_fp8<D, 3>(a, sg, keep ? stash : nullptr);
+  });
+  if (count > 1) flush_stash<D>(a, first, stash);
 }
 
 // ---------------------------------------------------------------------------
