@@ -329,11 +329,16 @@ __device__ __forceinline__ Segment segment_at(int v, int i) {
   return sg;
 }
 
+// Number of segments of this wave's worker.
+__device__ __forceinline__ int worker_segments(const AttnArgs& a) {
+  return as_constant(a.worker_table)[2 * size_t(blockIdx.x) + 1];
+}
+
 // Calls f(segment, next, has_next, index) for each of this wave's worker's
 // segments, in order; next is the following segment when it came in the same
-// load (has_next). Returns the worker's segment count.
+// load (has_next).
 template <class F>
-__device__ __forceinline__ int for_each_segment(const AttnArgs& a, F&& f) {
+__device__ __forceinline__ void for_each_segment(const AttnArgs& a, F&& f) {
   const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
   const int first = wt[0];
   const int count = wt[1];
@@ -347,7 +352,6 @@ __device__ __forceinline__ int for_each_segment(const AttnArgs& a, F&& f) {
       f(segment_at(v, i), segment_at(v, has_next ? i + 1 : i), has_next, b + i);
     }
   }
-  return count;
 }
 
 // Address context of a segment. When appending, the segment that ends the
@@ -547,10 +551,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   SegmentRegs<D> regs;
   bool primed = false;
   Segment first = {0, 0, 0, 0, 0, -1};
-  const int count = for_each_segment(a, [&](const Segment& sg, const Segment& nx, bool has_next, int index) {
-    const bool keep = index == 0 && (has_next || int(as_constant(a.worker_table)[2 * size_t(blockIdx.x) + 1]) > 1);
+  const int count = worker_segments(a);
+  for_each_segment(a, [&](const Segment& sg, const Segment& nx, bool has_next, int index) {
     if (index == 0) first = sg;
-    attend_segment<D, kAppend>(a, sg, nx, has_next, regs, primed, keep ? stash : nullptr);
+    attend_segment<D, kAppend>(a, sg, nx, has_next, regs, primed, index == 0 && count > 1 ? stash : nullptr);
   });
   if (count > 1) flush_stash<D>(a, first, stash);
 }
@@ -771,10 +775,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   // The worker's first result waits in LDS, as in attn_worker_kernel.
   __shared__ float stash[(4 * Shape<D>::JB + 1) * 64];
   Segment first = {0, 0, 0, 0, 0, -1};
-  const int count = for_each_segment(a, [&](const Segment& sg, const Segment& nx, bool has_next, int index) {
-    const bool keep = index == 0 && (has_next || int(as_constant(a.worker_table)[2 * size_t(blockIdx.x) + 1]) > 1);
+  const int count = worker_segments(a);
+  for_each_segment(a, [&](const Segment& sg, const Segment&, bool, int index) {
     if (index == 0) first = sg;
-    attend_segment_fp8<D, 3>(a, sg, keep ? stash : nullptr);
+    attend_segment_fp8<D, 3>(a, sg, index == 0 && count > 1 ? stash : nullptr);
   });
   if (count > 1) flush_stash<D>(a, first, stash);
 }
