@@ -34,6 +34,8 @@ struct AppendArgs {
   const void* k_new;
   const void* v_new;
   const int32_t* new_pages;
+  const int32_t* single_rows;   // optional (see decode_attn_append_rows)
+  int32_t num_single;
 };
 
 // Merge rows of a plan; with `app`, also the newest-token stores.
@@ -66,6 +68,8 @@ CombineArgs combine_args(const sf_attn_desc* desc, const sf_plan_info* info, con
     a.v_dst = static_cast<uint16_t*>(v_pool);
     a.num_kv_heads = desc->num_kv_heads;
     a.bt_stride = desc->block_table_stride;
+    a.single_rows = app->single_rows;
+    a.num_single = app->num_single;
   }
   return a;
 }
@@ -134,6 +138,19 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
 
 }  // namespace
 
+sf_status sf::decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_info* info, int32_t* work_dev,
+                                      const void* q, const void* k_new, const void* v_new,
+                                      const int32_t* new_pages, const int32_t* single_rows, int32_t num_single,
+                                      void* k_pool, void* v_pool, int32_t* block_table, float* out, float* lse,
+                                      void* workspace, uint64_t workspace_bytes, void* stream) {
+  if (num_single < 0 || (info && num_single > info->num_work) || (num_single > 0 && !single_rows) ||
+      (single_rows && !aligned16(single_rows)))
+    return SF_ERR_INVALID_ARG;
+  const AppendArgs app = {q, k_new, v_new, new_pages, single_rows, num_single};
+  return attend(desc, info, nullptr, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
+                workspace_bytes, stream, &app);
+}
+
 extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info* info,
                                     const int32_t* work_host, int32_t* work_dev, const void* q,
                                     const void* k_pool, const void* v_pool,
@@ -149,7 +166,7 @@ extern "C" sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_pl
                                            void* k_pool, void* v_pool, int32_t* block_table, float* out,
                                            float* lse, void* workspace, uint64_t workspace_bytes,
                                            void* stream) {
-  const AppendArgs app = {q, k_new, v_new, new_pages};
+  const AppendArgs app = {q, k_new, v_new, new_pages, nullptr, 0};
   return attend(desc, info, work_host, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
                 workspace_bytes, stream, &app);
 }

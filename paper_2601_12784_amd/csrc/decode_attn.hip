@@ -919,13 +919,15 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) { merge_row
 // attention pass finished. Then the token is stored into its page slot, and
 // a page newly given to it is recorded in the block table (KV head 0).
 // Blocks [0, num_items) take the split pairs' merge rows; the rest take one
-// work item each, acting on the single-segment pairs.
+// work item each (or one of single_rows, when given), acting on the
+// single-segment pairs.
 template <int D>
 __global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
   __shared__ float z_new[kMaxGroup];
   const bool split = int(blockIdx.x) < a.num_items;
+  const const_i32_ptr rest = a.single_rows ? as_constant(a.single_rows) : as_constant(a.work_items);
   const_i32_ptr row = split ? as_constant(a.items) + size_t(blockIdx.x) * kItemInts
-                            : as_constant(a.work_items) + size_t(int(blockIdx.x) - a.num_items) * kItemInts;
+                            : rest + size_t(int(blockIdx.x) - a.num_items) * kItemInts;
   const int seq = row[0];
   const int kvh = row[1];
   const int base = row[2];
@@ -1043,7 +1045,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
   if (a.k_new) {
-    const int blocks = a.num_items + a.num_work;
+    const int blocks = a.num_items + (a.single_rows ? a.num_single : a.num_work);
     if (blocks == 0) return hipSuccess;
     if (a.head_dim == 128)
       hipLaunchKernelGGL(merge_append_kernel<128>, dim3(blocks), dim3(256), 0, stream, a);

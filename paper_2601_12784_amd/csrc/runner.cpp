@@ -153,7 +153,9 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   //    ended); grow it and plan again only if the plan does not fit
   Pinned& pin = r->ring[r->steps % kRing];
   if (pin.used && hipEventSynchronize(pin.released) != hipSuccess) return SF_ERR_HIP;
-  const uint64_t extra = append ? uint64_t(desc->num_seqs) * 4 : 0;
+  // Appending: new_pages (padded to 32 bytes), then copies of the rows the
+  // merge launch acts on (pairs with one segment and len > 0), at most one per item.
+  const uint64_t pages_bytes = append ? (uint64_t(desc->num_seqs) * 4 + 31) / 32 * 32 : 0;
   // An fp8 block moves half the bytes of a bf16 one: unless the caller chose,
   // fp8 steps plan two waves per SIMD (measured: kernel 129 us instead of 136
   // on the long-tail batch; bf16 is slower at 8).
@@ -161,14 +163,24 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   if (fp8 && opts.workers_per_cu == 0) opts.workers_per_cu = kFp8WorkersPerCu;
   sf_plan_info info;
   sf_status st = sf_decode_attn_plan(desc, seq_lens_host, &opts, pin.ptr, pin.bytes, &info);
-  if (st == SF_ERR_CAPACITY || (st == SF_OK && pin.bytes < info.work_bytes + extra)) {
-    if ((st = grow_pinned(pin, info.work_bytes + extra)) != SF_OK) return st;
+  auto need = [&]() { return info.work_bytes + (append ? pages_bytes + uint64_t(info.num_work) * 32 : 0); };
+  if (st == SF_ERR_CAPACITY || (st == SF_OK && pin.bytes < need())) {
+    if ((st = grow_pinned(pin, need())) != SF_OK) return st;
     st = sf_decode_attn_plan(desc, seq_lens_host, &opts, pin.ptr, pin.bytes, &info);
   }
   if (st != SF_OK) return st;
+  int32_t num_single = 0;
   if (append && desc->num_seqs > 0) {
     if (!extras->new_pages_host) return SF_ERR_INVALID_ARG;
-    std::memcpy(reinterpret_cast<char*>(pin.ptr) + info.work_bytes, extras->new_pages_host, extra);
+    char* base = reinterpret_cast<char*>(pin.ptr);
+    std::memcpy(base + info.work_bytes, extras->new_pages_host, uint64_t(desc->num_seqs) * 4);
+    const int32_t* items = pin.ptr + sf::table_rows(info.num_workers) * sf::kItemInts;
+    int32_t* singles = reinterpret_cast<int32_t*>(base + info.work_bytes + pages_bytes);
+    for (int32_t i = 0; i < info.num_work; ++i) {
+      const int32_t* row = items + int64_t(i) * sf::kItemInts;
+      if (row[7] == 1 && row[4] > 0)
+        std::memcpy(singles + int64_t(num_single++) * sf::kItemInts, row, sf::kItemInts * 4);
+    }
   }
   if (info_out) *info_out = info;
   r->last = info;
@@ -183,10 +195,13 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   hipEvent_t ev1 = extras ? static_cast<hipEvent_t>(extras->attn_end) : nullptr;
   if (ev0 && hipEventRecord(ev0, main) != hipSuccess) return SF_ERR_HIP;
   if (append) {
-    st = sf_decode_attn_append(desc, &info, nullptr, work, q, extras->k_new, extras->v_new,
-                               reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(work) + info.work_bytes),
-                               const_cast<void*>(k_pool), const_cast<void*>(v_pool),
-                               const_cast<int32_t*>(block_table), out, lse, r->workspace, r->workspace_bytes, stream);
+    const char* wbase = reinterpret_cast<const char*>(work);
+    st = sf::decode_attn_append_rows(desc, &info, work, q, extras->k_new, extras->v_new,
+                                     reinterpret_cast<const int32_t*>(wbase + info.work_bytes),
+                                     reinterpret_cast<const int32_t*>(wbase + info.work_bytes + pages_bytes),
+                                     num_single, const_cast<void*>(k_pool), const_cast<void*>(v_pool),
+                                     const_cast<int32_t*>(block_table), out, lse, r->workspace,
+                                     r->workspace_bytes, stream);
   } else if (fp8) {
     st = sf_decode_attn_fp8(desc, &info, nullptr, work, q, k_pool, v_pool, extras->k_scale, extras->v_scale,
                             block_table, out, lse, r->workspace, r->workspace_bytes, stream);

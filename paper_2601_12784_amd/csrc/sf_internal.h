@@ -85,6 +85,10 @@ struct CombineArgs {
   uint16_t* v_dst;
   int32_t num_kv_heads;
   int32_t bt_stride;
+  // Optional: copies of just the segment rows of pairs with one segment and
+  // len > 0 (the rows the merge launch acts on); NULL: walk all work_items.
+  const int32_t* single_rows;
+  int32_t num_single;
 };
 
 struct QuantArgs {
@@ -143,6 +147,15 @@ struct ExtendArgs {
 constexpr int kExtendRows = 256;
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+
+// sf_decode_attn_append with the merge launch restricted to single_rows
+// (num_single copies, in work-item format, of the rows of pairs that have one
+// segment and len > 0; device-accessible). The native runner's path.
+sf_status decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_info* info, int32_t* work_dev,
+                                  const void* q, const void* k_new, const void* v_new, const int32_t* new_pages,
+                                  const int32_t* single_rows, int32_t num_single, void* k_pool, void* v_pool,
+                                  int32_t* block_table, float* out, float* lse, void* workspace,
+                                  uint64_t workspace_bytes, void* stream);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
