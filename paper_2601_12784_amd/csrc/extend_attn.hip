@@ -52,8 +52,7 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRowTiles = 2;      // 16-row MFMA tiles per wave
 constexpr int kStepKeys = 2 * kPage;   // keys per step (two pages)
 constexpr int kSub = 2;                // steps per barrier interval
-constexpr float kRescaleLog2 = 8.f;  // headroom of the lazily moved softmax reference
-constexpr float kRescaleMax = 256.f; // 2^kRescaleLog2
+constexpr float kRescaleMax = 256.f; // headroom of the lazily moved softmax reference, 2^8
 static_assert(kWaves * kRowTiles * 16 == kExtendRows, "rows per item");
 
 __device__ __forceinline__ const_i32_ptr as_constant(const int32_t* p) { return (const_i32_ptr)(p); }
@@ -93,22 +92,33 @@ struct Tiles {
   static_assert(kWaveChunks * 64 * kWaves == 4 * kChunks, "staging split");
 };
 
+// Sum of a lane's eight weights of a step.
+__device__ __forceinline__ float weight_sum(const float* p) {
+  return ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+}
+
 // Online-softmax update of one 16-row tile for one step of 32 keys, in two
 // parts so that each can be interleaved with matrix-core work.
 //
 // Lazy reference: each row keeps a reference max m (log2 units) and the
-// weights are p = 2^(z - m). m moves only when some weight of the wave would
-// exceed 2^kRescaleLog2; until then the lanes of a row need not agree on the
-// row's max at all, so the common step has no cross-lane reduction. Weights
-// below 2^kRescaleLog2 are exact in fp32 and keep bf16's relative precision,
-// and O and l share the reference, so O / l does not change. When m moves,
-// the row's max over all four lane groups is formed and O and l are
-// rescaled. Key 0 is in every row's first step, so m is finite after it.
+// weights are p = 2^(z - m). m moves only when, in some lane of the wave, the
+// sum of the lane's eight weights of the step exceeds kRescaleMax. That
+// sum is needed for the row sum anyway, and it bounds each of its weights,
+// so the check costs one compare. Until it fires the lanes of a row need not
+// agree on the row's max at all, so the common step has no cross-lane
+// reduction. Weights below kRescaleMax are exact in fp32 and keep bf16's
+// relative precision, and O and l share the reference, so O / l does not
+// change. When the check fires, each row of the tile whose max has risen
+// moves m to it (the max over all four lane groups) and O and l are
+// rescaled; every weight is then at most 1, so the check stays quiet until a
+// row's scores rise by 2^5 over its reference. Key 0 is in every row's first
+// step, so m is finite after it.
 struct TileWeights {
   float sc[8];   // raw scores of this lane (masked ones -inf)
   float p[8];    // 2^(sc * c - m)
   bool ok[8];    // key inside the row's causal limit (masked steps)
-  bool need;     // some weight exceeds the headroom (or is inf / NaN)
+  float part;    // sum of the eight weights
+  bool need;     // the sum exceeds the headroom (or is inf / NaN)
 };
 
 // Part 1: exponentiate against the current reference. s0 / s1: this lane's
@@ -131,15 +141,14 @@ __device__ __forceinline__ TileWeights exponentiate(const f32x4& s0, const f32x4
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) t.p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(t.sc[e], c, -m));
-  const float pm = fmaxf(fmaxf(fmaxf(t.p[0], t.p[1]), fmaxf(t.p[2], t.p[3])),
-                         fmaxf(fmaxf(t.p[4], t.p[5]), fmaxf(t.p[6], t.p[7])));
+  t.part = weight_sum(t.p);
   // Also true for inf (the first step, m = -inf) and NaN (-inf * 0 for a
   // zero scale), which settle() sorts out.
-  t.need = !(pm <= kRescaleMax);
+  t.need = !(t.part <= kRescaleMax);
   return t;
 }
 
-// Part 2: move the reference if needed (rare), then sum and pack the
+// Part 2: move the reference if needed (rare), then add the sum and pack the
 // weights as the P^T operand.
 template <int D, bool kMasked>
 __device__ __forceinline__ u32x4 settle(TileWeights& t, float c, float& m, float& lsum, f32x4* o) {
@@ -151,7 +160,7 @@ __device__ __forceinline__ u32x4 settle(TileWeights& t, float c, float& m, float
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float mx_s = mx * c;
-    const bool grow = mx_s > m + kRescaleLog2;   // NaN (fully masked, zero scale) compares false
+    const bool grow = mx_s > m;   // NaN (fully masked, zero scale) compares false
     const float mnew = grow ? mx_s : m;
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
@@ -160,12 +169,14 @@ __device__ __forceinline__ u32x4 settle(TileWeights& t, float c, float& m, float
     for (int jb = 0; jb < D / 16; ++jb) o[jb] *= alpha;
 #pragma unroll
     for (int e = 0; e < 8; ++e) t.p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(t.sc[e], c, -m));
+    t.part = weight_sum(t.p);
   }
   if constexpr (kMasked) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) t.p[e] = t.ok[e] ? t.p[e] : 0.f;
+    t.part = weight_sum(t.p);
   }
-  lsum += ((t.p[0] + t.p[1]) + (t.p[2] + t.p[3])) + ((t.p[4] + t.p[5]) + (t.p[6] + t.p[7]));
+  lsum += t.part;
   return u32x4{pack_bf16(t.p[0], t.p[1]), pack_bf16(t.p[2], t.p[3]), pack_bf16(t.p[4], t.p[5]),
                pack_bf16(t.p[6], t.p[7])};
 }
