@@ -74,7 +74,8 @@ typedef struct sf_attn_desc {
   int32_t page_size;           /* tokens per page: 16 */
   int32_t block_table_stride;  /* int32 entries per block-table row, >= max_s ceil(L_s/16) */
   int32_t num_pages;           /* pages in each pool (0: all lengths must be 0) */
-  float softmax_scale;         /* multiplies q.k; must be finite */
+  float softmax_scale;         /* multiplies q.k; |scale| * log2(e) must be a finite float
+                                  (|scale| <= 2.35e38) */
 } sf_attn_desc;
 
 /* Planner knobs; a zero field takes its default. */

@@ -10,6 +10,8 @@
 // whatever the skew. The exact rule is stated in sf_decode_attn.h next to
 // sf_decode_attn_plan.
 #include <algorithm>
+#include <cfloat>
+#include <cmath>
 #include <cstring>
 #include <vector>
 
@@ -30,8 +32,9 @@ sf_status validate_desc(const sf_attn_desc* d) {
   if (d->num_seqs < 0 || d->num_q_heads < 1 || d->num_kv_heads < 1) return SF_ERR_INVALID_ARG;
   if (d->num_q_heads % d->num_kv_heads != 0) return SF_ERR_INVALID_ARG;
   if (d->block_table_stride < 1 || d->num_pages < 0) return SF_ERR_INVALID_ARG;
-  if (!(d->softmax_scale == d->softmax_scale) ||
-      d->softmax_scale > 3.0e38f || d->softmax_scale < -3.0e38f) return SF_ERR_INVALID_ARG;
+  // The kernels scale scores by |softmax_scale| * log2(e) in float, which must
+  // be finite (false for NaN as well).
+  if (!(std::fabs(double(d->softmax_scale)) * 1.4426950408889634074 <= double(FLT_MAX))) return SF_ERR_INVALID_ARG;
   if (d->head_dim != 64 && d->head_dim != 128) return SF_ERR_UNSUPPORTED;
   if (d->page_size != kPage) return SF_ERR_UNSUPPORTED;
   if (d->num_q_heads / d->num_kv_heads > kMaxGroup) return SF_ERR_UNSUPPORTED;

@@ -196,7 +196,8 @@ def test_plan_size_query_and_capacity(lib):
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 96, 2), ("page_size", 32, 2), ("num_q_heads", 34, 2),
     ("num_q_heads", 31, 1), ("num_seqs", -1, 1), ("block_table_stride", 0, 1),
-    ("softmax_scale", float("nan"), 1),
+    ("softmax_scale", float("nan"), 1), ("softmax_scale", float("inf"), 1),
+    ("softmax_scale", -2.4e38, 1),  # finite, but scale * log2(e) is not
 ])
 def test_plan_rejects_bad_descriptor(lib, field, value, status):
     desc = B.make_desc(2, 8, 2, 128, 10, 4, 0.1)
