@@ -487,7 +487,10 @@ def summarize_trace(stats_csv, command, out_md, bench_json=None):
     rows = _csv_rows(stats_csv)
     b = json.load(open(bench_json)) if bench_json else None
     reprefill = b is not None and "causal_flops" in b
+    fp8 = (not reprefill and b is not None and "fp8" in b
+           and any("attn_worker_fp8_kernel" in r["Name"] for r in rows))
     title = (f"# Kernel trace: {EXTEND_KERNEL} on the full re-prefill batch" if reprefill
+             else "# Kernel trace: the decode step on the long-tail batch, bf16 and fp8 caches" if fp8
              else f"# Kernel trace: {ATTN_KERNEL} on the long-tail batch")
     src = EXTEND_SRC if reprefill else KERNEL_SRC
     lines = [title, "", "Command (from the repository root):", "", "```", command, "```", "",
@@ -507,6 +510,11 @@ def summarize_trace(stats_csv, command, out_md, bench_json=None):
                   f"- attention kernel mean: {b['attn_kernel_us']} us",
                   f"- step: {b['ms_per_step'] * 1e3:.1f} us; value {b['value']} GB/s",
                   f"- roofline achieved: {b['roofline']['achieved']} GB/s ({100 * b['roofline']['frac']:.1f}% of 8000)"]
+        if fp8:
+            f8 = b["fp8"]
+            lines += [f"- fp8 cache: attention kernel mean {f8['attn_kernel_us']} us, step {f8['ms_per_step'] * 1e3:.1f} us, "
+                      f"{f8['roofline']['achieved']} GB/s of codes ({100 * f8['roofline']['frac']:.1f}% of 8000), "
+                      f"{f8['read_ceiling']['attn_kernel_over_ceiling']} of a plain read of the same bytes"]
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
 
