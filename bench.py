@@ -456,13 +456,14 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
         json.dump(doc, f, indent=1)
     md = out_path[:-len(".json")] + ".md"
     cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
-           "-d $REPO/gpurun_out/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
+           "-d $OUT/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
            "--no-skew --no-loop --no-cost --no-reprefill --no-fp8 --copy-probe " + str(int(copy_mib)))
     lines = [f"# HBM traffic of {ATTN_KERNEL} on the long-tail batch (rocprofv3 counters)", "",
              "Two counter passes (one counter each), then the summary:", "", "```",
              cmd.format(c="FETCH_SIZE", d="pmc_fetch", o="f"), cmd.format(c="WRITE_SIZE", d="pmc_write", o="w"),
-             "python bench.py --summarize-counters gpurun_out/pmc_fetch/f_counter_collection.csv "
-             f"gpurun_out/pmc_write/w_counter_collection.csv --copy-probe {int(copy_mib)}", "```", "",
+             "python bench.py --summarize-counters $OUT/pmc_fetch/f_counter_collection.csv "
+             f"$OUT/pmc_write/w_counter_collection.csv --copy-probe {int(copy_mib)}", "```", "",
+             "($REPO: the repository root; $OUT: any directory for the profiler's output.)", "",
              f"Kernel source sha256[:16]: `{doc['kernel_source_sha256_16']}`", "",
              "Calibration: a plain device copy (`__amd_rocclr_copyBuffer`) of "
              f"{int(copy_mib)} MiB reads FETCH_SIZE = {doc['raw_counter_bytes_per_launch']['copy_FETCH_SIZE']} B "
