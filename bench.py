@@ -553,7 +553,7 @@ def main():
         summarize_trace(*args.summarize_trace, bench_json=args.bench_json)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU; --gpus must be 1"}))
+        print(json.dumps({"error": "bench.py measures a single GPU (the decode path runs on one device); --gpus must be 1"}))
         log("bench.py runs on exactly one GPU: the decode-attention path here is single-GPU "
             "(sharding is described, not built). Use --gpus 1.")
         sys.exit(2)
