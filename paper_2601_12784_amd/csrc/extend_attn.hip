@@ -52,7 +52,7 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRowTiles = 2;      // 16-row MFMA tiles per wave
 constexpr int kStepKeys = 2 * kPage;   // keys per step (two pages)
 constexpr int kSub = 2;                // steps per barrier interval
-constexpr float kRescaleMax = 256.f; // headroom of the lazily moved softmax reference, 2^8
+constexpr float kRescaleMax = 65536.f; // headroom of the lazily moved softmax reference, 2^16
 static_assert(kWaves * kRowTiles * 16 == kExtendRows, "rows per item");
 
 __device__ __forceinline__ const_i32_ptr as_constant(const int32_t* p) { return (const_i32_ptr)(p); }
@@ -111,8 +111,8 @@ __device__ __forceinline__ float weight_sum(const float* p) {
 // change. When the check fires, each row of the tile whose max has risen
 // moves m to it (the max over all four lane groups) and O and l are
 // rescaled; every weight is then at most 1, so the check stays quiet until a
-// row's scores rise by 2^5 over its reference. Key 0 is in every row's first
-// step, so m is finite after it.
+// row's scores rise more than 13 (log2 units) above its reference. Key 0 is
+// in every row's first step, so m is finite after it.
 struct TileWeights {
   float sc[8];   // raw scores of this lane (masked ones -inf)
   float p[8];    // 2^(sc * c - m)

@@ -148,13 +148,13 @@ def test_extend_peaked_scores():
 
 
 def test_extend_rising_scores_move_the_reference():
-    """Scores that climb along the keys (about 30 log2 units over 1200 keys)
-    make each row move its softmax reference many times during its walk, and
+    """Scores that climb along the keys (about 90 log2 units over 1200 keys)
+    make each row move its softmax reference several times during its walk, and
     make the last keys of a row its heaviest."""
     eb = build_extend([1200, 333], [1200, 333], 28, 4, 128, seed=17)
     pages, slots = eb.slots()
     pos = np.concatenate([np.arange(1200), np.arange(333)])
-    ramp = torch.from_numpy(pos * 0.05).float().to(torch.bfloat16).view(torch.int16).numpy()
+    ramp = torch.from_numpy(pos * 0.15).float().to(torch.bfloat16).view(torch.int16).numpy()
     kp = eb.batch.k_pool.view(torch.int16).numpy()   # [page, KV head, D/8, slot, 8], shares memory
     for h in range(kp.shape[1]):
         kp[pages, h, 0, slots, 0] = ramp
