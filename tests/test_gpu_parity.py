@@ -285,6 +285,25 @@ def test_sharp_softmax_scaled_keys():
     check_batch(b)
 
 
+
+@pytest.mark.parametrize("chunk", [None, 3])
+def test_rising_scores_across_split_pairs(chunk):
+    """Scores that climb along the keys (about 130 log2 units over 3000 keys):
+    a pair cut into many segments then has partials whose maxima lie far
+    apart, so the combine weights its early partials by factors that
+    underflow to zero, and the last keys carry the row."""
+    lens = np.array([3000, 1000, 17, 1], np.int32)
+    b = build_batch(lens, 8, 2, 128, 43)
+    kp = b.k_pool.view(torch.int16).numpy()   # [page, KV head, D/8, slot, 8], shares memory
+    for s, L in enumerate(lens):
+        pos = np.arange(int(L))
+        ramp = torch.from_numpy(pos * 0.15).float().to(torch.bfloat16).view(torch.int16).numpy()
+        for h in range(b.num_kv_heads):
+            kp[b.block_table[s, pos // 16], h, 0, pos % 16, 0] = ramp
+    b.q[:, :, 0] = 4.0
+    _say(f"rising scores chunk={chunk}")
+    check_batch(b, chunk_pages=chunk)
+
 # ---------------------------------------------------------------------------
 # the named workloads at full size
 # ---------------------------------------------------------------------------
