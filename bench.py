@@ -40,9 +40,11 @@ def kernel_source_hash(path=None) -> str:
 class Stepper:
     """Runs plan -> upload -> attention (+ merge) for a fixed batch on one stream."""
 
-    def __init__(self, batch, chunk_pages=0, workers_per_cu=0, fp8=None):
+    def __init__(self, batch, chunk_pages=0, workers_per_cu=0, fp8=None, rotate=1):
         """fp8 = (k8, v8, k_scale, v_scale) device tensors: step over that fp8
-        cache instead of the batch's bf16 pools."""
+        cache instead of the batch's bf16 pools. rotate > 1 keeps that many
+        device copies of the pools and moves to the next copy every step, so a
+        batch smaller than the 256 MB last-level cache is still read from HBM."""
         import torch
         from paper_2601_12784_amd import binding as B
         self.torch = torch
@@ -50,6 +52,8 @@ class Stepper:
         self.fp8 = None if fp8 is None else (fp8[2], fp8[3])
         k, v = (batch.k_pool.cuda(), batch.v_pool.cuda()) if fp8 is None else (fp8[0], fp8[1])
         self.dev = dict(q=batch.q.cuda(), k=k, v=v, bt=torch.from_numpy(batch.block_table).cuda())
+        self.pools = [(k, v)] + [(k.clone(), v.clone()) for _ in range(rotate - 1)]
+        self.turn = 0
         self.lens = np.ascontiguousarray(batch.seq_lens, dtype=np.int32)
         self.chunk = chunk_pages or None
         cus = torch.cuda.get_device_properties(0).multi_processor_count
@@ -65,7 +69,9 @@ class Stepper:
     def step(self, ev_attn=None):
         """One decode step; ev_attn = (start, end) events bracketing the attention kernel."""
         d = self.dev
-        self.runner(d["q"], d["k"], d["v"], d["bt"], self.lens, self.batch.scale, out=self.out, lse=self.lse,
+        k, v = self.pools[self.turn]
+        self.turn = (self.turn + 1) % len(self.pools)
+        self.runner(d["q"], k, v, d["bt"], self.lens, self.batch.scale, out=self.out, lse=self.lse,
                     chunk_pages=self.chunk, stream=self.stream, attn_events=ev_attn, fp8=self.fp8)
 
 
@@ -141,6 +147,94 @@ def decode_loop_bench(reps=5):
             "seq_steps_per_s": round(seq_steps / wall, 1),
             "kv_gb_per_s": round(kv_read / wall / 1e9, 2), "kv_bytes_read": int(kv_read),
             "host_issue_ms": round(float(np.median(issue)) * 1e3, 3), "timed_loops": reps}
+
+
+LLC_BYTES = 256 << 20   # MI355X last-level (Infinity) cache
+
+
+def config_bench(name, steps, warmup):
+    """One decode step of a named workload (tiny, gqa7b, gqa32b), timed as the
+    long-tail step is: plan -> attention -> combine back to back on one
+    stream, wall time per step, attention kernel from HIP events. Batches
+    whose pools would fit in the last-level cache rotate over enough device
+    copies (at least 4) that every step reads its bytes from HBM."""
+    import torch
+    from paper_2601_12784_amd.workloads import make_batch, CONFIGS
+    b = make_batch(name, poison=False)
+    kv = b.kv_bytes()
+    pool_bytes = b.k_pool.numel() * 4
+    rotate = 1 if pool_bytes > 2 * LLC_BYTES else max(4, -(-4 * LLC_BYTES // pool_bytes))
+    if name == "tiny":
+        rotate = 1   # 130 KB: a latency figure, cache-resident by nature
+    st = Stepper(b, rotate=rotate)
+    ms_step, k_mean, k_med = time_steps(st, steps, warmup)
+    info = st.info0
+    gbs = kv / (k_mean * 1e-3) / 1e9
+    _, bsz, hq, hkv, d = CONFIGS[name]
+    res = {"workload": f"{name}: {bsz} sequences, {hq} q / {hkv} kv heads, head_dim {d}, page 16",
+           "tokens": int(b.seq_lens.sum()), "kv_bytes_per_step": kv, "pool_copies_rotated": rotate,
+           "ms_per_step": round(ms_step, 5), "attn_kernel_us": round(k_mean * 1e3, 2),
+           "attn_kernel_us_median": round(k_med * 1e3, 2),
+           "kv_gb_per_s_step": round(kv / (ms_step * 1e-3) / 1e9, 2),
+           "kv_gb_per_s_kernel": round(gbs, 2), "pct_of_peak_hbm_kernel": round(100 * gbs / PEAK_HBM_GBPS, 2),
+           "seq_steps_per_s": round(b.num_seqs / (ms_step * 1e-3), 1),
+           "workers": info.num_workers, "segments": info.num_work, "cut_pairs": info.num_combine}
+    del st
+    torch.cuda.empty_cache()
+    return res
+
+
+def straggler_bench(reps=5):
+    """The extreme-straggler schedule over its pre-filled pool: 64 decode
+    steps, the batch shrinking as sequences reach their caps. Every step's
+    queries and compacted block table are uploaded before timing; the timed
+    loop is the runner's plan, attention and combine per step, host planning
+    included. Returns seq-steps/s over whole loops (median of `reps` after one
+    untimed loop) and the attention kernels' summed time from one loop timed
+    with HIP events."""
+    import torch
+    from paper_2601_12784_amd import binding as B
+    from paper_2601_12784_amd.workloads import make_straggler
+    run = make_straggler(poison=False)
+    b = run.base
+    k, v = b.k_pool.cuda(), b.v_pool.cuda()
+    steps = [run.step_batch(t) for t in range(run.steps)]
+    dev = [(s.q.cuda(), torch.from_numpy(s.block_table).cuda(), np.ascontiguousarray(s.seq_lens, np.int32))
+           for s in steps]
+    kv_read = sum(s.kv_bytes() for s in steps)
+    seq_steps = run.seq_steps()
+    out = torch.empty((b.num_seqs, b.num_q_heads, b.head_dim), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.Stream()
+    attn = B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim)
+
+    def loop(events=None):
+        for t, (q, bt, lens) in enumerate(dev):
+            attn(q, k, v, bt, lens, b.scale, out=out[: q.shape[0]], stream=stream,
+                 attn_events=None if events is None else events[t])
+
+    times = []
+    for rep in range(reps + 1):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        loop()
+        torch.cuda.synchronize()
+        if rep:
+            times.append(time.perf_counter() - t0)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in dev]
+    loop(evs)
+    torch.cuda.synchronize()
+    kernel_ms = float(sum(a.elapsed_time(z) for a, z in evs))
+    wall = float(np.median(times))
+    return {"workload": f"extreme straggler, pre-filled pool: {b.num_seqs} sequences at step 0 (502 x U[1,2048] "
+                        f"+ 10 x 32768 tokens), caps +U[0,64], {run.steps} steps, finished sequences dropped, "
+                        "28 q / 4 kv heads, head_dim 128",
+            "seq_steps": seq_steps, "loop_ms": round(wall * 1e3, 3),
+            "seq_steps_per_s": round(seq_steps / wall, 1),
+            "kv_bytes_read": int(kv_read), "kv_gb_per_s": round(kv_read / wall / 1e9, 2),
+            "pct_of_peak_hbm": round(100 * kv_read / wall / 1e9 / PEAK_HBM_GBPS, 2),
+            "attn_kernels_ms_sum": round(kernel_ms, 3),
+            "kv_gb_per_s_kernels": round(kv_read / (kernel_ms * 1e-3) / 1e9, 2),
+            "active_at_steps_0_32_63": [int(steps[t].num_seqs) for t in (0, 32, 63)], "timed_loops": reps}
 
 
 # KV bytes per token of one decode step over all layers of the paper's
@@ -357,14 +451,16 @@ def read_ceiling(nbytes, grids=(2048, 4096, 8192), reps=15, warmup=3):
 def cpu_baseline(batch, min_s=10.0, max_s=30.0):
     """The fp64 oracle, timed on the host cores over repeated passes of the
     batch (or of a prefix of it, if one pass would exceed max_s)."""
+    import tempfile
     import oracle
     from paper_2601_12784_amd.workloads import bf16_bits
     qb, kb, vb = bf16_bits(batch.q), bf16_bits(batch.k_pool), bf16_bits(batch.v_pool)
-    threads = oracle.max_threads()
+    native = oracle.load(oracle.build_native(tempfile.mkdtemp(prefix="sf_oracle_")))
+    threads = int(native.sf_oracle_max_threads())
 
     def run(n):
         t = time.perf_counter()
-        oracle.decode_attn(qb[:n], kb, vb, batch.block_table[:n], batch.seq_lens[:n], batch.scale)
+        oracle.decode_attn(qb[:n], kb, vb, batch.block_table[:n], batch.seq_lens[:n], batch.scale, using=native)
         return time.perf_counter() - t
 
     cum = np.cumsum(batch.seq_lens.astype(np.int64))
@@ -380,7 +476,8 @@ def cpu_baseline(batch, min_s=10.0, max_s=30.0):
     return {"value": round(kv / total / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{passes} passes over the first {n} of {batch.num_seqs} sequences "
                       f"({int(cum[n - 1])} tokens, {kv / passes / 1e9:.3f} GB KV per pass), "
-                      f"fp64 C oracle with {threads} OpenMP threads, {total:.1f} s"}
+                      f"fp64 C oracle (gcc {' '.join(oracle.NATIVE_FLAGS[:3])}, built on this host) with "
+                      f"{threads} OpenMP threads, {total:.1f} s"}
 
 
 def stored_traffic(kv_bytes_per_launch):
@@ -534,6 +631,8 @@ def main():
     ap.add_argument("--no-cost", action="store_true", help="skip the cost-model k1 fit")
     ap.add_argument("--no-reprefill", action="store_true", help="skip the extend (re-prefill) leg")
     ap.add_argument("--no-fp8", action="store_true", help="skip the fp8-cache leg")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the tiny, 7B-like, 32B-like and pre-filled straggler legs")
     ap.add_argument("--only-reprefill", action="store_true", help="run only the extend leg and print it")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
@@ -664,6 +763,20 @@ def main():
         log(f"  step {f8['ms_per_step'] * 1e3:.1f} us, kernel {f8['attn_kernel_us']} us "
             f"({f8['roofline']['achieved']} GB/s of fp8 codes, {f8['kernel_speedup_vs_bf16']}x the bf16 kernel; "
             f"{f8['read_ceiling']['attn_kernel_over_ceiling']:.3f} of a plain read of the same bytes)")
+
+    if not args.no_configs:
+        legs = {}
+        for name in ("tiny", "gqa7b", "gqa32b"):
+            log(f"config {name}")
+            legs[name] = config_bench(name, args.steps, min(args.warmup, 500))
+            log(f"  step {legs[name]['ms_per_step'] * 1e3:.1f} us, kernel {legs[name]['attn_kernel_us']} us, "
+                f"{legs[name]['kv_gb_per_s_kernel']} GB/s ({legs[name]['pct_of_peak_hbm_kernel']} % of peak), "
+                f"{legs[name]['seq_steps_per_s']} seq-steps/s")
+        log("config straggler (pre-filled, 64 steps)")
+        legs["straggler"] = straggler_bench()
+        log(f"  {legs['straggler']['loop_ms']} ms per loop, {legs['straggler']['seq_steps_per_s']} seq-steps/s, "
+            f"{legs['straggler']['kv_gb_per_s']} GB/s")
+        result["configs"] = legs
 
     if not args.no_reprefill:
         log("extend attention: full re-prefill of 32 trajectories")

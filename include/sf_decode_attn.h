@@ -305,7 +305,7 @@ sf_status sf_kv_quantize_fp8(const sf_attn_desc* desc, const void* k_pool, const
  * entries 0 .. ceil(L_s / 16) - 1 of every sequence with E_s > 0 are read.
  */
 typedef struct sf_extend_info {
-  int32_t num_items;        /* work items (thread blocks of 256) */
+  int32_t num_items;        /* work items (one 512-thread block each, up to 256 rows) */
   int32_t tokens_per_item;  /* new tokens per item: floor(256 / g) */
   int32_t num_q_rows;       /* T */
   int32_t reserved;         /* 0 */
@@ -340,7 +340,14 @@ sf_status sf_extend_attn_plan(const sf_attn_desc* desc, const int32_t* seq_lens_
  * for position p = P_s + j, before the attention reads them; the pools are
  * then written, and the block table must already hold every page the new
  * tokens land in. With both NULL the pool must already hold them. One
- * launch of the attention kernel follows (one 256-thread block per item).
+ * launch of the attention kernel follows (one 512-thread block per item).
+ * Numerics: scores from bf16 q and K with fp32 accumulation; the softmax
+ * weights and the values enter the P.V product as fp16, with fp32
+ * accumulation. Every bf16 V element of magnitude in [2^-17, 65280] is exact
+ * in fp16 and smaller ones round by at most 2^-25; a V element of magnitude
+ * 65536 or more at a position a row attends to makes that row's out
+ * non-finite. Within that range out and lse meet
+ * |err| <= 2e-3 + 1e-2 |exact| (the decode step's bound).
  * Errors as sf_decode_attn; SF_ERR_INVALID_ARG also if only one of k_new and
  * v_new is given, or either is not 16-byte aligned.
  */

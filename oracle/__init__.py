@@ -27,16 +27,45 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "sf_oracle.c")
 _LIB = os.path.join(_HERE, "libsf_oracle.so")
 _lib = None
+BASE_FLAGS = ["-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared"]
+# The CPU-baseline timing build: tuned for the host it runs on, so it is
+# built on that host (bench.py does it at run time) and never shipped.
+# -ffp-contract=off keeps a * b + c as two roundings, as in the test build.
+NATIVE_FLAGS = ["-O3", "-march=native", "-ffp-contract=off", "-std=c11", "-fopenmp", "-fPIC", "-shared"]
 
 
 def build(force: bool = True) -> str:
     """Compile sf_oracle.c with the host C compiler (plain -O2, OpenMP)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
-        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+        cmd = ["gcc", *BASE_FLAGS, _SRC, "-o", tmp, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, _LIB)
     return _LIB
+
+
+def build_native(out_dir: str) -> str:
+    """Compile sf_oracle.c with NATIVE_FLAGS into out_dir (for timing on this
+    host only); returns the library path."""
+    os.makedirs(out_dir, exist_ok=True)
+    path = os.path.join(out_dir, "libsf_oracle_native.so")
+    subprocess.run(["gcc", *NATIVE_FLAGS, _SRC, "-o", path, "-lm"], check=True)
+    return path
+
+
+def _declare(L):
+    p = ctypes.c_void_p
+    i = ctypes.c_int
+    L.sf_oracle_decode_attn.argtypes = [i, i, i, i, i, i, i, p, p, p, p, p, ctypes.c_double, p, p, i]
+    L.sf_oracle_decode_attn.restype = i
+    L.sf_oracle_gather.argtypes = [i, i, i, i, i, p, p, p, i, i, i, p, p]
+    L.sf_oracle_gather.restype = i
+    L.sf_oracle_max_threads.restype = i
+    L.sf_oracle_decode_attn_fp8.argtypes = [i, i, i, i, i, i, i, p, p, p, p, p, p, p, ctypes.c_double, p, p, i]
+    L.sf_oracle_decode_attn_fp8.restype = i
+    L.sf_oracle_e4m3_value.argtypes = [i]
+    L.sf_oracle_e4m3_value.restype = ctypes.c_double
+    return L
 
 
 def lib():
@@ -44,20 +73,13 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB):
             build()
-        L = ctypes.CDLL(_LIB)
-        p = ctypes.c_void_p
-        i = ctypes.c_int
-        L.sf_oracle_decode_attn.argtypes = [i, i, i, i, i, i, i, p, p, p, p, p, ctypes.c_double, p, p, i]
-        L.sf_oracle_decode_attn.restype = i
-        L.sf_oracle_gather.argtypes = [i, i, i, i, i, p, p, p, i, i, i, p, p]
-        L.sf_oracle_gather.restype = i
-        L.sf_oracle_max_threads.restype = i
-        L.sf_oracle_decode_attn_fp8.argtypes = [i, i, i, i, i, i, i, p, p, p, p, p, p, p, ctypes.c_double, p, p, i]
-        L.sf_oracle_decode_attn_fp8.restype = i
-        L.sf_oracle_e4m3_value.argtypes = [i]
-        L.sf_oracle_e4m3_value.restype = ctypes.c_double
-        _lib = L
+        _lib = _declare(ctypes.CDLL(_LIB))
     return _lib
+
+
+def load(path: str):
+    """A separately built copy of the oracle (build_native)."""
+    return _declare(ctypes.CDLL(path))
 
 
 def _ptr(a: np.ndarray):
@@ -70,10 +92,10 @@ def _u16(a) -> np.ndarray:
     return a
 
 
-def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale, nthreads: int = 0):
+def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale, nthreads: int = 0, using=None):
     """fp64 reference. q [B,Hq,D], k_pool [N,Hkv,D/8,16,8] and v_pool
     [N,Hkv,D,16] are uint16 bf16 bit arrays; returns (out [B,Hq,D] float64,
-    lse [B,Hq] float64)."""
+    lse [B,Hq] float64). using: a library from load() instead of the default."""
     q = _u16(q)
     k_pool = _u16(k_pool)
     v_pool = _u16(v_pool)
@@ -85,7 +107,7 @@ def decode_attn(q, k_pool, v_pool, block_table, seq_lens, scale, nthreads: int =
     assert v_pool.shape == (n, hkv, d, p) and bt.shape[0] == b and lens.shape == (b,)
     out = np.empty((b, hq, d), dtype=np.float64)
     lse = np.empty((b, hq), dtype=np.float64)
-    rc = lib().sf_oracle_decode_attn(b, hq, hkv, d, p, bt.shape[1], n, _ptr(q), _ptr(k_pool),
+    rc = (using or lib()).sf_oracle_decode_attn(b, hq, hkv, d, p, bt.shape[1], n, _ptr(q), _ptr(k_pool),
                                      _ptr(v_pool), _ptr(bt), _ptr(lens), float(scale),
                                      _ptr(out), _ptr(lse), int(nthreads))
     if rc != 0:

@@ -527,59 +527,6 @@ def sf_debug_gather_kv(desc, k_pool, v_pool, block_table, seq, kv_head, length, 
 
 
 # ----------------------------------------------------------------------------
-# HIP runtime calls used by the runner for stream plumbing (copies and events)
-# ----------------------------------------------------------------------------
-_hip = None
-
-
-def hip():
-    global _hip
-    if _hip is None:
-        h = ctypes.CDLL("libamdhip64.so")
-        vp = ctypes.c_void_p
-        h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
-        h.hipEventRecord.argtypes = [vp, vp]
-        h.hipStreamWaitEvent.argtypes = [vp, vp, ctypes.c_uint]
-        h.hipEventSynchronize.argtypes = [vp]
-        h.hipEventDestroy.argtypes = [vp]
-        h.hipMemcpyAsync.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, vp]
-        for fn in ("hipEventCreateWithFlags", "hipEventRecord", "hipStreamWaitEvent",
-                   "hipEventSynchronize", "hipEventDestroy", "hipMemcpyAsync"):
-            getattr(h, fn).restype = ctypes.c_int
-        _hip = h
-    return _hip
-
-
-def _hip_check(where, err):
-    if err != 0:
-        raise RuntimeError(f"{where} failed with hipError {err}")
-
-
-class _HipEvent:
-    """A timing-free HIP event (cheap to record and wait on)."""
-
-    def __init__(self):
-        self.ev = ctypes.c_void_p()
-        _hip_check("hipEventCreateWithFlags", hip().hipEventCreateWithFlags(ctypes.byref(self.ev), 0x2))
-        self.used = False
-
-    def record(self, stream_handle):
-        _hip_check("hipEventRecord", hip().hipEventRecord(self.ev, stream_handle))
-        self.used = True
-
-    def wait_on(self, stream_handle):
-        _hip_check("hipStreamWaitEvent", hip().hipStreamWaitEvent(stream_handle, self.ev, 0))
-
-    def synchronize(self):
-        if self.used:
-            _hip_check("hipEventSynchronize", hip().hipEventSynchronize(self.ev))
-
-    def __del__(self):
-        if _hip is not None and self.ev:
-            _hip.hipEventDestroy(self.ev)
-
-
-# ----------------------------------------------------------------------------
 # convenience runner: owns the pinned work-list ring and the device buffers
 # ----------------------------------------------------------------------------
 class DecodeAttention:
@@ -587,7 +534,7 @@ class DecodeAttention:
     library's native runner (sf_runner_create / sf_runner_step): one call per
     step plans into the runner's pinned, device-mapped ring and launches the
     kernels, which read that work list in place, on the caller's stream. Tensor checks run once per
-    distinct set of tensors."""
+    distinct set of tensors (the last 64 sets are remembered)."""
 
     def __init__(self, num_q_heads, num_kv_heads, head_dim, device=None, num_cus=None,
                  ring: int = 4, opts: sf_plan_opts | None = None):
@@ -602,7 +549,7 @@ class DecodeAttention:
         self._runners = {}
         self._info = sf_plan_info()
         self._extras = sf_runner_extras()
-        self._checked = None
+        self._checked = {}
         self._desc_key = None
         self._desc = None
         self.last_info = None
@@ -627,7 +574,7 @@ class DecodeAttention:
                out.data_ptr(), None if lse is None else lse.data_ptr(), tuple(q.shape),
                tuple(k_pool.shape), tuple(v_pool.shape), tuple(block_table.shape),
                None if fp8 is None else (fp8[0].data_ptr(), fp8[1].data_ptr()))
-        if key == self._checked:
+        if key in self._checked:
             return
         b, hkv, d = q.shape[0], self.hkv, self.d
         _dev(q, "q", torch.bfloat16, (b, self.hq, d))
@@ -643,7 +590,9 @@ class DecodeAttention:
         _dev(out, "out", torch.float32, (b, self.hq, d))
         if lse is not None:
             _dev(lse, "lse", torch.float32, (b, self.hq))
-        self._checked = key
+        if len(self._checked) >= 64:      # a few tensor sets in rotation stay checked
+            self._checked.clear()
+        self._checked[key] = True
 
     @staticmethod
     def _event_handle(ev, stream):

@@ -18,13 +18,23 @@
 //
 //   S^T[32 keys][16 rows] = K Q^T        2 x (D/32) v_mfma_f32_16x16x32_bf16
 //   online softmax in base 2             (row = lane column; lazily moved reference)
-//   O^T[D][16 rows]      += V^T P^T      (D/16) MFMAs, P rounded to bf16
+//   O^T[D][16 rows]      += V^T P^T      (D/16) v_mfma_f32_16x16x32_f16
 //
 // with each K and V operand read from LDS once per wave and used for both of
 // its row tiles, and the two tiles pipelined so that one tile's matrix-core
 // work overlaps the other's exponentials. The operand mapping is the decode
 // kernel's: each lane's eight scores are keys 4*grp .. 4*grp+3 of both
 // pages, the eight P^T values its P.V operand needs.
+//
+// The P.V product runs on fp16 operands. The weights P are rounded to fp16
+// (relative error 2^-11) instead of bf16 (2^-8): with bf16 weights a row
+// with a few comparable keys and values of opposite sign can miss the
+// 2e-3 + 1e-2 |ref| acceptance bound, with fp16 weights it stays an order
+// of magnitude inside it. V is widened from bf16 to fp16 once, while it is
+// staged into LDS; that is exact for every bf16 value of magnitude in
+// [2^-17, 65280], rounds smaller ones by at most 2^-25, and turns values of
+// magnitude 65536 and above into infinities (fp16's range; the header
+// states the limit).
 //
 // Measured alternatives (full re-prefill of 32 long-tail trajectories):
 // 64 rows per wave (4 waves, one per SIMD) halves the LDS operand reads but
@@ -41,6 +51,7 @@ namespace sf {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -52,7 +63,7 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRowTiles = 2;      // 16-row MFMA tiles per wave
 constexpr int kStepKeys = 2 * kPage;   // keys per step (two pages)
 constexpr int kSub = 2;                // steps per barrier interval
-constexpr float kRescaleMax = 65536.f; // headroom of the lazily moved softmax reference, 2^16
+constexpr float kRescaleMax = 32768.f; // headroom of the lazily moved softmax reference, 2^15 (fp16 weights)
 static_assert(kWaves * kRowTiles * 16 == kExtendRows, "rows per item");
 
 __device__ __forceinline__ const_i32_ptr as_constant(const int32_t* p) { return (const_i32_ptr)(p); }
@@ -62,11 +73,20 @@ __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ f32x4 mfma_f16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                0, 0);
+}
+
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-// Two floats to two bf16 (round to nearest even) in one conversion.
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+// Two floats to two fp16 (round to nearest even) in one conversion.
+__device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, f16x2));
+}
+// Two bf16 (one 32-bit word) to two fp16: widen to fp32 (exact), then round.
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
+  return pack_f16(__builtin_bit_cast(float, w << 16), __builtin_bit_cast(float, w & 0xFFFF0000u));
 }
 
 // Element offset of a (page, KV head) tile in either pool.
@@ -106,13 +126,13 @@ __device__ __forceinline__ float weight_sum(const float* p) {
 // sum is needed for the row sum anyway, and it bounds each of its weights,
 // so the check costs one compare. Until it fires the lanes of a row need not
 // agree on the row's max at all, so the common step has no cross-lane
-// reduction. Weights below kRescaleMax are exact in fp32 and keep bf16's
-// relative precision, and O and l share the reference, so O / l does not
-// change. When the check fires, each row of the tile whose max has risen
-// moves m to it (the max over all four lane groups) and O and l are
-// rescaled; every weight is then at most 1, so the check stays quiet until a
-// row's scores rise more than 13 (log2 units) above its reference. Key 0 is
-// in every row's first step, so m is finite after it.
+// reduction. Weights up to kRescaleMax = 2^15 stay finite in fp16 (largest
+// finite value 65504) with fp16's relative precision, and O and l share the
+// reference, so O / l does not change. When the check fires, each row of the
+// tile whose max has risen moves m to it (the max over all four lane groups)
+// and O and l are rescaled; every weight is then at most 1, so the check
+// stays quiet until a row's scores rise more than 12 (log2 units) above its
+// reference. Key 0 is in every row's first step, so m is finite after it.
 struct TileWeights {
   float sc[8];   // raw scores of this lane (masked ones -inf)
   float p[8];    // 2^(sc * c - m)
@@ -177,8 +197,8 @@ __device__ __forceinline__ u32x4 settle(TileWeights& t, float c, float& m, float
     t.part = weight_sum(t.p);
   }
   lsum += t.part;
-  return u32x4{pack_bf16(t.p[0], t.p[1]), pack_bf16(t.p[2], t.p[3]), pack_bf16(t.p[4], t.p[5]),
-               pack_bf16(t.p[6], t.p[7])};
+  return u32x4{pack_f16(t.p[0], t.p[1]), pack_f16(t.p[2], t.p[3]), pack_f16(t.p[4], t.p[5]),
+               pack_f16(t.p[6], t.p[7])};
 }
 
 // Scheduling hints: n times {one MFMA, then k vector ALU ops}, so the
@@ -309,10 +329,10 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
     }
   };
   // Writes the fetched pieces of interval j into LDS buffer `base` (one per
-  // step of the interval). V pieces are split into their two token quads
-  // (8 bytes each) at their interleaved slots; in the step that reaches kend,
-  // V tokens at or past it are zeroed here (they may be stale or NaN, and a
-  // zero weight times NaN is still NaN).
+  // step of the interval). V pieces are widened to fp16 and split into their
+  // two token quads (8 bytes each) at their interleaved slots; in the step
+  // that reaches kend, V tokens at or past it are zeroed first (they may be
+  // stale or NaN, and a zero weight times NaN is still NaN).
   auto stage = [&](uint16_t (*base)[4 * TE], int j) {
 #pragma unroll
     for (int u = 0; u < kSub; ++u) {
@@ -335,6 +355,8 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
               x[w] &= (key < kend ? 0x0000FFFFu : 0u) | (key + 1 < kend ? 0xFFFF0000u : 0u);
             }
           }
+#pragma unroll
+          for (int w = 0; w < 4; ++w) x[w] = bf16x2_to_f16x2(x[w]);
           *reinterpret_cast<u32x2*>(L + sdst0[q]) = u32x2{x[0], x[1]};
           *reinterpret_cast<u32x2*>(L + sdst1[q]) = u32x2{x[2], x[3]};
         }
@@ -379,7 +401,7 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
         interleave_mfma_valu<3>((rt + 1 < kRowTiles ? 2 * KB : 0) + (rt > 0 ? JB : 0));
         const u32x4 pf = settle<D, kMasked>(t, c, m[rt], lsum[rt], o[rt]);
 #pragma unroll
-        for (int jb = 0; jb < JB; ++jb) o[rt][jb] = mfma_bf16(vf[jb], pf, o[rt][jb]);
+        for (int jb = 0; jb < JB; ++jb) o[rt][jb] = mfma_f16(vf[jb], pf, o[rt][jb]);
       }
     };
     if (key0 + kStepKeys - 1 > wave_kmin)

@@ -91,6 +91,44 @@ def test_extend_oracle_matches_torch_sdpa_with_causal_mask(oracle_lib, ci, heads
     np.testing.assert_allclose(lse, want_l, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("ci", range(len(CASES)))
+@pytest.mark.parametrize("heads", [(4, 2, 64), (7, 1, 128), (3, 3, 64)])
+def test_dense_extend_oracle_matches_torch_sdpa_and_the_per_row_oracle(oracle_lib, ci, heads):
+    """The whole-sequence fp64 path (matrix products, mask, softmax written
+    out) against torch's SDPA and against a decode step per row; chunks of
+    new tokens smaller than the sequences, so chunk edges are crossed."""
+    hq, hkv, d = heads
+    q, k, v, bt, lens, ql, scale = _case(20 + ci, *CASES[ci], hq=hq, hkv=hkv, d=d)
+    seqs = list(range(lens.size))[::-1]
+    rows, out, lse = extend_ref.extend_attn_dense(q, k, v, bt, lens, ql, scale, seqs, nthreads=3, tok_chunk=7)
+    cu = extend_ref.cu_lens(ql)
+    assert rows.tolist() == [r for s in seqs for r in range(cu[s], cu[s + 1])]
+    want_o, want_l = _sdpa_reference(q, k, v, bt, lens, ql, scale)
+    np.testing.assert_allclose(out, want_o[rows], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(lse, want_l[rows], rtol=1e-12, atol=1e-12)
+    o2, l2 = extend_ref.extend_attn(q, k, v, bt, lens, ql, scale, rows=rows)
+    np.testing.assert_allclose(out, o2, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(lse, l2, rtol=1e-13, atol=1e-13)
+
+
+def test_dense_extend_oracle_first_row_and_causal_limit(oracle_lib):
+    """A full re-prefill's first row returns its own value row exactly, and a
+    key past a row's causal limit changes nothing: poisoning the last key of
+    a sequence leaves every earlier row's result unchanged."""
+    q, k, v, bt, lens, ql, scale = _case(8, [45], [45], hq=2, hkv=1, d=64)
+    rows, out, lse = extend_ref.extend_attn_dense(q, k, v, bt, lens, ql, scale, [0], tok_chunk=16)
+    kd, vd = dense_ref.gather_dense(k, v, bt, 0, 0, 1)
+    assert np.array_equal(out[0, 0], vd[0]) and np.array_equal(out[0, 1], vd[0])
+    k2, v2 = k.copy(), v.copy()
+    last = 44
+    pg, sl = int(bt[0, last // PAGE]), last % PAGE
+    k2[pg, 0, :, sl, :] = 0x7F80   # +inf keys
+    v2[pg, 0, :, sl] = 0x7FC0      # NaN values
+    _, out2, lse2 = extend_ref.extend_attn_dense(q, k2, v2, bt, lens, ql, scale, [0], tok_chunk=16)
+    assert np.array_equal(out2[:last], out[:last]) and np.array_equal(lse2[:last], lse[:last])
+    assert not np.all(np.isfinite(out2[last]))
+
+
 def test_first_token_of_a_full_reprefill_is_its_own_value_row(oracle_lib):
     q, k, v, bt, lens, ql, scale = _case(3, [50, 20], [50, 20], hq=6, hkv=2, d=64)
     out, lse = extend_ref.extend_attn(q, k, v, bt, lens, ql, scale)
