@@ -169,6 +169,29 @@ sf_status sf_decode_attn_combine(const sf_attn_desc* desc, const sf_plan_info* i
                                  uint64_t workspace_bytes, float* out, float* lse, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the decode
+ * step of sf_decode_attn followed by sf_decode_attn_combine, with the split-K
+ * partial results in a device array the library owns (SF_SCRATCH_BYTES per
+ * device, set up on the first call on that device and held until the
+ * process ends) instead of a caller workspace. The plan must come from
+ * sf_decode_attn_plan for desc and already sit in device memory at work_dev
+ * (the call copies nothing to it); the other arguments are as for
+ * sf_decode_attn and sf_decode_attn_combine. The call allocates nothing
+ * (no hipMalloc, no hipFree). The stream's device must be the current device.
+ * Every call on one device shares that device's array: calls that overlap
+ * on one device (other streams, other threads) race and give wrong results.
+ * Nothing in the array needs to start at zero: the attention launch writes
+ * every partial result the combine launch reads.
+ * Errors as sf_decode_attn; SF_ERR_CAPACITY if info->workspace_bytes exceeds
+ * SF_SCRATCH_BYTES (plan with fewer workers, e.g. the default options).
+ */
+#define SF_SCRATCH_BYTES (32ull << 20)
+sf_status sf_decode_attn_scratch(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,
+                                 const void* q, const void* k_pool, const void* v_pool,
+                                 const int32_t* block_table, float* out, float* lse, void* stream);
+
+/*
  * Append, then attend: the decode step of a growing cache. Each step of a
  * batched decode produces one new token per running trajectory (App. B.1),
  * whose key and value join the trajectory's cache before its query attends.

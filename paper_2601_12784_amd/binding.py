@@ -96,6 +96,7 @@ def lib():
                                  vp, ctypes.c_uint64, vp]
     L.sf_decode_attn_combine.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, ctypes.c_uint64,
                                          vp, vp, vp]
+    L.sf_decode_attn_scratch.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp]
     L.sf_debug_gather_kv.argtypes = [P(sf_attn_desc), vp, vp, vp, ctypes.c_int32, ctypes.c_int32,
                                      ctypes.c_int32, vp, vp, vp]
     L.sf_decode_attn_append.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp,
@@ -131,7 +132,7 @@ def lib():
                "sf_decode_attn_append", "sf_page_pool_create", "sf_page_pool_claim", "sf_page_pool_alloc",
                "sf_page_pool_release", "sf_page_table_step", "sf_route", "sf_extend_attn_plan",
                "sf_extend_attn", "sf_decode_attn_fp8", "sf_kv_quantize_fp8", "sf_runner_create",
-               "sf_runner_step", "sf_debug_stream_read"):
+               "sf_runner_step", "sf_debug_stream_read", "sf_decode_attn_scratch"):
         getattr(L, fn).restype = ctypes.c_int
     L.sf_status_string.argtypes = [ctypes.c_int]
     L.sf_status_string.restype = ctypes.c_char_p
@@ -499,6 +500,29 @@ def sf_decode_attn_combine(desc, info, work_dev, workspace, out, lse=None, strea
     _check("sf_decode_attn_combine", lib().sf_decode_attn_combine(
         ctypes.byref(desc), ctypes.byref(info), _addr(work_dev), _addr(workspace),
         workspace.numel() * workspace.element_size(), _addr(out), _addr(lse), _stream(stream)))
+
+
+SCRATCH_BYTES = 32 << 20   # SF_SCRATCH_BYTES of the header
+
+
+def sf_decode_attn_scratch(desc, info, work_dev, q, k_pool, v_pool, block_table, out, lse=None, stream=None):
+    """sf_decode_attn + sf_decode_attn_combine with the partials in the
+    library's own device array (allocates nothing). work_dev: the plan,
+    already on the device."""
+    b, hq, hkv, d = desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim
+    _dev(q, "q", torch.bfloat16, (b, hq, d))
+    _dev(k_pool, "k_pool", torch.bfloat16, (desc.num_pages, hkv, d // 8, PAGE, 8))
+    _dev(v_pool, "v_pool", torch.bfloat16, (desc.num_pages, hkv, d, PAGE))
+    _dev(block_table, "block_table", torch.int32, (b, desc.block_table_stride))
+    _dev(out, "out", torch.float32, (b, hq, d))
+    _dev(work_dev, "work_dev", torch.int32)
+    if work_dev.numel() * 4 < info.work_bytes:
+        raise ValueError("work_dev is smaller than the plan")
+    if lse is not None:
+        _dev(lse, "lse", torch.float32, (b, hq))
+    _check("sf_decode_attn_scratch", lib().sf_decode_attn_scratch(
+        ctypes.byref(desc), ctypes.byref(info), _addr(work_dev), _addr(q), _addr(k_pool), _addr(v_pool),
+        _addr(block_table), _addr(out), _addr(lse), _stream(stream)))
 
 
 def sf_debug_stream_read(buf, sink, blocks=16384, stream=None):

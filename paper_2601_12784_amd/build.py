@@ -14,7 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsf_decode_attn.so")
-SOURCES = ["plan.cpp", "pages.cpp", "cost.cpp", "extend.cpp", "runner.cpp", "api.cpp", "decode_attn.hip", "extend_attn.hip", "probe.hip"]
+SOURCES = ["plan.cpp", "pages.cpp", "cost.cpp", "extend.cpp", "runner.cpp", "api.cpp", "decode_attn.hip", "extend_attn.hip", "probe.hip",
+           "scratch.hip"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 VALU ops.

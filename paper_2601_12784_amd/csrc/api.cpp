@@ -74,14 +74,13 @@ CombineArgs combine_args(const sf_attn_desc* desc, const sf_plan_info* info, con
   return a;
 }
 
-// Shared by sf_decode_attn and sf_decode_attn_append: checks, optional
-// work-list upload, the attention launch; when appending, also the merge
-// launch that stores the newest tokens.
-sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_host,
-                 int32_t* work_dev, const void* q, const void* k_pool, const void* v_pool,
-                 const int32_t* block_table, float* out, float* lse, void* workspace,
-                 uint64_t workspace_bytes, void* stream, const AppendArgs* app,
-                 const float* k_scale = nullptr, const float* v_scale = nullptr) {
+}  // namespace
+
+// Every host-side check of a decode step's arguments except the workspace.
+sf_status sf::check_step_args(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,
+                              const void* q, const void* k_pool, const void* v_pool, const int32_t* block_table,
+                              const float* out, const float* lse, const void* k_new, const void* v_new,
+                              const int32_t* new_pages, const float* k_scale, const float* v_scale) {
   sf_status st = validate_desc(desc);
   if (st != SF_OK) return st;
   if ((st = check_plan(desc, info)) != SF_OK) return st;
@@ -94,9 +93,29 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
     return SF_ERR_INVALID_ARG;
   if ((k_scale == nullptr) != (v_scale == nullptr)) return SF_ERR_INVALID_ARG;
   if (k_scale && desc->num_pages > 0 && (!aligned4(k_scale) || !aligned4(v_scale))) return SF_ERR_INVALID_ARG;
-  if (app && (!app->k_new || !app->v_new || !aligned16(app->k_new) || !aligned16(app->v_new) ||
-              (app->new_pages && !aligned4(app->new_pages)) || !lse))
+  if ((k_new || v_new) && (!k_new || !v_new || !aligned16(k_new) || !aligned16(v_new) ||
+                           (new_pages && !aligned4(new_pages)) || !lse))
     return SF_ERR_INVALID_ARG;
+  return SF_OK;
+}
+
+namespace {
+
+// Shared by sf_decode_attn and sf_decode_attn_append: checks, optional
+// work-list upload, the attention launch; when appending, also the merge
+// launch that stores the newest tokens.
+sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_host,
+                 int32_t* work_dev, const void* q, const void* k_pool, const void* v_pool,
+                 const int32_t* block_table, float* out, float* lse, void* workspace,
+                 uint64_t workspace_bytes, void* stream, const AppendArgs* app,
+                 const float* k_scale = nullptr, const float* v_scale = nullptr) {
+  sf_status st = check_step_args(desc, info, work_dev, q, k_pool, v_pool, block_table, out, lse,
+                                 app ? app->k_new : nullptr, app ? app->v_new : nullptr,
+                                 app ? app->new_pages : nullptr, k_scale, v_scale);
+  if (st != SF_OK) return st;
+  if (info->num_workers == 0) return SF_OK;
+  // An appending step must name both new-token arrays.
+  if (app && (!app->k_new || !app->v_new)) return SF_ERR_INVALID_ARG;
   if (workspace_bytes < info->workspace_bytes) return SF_ERR_CAPACITY;
   if (info->workspace_bytes && (!workspace || !aligned16(workspace))) return SF_ERR_INVALID_ARG;
 
@@ -149,6 +168,18 @@ sf_status sf::decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_in
   const AppendArgs app = {q, k_new, v_new, new_pages, single_rows, num_single};
   return attend(desc, info, nullptr, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
                 workspace_bytes, stream, &app);
+}
+
+sf_status sf::decode_attn_and_combine(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,
+                                     const void* q, const void* k_pool, const void* v_pool,
+                                     const int32_t* block_table, float* out, float* lse, void* workspace,
+                                     uint64_t workspace_bytes, void* stream) {
+  int32_t* wd = const_cast<int32_t*>(work_dev);   // read only: no work_host, so nothing is copied into it
+  sf_status st = attend(desc, info, nullptr, wd, q, k_pool, v_pool, block_table, out, lse, workspace,
+                        workspace_bytes, stream, nullptr);
+  if (st != SF_OK || info->num_workers == 0 || info->num_combine == 0) return st;
+  const CombineArgs a = combine_args(desc, info, wd, workspace, out, lse, nullptr, nullptr, nullptr, nullptr);
+  return from_hip(launch_combine(a, static_cast<hipStream_t>(stream)));
 }
 
 extern "C" sf_status sf_decode_attn(const sf_attn_desc* desc, const sf_plan_info* info,

@@ -157,6 +157,20 @@ sf_status decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_info* 
                                   int32_t* block_table, float* out, float* lse, void* workspace,
                                   uint64_t workspace_bytes, void* stream);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream);
+
+// Every host-side check of a decode step's arguments except the workspace
+// (k_new / v_new / new_pages: an appending step; k_scale / v_scale: fp8).
+sf_status check_step_args(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,
+                          const void* q, const void* k_pool, const void* v_pool, const int32_t* block_table,
+                          const float* out, const float* lse, const void* k_new, const void* v_new,
+                          const int32_t* new_pages, const float* k_scale, const float* v_scale);
+
+// sf_decode_attn (work list already on the device) then
+// sf_decode_attn_combine, both on `workspace`; the body of
+// sf_decode_attn_scratch.
+sf_status decode_attn_and_combine(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,
+                                  const void* q, const void* k_pool, const void* v_pool, const int32_t* block_table,
+                                  float* out, float* lse, void* workspace, uint64_t workspace_bytes, void* stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
 // Streaming-read probe: reads bytes (a multiple of 16) of buf once; sink: 16 B.

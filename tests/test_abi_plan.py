@@ -275,6 +275,33 @@ def test_combine_rejects_bad_arguments(lib):
     assert c(ctypes.byref(desc), ctypes.byref(one), None, None, 0, None, None, None) == 0
 
 
+def test_scratch_step_checks_everything_before_touching_the_device(lib):
+    """sf_decode_attn_scratch rejects bad arguments, and a plan whose partials
+    exceed its array, before its first HIP call (this runs without a GPU)."""
+    desc, info, _ = _planned()
+    assert 0 < info.workspace_bytes <= B.SCRATCH_BYTES
+    f = lib.sf_decode_attn_scratch
+
+    def call(d=desc, i=info, work=FAKE, q=FAKE, k=FAKE, v=FAKE, bt=FAKE, out=FAKE, lse=None):
+        return f(ctypes.byref(d), None if i is None else ctypes.byref(i), work, q, k, v, bt, out, lse, None)
+
+    assert call(i=None) == 1
+    assert call(q=None) == 1 and call(work=None) == 1 and call(out=FAKE + 4) == 1 and call(lse=FAKE + 2) == 1
+    other = B.make_desc(desc.num_seqs, desc.num_q_heads, desc.num_kv_heads, desc.head_dim,
+                        desc.block_table_stride + 1, desc.num_pages, desc.softmax_scale)
+    assert call(d=other) == 4
+    lens = np.full(64, 4096, np.int32)
+    big_desc = B.make_desc(64, 28, 4, 128, 256, 64 * 256, 0.1)
+    big, _ = B.sf_decode_attn_plan(big_desc, lens, B.make_opts(num_cus=256, chunk_pages=1))
+    assert big.workspace_bytes > B.SCRATCH_BYTES
+    assert call(d=big_desc, i=big) == 3
+    # a batch of no sequences launches nothing and needs no array
+    none_desc = B.make_desc(0, 28, 4, 128, 1, 0, 0.1)
+    none, _ = B.sf_decode_attn_plan(none_desc, np.zeros(0, np.int32))
+    assert none.num_workers == 0
+    assert call(d=none_desc, i=none, work=None, q=None, k=None, v=None, bt=None, out=None) == 0
+
+
 def test_gather_rejects_bad_arguments(lib):
     desc = B.make_desc(2, 8, 2, 128, 4, 10, 0.1)
     g = lib.sf_debug_gather_kv
