@@ -96,7 +96,7 @@ typedef struct sf_plan_info {
   int32_t chunk_pages;       /* pages per worker, ceil(T / num_workers) (0 if T = 0) */
   int32_t reserved;          /* 0 */
   uint64_t work_bytes;       /* bytes of the work list:
-                                (ceil(num_workers / 4) + num_work + num_combine) * 32 */
+                                (num_workers + num_work + num_combine) * 32 */
   uint64_t workspace_bytes;  /* device scratch sf_decode_attn needs (0 if no partials) */
   uint64_t desc_key;         /* fingerprint of the descriptor's shape and pool-size fields */
 } sf_plan_info;
@@ -122,8 +122,9 @@ typedef struct sf_plan_info {
  * counted in page order, -> slot_base + c) and one combine item each.
  *
  * Work list, int32 rows of 8:
- *   ceil(W / 4) rows of worker table: worker w at ints 2w, 2w+1 =
- *     (first item, item count); the worker's items are consecutive
+ *   W rows of worker table, row w: first item, item count (the worker's
+ *     items are consecutive), then ints 0 .. 5 of its first item's row
+ *     (all zero for a worker without items)
  *   num_work item rows, worker by worker:
  *     seq, kv_head, page_begin, page_end (pages of the pair), seq_len,
  *     slot (-1 = write out directly), combine index (-1 if n_p = 1), n_p
@@ -230,10 +231,9 @@ sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* in
  * mapped host buffer, then on the caller's stream the attention (plain,
  * appending or fp8) and the merge of split sequences, whose kernels read that
  * work list in place (no separate upload). The runner owns a ring of 4 such
- * buffers, the split-K workspace (grown on demand, after synchronizing the
- * caller's stream) and one event per buffer: a buffer is rewritten only
- * after the step that read it has ended, so the host plans step i + 1 while
- * the kernels of step i run. One runner serves one device (the current one at
+ * buffers, the split-K workspace and one event per buffer: a buffer is
+ * rewritten only after the step that read it has ended, so the host plans
+ * step i + 1 while the kernels of step i run. One runner serves one device (the current one at
  * creation) and one caller stream at a time; steps on different streams, or
  * calls that overlap, are not supported.
  */
@@ -255,6 +255,19 @@ typedef struct sf_runner_extras {
 sf_status sf_runner_create(const sf_attn_desc* shape, const sf_plan_opts* opts, sf_runner** runner);
 /* Waits for the runner's work to finish, then frees everything it owns. */
 void sf_runner_destroy(sf_runner* runner);
+/* Sizes the runner's buffers ahead of its steps: the split-K workspace to at
+ * least workspace_bytes, and every ring buffer to hold a work list of
+ * work_bytes plus an appending step's extras for up to max_num_seqs
+ * sequences; workspace_bytes and work_bytes as sf_decode_attn_plan reports
+ * them (work_host NULL) for the largest batch the caller will step, with the
+ * runner's options. Growing the workspace synchronizes `stream` first (the
+ * old one may still be in use); a ring buffer grows after the step that last
+ * read it has ended. A step whose plan needs more than the runner holds grows
+ * it the same way inside sf_runner_step: a stall in that step, which a
+ * reserve beforehand avoids. SF_ERR_INVALID_ARG for a NULL runner or a
+ * negative max_num_seqs, SF_ERR_HIP if an allocation fails. */
+sf_status sf_runner_reserve(sf_runner* runner, uint64_t workspace_bytes, uint64_t work_bytes,
+                            int32_t max_num_seqs, void* stream);
 /* One decode step: desc (its head counts, head_dim and page size as at
  * creation), seq_lens_host (host int32 [num_seqs]) and the device tensors as
  * for sf_decode_attn; extras may be NULL. *info (may be NULL) receives the
@@ -426,6 +439,21 @@ sf_status sf_page_pool_release(sf_page_pool* pool, const int32_t* pages, int32_t
 sf_status sf_page_table_step(sf_page_pool* pool, int32_t* block_table, int32_t stride,
                              int32_t num_seqs, const int32_t* prev_lens, const int32_t* lens,
                              int32_t appending, int32_t* new_pages);
+
+/*
+ * Host check of a block table before it is used on the device: the kernels
+ * read block-table entries without checking them (a bad page id is an
+ * out-of-bounds device read), so a caller holding a host copy can check it
+ * first. For every sequence s with seq_lens_host[s] = L > 0 (L <= 0 for a
+ * sequence that reads nothing), the entries block_table_host[s][0 ..
+ * ceil(L / 16) - 1] must lie in [0, desc->num_pages) and ceil(L / 16) must
+ * not exceed desc->block_table_stride. Host memory only, no device calls.
+ * Returns SF_OK, or SF_ERR_INVALID_ARG with *bad_seq (may be NULL) = the
+ * first sequence that breaks the rule (-1 for a bad descriptor or a NULL
+ * array).
+ */
+sf_status sf_check_block_table(const sf_attn_desc* desc, const int32_t* block_table_host,
+                               const int32_t* seq_lens_host, int32_t* bad_seq);
 
 /*
  * Throughput cost model and trajectory routing (host only, no device calls).

@@ -14,8 +14,8 @@ planner, so the two can be compared bit for bit:
   its segments; n_p = segments of pair p
   partial slots for pairs with n_p > 1 in pair order, segment c -> base + c
 
-Work list rows (int32 x 8): ceil(W/4) worker-table rows (first item, count
-per worker), then the items worker by worker
+Work list rows (int32 x 8): W worker-table rows (first item, count, then the
+first six ints of that item's row), then the items worker by worker
   (seq, kv_head, page_begin, page_end, seq_len, slot or -1, combine index or -1, n_p),
 then one combine row per cut pair (seq, kv_head, slot_base, n_p, seq_len, 0, 0, 0).
 """
@@ -82,11 +82,11 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
             combine.append([s, kvh, slot, n, lens[s], 0, 0, 0])
             slot += n
 
-    table = np.zeros((_ceil(workers, 4), 8), dtype=np.int32)
+    table = np.zeros((workers, 8), dtype=np.int32)
     rows = []
     for w in range(workers):
-        table.reshape(-1)[2 * w] = len(rows)
-        table.reshape(-1)[2 * w + 1] = len(per_worker[w])
+        table[w, 0] = len(rows)
+        table[w, 1] = len(per_worker[w])
         for p, b, e in per_worker[w]:
             s, kvh = pairs[p]
             if p in meta:
@@ -96,6 +96,9 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
             else:
                 rows.append([s, kvh, b, e, lens[s] if e > b else 0, -1, -1, 1])
     items = np.array(rows, dtype=np.int32).reshape(-1, 8)
+    for w in range(workers):
+        if table[w, 1]:
+            table[w, 2:] = items[table[w, 0], :6]
     comb = np.array(combine, dtype=np.int32).reshape(-1, 8)
     g = num_q_heads // num_kv_heads
     ws = _align(slot * g * head_dim * 4) + _align(slot * g * 4) if slot else 0

@@ -15,7 +15,9 @@ import numpy as np
 import torch
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libsf_decode_attn.so")
+# SF_DECODE_ATTN_LIB selects another build of the same library (the
+# sanitized CPU-test copy of build.py --sanitize); default: the in-tree one.
+LIB_PATH = os.environ.get("SF_DECODE_ATTN_LIB") or os.path.join(PKG, "libsf_decode_attn.so")
 HEADER = os.path.join(os.path.dirname(PKG), "include", "sf_decode_attn.h")
 PAGE = 16
 ITEM_INTS = 8
@@ -102,6 +104,8 @@ def lib():
     L.sf_decode_attn_append.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp,
                                         vp, vp, vp, vp, ctypes.c_uint64, vp]
     L.sf_runner_create.argtypes = [P(sf_attn_desc), P(sf_plan_opts), P(vp)]
+    L.sf_runner_reserve.argtypes = [vp, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, vp]
+    L.sf_runner_reserve.restype = ctypes.c_int
     L.sf_runner_destroy.argtypes = [vp]
     L.sf_runner_destroy.restype = None
     L.sf_runner_step.argtypes = [vp, P(sf_attn_desc), vp, vp, vp, vp, vp, vp, vp, P(sf_runner_extras), vp,
@@ -126,6 +130,8 @@ def lib():
     L.sf_cost_ideal_gain.argtypes = [P(sf_cost_model), ctypes.c_double]
     for fn in ("sf_cost_throughput", "sf_cost_marginal_gain", "sf_cost_ideal_gain"):
         getattr(L, fn).restype = ctypes.c_double
+    L.sf_check_block_table.argtypes = [P(sf_attn_desc), vp, vp, P(ctypes.c_int32)]
+    L.sf_check_block_table.restype = ctypes.c_int
     L.sf_route.argtypes = [P(sf_cost_model), ctypes.c_double, ctypes.c_int32, vp, ctypes.c_int32, vp,
                            ctypes.c_int32, vp, P(ctypes.c_int32)]
     for fn in ("sf_decode_attn_plan", "sf_decode_attn", "sf_decode_attn_combine", "sf_debug_gather_kv",
@@ -146,6 +152,27 @@ def header_functions() -> list[str]:
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(sf_[a-z0-9_]+)\s*\(", text)))
+
+
+# SF_DEBUG_CHECKS=1: before each launch the classes below check every block-
+# table entry the launch will read against the pool size (sf_check_block_table),
+# on a host copy (DecodeLoopRunner keeps one; the others copy the device table
+# back, which synchronizes: a debugging aid, not for timing).
+DEBUG_CHECKS = os.environ.get("SF_DEBUG_CHECKS", "") not in ("", "0")
+
+
+def check_block_table(desc: sf_attn_desc, block_table_host, seq_lens) -> None:
+    """Raises SfError (naming the first bad sequence) unless every block-table
+    entry a step over seq_lens reads lies in [0, desc.num_pages)."""
+    bt = np.ascontiguousarray(block_table_host.cpu().numpy() if isinstance(block_table_host, torch.Tensor)
+                              else block_table_host, dtype=np.int32)
+    lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    if bt.shape != (desc.num_seqs, desc.block_table_stride) or lens.shape != (desc.num_seqs,):
+        raise ValueError("block table or lengths do not match the descriptor")
+    bad = ctypes.c_int32(-1)
+    st = lib().sf_check_block_table(ctypes.byref(desc), bt.ctypes.data, lens.ctypes.data, ctypes.byref(bad))
+    if st != 0:
+        raise SfError(f"sf_check_block_table (sequence {bad.value})", st)
 
 
 def status_string(status: int) -> str:
@@ -409,6 +436,8 @@ class ExtendAttention:
             self._work_host = torch.empty(need, dtype=torch.int32, pin_memory=True)
             self._work_dev = torch.empty(need, dtype=torch.int32, device=self.device)
         info, _ = sf_extend_attn_plan(desc, lens, qls, work_host=self._work_host)
+        if DEBUG_CHECKS:
+            check_block_table(desc, block_table, np.where(qls > 0, lens, 0))
         if out is None:
             out = torch.empty((info.num_q_rows, self.hq, self.d), dtype=torch.float32, device=self.device)
         sf_extend_attn(desc, info, self._work_host, self._work_dev, q, k_pool, v_pool, block_table, out, lse,
@@ -578,6 +607,7 @@ class DecodeAttention:
         self._desc = None
         self.last_info = None
         self._lse = None
+        self._host_checked = False   # set by a caller that checked its own host copy
 
     def _runner(self, chunk_pages):
         o = self.opts
@@ -617,6 +647,24 @@ class DecodeAttention:
         if len(self._checked) >= 64:      # a few tensor sets in rotation stay checked
             self._checked.clear()
         self._checked[key] = True
+
+    def reserve(self, seq_lens, num_pages, block_table_stride, chunk_pages=None, fp8=False, stream=None):
+        """Sizes the native runner's workspace and work-list ring for a step
+        over seq_lens (the largest batch to come) ahead of the steps, so no
+        step stalls to grow them (sf_runner_reserve)."""
+        lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+        desc = make_desc(lens.size, self.hq, self.hkv, self.d, block_table_stride, num_pages, 1.0)
+        o = self.opts
+        wpc = o.workers_per_cu or (8 if fp8 else 0)
+        opts = sf_plan_opts(o.num_cus, int(chunk_pages or 0), wpc, o.min_chunk_pages, 0)
+        info = sf_plan_info()
+        st = self.L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts), None, 0,
+                                        ctypes.byref(info))
+        _check("sf_decode_attn_plan", st)
+        main = stream or torch.cuda.current_stream(self.device)
+        with torch.cuda.device(self.device):
+            _check("sf_runner_reserve", self.L.sf_runner_reserve(self._runner(chunk_pages), info.workspace_bytes,
+                                                                 info.work_bytes, lens.size, main.cuda_stream))
 
     @staticmethod
     def _event_handle(ev, stream):
@@ -669,6 +717,13 @@ class DecodeAttention:
                 lse = self._lse[: b * self.hq].view(b, self.hq)
         if fp8 is not None:
             ex.k_scale, ex.v_scale = fp8[0].data_ptr(), fp8[1].data_ptr()
+        if DEBUG_CHECKS and not self._host_checked:
+            # an appending step reads the pool for its L - 1 cached tokens only
+            # (the newest token's page may still be -1: the step writes it)
+            check_block_table(self._desc, block_table, lens - 1 if append is not None else lens)
+            if pages is not None and np.any((pages < -1) | (pages >= k_pool.shape[0])):
+                raise ValueError("new_pages holds a page id outside the pool")
+        self._host_checked = False
         if attn_events is not None:
             ex.attn_start = self._event_handle(attn_events[0], main)
             ex.attn_end = self._event_handle(attn_events[1], main)
@@ -757,6 +812,11 @@ class DecodeLoopRunner:
         if appending and (k_new is None or v_new is None):
             raise ValueError("every step after the first appends a token: pass k_new and v_new")
         new_pages = self.table.advance(lens, appending)
+        if DEBUG_CHECKS:
+            desc = make_desc(lens.size, self.attn.hq, self.attn.hkv, self.attn.d, self.table.bt.shape[1],
+                             self.k_pool.shape[0], self.scale)
+            check_block_table(desc, self.table.bt, lens)
+            self.attn._host_checked = True
         append = (k_new, v_new, new_pages) if appending else None
         out = self.attn(q, self.k_pool, self.v_pool, self.block_table, lens.astype(np.int32), self.scale,
                         out=out, lse=lse, stream=stream, attn_events=attn_events, append=append)

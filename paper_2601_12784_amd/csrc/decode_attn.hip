@@ -312,10 +312,13 @@ struct Segment {
   int seq, kvh, pb, pe, len, slot;
 };
 
-// A worker's segment rows, kRowsPerLoad at a time: one vector load brings
-// them into the wave (lane l holds int l of the rows), so a worker pays one
-// memory round trip for its rows instead of one per segment. That matters
-// when the work list is read in place from pinned host memory.
+// A worker's segment rows. The worker's table row holds its first item's
+// index, its item count and its first segment's fields, so one scalar load
+// starts the worker: its first segment's loads go out right after it. The
+// other rows come kRowsPerLoad at a time, one vector load each (lane l holds
+// int l of the rows), requested behind the loads of the segment before them:
+// vector memory completes in issue order, so the work list, read in place
+// from pinned host memory, never holds up a K/V block requested before it.
 constexpr int kRowsPerLoad = 64 / kItemInts;
 
 __device__ __forceinline__ Segment segment_at(int v, int i) {
@@ -329,29 +332,46 @@ __device__ __forceinline__ Segment segment_at(int v, int i) {
   return sg;
 }
 
-// Number of segments of this wave's worker.
-__device__ __forceinline__ int worker_segments(const AttnArgs& a) {
-  return as_constant(a.worker_table)[2 * size_t(blockIdx.x) + 1];
+struct WorkerRows {
+  int first;      // index of the worker's first item
+  int count;      // its items
+  Segment head;   // item 0, from the table row
+  int v;          // rows of items 1 + kRowsPerLoad * group .. (lane l: int l)
+  int group;      // the group v holds, -1 for none
+};
+
+__device__ __forceinline__ WorkerRows worker_rows(const AttnArgs& a) {
+  const const_i32_ptr wt = as_constant(a.worker_table) + size_t(blockIdx.x) * kItemInts;
+  WorkerRows w;
+  w.first = wt[0];
+  w.count = wt[1];
+  w.head.seq = wt[2];
+  w.head.kvh = wt[3];
+  w.head.pb = wt[4];
+  w.head.pe = wt[5];
+  w.head.len = wt[6];
+  w.head.slot = wt[7];
+  w.v = 0;
+  w.group = -1;
+  return w;
 }
 
-// Calls f(segment, next, has_next, index) for each of this wave's worker's
-// segments, in order; next is the following segment when it came in the same
-// load (has_next).
-template <class F>
-__device__ __forceinline__ void for_each_segment(const AttnArgs& a, F&& f) {
-  const_i32_ptr wt = as_constant(a.worker_table) + 2 * size_t(blockIdx.x);
-  const int first = wt[0];
-  const int count = wt[1];
+// Requests the group of rows that holds item i (1 <= i < count), unless held.
+__device__ __forceinline__ void request_rows(const AttnArgs& a, WorkerRows& w, int i) {
+  if (i < 1 || i >= w.count) return;
+  const int group = (i - 1) / kRowsPerLoad;
+  if (group == w.group) return;
+  const int b = 1 + group * kRowsPerLoad;
+  const int n = min(w.count - b, kRowsPerLoad);
+  const int32_t* rows = a.items + size_t(w.first + b) * kItemInts;
   const int lane = threadIdx.x;
-  for (int b = 0; b < count; b += kRowsPerLoad) {
-    const int n = min(count - b, kRowsPerLoad);
-    const int32_t* rows = a.items + size_t(first + b) * kItemInts;
-    const int v = lane < n * kItemInts ? rows[lane] : 0;
-    for (int i = 0; i < n; ++i) {
-      const bool has_next = i + 1 < n;
-      f(segment_at(v, i), segment_at(v, has_next ? i + 1 : i), has_next, b + i);
-    }
-  }
+  w.v = lane < n * kItemInts ? rows[lane] : 0;
+  w.group = group;
+}
+
+// Item i of the worker (0: the head; else its group must have been requested).
+__device__ __forceinline__ Segment worker_item(const WorkerRows& w, int i) {
+  return i == 0 ? w.head : segment_at(w.v, (i - 1) % kRowsPerLoad);
 }
 
 // Address context of a segment. When appending, the segment that ends the
@@ -459,16 +479,18 @@ __device__ __forceinline__ void flush_stash(const AttnArgs& a, const Segment& sg
   write_result<D>(a, sg, o, stash[4 * JB * 64 + lane]);
 }
 
-// One segment: pages [page_begin, page_end) of one (sequence, KV head) pair.
-// primed: its first block and query are already in flight (fetched by the
-// previous segment). Once its last block is done, a segment fetches the next
-// one's first block and query (has_next) before it stores its own result:
-// vector memory operations complete in issue order, so loads issued after
-// the stores would wait for the stores' completion too. stash (LDS, or NULL):
-// keep the result there instead of storing it (the worker stores it last).
+// One segment, item `index` of the worker: pages [page_begin, page_end) of
+// one (sequence, KV head) pair. primed: its first block and query are already
+// in flight (fetched by the previous segment). Once its first loads are out
+// it requests the row of the next item; once its last block is done, it
+// fetches the next item's first block and query before it stores its own
+// result: vector memory operations complete in issue order, so loads issued
+// after the stores would wait for the stores' completion too. stash (LDS, or
+// NULL): keep the result there instead of storing it (the worker stores it
+// last).
 template <int D, bool kAppend>
-__device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment& item, const Segment& next,
-                                               bool has_next, SegmentRegs<D>& r, bool& primed, float* stash) {
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment& item, WorkerRows& w, int index,
+                                               SegmentRegs<D>& r, bool& primed, float* stash) {
   constexpr int JB = Shape<D>::JB;
   const int lane = threadIdx.x;
   const int grp = lane >> 4;   // MFMA k-group
@@ -480,6 +502,7 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment&
   int len_pages;
   const ChunkCtx<D> c = segment_ctx<D, kAppend>(a, item, len_pages);
   if (!primed) fetch_segment_start<D, kAppend>(a, item, c, r);
+  request_rows(a, w, index + 1);
   KHalf<D>* kb_ = r.k;
   VHalf<D>* vb_ = r.v;
   const u32x4* qf = r.qf;
@@ -511,6 +534,8 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment&
     step(pg + 2, kb_[1], vb_[1], kb_[0], vb_[0]);
   }
 
+  const bool has_next = index + 1 < w.count;
+  const Segment next = worker_item(w, has_next ? index + 1 : index);
   primed = has_next && next.pb < next.pe;
   if (primed) {
     int unused;
@@ -550,13 +575,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   __shared__ float stash[(4 * Shape<D>::JB + 1) * 64];
   SegmentRegs<D> regs;
   bool primed = false;
-  Segment first = {0, 0, 0, 0, 0, -1};
-  const int count = worker_segments(a);
-  for_each_segment(a, [&](const Segment& sg, const Segment& nx, bool has_next, int index) {
-    if (index == 0) first = sg;
-    attend_segment<D, kAppend>(a, sg, nx, has_next, regs, primed, index == 0 && count > 1 ? stash : nullptr);
-  });
-  if (count > 1) flush_stash<D>(a, first, stash);
+  WorkerRows w = worker_rows(a);
+  Segment sg = w.head;
+  for (int i = 0; i < w.count; ++i) {
+    attend_segment<D, kAppend>(a, sg, w, i, regs, primed, i == 0 && w.count > 1 ? stash : nullptr);
+    if (i + 1 < w.count) sg = worker_item(w, i + 1);
+  }
+  if (w.count > 1) flush_stash<D>(a, w.head, stash);
 }
 
 // ---------------------------------------------------------------------------
@@ -673,7 +698,8 @@ __device__ __forceinline__ void widen_v(const VHalf8<D>& r, VHalf<D>& b) {
 
 // One segment over an fp8 cache; otherwise as attend_segment.
 template <int D, int R>
-__device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segment& item, float* stash) {
+__device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segment& item, WorkerRows& w, int index,
+                                                   float* stash) {
   constexpr int KB = Shape<D>::KB;
   constexpr int JB = Shape<D>::JB;
   const int lane = threadIdx.x;
@@ -720,6 +746,8 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
       qf[kb] = head_ok ? v : u32x4{0u, 0u, 0u, 0u};
     }
   }
+  // the next item's row, behind this segment's first loads
+  request_rows(a, w, index + 1);
   SoftmaxState<D> st;
 #pragma unroll
   for (int jb = 0; jb < JB; ++jb) st.o[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -774,13 +802,13 @@ template <int D>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_fp8_kernel(AttnArgs a) {
   // The worker's first result waits in LDS, as in attn_worker_kernel.
   __shared__ float stash[(4 * Shape<D>::JB + 1) * 64];
-  Segment first = {0, 0, 0, 0, 0, -1};
-  const int count = worker_segments(a);
-  for_each_segment(a, [&](const Segment& sg, const Segment&, bool, int index) {
-    if (index == 0) first = sg;
-    attend_segment_fp8<D, 3>(a, sg, index == 0 && count > 1 ? stash : nullptr);
-  });
-  if (count > 1) flush_stash<D>(a, first, stash);
+  WorkerRows w = worker_rows(a);
+  Segment sg = w.head;
+  for (int i = 0; i < w.count; ++i) {
+    attend_segment_fp8<D, 3>(a, sg, w, i, i == 0 && w.count > 1 ? stash : nullptr);
+    if (i + 1 < w.count) sg = worker_item(w, i + 1);
+  }
+  if (w.count > 1) flush_stash<D>(a, w.head, stash);
 }
 
 // ---------------------------------------------------------------------------

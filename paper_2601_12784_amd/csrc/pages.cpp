@@ -138,3 +138,23 @@ extern "C" sf_status sf_page_table_step(sf_page_pool* pool, int32_t* block_table
   }
   return SF_OK;
 }
+
+extern "C" sf_status sf_check_block_table(const sf_attn_desc* desc, const int32_t* block_table_host,
+                                          const int32_t* seq_lens_host, int32_t* bad_seq) {
+  if (bad_seq) *bad_seq = -1;
+  if (sf::validate_desc(desc) != SF_OK) return SF_ERR_INVALID_ARG;
+  if (desc->num_seqs > 0 && (!block_table_host || !seq_lens_host)) return SF_ERR_INVALID_ARG;
+  for (int32_t s = 0; s < desc->num_seqs; ++s) {
+    const int64_t len = seq_lens_host[s];
+    if (len <= 0) continue;
+    const int64_t pages = (len + sf::kPage - 1) / sf::kPage;
+    bool ok = pages <= desc->block_table_stride;
+    const int32_t* row = block_table_host + int64_t(s) * desc->block_table_stride;
+    for (int64_t j = 0; ok && j < pages; ++j) ok = row[j] >= 0 && row[j] < desc->num_pages;
+    if (!ok) {
+      if (bad_seq) *bad_seq = s;
+      return SF_ERR_INVALID_ARG;
+    }
+  }
+  return SF_OK;
+}

@@ -177,7 +177,7 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
       n_part += nseg[p];
     }
   }
-  const int64_t table_rows = (workers + 3) / 4;
+  const int64_t table_rows = workers;   // one row per worker
   if (table_rows + n_work + n_comb > INT32_MAX / kItemInts || n_part > INT32_MAX) return SF_ERR_INVALID_ARG;
   const int32_t g = desc->num_q_heads / hkv;
   info->num_workers = int32_t(workers);
@@ -254,7 +254,7 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   hi_w.next();
   for (int64_t w = 0; w < workers; ++w, lo_w.next(), hi_w.next()) {
     const int64_t lo = lo_w.q, hi = hi_w.q;
-    table[2 * w] = int32_t(row);
+    const int64_t first = row;
     int64_t cnt = 0;
     while (ps < B && pstart < hi) {
       const int64_t npg = spg[ps];
@@ -287,7 +287,11 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
       ++row;
       ++cnt;
     }
-    table[2 * w + 1] = int32_t(cnt);
+    // the worker's row: first item, item count, the first item's fields
+    int32_t* t = table + w * kItemInts;
+    t[0] = int32_t(first);
+    t[1] = int32_t(cnt);
+    if (cnt > 0) std::memcpy(t + 2, items + first * kItemInts, 6 * sizeof(int32_t));
   }
   return row == n_work ? SF_OK : SF_ERR_INVALID_ARG;
 }

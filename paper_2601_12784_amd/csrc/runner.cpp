@@ -70,7 +70,8 @@ sf_status grow_pinned(Pinned& p, uint64_t bytes) {
   return SF_OK;
 }
 
-// The workspace grows only when nothing in flight can still use it.
+// The workspace grows only when nothing in flight can still use it: growing
+// synchronizes the stream (sf_runner_reserve does it ahead of the steps).
 sf_status grow_device(void** ptr, uint64_t* have, uint64_t bytes, hipStream_t main) {
   if (*have >= bytes) return SF_OK;
   if (hipStreamSynchronize(main) != hipSuccess) return SF_ERR_HIP;
@@ -194,6 +195,8 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   hipEvent_t ev0 = extras ? static_cast<hipEvent_t>(extras->attn_start) : nullptr;
   hipEvent_t ev1 = extras ? static_cast<hipEvent_t>(extras->attn_end) : nullptr;
   if (ev0 && hipEventRecord(ev0, main) != hipSuccess) return SF_ERR_HIP;
+  // From here on a launch may have been enqueued that reads the slot, so the
+  // slot is released through its event whatever the launches return.
   if (append) {
     const char* wbase = reinterpret_cast<const char*>(work);
     st = sf::decode_attn_append_rows(desc, &info, work, q, extras->k_new, extras->v_new,
@@ -209,12 +212,35 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
     st = sf_decode_attn(desc, &info, nullptr, work, q, k_pool, v_pool, block_table, out, lse, r->workspace,
                         r->workspace_bytes, stream);
   }
-  if (st == SF_OK && ev1 && hipEventRecord(ev1, main) != hipSuccess) return SF_ERR_HIP;
+  if (st == SF_OK && ev1 && hipEventRecord(ev1, main) != hipSuccess) st = SF_ERR_HIP;
   if (st == SF_OK && !append && info.num_combine > 0)
     st = sf_decode_attn_combine(desc, &info, work, r->workspace, r->workspace_bytes, out, lse, stream);
-  if (st != SF_OK) return st;
-  if (hipEventRecord(pin.released, main) != hipSuccess) return SF_ERR_HIP;
-  pin.used = true;
+  if (hipEventRecord(pin.released, main) == hipSuccess) {
+    pin.used = true;
+  } else {
+    // Without the event nothing orders a later rewrite of the slot after
+    // this step's reads: wait for the stream instead.
+    pin.used = false;
+    (void)hipStreamSynchronize(main);
+    if (st == SF_OK) st = SF_ERR_HIP;
+  }
   ++r->steps;
+  return st;
+}
+
+extern "C" sf_status sf_runner_reserve(sf_runner* r, uint64_t workspace_bytes, uint64_t work_bytes,
+                                       int32_t max_num_seqs, void* stream) {
+  if (!r || max_num_seqs < 0) return SF_ERR_INVALID_ARG;
+  hipStream_t main = static_cast<hipStream_t>(stream);
+  sf_status st = grow_device(&r->workspace, &r->workspace_bytes, workspace_bytes, main);
+  if (st != SF_OK) return st;
+  // An appending step also keeps its new-page array (padded to 32 bytes) and
+  // copies of at most one 32-byte row per row of the work list in the slot.
+  const uint64_t slot = work_bytes + (uint64_t(max_num_seqs) * 4 + 31) / 32 * 32 + work_bytes;
+  for (auto& p : r->ring) {
+    if (p.bytes >= slot) continue;
+    if (p.used && hipEventSynchronize(p.released) != hipSuccess) return SF_ERR_HIP;
+    if ((st = grow_pinned(p, slot)) != SF_OK) return st;
+  }
   return SF_OK;
 }

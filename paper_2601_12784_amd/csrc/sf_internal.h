@@ -20,7 +20,7 @@ constexpr int kDefaultWorkersPerCu = 4;  // attention waves per CU (one per SIMD
 constexpr int kDefaultMinChunk = 8;      // pages: fewer workers rather than thinner slices
 
 sf_status validate_desc(const sf_attn_desc* d);
-inline int64_t table_rows(int64_t workers) { return (workers + 3) / 4; }
+inline int64_t table_rows(int64_t workers) { return workers; }   // worker-table rows of a plan
 uint64_t desc_key(const sf_attn_desc* d);
 uint64_t align256(uint64_t x);
 

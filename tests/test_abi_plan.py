@@ -53,7 +53,7 @@ def _plan_both(lens, hq, hkv, d, num_cus=256, chunk=0, wpc=0, mn=0, stride=None)
 
 
 def _split(info, work):
-    t = (info.num_workers + 3) // 4
+    t = info.num_workers
     return work[:t], work[t:t + info.num_work], work[t + info.num_work:]
 
 
@@ -115,7 +115,12 @@ def test_tiny_plan_by_hand():
     assert (info.num_workers, info.num_work, info.num_combine, info.num_partials, info.chunk_pages) == \
         (5, 7, 2, 5, 7)
     table, items, comb = _split(info, work)
-    assert np.array_equal(table, np.array([[0, 2, 2, 1, 3, 2, 5, 1], [6, 1, 0, 0, 0, 0, 0, 0]], np.int32))
+    # per worker: first item, count, then the first item's seq, kv_head, pages, length, slot
+    assert np.array_equal(table, np.array([[0, 2, 0, 0, 0, 2, 17, -1],
+                                           [2, 1, 2, 0, 0, 7, 130, 0],
+                                           [3, 2, 2, 0, 7, 9, 130, 1],
+                                           [5, 1, 3, 0, 5, 12, 300, 3],
+                                           [6, 1, 3, 0, 12, 19, 300, 4]], np.int32))
     expect = [[0, 0, 0, 2, 17, -1, -1, 1],
               [1, 0, 0, 4, 64, -1, -1, 1],
               [2, 0, 0, 7, 130, 0, 0, 2],
@@ -139,7 +144,9 @@ def test_plan_invariants(seed):
     hkv = 4
     info, work, _ = _plan_both(lens, 28, hkv, 128, num_cus=int(rng.integers(1, 300)))
     table, items, comb = _split(info, work)
-    tab = table.reshape(-1)[: 2 * info.num_workers].reshape(-1, 2)
+    tab = table[:, :2]
+    # each worker's row repeats the first six ints of its first item
+    assert np.array_equal(table[:, 2:], items[tab[:, 0], :6])
     pages = (lens.astype(np.int64) + PAGE - 1) // PAGE
     total = int(pages.sum()) * hkv
     W = info.num_workers

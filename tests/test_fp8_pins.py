@@ -191,3 +191,37 @@ def test_quantize_pages_places_codes_by_the_layouts():
         for dim in (0, 9, 33, 63):
             assert k8[1, 0, fp8_ref.k_offset(t, dim)] == kc[dim // 8, t, dim % 8]
             assert v8[1, 0, fp8_ref.v_offset(t, dim)] == vc[dim, t]
+
+
+@pytest.mark.parametrize("d,hkv", [(64, 1), (128, 3)])
+def test_batched_quantizer_equals_the_per_tile_one(d, hkv):
+    """quantize_pages_batched against quantize_pages, bit for bit: partial
+    pages (NaN past their valid slots), an all-zero tile, negative zeros, the
+    largest and smallest bf16 magnitudes, unlisted pages left alone, and chunk
+    edges crossed."""
+    rng = np.random.default_rng(31 + d)
+    n = 23
+
+    def draw(shape):
+        return (rng.standard_normal(shape).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+    kb = draw((n, hkv, d // 8, PAGE, 8))
+    vb = draw((n, hkv, d, PAGE))
+    pages = rng.permutation(n)[:17]
+    valid = rng.integers(1, PAGE + 1, size=pages.size)
+    for pg, nv in zip(pages, valid):
+        kb[pg, :, :, nv:, :] = 0x7FC0
+        vb[pg, :, :, nv:] = 0x7FC0
+    kb[pages[0]] = 0x8000 * (rng.random(kb[pages[0]].shape) < 0.5)   # all-zero tiles, signed zeros
+    vb[pages[1], 0, 0, 0], vb[pages[1], 0, 1, 0] = 0x7F7F, 0x0001
+    outs = []
+    for fn, kw in ((fp8_ref.quantize_pages, {}), (fp8_ref.quantize_pages_batched, {"chunk": 5})):
+        k8 = np.full((n, hkv, PAGE * d), 0xAA, np.uint8)
+        v8 = np.full((n, hkv, PAGE * d), 0xAA, np.uint8)
+        ks = np.full((n, hkv), -1.0, np.float32)
+        vs = np.full((n, hkv), -1.0, np.float32)
+        fn(kb, vb, pages, valid, k8, v8, ks, vs, **kw)
+        outs.append((k8, v8, ks, vs))
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
+    assert outs[0][2][pages[0], 0] == 1.0

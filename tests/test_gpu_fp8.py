@@ -155,24 +155,27 @@ def test_quantizer_zero_tile_and_extremes():
 
 
 def test_quantize_then_attend_end_to_end():
-    """The library's quantizer, then its fp8 attention, against the oracle's
-    quantizer and fp8 attention (the codes are compared bit for bit first)."""
+    """The library's quantizer, then its fp8 attention, on the full 32B-like
+    cache: every page's codes and scales against the oracle's quantizer bit
+    for bit, then the GPU attention over the GPU's codes against the oracle's
+    attention over the oracle's own codes."""
     batch = make_batch("gqa32b")
     pages, valid = page_fill(batch)
-    _say("fp8 quantize + attend gqa32b")
+    _say(f"fp8 quantize + attend gqa32b: {pages.size} pages")
     k8, v8, ks, vs = _quantize_gpu(batch, pages, valid)
-    sub = pages[::7]
-    rk = np.zeros(k8.shape, np.uint8)
-    rv = np.zeros(v8.shape, np.uint8)
-    rks = np.zeros(ks.shape, np.float32)
-    rvs = np.zeros(vs.shape, np.float32)
-    fp8_ref.quantize_pages(bf16_bits(batch.k_pool), bf16_bits(batch.v_pool), sub, valid[::7], rk, rv, rks, rvs)
-    assert np.array_equal(k8[sub], rk[sub]) and np.array_equal(v8[sub], rv[sub])
-    assert np.array_equal(ks[sub], rks[sub]) and np.array_equal(vs[sub], rvs[sub])
+    rk = np.full(k8.shape, 0xAA, np.uint8)
+    rv = np.full(v8.shape, 0xAA, np.uint8)
+    rks = np.full(ks.shape, -1.0, np.float32)
+    rvs = np.full(vs.shape, -1.0, np.float32)
+    fp8_ref.quantize_pages_batched(bf16_bits(batch.k_pool), bf16_bits(batch.v_pool), pages, valid, rk, rv, rks, rvs)
+    assert np.array_equal(ks, rks) and np.array_equal(vs, rvs), "scales differ"
+    assert np.array_equal(k8, rk), "key codes differ"
+    assert np.array_equal(v8, rv), "value codes differ"
 
     from paper_2601_12784_amd.workloads import Fp8Cache
-    cache = Fp8Cache(torch.from_numpy(k8), torch.from_numpy(v8), torch.from_numpy(ks), torch.from_numpy(vs))
-    out, lse, _ = run_fp8(batch, cache)
-    ro, rl = ref_fp8(batch, cache)
+    gpu_cache = Fp8Cache(torch.from_numpy(k8), torch.from_numpy(v8), torch.from_numpy(ks), torch.from_numpy(vs))
+    ref_cache = Fp8Cache(torch.from_numpy(rk), torch.from_numpy(rv), torch.from_numpy(rks), torch.from_numpy(rvs))
+    out, lse, _ = run_fp8(batch, gpu_cache)
+    ro, rl = ref_fp8(batch, ref_cache)
     assert_close(out, ro, "quantized gqa32b out")
     assert_close(lse, rl, "quantized gqa32b lse")

@@ -370,3 +370,41 @@ def test_runner_ring_reuse_with_growing_and_shrinking_plans():
         ref = run_oracle(b)
         assert_close(o, ref[0], f"ring step {i} out")
         assert_close(l, ref[1], f"ring step {i} lse")
+
+
+@pytest.mark.parametrize("reserve", [False, True])
+def test_runner_steps_in_flight_with_growing_and_shrinking_plans(reserve):
+    """Twelve runner steps enqueued back to back, with no synchronization
+    between them, on batches whose plans grow and shrink: each step plans into
+    a ring slot while earlier steps still run, waits on the slot's event, and
+    regrows slots (reserve=False) while other slots are in use. Every step
+    writes its own out and lse; one synchronization at the end, then every step
+    against the oracle. With reserve=True the runner is sized for the largest
+    batch first (sf_runner_reserve)."""
+    runner = B.DecodeAttention(28, 4, 128)
+    sizes = [3, 40, 7, 120, 1, 64, 200, 5, 90, 2, 150, 30]
+    batches = []
+    for i, nseq in enumerate(sizes):
+        rng = np.random.default_rng(1900 + i)
+        lens = np.exp(rng.normal(np.log(600), 1.0, size=nseq)).astype(np.int64).clip(0, 6000)
+        lens[rng.random(nseq) < 0.1] = 0
+        batches.append(build_batch(lens, 28, 4, 128, 1910 + i))
+    devs = [to_dev(b) for b in batches]
+    outs = [torch.full((b.num_seqs, 28, 128), float("nan"), device="cuda") for b in batches]
+    lses = [torch.full((b.num_seqs, 28), float("nan"), device="cuda") for b in batches]
+    stream = torch.cuda.Stream()
+    if reserve:
+        big = max(range(len(batches)), key=lambda i: int(batches[i].seq_lens.sum()))
+        for chunk in (None, 5):
+            runner.reserve(batches[big].seq_lens, batches[big].num_pages, batches[big].block_table.shape[1],
+                           chunk_pages=chunk, stream=stream)
+    torch.cuda.synchronize()
+    _say(f"in-flight runner steps (reserve={reserve})")
+    for i, (b, d) in enumerate(zip(batches, devs)):
+        runner(d["q"], d["k"], d["v"], d["bt"], b.seq_lens, b.scale, out=outs[i], lse=lses[i],
+               chunk_pages=(None if i % 3 else 5), stream=stream)
+    torch.cuda.synchronize()
+    for i, b in enumerate(batches):
+        ref = run_oracle(b)
+        assert_close(outs[i].cpu().numpy(), ref[0], f"in-flight step {i} out")
+        assert_close(lses[i].cpu().numpy(), ref[1], f"in-flight step {i} lse")

@@ -114,3 +114,38 @@ def test_page_table_follows_the_oracle_loop():
             assert np.array_equal(table.bt[s, :npg], ref.bt[s, :npg])
         assert table.pool.available() == ref.pool.available()
     assert reused > 0  # some steps took pages that sequences released in the same step
+
+
+def test_block_table_check_accepts_what_a_step_reads_and_names_the_first_bad_sequence():
+    """sf_check_block_table: entries 0 .. ceil(L/16) - 1 of every sequence must
+    lie in [0, num_pages); entries past that, and rows of empty sequences, are
+    never read and may hold anything."""
+    desc = B.make_desc(4, 8, 2, 128, 3, 10, 0.1)
+    bt = np.array([[0, 1, -1], [9, -7, 55], [2, 3, 4], [-1, -1, -1]], np.int32)
+    lens = np.array([17, 16, 48, 0], np.int32)
+    B.check_block_table(desc, bt, lens)                      # all in range where read
+    for s, (row, col, val) in enumerate([(0, 1, 10), (1, 0, -1), (2, 2, 10)]):
+        bad = bt.copy()
+        bad[row, col] = val
+        with pytest.raises(B.SfError) as e:
+            B.check_block_table(desc, bad, lens)
+        assert f"sequence {row}" in str(e.value) and e.value.status == 1
+    longer = lens.copy()
+    longer[2] = 49                                           # needs a 4th page: more than the stride
+    with pytest.raises(B.SfError) as e:
+        B.check_block_table(desc, bt, longer)
+    assert "sequence 2" in str(e.value)
+    # the first bad sequence is the one named
+    bad = bt.copy()
+    bad[2, 0] = 10
+    bad[0, 0] = -3
+    with pytest.raises(B.SfError) as e:
+        B.check_block_table(desc, bad, lens)
+    assert "sequence 0" in str(e.value)
+    # raw call: NULL arrays and a bad descriptor
+    L = B.lib()
+    out = ctypes.c_int32(5)
+    assert L.sf_check_block_table(ctypes.byref(desc), None, lens.ctypes.data, ctypes.byref(out)) == 1
+    assert out.value == -1
+    bad_desc = B.make_desc(4, 8, 3, 128, 3, 10, 0.1)       # 8 q heads over 3 kv heads
+    assert L.sf_check_block_table(ctypes.byref(bad_desc), bt.ctypes.data, lens.ctypes.data, None) == 1

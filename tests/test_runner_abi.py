@@ -27,6 +27,7 @@ def test_runner_rejects_bad_arguments_without_a_device():
     desc = B.make_desc(1, 4, 1, 128, 1, 1, 1.0)
     assert L.sf_runner_step(None, ctypes.byref(desc), None, None, None, None, None, None, None, None, None,
                             None) == 1
+    assert L.sf_runner_reserve(None, 0, 0, 0, None) == 1
     L.sf_runner_destroy(None)                                # a NULL runner is a no-op
 
 
