@@ -38,14 +38,15 @@ struct AppendArgs {
   int32_t num_single;
 };
 
-// Merge rows of a plan; with `app`, also the newest-token stores.
+// Merge rows of a plan; with `app`, also the newest-token stores. rows: the
+// combine rows' device copy (NULL: read them from the work list).
 CombineArgs combine_args(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,
                          void* workspace, float* out, float* lse, const AppendArgs* app, void* k_pool,
-                         void* v_pool, int32_t* block_table) {
+                         void* v_pool, int32_t* block_table, const int32_t* rows = nullptr) {
   const int32_t g = desc->num_q_heads / desc->num_kv_heads;
   Workspace ws = carve_workspace(workspace, info->num_partials, g, desc->head_dim);
   CombineArgs a = {};
-  a.items = work_dev + (table_rows(info->num_workers) + info->num_work) * kItemInts;
+  a.items = rows ? rows : work_dev + (table_rows(info->num_workers) + info->num_work) * kItemInts;
   a.num_items = info->num_combine;
   a.part_o = info->num_partials ? ws.part_o : nullptr;
   a.part_lse = info->num_partials ? ws.part_lse : nullptr;
@@ -108,7 +109,7 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
                  int32_t* work_dev, const void* q, const void* k_pool, const void* v_pool,
                  const int32_t* block_table, float* out, float* lse, void* workspace,
                  uint64_t workspace_bytes, void* stream, const AppendArgs* app,
-                 const float* k_scale = nullptr, const float* v_scale = nullptr) {
+                 const float* k_scale = nullptr, const float* v_scale = nullptr, const RowCopy* copy = nullptr) {
   sf_status st = check_step_args(desc, info, work_dev, q, k_pool, v_pool, block_table, out, lse,
                                  app ? app->k_new : nullptr, app ? app->v_new : nullptr,
                                  app ? app->new_pages : nullptr, k_scale, v_scale);
@@ -149,9 +150,16 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
   a.new_pages = app ? app->new_pages : nullptr;
   a.k_scale = k_scale;
   a.v_scale = v_scale;
+  const bool copying = copy && copy->ints > 0 && copy->ints <= int64_t(64) * info->num_workers;
+  a.copy_src = copying ? copy->src : nullptr;
+  a.copy_dst = copying ? copy->dst : nullptr;
+  a.copy_ints = copying ? copy->ints : 0;
   if ((st = from_hip(launch_attention(a, s))) != SF_OK || !app) return st;
-  const CombineArgs m = combine_args(desc, info, work_dev, workspace, out, lse, app, const_cast<void*>(k_pool),
-                                     const_cast<void*>(v_pool), const_cast<int32_t*>(block_table));
+  AppendArgs app_rows = *app;
+  if (copying && app->single_rows) app_rows.single_rows = copy->dst + int64_t(info->num_combine) * kItemInts;
+  const CombineArgs m = combine_args(desc, info, work_dev, workspace, out, lse, &app_rows,
+                                     const_cast<void*>(k_pool), const_cast<void*>(v_pool),
+                                     const_cast<int32_t*>(block_table), copying ? copy->dst : nullptr);
   return from_hip(launch_combine(m, s));
 }
 
@@ -161,13 +169,31 @@ sf_status sf::decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_in
                                       const void* q, const void* k_new, const void* v_new,
                                       const int32_t* new_pages, const int32_t* single_rows, int32_t num_single,
                                       void* k_pool, void* v_pool, int32_t* block_table, float* out, float* lse,
-                                      void* workspace, uint64_t workspace_bytes, void* stream) {
+                                      void* workspace, uint64_t workspace_bytes, void* stream,
+                                      const RowCopy* copy) {
   if (num_single < 0 || (info && num_single > info->num_work) || (num_single > 0 && !single_rows) ||
       (single_rows && !aligned16(single_rows)))
     return SF_ERR_INVALID_ARG;
   const AppendArgs app = {q, k_new, v_new, new_pages, single_rows, num_single};
   return attend(desc, info, nullptr, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
-                workspace_bytes, stream, &app);
+                workspace_bytes, stream, &app, nullptr, nullptr, copy);
+}
+
+sf_status sf::decode_attn_rows(const sf_attn_desc* desc, const sf_plan_info* info, int32_t* work_dev, const void* q,
+                               const void* k_pool, const void* v_pool, const float* k_scale, const float* v_scale,
+                               const int32_t* block_table, float* out, float* lse, void* workspace,
+                               uint64_t workspace_bytes, void* stream, const RowCopy* copy, void* after_attention) {
+  sf_status st = attend(desc, info, nullptr, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
+                        workspace_bytes, stream, nullptr, k_scale, v_scale, copy);
+  if (st != SF_OK) return st;
+  if (after_attention &&
+      hipEventRecord(static_cast<hipEvent_t>(after_attention), static_cast<hipStream_t>(stream)) != hipSuccess)
+    return SF_ERR_HIP;
+  if (info->num_workers == 0 || info->num_combine == 0) return st;
+  const bool copying = copy && copy->ints > 0 && copy->ints <= int64_t(64) * info->num_workers;
+  const CombineArgs a = combine_args(desc, info, work_dev, workspace, out, lse, nullptr, nullptr, nullptr, nullptr,
+                                     copying ? copy->dst : nullptr);
+  return from_hip(launch_combine(a, static_cast<hipStream_t>(stream)));
 }
 
 sf_status sf::decode_attn_and_combine(const sf_attn_desc* desc, const sf_plan_info* info, const int32_t* work_dev,

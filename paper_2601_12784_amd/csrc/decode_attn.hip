@@ -338,7 +338,23 @@ struct WorkerRows {
   Segment head;   // item 0, from the table row
   int v;          // rows of items 1 + kRowsPerLoad * group .. (lane l: int l)
   int group;      // the group v holds, -1 for none
+  int copy_val;   // the launch's side job (AttnArgs::copy_*): this lane's int
 };
+
+// The side job: this worker's 64 ints of the merge rows, requested once its
+// first segment's first loads are out (like the work-list rows) and stored
+// after its last result.
+__device__ __forceinline__ bool copies_rows(const AttnArgs& a) {
+  return a.copy_dst != nullptr && int(blockIdx.x) * 64 + int(threadIdx.x) < a.copy_ints;
+}
+
+__device__ __forceinline__ void row_copy_load(const AttnArgs& a, WorkerRows& w) {
+  if (copies_rows(a)) w.copy_val = a.copy_src[int(blockIdx.x) * 64 + int(threadIdx.x)];
+}
+
+__device__ __forceinline__ void row_copy_store(const AttnArgs& a, const WorkerRows& w) {
+  if (copies_rows(a)) a.copy_dst[int(blockIdx.x) * 64 + int(threadIdx.x)] = w.copy_val;
+}
 
 __device__ __forceinline__ WorkerRows worker_rows(const AttnArgs& a) {
   const const_i32_ptr wt = as_constant(a.worker_table) + size_t(blockIdx.x) * kItemInts;
@@ -353,6 +369,7 @@ __device__ __forceinline__ WorkerRows worker_rows(const AttnArgs& a) {
   w.head.slot = wt[7];
   w.v = 0;
   w.group = -1;
+  w.copy_val = 0;
   return w;
 }
 
@@ -503,6 +520,7 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment&
   const ChunkCtx<D> c = segment_ctx<D, kAppend>(a, item, len_pages);
   if (!primed) fetch_segment_start<D, kAppend>(a, item, c, r);
   request_rows(a, w, index + 1);
+  if (index == 0) row_copy_load(a, w);
   KHalf<D>* kb_ = r.k;
   VHalf<D>* vb_ = r.v;
   const u32x4* qf = r.qf;
@@ -582,6 +600,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     if (i + 1 < w.count) sg = worker_item(w, i + 1);
   }
   if (w.count > 1) flush_stash<D>(a, w.head, stash);
+  row_copy_store(a, w);
 }
 
 // ---------------------------------------------------------------------------
@@ -746,8 +765,9 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
       qf[kb] = head_ok ? v : u32x4{0u, 0u, 0u, 0u};
     }
   }
-  // the next item's row, behind this segment's first loads
+  // the next item's row (and the side job), behind this segment's first loads
   request_rows(a, w, index + 1);
+  if (index == 0) row_copy_load(a, w);
   SoftmaxState<D> st;
 #pragma unroll
   for (int jb = 0; jb < JB; ++jb) st.o[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -809,6 +829,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     if (i + 1 < w.count) sg = worker_item(w, i + 1);
   }
   if (w.count > 1) flush_stash<D>(a, w.head, stash);
+  row_copy_store(a, w);
 }
 
 // ---------------------------------------------------------------------------

@@ -154,8 +154,11 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   //    ended); grow it and plan again only if the plan does not fit
   Pinned& pin = r->ring[r->steps % kRing];
   if (pin.used && hipEventSynchronize(pin.released) != hipSuccess) return SF_ERR_HIP;
-  // Appending: new_pages (padded to 32 bytes), then copies of the rows the
-  // merge launch acts on (pairs with one segment and len > 0), at most one per item.
+  // Appending: after the work list, copies of the rows the merge launch acts
+  // on (pairs with one segment and len > 0, at most one per item), then
+  // new_pages. The work list ends with the combine rows, so the merge
+  // launch's rows are one contiguous range, which the attention launch
+  // copies to device memory (RowCopy).
   const uint64_t pages_bytes = append ? (uint64_t(desc->num_seqs) * 4 + 31) / 32 * 32 : 0;
   // An fp8 block moves half the bytes of a bf16 one: unless the caller chose,
   // fp8 steps plan two waves per SIMD (measured: kernel 129 us instead of 136
@@ -164,32 +167,42 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   if (fp8 && opts.workers_per_cu == 0) opts.workers_per_cu = kFp8WorkersPerCu;
   sf_plan_info info;
   sf_status st = sf_decode_attn_plan(desc, seq_lens_host, &opts, pin.ptr, pin.bytes, &info);
-  auto need = [&]() { return info.work_bytes + (append ? pages_bytes + uint64_t(info.num_work) * 32 : 0); };
+  auto need = [&]() { return info.work_bytes + (append ? uint64_t(info.num_work) * 32 + pages_bytes : 0); };
   if (st == SF_ERR_CAPACITY || (st == SF_OK && pin.bytes < need())) {
     if ((st = grow_pinned(pin, need())) != SF_OK) return st;
     st = sf_decode_attn_plan(desc, seq_lens_host, &opts, pin.ptr, pin.bytes, &info);
   }
   if (st != SF_OK) return st;
   int32_t num_single = 0;
+  uint64_t pages_off = info.work_bytes;
   if (append && desc->num_seqs > 0) {
     if (!extras->new_pages_host) return SF_ERR_INVALID_ARG;
     char* base = reinterpret_cast<char*>(pin.ptr);
-    std::memcpy(base + info.work_bytes, extras->new_pages_host, uint64_t(desc->num_seqs) * 4);
     const int32_t* items = pin.ptr + sf::table_rows(info.num_workers) * sf::kItemInts;
-    int32_t* singles = reinterpret_cast<int32_t*>(base + info.work_bytes + pages_bytes);
+    int32_t* singles = reinterpret_cast<int32_t*>(base + info.work_bytes);
     for (int32_t i = 0; i < info.num_work; ++i) {
       const int32_t* row = items + int64_t(i) * sf::kItemInts;
       if (row[7] == 1 && row[4] > 0)
         std::memcpy(singles + int64_t(num_single++) * sf::kItemInts, row, sf::kItemInts * 4);
     }
+    pages_off = info.work_bytes + uint64_t(num_single) * 32;
+    std::memcpy(base + pages_off, extras->new_pages_host, uint64_t(desc->num_seqs) * 4);
   }
   if (info_out) *info_out = info;
   r->last = info;
   if (info.num_workers == 0) return SF_OK;
 
-  // 2. workspace (grown only while idle)
-  if ((st = grow_device(&r->workspace, &r->workspace_bytes, info.workspace_bytes, main)) != SF_OK) return st;
+  // 2. workspace (grown only while idle): the partial results, then the
+  //    device copy of the merge launch's rows
+  const uint64_t rows_off = sf::align256(info.workspace_bytes);
+  const int64_t copy_rows = int64_t(info.num_combine) + (append ? num_single : 0);
+  if ((st = grow_device(&r->workspace, &r->workspace_bytes, rows_off + uint64_t(copy_rows) * 32, main)) != SF_OK)
+    return st;
   int32_t* work = const_cast<int32_t*>(pin.dev);
+  const sf::RowCopy copy = {work + (sf::table_rows(info.num_workers) + info.num_work) * sf::kItemInts,
+                            reinterpret_cast<int32_t*>(static_cast<char*>(r->workspace) + rows_off),
+                            int32_t(copy_rows * sf::kItemInts)};
+  const sf::RowCopy* cp = copy_rows > 0 ? &copy : nullptr;
 
   // 3. kernels on the caller's stream (optionally bracketed by the caller's events)
   hipEvent_t ev0 = extras ? static_cast<hipEvent_t>(extras->attn_start) : nullptr;
@@ -200,21 +213,17 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   if (append) {
     const char* wbase = reinterpret_cast<const char*>(work);
     st = sf::decode_attn_append_rows(desc, &info, work, q, extras->k_new, extras->v_new,
-                                     reinterpret_cast<const int32_t*>(wbase + info.work_bytes),
-                                     reinterpret_cast<const int32_t*>(wbase + info.work_bytes + pages_bytes),
-                                     num_single, const_cast<void*>(k_pool), const_cast<void*>(v_pool),
+                                     reinterpret_cast<const int32_t*>(wbase + pages_off),
+                                     reinterpret_cast<const int32_t*>(wbase + info.work_bytes), num_single,
+                                     const_cast<void*>(k_pool), const_cast<void*>(v_pool),
                                      const_cast<int32_t*>(block_table), out, lse, r->workspace,
-                                     r->workspace_bytes, stream);
-  } else if (fp8) {
-    st = sf_decode_attn_fp8(desc, &info, nullptr, work, q, k_pool, v_pool, extras->k_scale, extras->v_scale,
-                            block_table, out, lse, r->workspace, r->workspace_bytes, stream);
+                                     r->workspace_bytes, stream, cp);
+    if (st == SF_OK && ev1 && hipEventRecord(ev1, main) != hipSuccess) st = SF_ERR_HIP;
   } else {
-    st = sf_decode_attn(desc, &info, nullptr, work, q, k_pool, v_pool, block_table, out, lse, r->workspace,
-                        r->workspace_bytes, stream);
+    st = sf::decode_attn_rows(desc, &info, work, q, k_pool, v_pool, fp8 ? extras->k_scale : nullptr,
+                              fp8 ? extras->v_scale : nullptr, block_table, out, lse, r->workspace,
+                              r->workspace_bytes, stream, cp, ev1);
   }
-  if (st == SF_OK && ev1 && hipEventRecord(ev1, main) != hipSuccess) st = SF_ERR_HIP;
-  if (st == SF_OK && !append && info.num_combine > 0)
-    st = sf_decode_attn_combine(desc, &info, work, r->workspace, r->workspace_bytes, out, lse, stream);
   if (hipEventRecord(pin.released, main) == hipSuccess) {
     pin.used = true;
   } else {
@@ -232,7 +241,8 @@ extern "C" sf_status sf_runner_reserve(sf_runner* r, uint64_t workspace_bytes, u
                                        int32_t max_num_seqs, void* stream) {
   if (!r || max_num_seqs < 0) return SF_ERR_INVALID_ARG;
   hipStream_t main = static_cast<hipStream_t>(stream);
-  sf_status st = grow_device(&r->workspace, &r->workspace_bytes, workspace_bytes, main);
+  // partials, then the merge rows' device copy (at most the work list's size)
+  sf_status st = grow_device(&r->workspace, &r->workspace_bytes, sf::align256(workspace_bytes) + work_bytes, main);
   if (st != SF_OK) return st;
   // An appending step also keeps its new-page array (padded to 32 bytes) and
   // copies of at most one 32-byte row per row of the work list in the slot.

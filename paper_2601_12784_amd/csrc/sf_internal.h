@@ -58,6 +58,19 @@ struct AttnArgs {
   // hold E4M3 codes, and these the per-(page, KV head) scales.
   const float* k_scale;
   const float* v_scale;
+  // Optional side job: copy_ints ints from copy_src (the merge rows in
+  // pinned host memory) to copy_dst (device), 64 per worker, so that the
+  // launch after this one reads its rows from device memory. NULL dst: none.
+  const int32_t* copy_src;
+  int32_t* copy_dst;
+  int32_t copy_ints;
+};
+
+// The row copy an attention launch makes for the merge launch after it.
+struct RowCopy {
+  const int32_t* src;   // device-accessible (mapped pinned host memory)
+  int32_t* dst;         // device memory
+  int32_t ints;         // at most 64 per worker
 };
 
 struct CombineArgs {
@@ -150,12 +163,24 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 
 // sf_decode_attn_append with the merge launch restricted to single_rows
 // (num_single copies, in work-item format, of the rows of pairs that have one
-// segment and len > 0; device-accessible). The native runner's path.
+// segment and len > 0; device-accessible). The native runner's path. With
+// `copy`, the attention launch copies the merge rows to copy->dst (the plan's
+// combine rows, then the single rows) and the merge launch reads them there.
 sf_status decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_info* info, int32_t* work_dev,
                                   const void* q, const void* k_new, const void* v_new, const int32_t* new_pages,
                                   const int32_t* single_rows, int32_t num_single, void* k_pool, void* v_pool,
                                   int32_t* block_table, float* out, float* lse, void* workspace,
-                                  uint64_t workspace_bytes, void* stream);
+                                  uint64_t workspace_bytes, void* stream, const RowCopy* copy);
+
+// sf_decode_attn (k_scale NULL) or sf_decode_attn_fp8, then the combine of
+// split pairs, on a device-resident or mapped work list; with `copy`, the
+// attention launch copies the plan's combine rows to copy->dst and the
+// combine launch reads them there. The native runner's other path.
+// after_attention (a hipEvent_t, may be NULL) is recorded between the two.
+sf_status decode_attn_rows(const sf_attn_desc* desc, const sf_plan_info* info, int32_t* work_dev, const void* q,
+                           const void* k_pool, const void* v_pool, const float* k_scale, const float* v_scale,
+                           const int32_t* block_table, float* out, float* lse, void* workspace,
+                           uint64_t workspace_bytes, void* stream, const RowCopy* copy, void* after_attention);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream);
 
 // Every host-side check of a decode step's arguments except the workspace
