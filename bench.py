@@ -579,11 +579,90 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
     return doc
 
 
+EXTEND_COUNTERS = {
+    "SQ_INSTS_MFMA": "matrix-core instructions (all waves)",
+    "SQ_INSTS_VALU": "vector ALU instructions, matrix-core ones included",
+    "SQ_INSTS_VALU_TRANS_F32": "transcendental (exp2) instructions",
+    "SQ_INSTS_LDS": "LDS instructions",
+    "SQ_INSTS_SALU": "scalar ALU instructions",
+    "SQ_VALU_MFMA_BUSY_CYCLES": "matrix-core busy cycles, summed over SIMDs",
+    "SQ_VALU_MFMA_COEXEC_CYCLES": "cycles with vector ALU and matrix core both busy, summed over SIMDs",
+    "SQ_BUSY_CYCLES": "sequencer busy cycles",
+    "SQ_WAVE_CYCLES": "wave-cycles (units of 4 cycles)",
+    "SQ_ACTIVE_INST_VALU": "wave-cycles issuing vector ALU work (units of 4 cycles)",
+    "SQ_ACTIVE_INST_LDS": "wave-cycles issuing LDS work (units of 4 cycles)",
+    "SQ_WAIT_INST_ANY": "wave-cycles waiting on a dependency (units of 4 cycles)",
+    "SQ_WAIT_INST_LDS": "wave-cycles waiting on LDS (units of 4 cycles)",
+    "SQ_LDS_IDX_ACTIVE": "LDS busy cycles",
+    "SQ_LDS_BANK_CONFLICT": "LDS bank-conflict cycles",
+    "SQ_BUSY_CU_CYCLES": "CU busy cycles",
+}
+
+
+def summarize_extend_counters(csvs, stats_csv, command, out_md, simds=1024, clock_ghz=2.4):
+    """Markdown summary of rocprofv3 --pmc passes over the re-prefill leg:
+    per-launch means of the counters in EXTEND_COUNTERS and what they say
+    about the extend kernel's bound (matrix-core busy share, vector work,
+    their overlap)."""
+    import collections
+    vals = collections.defaultdict(list)
+    for path in csvs:
+        for r in _csv_rows(path):
+            if EXTEND_KERNEL.split("<")[0] in r["Kernel_Name"]:
+                vals[r["Counter_Name"]].append(float(r["Counter_Value"]))
+    mean = {k: sum(v) / len(v) for k, v in vals.items()}
+    kt = [r for r in _csv_rows(stats_csv) if EXTEND_KERNEL.split("<")[0] in r["Name"]]
+    us = float(kt[0]["AverageNs"]) / 1e3 if kt else float("nan")
+    simd_cycles = us * 1e-6 * clock_ghz * 1e9 * simds
+    lines = [f"# Counters: {EXTEND_KERNEL} on the full re-prefill batch", "",
+             "Commands (from the repository root; one counter pass per line, then the kernel trace):", "", "```"]
+    lines += command.split(" ;; ") + ["```", "",
+             "($REPO: the repository root; $OUT: any directory for the profiler's output.)", "",
+             f"Kernel source sha256[:16]: `{kernel_source_hash(EXTEND_SRC)}`; mean kernel duration {us:.1f} us "
+             f"(rocprofv3 trace); {simds} SIMDs at {clock_ghz} GHz = {simd_cycles:.3e} SIMD-cycles per launch.", "",
+             "| counter | per launch | meaning |", "|---|---|---|"]
+    for k, what in EXTEND_COUNTERS.items():
+        if k in mean:
+            lines.append(f"| `{k}` | {mean[k]:.4e} | {what} |")
+    if {"SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_MFMA", "SQ_INSTS_VALU"} <= mean.keys():
+        mf = mean["SQ_VALU_MFMA_BUSY_CYCLES"]
+        valu = mean["SQ_INSTS_VALU"] - mean["SQ_INSTS_MFMA"]
+        trans = mean.get("SQ_INSTS_VALU_TRANS_F32", 0.0)
+        co = mean.get("SQ_VALU_MFMA_COEXEC_CYCLES", float("nan"))
+        lines += ["", "Derived:", "",
+                  f"- matrix-core busy: {mf / simd_cycles:.1%} of SIMD-cycles "
+                  f"({mf / mean['SQ_INSTS_MFMA']:.1f} cycles per MFMA instruction)",
+                  f"- vector ALU instructions besides MFMA: {valu:.3e}, of which exp2 {trans:.3e}; "
+                  f"{valu / mean['SQ_INSTS_MFMA']:.2f} per MFMA",
+                  f"- vector ALU and matrix core busy together: {co / simd_cycles:.1%} of SIMD-cycles"]
+        if "SQ_WAVE_CYCLES" in mean and "SQ_WAIT_INST_ANY" in mean:
+            lines.append(f"- waves waiting on a dependency: {mean['SQ_WAIT_INST_ANY'] / mean['SQ_WAVE_CYCLES']:.1%} "
+                         f"of wave time (LDS: {mean.get('SQ_WAIT_INST_LDS', 0) / mean['SQ_WAVE_CYCLES']:.1%})")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def summarize_trace(stats_csv, command, out_md, bench_json=None):
     """Markdown summary of a rocprofv3 --kernel-trace --stats run (the decode
-    step, or the re-prefill leg when the bench line is an --only-reprefill one)."""
+    step, the re-prefill leg when the bench line is an --only-reprefill one,
+    or a named workload's step for an --only-config one)."""
     rows = _csv_rows(stats_csv)
     b = json.load(open(bench_json)) if bench_json else None
+    if b is not None and "pool_copies_rotated" in b:
+        lines = [f"# Kernel trace: the decode step on {b['workload']}", "", "Command (from the repository root):",
+                 "", "```", command, "```", "", f"Kernel source sha256[:16]: `{kernel_source_hash()}`", "",
+                 "| kernel | calls | average us | min us | max us | share % |", "|---|---|---|---|---|---|"]
+        for r in rows:
+            lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                         f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+        lines += ["", "bench.py line of the same run (HIP events on the kernel's stream):", "",
+                  f"- attention kernel mean: {b['attn_kernel_us']} us for {b['kv_bytes_per_step']} bytes of K and V "
+                  f"= {b['kv_gb_per_s_kernel']} GB/s ({b['pct_of_peak_hbm_kernel']} % of 8000)",
+                  f"- step: {b['ms_per_step'] * 1e3:.1f} us; {b['seq_steps_per_s']} seq-steps/s; "
+                  f"{b['pool_copies_rotated']} pool copies rotated"]
+        with open(out_md, "w") as f:
+            f.write("\n".join(lines) + "\n")
+        return
     reprefill = b is not None and "causal_flops" in b
     fp8 = (not reprefill and b is not None and "fp8" in b
            and any("attn_worker_fp8_kernel" in r["Name"] for r in rows))
@@ -634,6 +713,9 @@ def main():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the tiny, 7B-like, 32B-like and pre-filled straggler legs")
     ap.add_argument("--only-reprefill", action="store_true", help="run only the extend leg and print it")
+    ap.add_argument("--only-config", default=None, help="run only this named workload's leg and print it")
+    ap.add_argument("--summarize-extend-counters", nargs="+", metavar="FILE",
+                    help="PMC_CSV... STATS_CSV COMMANDS OUT_MD: counters summary of the re-prefill leg")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -651,6 +733,10 @@ def main():
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace, bench_json=args.bench_json)
         return
+    if args.summarize_extend_counters:
+        *pmc, stats, cmd, out = args.summarize_extend_counters
+        summarize_extend_counters(pmc, stats, cmd, out)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "bench.py measures a single GPU (the decode path runs on one device); --gpus must be 1"}))
         log("bench.py runs on exactly one GPU: the decode-attention path here is single-GPU "
@@ -667,6 +753,9 @@ def main():
 
     if args.only_reprefill:
         print(json.dumps(reprefill_bench()), flush=True)
+        return
+    if args.only_config:
+        print(json.dumps(config_bench(args.only_config, args.steps, args.warmup)), flush=True)
         return
 
     if args.copy_probe:
