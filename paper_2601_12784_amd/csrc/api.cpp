@@ -156,7 +156,8 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
   a.copy_ints = copying ? copy->ints : 0;
   if ((st = from_hip(launch_attention(a, s))) != SF_OK || !app) return st;
   AppendArgs app_rows = *app;
-  if (copying && app->single_rows) app_rows.single_rows = copy->dst + int64_t(info->num_combine) * kItemInts;
+  if (copying && app->single_rows && copy->single_off >= 0) app_rows.single_rows = copy->dst + copy->single_off;
+  if (copying && app->new_pages && copy->pages_off >= 0) app_rows.new_pages = copy->dst + copy->pages_off;
   const CombineArgs m = combine_args(desc, info, work_dev, workspace, out, lse, &app_rows,
                                      const_cast<void*>(k_pool), const_cast<void*>(v_pool),
                                      const_cast<int32_t*>(block_table), copying ? copy->dst : nullptr);

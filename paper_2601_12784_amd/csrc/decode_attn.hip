@@ -118,8 +118,7 @@ struct ChunkCtx {
   int pe;             // end of this segment (pages)
   int k_off;          // element offset of this lane's K piece inside a tile
   int v_off;          // element offset of this lane's V^T piece inside a tile
-  int last_idx;       // appending: logical page of the newest token (-1: none)
-  const_i32_ptr fresh;  // appending: that token's entry of new_pages (or NULL)
+  int empty_idx;      // appending: logical page that holds only the newest token (-1: none)
 };
 
 // Physical pages of the two-page block at logical page pg (a single page if
@@ -128,16 +127,14 @@ struct PagePair {
   int p0, p1;
 };
 // When appending, the newest token's page may be new in this very step and
-// not yet in the block table: it comes from the launch's arguments.
-// Looked up only when that block is prefetched, so the extra load overlaps
-// the previous block's work.
+// not yet in the block table. This pass leaves that token out, so a page
+// that holds only it (the token opened the page) has no slot to read: it is
+// replaced by a page already in the table (the one before it, or pool page 0
+// for a one-token sequence), whose loads the block's token count masks.
 template <int D, bool kAppend>
 __device__ __forceinline__ int page_of(const ChunkCtx<D>& c, int pg) {
   if constexpr (kAppend) {
-    if (pg == c.last_idx && c.fresh) {
-      const int p = *c.fresh;
-      if (p >= 0) return p;
-    }
+    if (pg == c.empty_idx) return pg > 0 ? c.bt[pg - 1] : 0;
   }
   return c.bt[pg];
 }
@@ -394,8 +391,8 @@ __device__ __forceinline__ Segment worker_item(const WorkerRows& w, int i) {
 // Address context of a segment. When appending, the segment that ends the
 // sequence leaves the newest token (index len - 1, not yet in the pool) out:
 // its pages hold tokens [0, len_pages), and the merge launch that follows
-// adds the newest one. Its page may be new in this step, so the page comes
-// from new_pages.
+// adds the newest one (its page may be new in this step: the merge launch
+// takes it from new_pages and stores the token there).
 template <int D, bool kAppend>
 __device__ __forceinline__ ChunkCtx<D> segment_ctx(const AttnArgs& a, const Segment& sg, int& len_pages) {
   const int lane = threadIdx.x;
@@ -412,13 +409,11 @@ __device__ __forceinline__ ChunkCtx<D> segment_ctx(const AttnArgs& a, const Segm
   c.k_off = k_elem(col, 8 * grp, D);
   // V operand: A-row = dim col (+16*jb), k-group grp = slots 4*grp .. +3.
   c.v_off = v_elem(4 * grp, col);
-  c.last_idx = -1;
-  c.fresh = nullptr;
+  c.empty_idx = -1;
   len_pages = sg.len;
   if constexpr (kAppend) {
     if (sg.len > 0 && sg.pe == (sg.len + kPage - 1) / kPage) {
-      c.last_idx = (sg.len - 1) / kPage;
-      c.fresh = a.new_pages ? as_constant(a.new_pages) + sg.seq : nullptr;
+      if ((sg.len - 1) % kPage == 0) c.empty_idx = (sg.len - 1) / kPage;
       len_pages = sg.len - 1;
     }
   }
@@ -972,6 +967,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) { merge_row
 // single-segment pairs.
 template <int D>
 __global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
+  constexpr int kPerThread = (kMaxGroup * (D / 4) + 255) / 256;   // (head, 4 dims) items per thread, at most
   __shared__ float z_new[kMaxGroup];
   const bool split = int(blockIdx.x) < a.num_items;
   const const_i32_ptr rest = a.single_rows ? as_constant(a.single_rows) : as_constant(a.work_items);
@@ -985,6 +981,35 @@ __global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
   if (!split && (row[7] != 1 || len <= 0)) return;   // split pairs come through their merge row
   const int g = a.group;
   const size_t new_row = (size_t(seq) * a.num_kv_heads + kvh) * D;
+  const int d4n = D / 4;
+
+  // Everything that depends on the row alone is requested first: the token's
+  // page (wave 0 stores the token), and this thread's first-pass result and
+  // new value; the score of the newest token and the block barrier follow.
+  const int t = len - 1;
+  const size_t entry = size_t(seq) * a.bt_stride + t / kPage;
+  const int fresh = a.new_pages ? as_constant(a.new_pages)[seq] : -1;
+  const int page = fresh >= 0 ? fresh : as_constant(a.block_table)[entry];
+  f32x4 acc0[kPerThread];
+  float l0[kPerThread];
+  u32x2 vv[kPerThread];
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int idx = int(threadIdx.x) + 256 * i;
+    acc0[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    l0[i] = 0.f;
+    vv[i] = u32x2{0u, 0u};
+    if (idx < g * d4n) {
+      const int h = idx / d4n;
+      const int d4 = idx - h * d4n;
+      const size_t orow = size_t(seq) * a.num_q_heads + kvh * g + h;
+      if (!split) {
+        acc0[i] = *reinterpret_cast<const f32x4*>(a.out + orow * D + 4 * d4);
+        l0[i] = a.lse[orow];
+      }
+      vv[i] = *reinterpret_cast<const u32x2*>(a.v_new + new_row + 4 * d4);
+    }
+  }
 
   // z for each query head of the group: 16 lanes per head, 8 dims each.
   {
@@ -1008,8 +1033,10 @@ __global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
   }
   __syncthreads();
 
-  const int d4n = D / 4;
-  for (int idx = threadIdx.x; idx < g * d4n; idx += blockDim.x) {
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int idx = int(threadIdx.x) + 256 * i;
+    if (idx >= g * d4n) break;
     const int h = idx / d4n;
     const int d4 = idx - h * d4n;
     const int head = kvh * g + h;
@@ -1019,13 +1046,12 @@ __global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
     if (split) {
       merge_partials(a, base, n, h, d4, mx, wsum, acc);
     } else {
-      acc = *reinterpret_cast<const f32x4*>(out);
-      mx = a.lse[size_t(seq) * a.num_q_heads + head] * kLog2e;   // -inf if the pages held no token
+      acc = acc0[i];
+      mx = l0[i] * kLog2e;   // -inf if the pages held no token
       wsum = 1.f;
     }
-    const u32x2 vv = *reinterpret_cast<const u32x2*>(a.v_new + new_row + 4 * d4);
-    const f32x4 v = {bf16_value(vv[0] & 0xFFFFu), bf16_value(vv[0] >> 16), bf16_value(vv[1] & 0xFFFFu),
-                     bf16_value(vv[1] >> 16)};
+    const f32x4 v = {bf16_value(vv[i][0] & 0xFFFFu), bf16_value(vv[i][0] >> 16), bf16_value(vv[i][1] & 0xFFFFu),
+                     bf16_value(vv[i][1] >> 16)};
     const float z = z_new[h];
     const float m = fmaxf(mx, z);
     const float a1 = fast_exp2(mx - m);
@@ -1037,10 +1063,6 @@ __global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
 
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
-    const int t = len - 1;
-    const int fresh = a.new_pages ? as_constant(a.new_pages)[seq] : -1;
-    const size_t entry = size_t(seq) * a.bt_stride + t / kPage;
-    const int page = fresh >= 0 ? fresh : as_constant(a.block_table)[entry];
     store_token<D>(a.k_dst, a.v_dst, a.k_new, a.v_new, a.num_kv_heads, seq, kvh, page, t % kPage, lane);
     if (fresh >= 0 && kvh == 0 && lane == 0) a.bt_dst[entry] = fresh;
   }

@@ -193,16 +193,19 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
   if (info.num_workers == 0) return SF_OK;
 
   // 2. workspace (grown only while idle): the partial results, then the
-  //    device copy of the merge launch's rows
+  //    device copy of what the merge launch reads from the ring: the combine
+  //    rows and, appending, the single rows and new_pages (contiguous there)
   const uint64_t rows_off = sf::align256(info.workspace_bytes);
-  const int64_t copy_rows = int64_t(info.num_combine) + (append ? num_single : 0);
-  if ((st = grow_device(&r->workspace, &r->workspace_bytes, rows_off + uint64_t(copy_rows) * 32, main)) != SF_OK)
+  const int64_t rows_ints = (int64_t(info.num_combine) + (append ? num_single : 0)) * sf::kItemInts;
+  const int64_t copy_ints = rows_ints + (append && desc->num_seqs > 0 ? int64_t(pages_bytes / 4) : 0);
+  if ((st = grow_device(&r->workspace, &r->workspace_bytes, rows_off + uint64_t(copy_ints) * 4, main)) != SF_OK)
     return st;
   int32_t* work = const_cast<int32_t*>(pin.dev);
   const sf::RowCopy copy = {work + (sf::table_rows(info.num_workers) + info.num_work) * sf::kItemInts,
                             reinterpret_cast<int32_t*>(static_cast<char*>(r->workspace) + rows_off),
-                            int32_t(copy_rows * sf::kItemInts)};
-  const sf::RowCopy* cp = copy_rows > 0 ? &copy : nullptr;
+                            int32_t(copy_ints), append ? int32_t(info.num_combine) * sf::kItemInts : -1,
+                            append && desc->num_seqs > 0 ? int32_t(rows_ints) : -1};
+  const sf::RowCopy* cp = copy_ints > 0 ? &copy : nullptr;
 
   // 3. kernels on the caller's stream (optionally bracketed by the caller's events)
   hipEvent_t ev0 = extras ? static_cast<hipEvent_t>(extras->attn_start) : nullptr;
@@ -241,12 +244,16 @@ extern "C" sf_status sf_runner_reserve(sf_runner* r, uint64_t workspace_bytes, u
                                        int32_t max_num_seqs, void* stream) {
   if (!r || max_num_seqs < 0) return SF_ERR_INVALID_ARG;
   hipStream_t main = static_cast<hipStream_t>(stream);
-  // partials, then the merge rows' device copy (at most the work list's size)
-  sf_status st = grow_device(&r->workspace, &r->workspace_bytes, sf::align256(workspace_bytes) + work_bytes, main);
+  // partials, then the device copy of the merge rows (at most the work
+  // list's size) and new_pages
+  sf_status st = grow_device(&r->workspace, &r->workspace_bytes,
+                             sf::align256(workspace_bytes) + work_bytes + (uint64_t(max_num_seqs) * 4 + 31) / 32 * 32,
+                             main);
   if (st != SF_OK) return st;
   // An appending step also keeps its new-page array (padded to 32 bytes) and
   // copies of at most one 32-byte row per row of the work list in the slot.
-  const uint64_t slot = work_bytes + (uint64_t(max_num_seqs) * 4 + 31) / 32 * 32 + work_bytes;
+  const uint64_t pages = (uint64_t(max_num_seqs) * 4 + 31) / 32 * 32;
+  const uint64_t slot = work_bytes + pages + work_bytes;
   for (auto& p : r->ring) {
     if (p.bytes >= slot) continue;
     if (p.used && hipEventSynchronize(p.released) != hipSuccess) return SF_ERR_HIP;

@@ -66,11 +66,15 @@ struct AttnArgs {
   int32_t copy_ints;
 };
 
-// The row copy an attention launch makes for the merge launch after it.
+// The row copy an attention launch makes for the merge launch after it:
+// the plan's combine rows, then (appending) the single-segment rows at int
+// single_off and new_pages at int pages_off of dst (-1: not in the copy).
 struct RowCopy {
   const int32_t* src;   // device-accessible (mapped pinned host memory)
   int32_t* dst;         // device memory
   int32_t ints;         // at most 64 per worker
+  int32_t single_off;
+  int32_t pages_off;
 };
 
 struct CombineArgs {
