@@ -75,21 +75,25 @@ class Stepper:
                     chunk_pages=self.chunk, stream=self.stream, attn_events=ev_attn, fp8=self.fp8)
 
 
-EVENT_EVERY = 8  # timing events bracket the attention kernel of every 8th timed step
+EVENT_EVERY = 16  # timing events take the attention kernel of every 16th timed step
 
 
 def time_steps(stepper, steps, warmup, every=EVENT_EVERY):
     """Times `steps` decode steps after `warmup` untimed ones.
     Returns (wall ms per step, mean and median attention-kernel ms from HIP
-    events). The events are recorded on the kernel's own stream around every
-    `every`-th timed step only: a timing event costs a few microseconds of
-    queue time, which would otherwise be charged to every step."""
+    events). The events take the kernel's own start and end times (the
+    library launches it with them, so no queue time is counted) on every
+    `every`-th timed step only, which keeps whatever a timed dispatch costs
+    off the other steps."""
     torch = stepper.torch
+    sampled = range(0, steps, max(1, every))
+    evs = {i: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for i in sampled}
+    for a, b in evs.values():           # torch creates an event on its first record: not in the timed region
+        a.record(stepper.stream)
+        b.record(stepper.stream)
     for _ in range(warmup):
         stepper.step()
     torch.cuda.synchronize()
-    sampled = range(0, steps, max(1, every))
-    evs = {i: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for i in sampled}
     t0 = time.perf_counter()
     for i in range(steps):
         stepper.step(evs.get(i))
@@ -414,9 +418,11 @@ def fp8_bench(batch, steps, warmup, bf16_kernel_us):
 
 def read_ceiling(nbytes, grids=(2048, 4096, 8192), reps=15, warmup=3):
     """Bandwidth of a plain streaming read of nbytes (the library's probe kernel:
-    every 16-byte piece loaded once), each launch timed on its own with HIP
-    events as the attention kernel is (median of reps), best of a few grid
-    sizes: the practical ceiling for a kernel reading that many bytes."""
+    every 16-byte piece loaded once), best of a few grid sizes: the practical
+    ceiling for a kernel reading that many bytes. Each launch is timed as the
+    attention kernel is, by HIP events handed to its launch, and the launches
+    of one grid size are queued back to back, as decode steps are, so the
+    events carry the same start latency (median of reps)."""
     import torch
     from paper_2601_12784_amd import binding as B
     nbytes -= nbytes % 16
@@ -426,17 +432,17 @@ def read_ceiling(nbytes, grids=(2048, 4096, 8192), reps=15, warmup=3):
     best = None
     with torch.cuda.stream(stream):
         for blocks in grids:
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(reps)]
+            for a, b in evs:             # create both events (torch does so on a first record)
+                a.record(stream)
+                b.record(stream)
             for _ in range(warmup):
                 B.sf_debug_stream_read(buf, sink, blocks, stream)
-            ts = []
-            for _ in range(reps):
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record(stream)
-                B.sf_debug_stream_read(buf, sink, blocks, stream)
-                b.record(stream)
-                b.synchronize()
-                ts.append(a.elapsed_time(b) * 1e3)
-            us = float(np.median(ts))
+            for ev in evs:
+                B.sf_debug_stream_read(buf, sink, blocks, stream, events=ev)
+            stream.synchronize()
+            us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
             if best is None or us < best[0]:
                 best = (us, blocks)
     del buf
@@ -444,8 +450,9 @@ def read_ceiling(nbytes, grids=(2048, 4096, 8192), reps=15, warmup=3):
     return {"gb_s": round(nbytes / us / 1e3, 1), "us": round(us, 2), "bytes": nbytes, "blocks": blocks,
             "kernel": "stream_read_kernel",
             "what": "plain streaming read of the step's K+V byte count: each block streams a contiguous "
-                    "range, every 16-byte piece loaded once (nontemporal, 8 in flight per lane); one launch "
-                    f"per HIP-event pair, median of {reps}, best of {len(grids)} grid sizes"}
+                    "range, every 16-byte piece loaded once (nontemporal, 8 in flight per lane); launches "
+                    "queued back to back, each timed by HIP events handed to its launch, median of "
+                    f"{reps}, best of {len(grids)} grid sizes"}
 
 
 def cpu_baseline(batch, min_s=10.0, max_s=30.0):
@@ -554,7 +561,7 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
     md = out_path[:-len(".json")] + ".md"
     cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
            "-d $OUT/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
-           "--no-skew --no-loop --no-cost --no-reprefill --no-fp8 --copy-probe " + str(int(copy_mib)))
+           "--no-skew --no-loop --no-cost --no-reprefill --no-fp8 --no-configs --copy-probe " + str(int(copy_mib)))
     lines = [f"# HBM traffic of {ATTN_KERNEL} on the long-tail batch (rocprofv3 counters)", "",
              "Two counter passes (one counter each), then the summary:", "", "```",
              cmd.format(c="FETCH_SIZE", d="pmc_fetch", o="f"), cmd.format(c="WRITE_SIZE", d="pmc_write", o="w"),
@@ -642,6 +649,16 @@ def summarize_extend_counters(csvs, stats_csv, command, out_md, simds=1024, cloc
         f.write("\n".join(lines) + "\n")
 
 
+def _events_vs_trace(rows, kernel, event_us):
+    """A line comparing the HIP-event mean of a kernel with the trace's."""
+    hit = [r for r in rows if kernel in r["Name"]]
+    if not hit:
+        return []
+    tr = float(hit[0]["AverageNs"]) / 1e3
+    return [f"- the trace's mean for `{kernel}`: {tr:.2f} us; the events read {event_us - tr:+.2f} us "
+            f"({100 * (event_us / tr - 1):+.1f} %) from it (the start event is a marker ahead of the dispatch)"]
+
+
 def summarize_trace(stats_csv, command, out_md, bench_json=None):
     """Markdown summary of a rocprofv3 --kernel-trace --stats run (the decode
     step, the re-prefill leg when the bench line is an --only-reprefill one,
@@ -659,7 +676,8 @@ def summarize_trace(stats_csv, command, out_md, bench_json=None):
                   f"- attention kernel mean: {b['attn_kernel_us']} us for {b['kv_bytes_per_step']} bytes of K and V "
                   f"= {b['kv_gb_per_s_kernel']} GB/s ({b['pct_of_peak_hbm_kernel']} % of 8000)",
                   f"- step: {b['ms_per_step'] * 1e3:.1f} us; {b['seq_steps_per_s']} seq-steps/s; "
-                  f"{b['pool_copies_rotated']} pool copies rotated"]
+                  f"{b['pool_copies_rotated']} pool copies rotated"] + _events_vs_trace(rows, ATTN_KERNEL,
+                                                                        b['attn_kernel_us'])
         with open(out_md, "w") as f:
             f.write("\n".join(lines) + "\n")
         return
@@ -687,6 +705,7 @@ def summarize_trace(stats_csv, command, out_md, bench_json=None):
                   f"- attention kernel mean: {b['attn_kernel_us']} us",
                   f"- step: {b['ms_per_step'] * 1e3:.1f} us; value {b['value']} GB/s",
                   f"- roofline achieved: {b['roofline']['achieved']} GB/s ({100 * b['roofline']['frac']:.1f}% of 8000)"]
+        lines += _events_vs_trace(rows, ATTN_KERNEL, b["attn_kernel_us"])
         if fp8:
             f8 = b["fp8"]
             lines += [f"- fp8 cache: attention kernel mean {f8['attn_kernel_us']} us, step {f8['ms_per_step'] * 1e3:.1f} us, "

@@ -245,8 +245,8 @@ typedef struct sf_runner_extras {
   const int32_t* new_pages_host; /* host int32 [num_seqs], copied next to the work list */
   const float* k_scale;          /* fp8 cache (sf_decode_attn_fp8's scales); not with k_new */
   const float* v_scale;
-  void* attn_start;              /* optional hipEvent_t recorded before the attention launch */
-  void* attn_end;                /* optional hipEvent_t recorded after it (before the merge) */
+  void* attn_start;              /* optional hipEvent_t: takes the attention kernel's own start time */
+  void* attn_end;                /* optional hipEvent_t: takes its end time (before the merge) */
 } sf_runner_extras;
 
 /* *runner = a runner for the shape's head counts, head_dim and page size
@@ -536,8 +536,11 @@ sf_status sf_debug_gather_kv(const sf_attn_desc* desc, const void* k_pool, const
  * buf and sink (16 bytes of device memory, written at most once with a
  * meaningless value) must be 16-byte aligned; bytes a multiple of 16;
  * 1 <= blocks <= 65536. bytes == 0 launches nothing. Asynchronous on stream.
+ * start_event / stop_event (hipEvent_t, may be NULL) take the kernel's own
+ * start and end times, as sf_runner_extras.attn_start / attn_end do.
  * Errors: SF_ERR_INVALID_ARG for the cases above, SF_ERR_HIP on a launch error. */
-sf_status sf_debug_stream_read(const void* buf, uint64_t bytes, void* sink, int32_t blocks, void* stream);
+sf_status sf_debug_stream_read(const void* buf, uint64_t bytes, void* sink, int32_t blocks, void* stream,
+                               void* start_event, void* stop_event);
 
 /* Static description of a status code. */
 const char* sf_status_string(sf_status status);

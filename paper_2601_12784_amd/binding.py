@@ -110,7 +110,7 @@ def lib():
     L.sf_runner_destroy.restype = None
     L.sf_runner_step.argtypes = [vp, P(sf_attn_desc), vp, vp, vp, vp, vp, vp, vp, P(sf_runner_extras), vp,
                                  P(sf_plan_info)]
-    L.sf_debug_stream_read.argtypes = [vp, ctypes.c_uint64, vp, ctypes.c_int32, vp]
+    L.sf_debug_stream_read.argtypes = [vp, ctypes.c_uint64, vp, ctypes.c_int32, vp, vp, vp]
     L.sf_decode_attn_fp8.argtypes = [P(sf_attn_desc), P(sf_plan_info), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                      ctypes.c_uint64, vp]
     L.sf_kv_quantize_fp8.argtypes = [P(sf_attn_desc), vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp, vp, vp]
@@ -554,15 +554,28 @@ def sf_decode_attn_scratch(desc, info, work_dev, q, k_pool, v_pool, block_table,
         _addr(block_table), _addr(out), _addr(lse), _stream(stream)))
 
 
-def sf_debug_stream_read(buf, sink, blocks=16384, stream=None):
+def kernel_event(ev, stream):
+    """The hipEvent_t behind a torch timing event, for an entry point that
+    records the kernel's own start or end time into it. torch creates an
+    event on its first record, so a fresh one is recorded on `stream` once."""
+    if ev.cuda_event == 0:
+        ev.record(stream)
+    return ev.cuda_event
+
+
+def sf_debug_stream_read(buf, sink, blocks=16384, stream=None, events=None):
     """Reads every byte of the uint8 device tensor buf once (measurement
-    support); sink: a uint8 device tensor of at least 16 bytes."""
+    support); sink: a uint8 device tensor of at least 16 bytes. events, if
+    given, is a (start, end) pair of torch timing events that take the
+    kernel's own start and end times."""
     _dev(buf, "buf", torch.uint8)
     _dev(sink, "sink", torch.uint8)
     if sink.numel() * sink.element_size() < 16:
         raise ValueError("sink must hold at least 16 bytes")
+    s = stream or torch.cuda.current_stream(buf.device)
+    ev = (None, None) if events is None else (kernel_event(events[0], s), kernel_event(events[1], s))
     _check("sf_debug_stream_read", lib().sf_debug_stream_read(
-        _addr(buf), buf.numel() * buf.element_size(), _addr(sink), int(blocks), _stream(stream)))
+        _addr(buf), buf.numel() * buf.element_size(), _addr(sink), int(blocks), s.cuda_stream, *ev))
 
 
 def sf_debug_gather_kv(desc, k_pool, v_pool, block_table, seq, kv_head, length, k_dense, v_dense,
@@ -666,18 +679,13 @@ class DecodeAttention:
             _check("sf_runner_reserve", self.L.sf_runner_reserve(self._runner(chunk_pages), info.workspace_bytes,
                                                                  info.work_bytes, lens.size, main.cuda_stream))
 
-    @staticmethod
-    def _event_handle(ev, stream):
-        if ev.cuda_event == 0:      # torch creates the event on its first record
-            ev.record(stream)
-        return ev.cuda_event
-
     def __call__(self, q, k_pool, v_pool, block_table, seq_lens, scale, out=None, lse=None,
                  chunk_pages=None, stream: torch.cuda.Stream | None = None, attn_events=None,
                  append=None, fp8=None):
         """One decode step on `stream` (default: the current stream). attn_events,
-        if given, is a (start, end) pair of torch events recorded around the
-        attention kernel. append = (k_new, v_new, new_pages) makes it an
+        if given, is a (start, end) pair of torch timing events that take the
+        attention kernel's own start and end times (none if the step launches
+        no attention kernel). append = (k_new, v_new, new_pages) makes it an
         append-then-attend step: k_new, v_new are device bf16 [B, Hkv, D] and
         new_pages a host int32 [B] array (-1 = the token's page is already
         held), uploaded together with the work list. fp8 = (k_scale, v_scale)
@@ -725,8 +733,8 @@ class DecodeAttention:
                 raise ValueError("new_pages holds a page id outside the pool")
         self._host_checked = False
         if attn_events is not None:
-            ex.attn_start = self._event_handle(attn_events[0], main)
-            ex.attn_end = self._event_handle(attn_events[1], main)
+            ex.attn_start = kernel_event(attn_events[0], main)
+            ex.attn_end = kernel_event(attn_events[1], main)
         info = self._info
         _check("sf_runner_step", self.L.sf_runner_step(
             self._runner(chunk_pages), ctypes.byref(self._desc), lens.ctypes.data, q.data_ptr(), k_pool.data_ptr(),

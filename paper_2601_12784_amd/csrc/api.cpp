@@ -109,7 +109,8 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
                  int32_t* work_dev, const void* q, const void* k_pool, const void* v_pool,
                  const int32_t* block_table, float* out, float* lse, void* workspace,
                  uint64_t workspace_bytes, void* stream, const AppendArgs* app,
-                 const float* k_scale = nullptr, const float* v_scale = nullptr, const RowCopy* copy = nullptr) {
+                 const float* k_scale = nullptr, const float* v_scale = nullptr, const RowCopy* copy = nullptr,
+                 void* attn_start = nullptr, void* attn_end = nullptr) {
   sf_status st = check_step_args(desc, info, work_dev, q, k_pool, v_pool, block_table, out, lse,
                                  app ? app->k_new : nullptr, app ? app->v_new : nullptr,
                                  app ? app->new_pages : nullptr, k_scale, v_scale);
@@ -154,7 +155,9 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
   a.copy_src = copying ? copy->src : nullptr;
   a.copy_dst = copying ? copy->dst : nullptr;
   a.copy_ints = copying ? copy->ints : 0;
-  if ((st = from_hip(launch_attention(a, s))) != SF_OK || !app) return st;
+  if ((st = from_hip(launch_attention(a, s, static_cast<hipEvent_t>(attn_start),
+                                      static_cast<hipEvent_t>(attn_end)))) != SF_OK || !app)
+    return st;
   AppendArgs app_rows = *app;
   if (copying && app->single_rows && copy->single_off >= 0) app_rows.single_rows = copy->dst + copy->single_off;
   if (copying && app->new_pages && copy->pages_off >= 0) app_rows.new_pages = copy->dst + copy->pages_off;
@@ -171,25 +174,23 @@ sf_status sf::decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_in
                                       const int32_t* new_pages, const int32_t* single_rows, int32_t num_single,
                                       void* k_pool, void* v_pool, int32_t* block_table, float* out, float* lse,
                                       void* workspace, uint64_t workspace_bytes, void* stream,
-                                      const RowCopy* copy) {
+                                      const RowCopy* copy, void* attn_start, void* attn_end) {
   if (num_single < 0 || (info && num_single > info->num_work) || (num_single > 0 && !single_rows) ||
       (single_rows && !aligned16(single_rows)))
     return SF_ERR_INVALID_ARG;
   const AppendArgs app = {q, k_new, v_new, new_pages, single_rows, num_single};
   return attend(desc, info, nullptr, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
-                workspace_bytes, stream, &app, nullptr, nullptr, copy);
+                workspace_bytes, stream, &app, nullptr, nullptr, copy, attn_start, attn_end);
 }
 
 sf_status sf::decode_attn_rows(const sf_attn_desc* desc, const sf_plan_info* info, int32_t* work_dev, const void* q,
                                const void* k_pool, const void* v_pool, const float* k_scale, const float* v_scale,
                                const int32_t* block_table, float* out, float* lse, void* workspace,
-                               uint64_t workspace_bytes, void* stream, const RowCopy* copy, void* after_attention) {
+                               uint64_t workspace_bytes, void* stream, const RowCopy* copy, void* attn_start,
+                               void* attn_end) {
   sf_status st = attend(desc, info, nullptr, work_dev, q, k_pool, v_pool, block_table, out, lse, workspace,
-                        workspace_bytes, stream, nullptr, k_scale, v_scale, copy);
+                        workspace_bytes, stream, nullptr, k_scale, v_scale, copy, attn_start, attn_end);
   if (st != SF_OK) return st;
-  if (after_attention &&
-      hipEventRecord(static_cast<hipEvent_t>(after_attention), static_cast<hipStream_t>(stream)) != hipSuccess)
-    return SF_ERR_HIP;
   if (info->num_workers == 0 || info->num_combine == 0) return st;
   const bool copying = copy && copy->ints > 0 && copy->ints <= int64_t(64) * info->num_workers;
   const CombineArgs a = combine_args(desc, info, work_dev, workspace, out, lse, nullptr, nullptr, nullptr, nullptr,
@@ -317,11 +318,12 @@ extern "C" sf_status sf_debug_gather_kv(const sf_attn_desc* desc, const void* k_
 }
 
 extern "C" sf_status sf_debug_stream_read(const void* buf, uint64_t bytes, void* sink, int32_t blocks,
-                                          void* stream) {
+                                          void* stream, void* start_event, void* stop_event) {
   if (bytes == 0) return SF_OK;
   if (!buf || !sink || !aligned16(buf) || !aligned16(sink) || bytes % 16 != 0 || blocks < 1 || blocks > 65536)
     return SF_ERR_INVALID_ARG;
-  return from_hip(launch_stream_read(buf, bytes, sink, blocks, static_cast<hipStream_t>(stream)));
+  return from_hip(launch_stream_read(buf, bytes, sink, blocks, static_cast<hipStream_t>(stream),
+                                     static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event)));
 }
 
 extern "C" const char* sf_status_string(sf_status s) {

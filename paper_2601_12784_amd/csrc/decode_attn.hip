@@ -21,6 +21,7 @@
 // 4*grp .. 4*grp+3 of both pages, exactly the eight P^T values its PV operand
 // needs (the contraction order inside an MFMA is free as long as both
 // operands agree).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -1089,28 +1090,20 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
+hipError_t launch_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
   if (a.num_workers == 0) return hipSuccess;
   const dim3 grid(a.num_workers), block(64);
-  if (a.k_scale) {
-    if (a.head_dim == 128)
-      hipLaunchKernelGGL(attn_worker_fp8_kernel<128>, grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL(attn_worker_fp8_kernel<64>, grid, block, 0, stream, a);
-    return hipGetLastError();
-  }
-  const bool append = a.k_new != nullptr;
-  if (a.head_dim == 128) {
-    if (append)
-      hipLaunchKernelGGL((attn_worker_kernel<128, true>), grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL((attn_worker_kernel<128, false>), grid, block, 0, stream, a);
-  } else {
-    if (append)
-      hipLaunchKernelGGL((attn_worker_kernel<64, true>), grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL((attn_worker_kernel<64, false>), grid, block, 0, stream, a);
-  }
+  void (*kernel)(AttnArgs);
+  if (a.k_scale)
+    kernel = a.head_dim == 128 ? attn_worker_fp8_kernel<128> : attn_worker_fp8_kernel<64>;
+  else if (a.k_new)
+    kernel = a.head_dim == 128 ? attn_worker_kernel<128, true> : attn_worker_kernel<64, true>;
+  else
+    kernel = a.head_dim == 128 ? attn_worker_kernel<128, false> : attn_worker_kernel<64, false>;
+  if (start || stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, a);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@
 // in flight per lane, and XOR-reduced. The reduction is stored only if it
 // equals an arbitrary constant, which keeps the loads live while writing
 // (practically) nothing.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "sf_internal.h"
@@ -38,11 +39,17 @@ __global__ __launch_bounds__(kProbeThreads) void stream_read_kernel(const u32x4*
 
 }  // namespace
 
-hipError_t launch_stream_read(const void* buf, uint64_t bytes, void* sink, int blocks, hipStream_t stream) {
+hipError_t launch_stream_read(const void* buf, uint64_t bytes, void* sink, int blocks, hipStream_t stream,
+                              hipEvent_t start, hipEvent_t stop) {
   const uint64_t n = bytes / 16;
   const uint64_t per_block = (n + blocks - 1) / blocks;
-  hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(kProbeThreads), 0, stream,
-                     static_cast<const u32x4*>(buf), n, per_block, static_cast<u32x4*>(sink));
+  const u32x4* p = static_cast<const u32x4*>(buf);
+  u32x4* s = static_cast<u32x4*>(sink);
+  if (start || stop)
+    hipExtLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(kProbeThreads), 0, stream, start, stop, 0, p, n,
+                          per_block, s);
+  else
+    hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(kProbeThreads), 0, stream, p, n, per_block, s);
   return hipGetLastError();
 }
 

@@ -207,10 +207,10 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
                             append && desc->num_seqs > 0 ? int32_t(rows_ints) : -1};
   const sf::RowCopy* cp = copy_ints > 0 ? &copy : nullptr;
 
-  // 3. kernels on the caller's stream (optionally bracketed by the caller's events)
-  hipEvent_t ev0 = extras ? static_cast<hipEvent_t>(extras->attn_start) : nullptr;
-  hipEvent_t ev1 = extras ? static_cast<hipEvent_t>(extras->attn_end) : nullptr;
-  if (ev0 && hipEventRecord(ev0, main) != hipSuccess) return SF_ERR_HIP;
+  // 3. kernels on the caller's stream (the caller's events, if any, take the
+  //    attention kernel's own start and end times)
+  void* ev0 = extras ? extras->attn_start : nullptr;
+  void* ev1 = extras ? extras->attn_end : nullptr;
   // From here on a launch may have been enqueued that reads the slot, so the
   // slot is released through its event whatever the launches return.
   if (append) {
@@ -220,12 +220,11 @@ extern "C" sf_status sf_runner_step(sf_runner* r, const sf_attn_desc* desc, cons
                                      reinterpret_cast<const int32_t*>(wbase + info.work_bytes), num_single,
                                      const_cast<void*>(k_pool), const_cast<void*>(v_pool),
                                      const_cast<int32_t*>(block_table), out, lse, r->workspace,
-                                     r->workspace_bytes, stream, cp);
-    if (st == SF_OK && ev1 && hipEventRecord(ev1, main) != hipSuccess) st = SF_ERR_HIP;
+                                     r->workspace_bytes, stream, cp, ev0, ev1);
   } else {
     st = sf::decode_attn_rows(desc, &info, work, q, k_pool, v_pool, fp8 ? extras->k_scale : nullptr,
                               fp8 ? extras->v_scale : nullptr, block_table, out, lse, r->workspace,
-                              r->workspace_bytes, stream, cp, ev1);
+                              r->workspace_bytes, stream, cp, ev0, ev1);
   }
   if (hipEventRecord(pin.released, main) == hipSuccess) {
     pin.used = true;

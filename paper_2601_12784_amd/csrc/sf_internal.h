@@ -163,7 +163,11 @@ struct ExtendArgs {
 // Rows (tokens x query heads of a group) of one extend work item.
 constexpr int kExtendRows = 256;
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+// start / stop (hipEvent_t, may be NULL) take the kernel's own start and end
+// times: the launch records them from its dispatch (hipExtLaunchKernel), so
+// their difference is the kernel's duration without queue time.
+hipError_t launch_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start = nullptr,
+                            hipEvent_t stop = nullptr);
 
 // sf_decode_attn_append with the merge launch restricted to single_rows
 // (num_single copies, in work-item format, of the rows of pairs that have one
@@ -174,17 +178,20 @@ sf_status decode_attn_append_rows(const sf_attn_desc* desc, const sf_plan_info* 
                                   const void* q, const void* k_new, const void* v_new, const int32_t* new_pages,
                                   const int32_t* single_rows, int32_t num_single, void* k_pool, void* v_pool,
                                   int32_t* block_table, float* out, float* lse, void* workspace,
-                                  uint64_t workspace_bytes, void* stream, const RowCopy* copy);
+                                  uint64_t workspace_bytes, void* stream, const RowCopy* copy,
+                                  void* attn_start = nullptr, void* attn_end = nullptr);
 
 // sf_decode_attn (k_scale NULL) or sf_decode_attn_fp8, then the combine of
 // split pairs, on a device-resident or mapped work list; with `copy`, the
 // attention launch copies the plan's combine rows to copy->dst and the
 // combine launch reads them there. The native runner's other path.
-// after_attention (a hipEvent_t, may be NULL) is recorded between the two.
+// attn_start / attn_end (hipEvent_t, may be NULL) take the attention
+// kernel's own start and end times (launch_attention).
 sf_status decode_attn_rows(const sf_attn_desc* desc, const sf_plan_info* info, int32_t* work_dev, const void* q,
                            const void* k_pool, const void* v_pool, const float* k_scale, const float* v_scale,
                            const int32_t* block_table, float* out, float* lse, void* workspace,
-                           uint64_t workspace_bytes, void* stream, const RowCopy* copy, void* after_attention);
+                           uint64_t workspace_bytes, void* stream, const RowCopy* copy, void* attn_start,
+                           void* attn_end);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream);
 
 // Every host-side check of a decode step's arguments except the workspace
@@ -203,7 +210,9 @@ sf_status decode_attn_and_combine(const sf_attn_desc* desc, const sf_plan_info* 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
 // Streaming-read probe: reads bytes (a multiple of 16) of buf once; sink: 16 B.
-hipError_t launch_stream_read(const void* buf, uint64_t bytes, void* sink, int blocks, hipStream_t stream);
+// start / stop: as for launch_attention.
+hipError_t launch_stream_read(const void* buf, uint64_t bytes, void* sink, int blocks, hipStream_t stream,
+                              hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_quantize_fp8(const QuantArgs& a, hipStream_t stream);
 
 }  // namespace sf

@@ -346,12 +346,77 @@ def test_stream_read_probe_runs_and_checks_its_arguments():
     assert not sink.any()                                             # 0x5A... XOR-reduces to 0: nothing stored
     L = B.lib()
     addr, sk = buf.data_ptr(), sink.data_ptr()
-    assert L.sf_debug_stream_read(addr, 0, sk, 1, None) == 0           # empty: nothing launched
-    assert L.sf_debug_stream_read(addr + 8, 1024, sk, 1, None) == 1    # misaligned buffer
-    assert L.sf_debug_stream_read(addr, 1000, sk, 1, None) == 1        # not a multiple of 16
-    assert L.sf_debug_stream_read(addr, 1024, sk, 0, None) == 1        # no blocks
-    assert L.sf_debug_stream_read(addr, 1024, sk, 65537, None) == 1    # too many blocks
-    assert L.sf_debug_stream_read(addr, 1024, None, 1, None) == 1      # no sink
+    assert L.sf_debug_stream_read(addr, 0, sk, 1, None, None, None) == 0           # empty: nothing launched
+    assert L.sf_debug_stream_read(addr + 8, 1024, sk, 1, None, None, None) == 1    # misaligned buffer
+    assert L.sf_debug_stream_read(addr, 1000, sk, 1, None, None, None) == 1        # not a multiple of 16
+    assert L.sf_debug_stream_read(addr, 1024, sk, 0, None, None, None) == 1        # no blocks
+    assert L.sf_debug_stream_read(addr, 1024, sk, 65537, None, None, None) == 1    # too many blocks
+    assert L.sf_debug_stream_read(addr, 1024, None, 1, None, None, None) == 1      # no sink
+
+
+def _elapsed_inside(inner, outer):
+    """Both intervals in ms; the kernel-timed one must be positive and lie
+    within the one that brackets the whole call."""
+    t_in, t_out = inner[0].elapsed_time(inner[1]), outer[0].elapsed_time(outer[1])
+    _say(f"  kernel {t_in * 1e3:.1f} us inside a {t_out * 1e3:.1f} us bracket")
+    assert 0.0 < t_in <= t_out
+    assert outer[0].elapsed_time(inner[0]) >= 0.0 and inner[1].elapsed_time(outer[1]) >= 0.0
+
+
+def _events(n=2):
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+@pytest.mark.parametrize("fp8", [False, True], ids=["bf16", "fp8"])
+def test_kernel_timed_events_leave_the_step_unchanged(fp8):
+    """Timing events handed to a runner step are filled by the attention
+    launch itself (the kernel's own start and end): that launch path must give
+    bit-identical results to the plain one, match the oracle, and time an
+    interval inside a bracket around the whole step."""
+    from paper_2601_12784_amd.workloads import random_fp8_cache
+    b = build_batch([3000, 17, 1, 700, 16, 2049], 28, 4, 128, 77, pool_pages=420)
+    _say(f"timed launch, fp8={fp8}: lens {b.seq_lens.tolist()}")
+    dev = to_dev(b)
+    if fp8:
+        cache = random_fp8_cache(b, seed=19)
+        k, v = cache.k8.cuda(), cache.v8.cuda()
+        scales = (cache.k_scale.cuda(), cache.v_scale.cuda())
+        ref = oracle.decode_attn_fp8(bf16_bits(b.q), cache.k8.numpy(), cache.v8.numpy(), cache.k_scale.numpy(),
+                                     cache.v_scale.numpy(), b.block_table, b.seq_lens, b.scale)
+    else:
+        k, v, scales, ref = dev["k"], dev["v"], None, run_oracle(b)
+    runner = B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim)
+    stream = torch.cuda.Stream()
+    outs = []
+    for timed in (False, True):
+        out = torch.full((b.num_seqs, b.num_q_heads, b.head_dim), float("nan"), device="cuda")
+        lse = torch.full((b.num_seqs, b.num_q_heads), float("nan"), device="cuda")
+        inner, outer = _events(), _events()
+        outer[0].record(stream)
+        runner(dev["q"], k, v, dev["bt"], b.seq_lens, b.scale, out=out, lse=lse, chunk_pages=40, stream=stream,
+               attn_events=inner if timed else None, fp8=scales)
+        outer[1].record(stream)
+        torch.cuda.synchronize()
+        assert runner.last_info.num_combine > 0             # cut pairs: the combine launch follows
+        if timed:
+            _elapsed_inside(inner, outer)
+        outs.append((out.cpu().numpy(), lse.cpu().numpy()))
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+    assert_close(outs[1][0], ref[0], "timed out")
+    assert_close(outs[1][1], ref[1], "timed lse")
+
+
+def test_kernel_timed_events_on_the_read_probe():
+    stream = torch.cuda.Stream()
+    buf = torch.full((64 << 20,), 0x5A, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    inner, outer = _events(), _events()
+    outer[0].record(stream)
+    B.sf_debug_stream_read(buf, sink, 2048, stream, events=inner)
+    outer[1].record(stream)
+    torch.cuda.synchronize()
+    _elapsed_inside(inner, outer)
+    assert not sink.any()
 
 
 def test_runner_ring_reuse_with_growing_and_shrinking_plans():
