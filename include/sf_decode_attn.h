@@ -230,10 +230,10 @@ sf_status sf_decode_attn_append(const sf_attn_desc* desc, const sf_plan_info* in
  * (sf_decode_attn_plan with the runner's options) into a pinned, device-
  * mapped host buffer, then on the caller's stream the attention (plain,
  * appending or fp8) and the merge of split sequences, whose kernels read that
- * work list in place (no separate upload). The runner owns a ring of 4 such
- * buffers, the split-K workspace and one event per buffer: a buffer is
- * rewritten only after the step that read it has ended, so the host plans
- * step i + 1 while the kernels of step i run. One runner serves one device (the current one at
+ * work list in place (no separate upload). The runner owns a ring of 32 such
+ * buffers, the split-K workspace and a few events, one recorded after every
+ * 16th step: a buffer is rewritten only after the step that read it has
+ * ended, so the host plans ahead while the kernels of earlier steps run. One runner serves one device (the current one at
  * creation) and one caller stream at a time; steps on different streams, or
  * calls that overlap, are not supported.
  */

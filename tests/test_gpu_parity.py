@@ -439,15 +439,19 @@ def test_runner_ring_reuse_with_growing_and_shrinking_plans():
 
 @pytest.mark.parametrize("reserve", [False, True])
 def test_runner_steps_in_flight_with_growing_and_shrinking_plans(reserve):
-    """Twelve runner steps enqueued back to back, with no synchronization
-    between them, on batches whose plans grow and shrink: each step plans into
-    a ring slot while earlier steps still run, waits on the slot's event, and
-    regrows slots (reserve=False) while other slots are in use. Every step
-    writes its own out and lse; one synchronization at the end, then every step
-    against the oracle. With reserve=True the runner is sized for the largest
-    batch first (sf_runner_reserve)."""
+    """Ninety-six runner steps enqueued back to back, with no synchronization
+    between them, cycling over batches whose plans grow and shrink: each step
+    plans into a ring slot (32 per runner) while earlier steps still run,
+    waits for the step that last read the slot (through the event that marks
+    its run of 16 steps, recycling those events as it goes), and regrows
+    slots (reserve=False) while other slots are in use. The default-chunk
+    runner takes 64 of the steps, twice round its ring. Every step writes its
+    own out and lse; one synchronization at the end, then every step against
+    the oracle. With reserve=True the runner is sized for the largest batch
+    first (sf_runner_reserve)."""
     runner = B.DecodeAttention(28, 4, 128)
     sizes = [3, 40, 7, 120, 1, 64, 200, 5, 90, 2, 150, 30]
+    num_steps = 8 * len(sizes)
     batches = []
     for i, nseq in enumerate(sizes):
         rng = np.random.default_rng(1900 + i)
@@ -455,8 +459,9 @@ def test_runner_steps_in_flight_with_growing_and_shrinking_plans(reserve):
         lens[rng.random(nseq) < 0.1] = 0
         batches.append(build_batch(lens, 28, 4, 128, 1910 + i))
     devs = [to_dev(b) for b in batches]
-    outs = [torch.full((b.num_seqs, 28, 128), float("nan"), device="cuda") for b in batches]
-    lses = [torch.full((b.num_seqs, 28), float("nan"), device="cuda") for b in batches]
+    which = [i % len(batches) for i in range(num_steps)]
+    outs = [torch.full((batches[j].num_seqs, 28, 128), float("nan"), device="cuda") for j in which]
+    lses = [torch.full((batches[j].num_seqs, 28), float("nan"), device="cuda") for j in which]
     stream = torch.cuda.Stream()
     if reserve:
         big = max(range(len(batches)), key=lambda i: int(batches[i].seq_lens.sum()))
@@ -465,11 +470,12 @@ def test_runner_steps_in_flight_with_growing_and_shrinking_plans(reserve):
                            chunk_pages=chunk, stream=stream)
     torch.cuda.synchronize()
     _say(f"in-flight runner steps (reserve={reserve})")
-    for i, (b, d) in enumerate(zip(batches, devs)):
+    for i, j in enumerate(which):
+        b, d = batches[j], devs[j]
         runner(d["q"], d["k"], d["v"], d["bt"], b.seq_lens, b.scale, out=outs[i], lse=lses[i],
                chunk_pages=(None if i % 3 else 5), stream=stream)
     torch.cuda.synchronize()
-    for i, b in enumerate(batches):
-        ref = run_oracle(b)
-        assert_close(outs[i].cpu().numpy(), ref[0], f"in-flight step {i} out")
-        assert_close(lses[i].cpu().numpy(), ref[1], f"in-flight step {i} lse")
+    refs = [run_oracle(b) for b in batches]
+    for i, j in enumerate(which):
+        assert_close(outs[i].cpu().numpy(), refs[j][0], f"in-flight step {i} (batch {j}) out")
+        assert_close(lses[i].cpu().numpy(), refs[j][1], f"in-flight step {i} (batch {j}) lse")
