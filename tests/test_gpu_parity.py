@@ -437,6 +437,44 @@ def test_runner_ring_reuse_with_growing_and_shrinking_plans():
         assert_close(l, ref[1], f"ring step {i} lse")
 
 
+def test_runner_steps_switching_streams_in_order():
+    """Forty runner steps that move between two streams every five steps, each
+    switch ordered by an event wait on the stream before (no host
+    synchronization): the runner closes its run of marked steps at every
+    switch, so a ring slot is rewritten only after its last reader ended on
+    whichever stream that was. Every step against the oracle."""
+    runner = B.DecodeAttention(28, 4, 128)
+    sizes = [3, 40, 120, 1, 64, 90, 2, 30]
+    batches = []
+    for i, nseq in enumerate(sizes):
+        rng = np.random.default_rng(2900 + i)
+        lens = np.exp(rng.normal(np.log(600), 1.0, size=nseq)).astype(np.int64).clip(0, 6000)
+        lens[rng.random(nseq) < 0.1] = 0
+        batches.append(build_batch(lens, 28, 4, 128, 2910 + i))
+    devs = [to_dev(b) for b in batches]
+    which = [i % len(batches) for i in range(40)]
+    outs = [torch.full((batches[j].num_seqs, 28, 128), float("nan"), device="cuda") for j in which]
+    lses = [torch.full((batches[j].num_seqs, 28), float("nan"), device="cuda") for j in which]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    _say("runner steps on two streams, switching every five steps")
+    cur = streams[0]
+    for i, j in enumerate(which):
+        if i and i % 5 == 0:
+            nxt = streams[(i // 5) % 2]
+            ev = torch.cuda.Event()
+            ev.record(cur)
+            nxt.wait_event(ev)
+            cur = nxt
+        b, d = batches[j], devs[j]
+        runner(d["q"], d["k"], d["v"], d["bt"], b.seq_lens, b.scale, out=outs[i], lse=lses[i], stream=cur)
+    torch.cuda.synchronize()
+    refs = [run_oracle(b) for b in batches]
+    for i, j in enumerate(which):
+        assert_close(outs[i].cpu().numpy(), refs[j][0], f"two-stream step {i} (batch {j}) out")
+        assert_close(lses[i].cpu().numpy(), refs[j][1], f"two-stream step {i} (batch {j}) lse")
+
+
 @pytest.mark.parametrize("reserve", [False, True])
 def test_runner_steps_in_flight_with_growing_and_shrinking_plans(reserve):
     """Ninety-six runner steps enqueued back to back, with no synchronization
