@@ -84,7 +84,8 @@ typedef struct sf_plan_opts {
   int32_t chunk_pages;      /* > 0 forces the pages per worker: workers = ceil(T / chunk_pages) */
   int32_t workers_per_cu;   /* default 4: attention waves per CU (one per SIMD) */
   int32_t min_chunk_pages;  /* default 8: fewer workers rather than slices thinner than this */
-  int32_t reserved;         /* must be 0 */
+  int32_t xcd_parity_skew;  /* p in the slice rule below, per mille: 0 = default 20, -1 = none,
+                               at most 250; ignored (none) when chunk_pages > 0 */
 } sf_plan_opts;
 
 /* Filled by the planner; passed back unchanged to the other calls. */
@@ -93,7 +94,7 @@ typedef struct sf_plan_info {
   int32_t num_work;          /* segments (work items) */
   int32_t num_combine;       /* (seq, KV head) pairs cut into more than one segment */
   int32_t num_partials;      /* partial-result slots = sum of their segment counts */
-  int32_t chunk_pages;       /* pages per worker, ceil(T / num_workers) (0 if T = 0) */
+  int32_t chunk_pages;       /* the most pages any worker owns (0 if T = 0) */
   int32_t reserved;          /* 0 */
   uint64_t work_bytes;       /* bytes of the work list:
                                 (num_workers + num_work + num_combine) * 32 */
@@ -112,8 +113,13 @@ typedef struct sf_plan_info {
  *   W = ceil(T / chunk_pages)                                   if chunk_pages > 0
  *   W = min(workers_per_cu * num_cus, ceil(T / min_chunk_pages)) otherwise
  * (W = 1 if T = 0 but B * Hkv > 0), worker w owns the global pages
- * [floor(w T / W), floor((w + 1) T / W)): every worker reads the same number
- * of pages (within one), however skewed the lengths are. A worker's range is
+ * [floor(T C(w) / C(W)), floor(T C(w + 1) / C(W))) with C(v) = 1000 v +
+ * p (v mod 2): every worker reads its share of the pages however skewed the
+ * lengths are, 1000 + p per mille of the mean for an even w, 1000 - p for an
+ * odd one (p = opts->xcd_parity_skew, default 20; p = 0, equal slices within
+ * one page, when chunk_pages is forced). Worker w runs as workgroup w, and
+ * workgroups are spread over the 8 XCDs round-robin: on MI355X the odd XCDs
+ * took 3-4 % longer than their even neighbours on the same work. A worker's range is
  * cut at pair boundaries into segments, each a work item on one pair; a pair
  * crossing k worker boundaries has n_p = k + 1 segments. Empty pairs
  * (L_s = 0) get one item each, handed to worker e mod W for the e-th empty

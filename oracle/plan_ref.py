@@ -9,9 +9,11 @@ planner, so the two can be compared bit for bit:
   pairs p = (s, kvh), s-major; pages_p = ceil(L_s / 16); T = sum_p pages_p
   W = ceil(T / chunk_pages) if chunk_pages > 0
       else min(workers_per_cu * num_cus, ceil(T / min_chunk))   (1 if T = 0 < #pairs)
-  worker w owns global pages [floor(w*T/W), floor((w+1)*T/W)), cut at pair
-  boundaries into segments (items); empty pairs go to worker e mod W after
-  its segments; n_p = segments of pair p
+  worker w owns global pages [floor(T*C(w)/C(W)), floor(T*C(w+1)/C(W))) with
+  C(v) = 1000*v + p*(v % 2): even workers weigh 1000 + p, odd ones 1000 - p
+  (p = xcd_parity_skew per mille, default 20, -1 for none; none when
+  chunk_pages is forced); cut at pair boundaries into segments (items); empty
+  pairs go to worker e mod W after its segments; n_p = segments of pair p
   partial slots for pairs with n_p > 1 in pair order, segment c -> base + c
 
 Work list rows (int32 x 8): W worker-table rows (first item, count, then the
@@ -24,7 +26,7 @@ from __future__ import annotations
 import numpy as np
 
 PAGE = 16
-DEFAULTS = dict(workers_per_cu=4, min_chunk=8)
+DEFAULTS = dict(workers_per_cu=4, min_chunk=8, xcd_parity_skew=20)
 
 
 def _ceil(a, b):
@@ -36,9 +38,12 @@ def _align(x, a=256):
 
 
 def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
-         workers_per_cu=None, min_chunk=None):
+         workers_per_cu=None, min_chunk=None, xcd_parity_skew=0):
     wpc = workers_per_cu or DEFAULTS["workers_per_cu"]
     mn = min_chunk or DEFAULTS["min_chunk"]
+    skew = xcd_parity_skew or DEFAULTS["xcd_parity_skew"]
+    if skew < 0 or chunk_pages > 0:
+        skew = 0
     lens = [int(x) for x in seq_lens]
     pairs = [(s, kvh) for s in range(len(lens)) for kvh in range(num_kv_heads)]
     pages = [_ceil(lens[s], PAGE) for s, _ in pairs]
@@ -54,7 +59,9 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
 
     # every (worker, pair) overlap is a segment
     starts = np.cumsum([0] + pages)
-    bounds = [w * total // workers for w in range(workers + 1)] if workers else [0]
+    def weight_upto(v):          # C(v): the weights of workers 0 .. v - 1
+        return 1000 * v + skew * (v % 2)
+    bounds = [total * weight_upto(w) // weight_upto(workers) for w in range(workers + 1)] if workers else [0]
     per_worker = [[] for _ in range(workers)]
     seg_of_pair = {p: [] for p in range(len(pairs))}
     for w in range(workers):
@@ -103,7 +110,7 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
     g = num_q_heads // num_kv_heads
     ws = _align(slot * g * head_dim * 4) + _align(slot * g * 4) if slot else 0
     return dict(table=table, items=items, combine=comb, num_workers=workers,
-                chunk_pages=_ceil(total, workers) if workers and total else 0,
+                chunk_pages=max(b - a for a, b in zip(bounds, bounds[1:])) if workers and total else 0,
                 num_partials=slot, workspace_bytes=ws,
                 work_bytes=(table.shape[0] + items.shape[0] + comb.shape[0]) * 8 * 4)
 

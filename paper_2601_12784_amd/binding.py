@@ -42,7 +42,7 @@ class sf_attn_desc(ctypes.Structure):
 class sf_plan_opts(ctypes.Structure):
     _fields_ = [("num_cus", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
                 ("workers_per_cu", ctypes.c_int32), ("min_chunk_pages", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("xcd_parity_skew", ctypes.c_int32)]
 
 
 class sf_plan_info(ctypes.Structure):
@@ -189,8 +189,9 @@ def make_desc(num_seqs, num_q_heads, num_kv_heads, head_dim, block_table_stride,
                         int(page_size), int(block_table_stride), int(num_pages), float(softmax_scale))
 
 
-def make_opts(num_cus=0, chunk_pages=0, workers_per_cu=0, min_chunk_pages=0):
-    return sf_plan_opts(int(num_cus), int(chunk_pages), int(workers_per_cu), int(min_chunk_pages), 0)
+def make_opts(num_cus=0, chunk_pages=0, workers_per_cu=0, min_chunk_pages=0, xcd_parity_skew=0):
+    return sf_plan_opts(int(num_cus), int(chunk_pages), int(workers_per_cu), int(min_chunk_pages),
+                        int(xcd_parity_skew))
 
 
 def _addr(x) -> int | None:

@@ -76,13 +76,16 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   const int32_t B = desc->num_seqs;
   const int32_t hkv = desc->num_kv_heads;
   int32_t num_cus = kDefaultNumCus, forced = 0, wpc = kDefaultWorkersPerCu, mn = kDefaultMinChunk;
+  int32_t skew = kDefaultParitySkew;
   if (opts) {
     if (opts->num_cus < 0 || opts->chunk_pages < 0 || opts->workers_per_cu < 0 ||
-        opts->min_chunk_pages < 0 || opts->reserved != 0) return SF_ERR_INVALID_ARG;
+        opts->min_chunk_pages < 0 || opts->xcd_parity_skew < -1 || opts->xcd_parity_skew > kMaxParitySkew)
+      return SF_ERR_INVALID_ARG;
     if (opts->num_cus) num_cus = opts->num_cus;
     forced = opts->chunk_pages;
     if (opts->workers_per_cu) wpc = opts->workers_per_cu;
     if (opts->min_chunk_pages) mn = opts->min_chunk_pages;
+    if (opts->xcd_parity_skew) skew = opts->xcd_parity_skew < 0 ? 0 : opts->xcd_parity_skew;
   }
 
   // Pages per sequence (every KV head of a sequence has the same count).
@@ -112,23 +115,32 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   }
   if (workers > INT32_MAX / 2) return SF_ERR_INVALID_ARG;
 
-  // Worker range starts lo(w) = floor(w T / W), walked forward without
-  // divisions: quotient and remainder advance by T / W and T mod W.
+  // Worker range starts lo(w) = floor(T C(w) / C(W)) with the cumulative
+  // weight C(v) = 1000 v + p (v mod 2): worker v weighs 1000 + p if v is
+  // even, 1000 - p if odd (p = 0 for a forced slice size). Walked forward
+  // without divisions: T C(v) grows by T (1000 + p) or T (1000 - p), each
+  // below 2^51, and quotient and remainder advance by those over C(W).
+  if (forced > 0) skew = 0;
   struct Cuts {
-    int64_t q = 0, r = 0, dq = 0, dr = 0, den = 1;
-    void init(int64_t t, int64_t w) {
-      q = r = 0;
-      den = w > 0 ? w : 1;
-      dq = t / den;
-      dr = t % den;
+    int64_t q = 0, r = 0, den = 1, idx = 0;
+    int64_t dq[2] = {0, 0}, dr[2] = {0, 0};   // [v mod 2]: step from C(v) to C(v + 1)
+    void init(int64_t t, int64_t w, int64_t p) {
+      q = r = idx = 0;
+      den = w > 0 ? 1000 * w + p * (w & 1) : 1;
+      for (int k = 0; k < 2; ++k) {
+        const int64_t inc = t * (k == 0 ? 1000 + p : 1000 - p);
+        dq[k] = inc / den;
+        dr[k] = inc % den;
+      }
     }
     void next() {
-      q += dq;
-      r += dr;
+      q += dq[idx & 1];
+      r += dr[idx & 1];
       if (r >= den) {
         r -= den;
         ++q;
       }
+      ++idx;
     }
   };
 
@@ -141,7 +153,7 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   int64_t n_work = 0, n_comb = 0, n_part = 0, n_empty = 0;
   {
     Cuts next_lo;           // lo(cur + 1)
-    next_lo.init(total, workers);
+    next_lo.init(total, workers, skew);
     next_lo.next();
     int64_t cur = 0;        // worker whose range holds `start`
     int64_t start = 0;      // global page where the current pair starts
@@ -184,7 +196,18 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   info->num_work = int32_t(n_work);
   info->num_combine = int32_t(n_comb);
   info->num_partials = int32_t(n_part);
-  info->chunk_pages = workers && total ? int32_t((total + workers - 1) / workers) : 0;
+  {
+    // the widest slice (an even worker's when the slices are skewed)
+    Cuts c;
+    c.init(total, workers, skew);
+    int64_t prev = 0, widest = 0;
+    for (int64_t w = 0; w < workers; ++w) {
+      c.next();
+      widest = std::max(widest, c.q - prev);
+      prev = c.q;
+    }
+    info->chunk_pages = int32_t(widest);
+  }
   info->reserved = 0;
   info->work_bytes = uint64_t(table_rows + n_work + n_comb) * kItemInts * 4;
   info->workspace_bytes =
@@ -249,8 +272,8 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   int64_t row = 0, pstart = 0;
   int32_t seg_c = 0;  // segment index within the current pair
   Cuts lo_w, hi_w;
-  lo_w.init(total, workers);
-  hi_w.init(total, workers);
+  lo_w.init(total, workers, skew);
+  hi_w.init(total, workers, skew);
   hi_w.next();
   for (int64_t w = 0; w < workers; ++w, lo_w.next(), hi_w.next()) {
     const int64_t lo = lo_w.q, hi = hi_w.q;

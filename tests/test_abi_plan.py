@@ -41,14 +41,15 @@ def test_struct_sizes_match_header():
 # ---------------------------------------------------------------------------
 # planner parity
 # ---------------------------------------------------------------------------
-def _plan_both(lens, hq, hkv, d, num_cus=256, chunk=0, wpc=0, mn=0, stride=None):
+def _plan_both(lens, hq, hkv, d, num_cus=256, chunk=0, wpc=0, mn=0, stride=None, skew=0):
     lens = np.asarray(lens, dtype=np.int32)
     if stride is None:
         stride = max(1, int(((lens.astype(np.int64) + PAGE - 1) // PAGE).max(initial=1)))
     desc = B.make_desc(lens.size, hq, hkv, d, stride, 1, 0.1)
-    opts = B.make_opts(num_cus=num_cus, chunk_pages=chunk, workers_per_cu=wpc, min_chunk_pages=mn)
+    opts = B.make_opts(num_cus=num_cus, chunk_pages=chunk, workers_per_cu=wpc, min_chunk_pages=mn,
+                       xcd_parity_skew=skew)
     info, work = B.sf_decode_attn_plan(desc, lens, opts)
-    ref = plan_ref.plan(lens, hkv, hq, d, num_cus, chunk, wpc or None, mn or None)
+    ref = plan_ref.plan(lens, hkv, hq, d, num_cus, chunk, wpc or None, mn or None, skew)
     return info, work[: info.work_bytes // 4].reshape(-1, 8), ref
 
 
@@ -97,6 +98,18 @@ def test_plan_matches_rederivation_knobs():
     assert info.num_workers == 96
 
 
+@pytest.mark.parametrize("skew", [-1, 1, 50, 250])
+def test_plan_matches_rederivation_parity_skew(skew):
+    rng = np.random.default_rng(40 + skew)
+    lens = np.exp(rng.normal(np.log(2000), 1.0, size=180)).astype(np.int64).clip(0, 16384)
+    info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=64, skew=skew)
+    _assert_same(info, work, ref)
+    # a forced slice size ignores the skew: the same plan with and without it
+    a, wa, _ = _plan_both(lens, 28, 4, 128, chunk=37, skew=skew)
+    b, wb, _ = _plan_both(lens, 28, 4, 128, chunk=37, skew=-1)
+    assert a.num_workers == b.num_workers and np.array_equal(wa, wb)
+
+
 def test_plan_all_empty_and_no_sequences():
     info, work, ref = _plan_both([0, 0, 0], 8, 2, 128)
     _assert_same(info, work, ref)
@@ -133,16 +146,20 @@ def test_tiny_plan_by_hand():
     assert info.workspace_bytes == 5 * 4 * 64 * 4 + 256
 
 
-@pytest.mark.parametrize("seed", range(4))
-def test_plan_invariants(seed):
-    """Every worker owns floor or ceil of T / W pages; each pair's segments tile
-    [0, pages) in worker order; slots of cut pairs are consecutive; every
-    pair appears; empty pairs have one empty item."""
+@pytest.mark.parametrize("seed,skew", [(0, 0), (1, 0), (2, -1), (3, -1), (4, 120)])
+def test_plan_invariants(seed, skew):
+    """Every worker owns its share of the T pages to within one page: T / W
+    without the parity skew, T (1000 + p) / (1000 W) for an even worker and
+    T (1000 - p) / (1000 W) for an odd one with it (W even; one more odd
+    worker's weight of 1000 + p in the total otherwise); the slices tile
+    [0, T) in order; each pair's segments tile [0, pages) in worker order;
+    slots of cut pairs are consecutive; every pair appears; empty pairs have
+    one empty item."""
     rng = np.random.default_rng(100 + seed)
     lens = rng.integers(0, 20000, size=int(rng.integers(1, 200)))
     lens[rng.random(lens.size) < 0.1] = 0
     hkv = 4
-    info, work, _ = _plan_both(lens, 28, hkv, 128, num_cus=int(rng.integers(1, 300)))
+    info, work, _ = _plan_both(lens, 28, hkv, 128, num_cus=int(rng.integers(1, 300)), skew=skew)
     table, items, comb = _split(info, work)
     tab = table[:, :2]
     # each worker's row repeats the first six ints of its first item
@@ -152,9 +169,18 @@ def test_plan_invariants(seed):
     W = info.num_workers
     assert np.array_equal(tab[:, 0], np.concatenate([[0], np.cumsum(tab[:, 1])[:-1]]))
     assert tab[:, 1].sum() == info.num_work
+    p = {0: 20, -1: 0}.get(skew, skew)
+    weight = [1000 + p if w % 2 == 0 else 1000 - p for w in range(W)]
+    owned = []
     for w in range(W):
         seg = items[tab[w, 0]: tab[w, 0] + tab[w, 1]]
-        assert (seg[:, 3] - seg[:, 2]).sum() in (total // W, -(-total // W))
+        got = int((seg[:, 3] - seg[:, 2]).sum())
+        share = total * weight[w] / sum(weight)
+        assert abs(got - share) < 1.0, (w, got, share)
+        owned.append(got)
+    assert sum(owned) == total
+    if p == 0:
+        assert set(owned) <= {total // W, -(-total // W)}
     for s, L in enumerate(lens):
         npg = int(pages[s])
         for kvh in range(hkv):
@@ -181,7 +207,7 @@ def test_plan_rejects_bad_knobs(lib):
     lens = np.array([10, 20], np.int32)
     info = B.sf_plan_info()
     for field, value in (("num_cus", -1), ("chunk_pages", -1), ("workers_per_cu", -1),
-                         ("min_chunk_pages", -1), ("reserved", 1)):
+                         ("min_chunk_pages", -1), ("xcd_parity_skew", -2), ("xcd_parity_skew", 251)):
         opts = B.make_opts()
         setattr(opts, field, value)
         assert lib.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts), None, 0,
