@@ -117,7 +117,9 @@ typedef struct sf_plan_info {
  * p (v mod 2): every worker reads its share of the pages however skewed the
  * lengths are, 1000 + p per mille of the mean for an even w, 1000 - p for an
  * odd one (p = opts->xcd_parity_skew, default 20; p = 0, equal slices within
- * one page, when chunk_pages is forced). Worker w runs as workgroup w, and
+ * one page, when chunk_pages is forced, and also when the skewed slices would
+ * cut more than floor(W / 8) more pairs than the equal ones: equal lengths
+ * can put every equal boundary on a pair boundary). Worker w runs as workgroup w, and
  * workgroups are spread over the 8 XCDs round-robin: on MI355X the odd XCDs
  * took 3-4 % longer than their even neighbours on the same work. A worker's range is
  * cut at pair boundaries into segments, each a work item on one pair; a pair

@@ -12,7 +12,8 @@ planner, so the two can be compared bit for bit:
   worker w owns global pages [floor(T*C(w)/C(W)), floor(T*C(w+1)/C(W))) with
   C(v) = 1000*v + p*(v % 2): even workers weigh 1000 + p, odd ones 1000 - p
   (p = xcd_parity_skew per mille, default 20, -1 for none; none when
-  chunk_pages is forced); cut at pair boundaries into segments (items); empty
+  chunk_pages is forced, or when these slices cut more than W // 8 pairs more
+  than the equal ones, p = 0, would); cut at pair boundaries into segments (items); empty
   pairs go to worker e mod W after its segments; n_p = segments of pair p
   partial slots for pairs with n_p > 1 in pair order, segment c -> base + c
 
@@ -59,9 +60,24 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
 
     # every (worker, pair) overlap is a segment
     starts = np.cumsum([0] + pages)
-    def weight_upto(v):          # C(v): the weights of workers 0 .. v - 1
-        return 1000 * v + skew * (v % 2)
-    bounds = [total * weight_upto(w) // weight_upto(workers) for w in range(workers + 1)] if workers else [0]
+
+    def cuts_for(p):
+        def weight_upto(v):      # C(v): the weights of workers 0 .. v - 1
+            return 1000 * v + p * (v % 2)
+        return [total * weight_upto(w) // weight_upto(workers) for w in range(workers + 1)] if workers else [0]
+
+    def pairs_cut(bounds):       # pairs with a worker boundary strictly inside them
+        inner = np.asarray(bounds[1:-1], dtype=np.int64)
+        lo, hi = np.asarray(starts[:-1], np.int64), np.asarray(starts[1:], np.int64)
+        first_after = np.searchsorted(inner, lo, side="right")   # boundaries > start
+        first_at_end = np.searchsorted(inner, hi, side="left")   # boundaries >= end
+        return int(np.count_nonzero(first_at_end > first_after))
+
+    bounds = cuts_for(skew)
+    if skew and workers > 1:
+        equal = cuts_for(0)
+        if pairs_cut(bounds) - pairs_cut(equal) > workers // 8:
+            bounds = equal
     per_worker = [[] for _ in range(workers)]
     seg_of_pair = {p: [] for p in range(len(pairs))}
     for w in range(workers):

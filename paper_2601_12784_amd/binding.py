@@ -604,7 +604,7 @@ class DecodeAttention:
     distinct set of tensors (the last 64 sets are remembered)."""
 
     def __init__(self, num_q_heads, num_kv_heads, head_dim, device=None, num_cus=None,
-                 ring: int = 4, opts: sf_plan_opts | None = None):
+                 opts: sf_plan_opts | None = None):
         self.hq, self.hkv, self.d = int(num_q_heads), int(num_kv_heads), int(head_dim)
         self.device = torch.device(device or "cuda")
         if num_cus is None:
@@ -625,10 +625,10 @@ class DecodeAttention:
 
     def _runner(self, chunk_pages):
         o = self.opts
-        key = (o.num_cus, int(chunk_pages or 0), o.workers_per_cu, o.min_chunk_pages)
+        key = (o.num_cus, int(chunk_pages or 0), o.workers_per_cu, o.min_chunk_pages, o.xcd_parity_skew)
         r = self._runners.get(key)
         if r is None:
-            opts = sf_plan_opts(key[0], key[1], key[2], key[3], 0)
+            opts = sf_plan_opts(*key)
             shape = make_desc(0, self.hq, self.hkv, self.d, 1, 0, 1.0)
             r = ctypes.c_void_p()
             with torch.cuda.device(self.device):

@@ -147,23 +147,19 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   // Pass 1: segments per pair. Worker ranges are cut at pair boundaries; a
   // pair spanning k worker boundaries has k + 1 segments. Pairs are walked in
   // order (s-major, kvh-minor) with a worker cursor that only moves forward.
-  thread_local std::vector<int32_t> nseg_buf;
-  nseg_buf.assign(size_t(num_pairs), 0);
-  int32_t* nseg = nseg_buf.data();
-  int64_t n_work = 0, n_comb = 0, n_part = 0, n_empty = 0;
-  {
+  // Returns the number of cut pairs.
+  auto segments = [&](int64_t p_skew, int32_t* nseg) -> int64_t {
     Cuts next_lo;           // lo(cur + 1)
-    next_lo.init(total, workers, skew);
+    next_lo.init(total, workers, p_skew);
     next_lo.next();
     int64_t cur = 0;        // worker whose range holds `start`
     int64_t start = 0;      // global page where the current pair starts
-    int64_t p = 0;
+    int64_t p = 0, cut = 0;
     for (int32_t s = 0; s < B; ++s) {
       const int64_t npg = spg[s];
       for (int32_t h = 0; h < hkv; ++h, ++p) {
         if (npg == 0) {
           nseg[p] = 1;
-          ++n_empty;
           continue;
         }
         while (cur + 1 < workers && next_lo.q <= start) {
@@ -178,10 +174,32 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
           ++k;
         }
         nseg[p] = k;
+        cut += k > 1;
         start += npg;
       }
     }
+    return cut;
+  };
+  thread_local std::vector<int32_t> nseg_buf, nseg_alt;
+  nseg_buf.resize(size_t(num_pairs));
+  int32_t* nseg = nseg_buf.data();
+  if (skew > 0 && workers > 1) {
+    // The skew moves every boundary off the equal cuts; where those fall on
+    // pair boundaries (equal lengths, page-aligned) it would cut pairs the
+    // equal slices leave whole. Keep it unless it cuts more than W / 8 pairs
+    // more than they do.
+    nseg_alt.resize(size_t(num_pairs));
+    const int64_t cut_skew = segments(skew, nseg);
+    const int64_t cut_equal = segments(0, nseg_alt.data());
+    if (cut_skew - cut_equal > workers / 8) {
+      skew = 0;
+      nseg_buf.swap(nseg_alt);
+      nseg = nseg_buf.data();
+    }
+  } else {
+    segments(skew, nseg);
   }
+  int64_t n_work = 0, n_comb = 0, n_part = 0;
   for (int64_t p = 0; p < num_pairs; ++p) {
     n_work += nseg[p];
     if (nseg[p] > 1) {
@@ -246,6 +264,8 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   // the empty pairs e with e mod workers == w.
   thread_local std::vector<int64_t> empty_buf;
   empty_buf.clear();
+  int64_t n_empty = 0;
+  for (int32_t s = 0; s < B; ++s) n_empty += spg[s] == 0 ? hkv : 0;
   empty_buf.reserve(size_t(n_empty));
   for (int32_t s = 0; s < B; ++s)
     if (spg[s] == 0)

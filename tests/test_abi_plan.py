@@ -98,6 +98,22 @@ def test_plan_matches_rederivation_knobs():
     assert info.num_workers == 96
 
 
+def test_plan_skew_kept_or_dropped_by_cut_count():
+    """The default skew is dropped where equal slices fall on pair boundaries
+    (equal, page-aligned lengths: one pair per worker, no cut) and it would
+    cut more than W / 8 pairs more; on skewed lengths it is kept."""
+    aligned = [1600] * 8
+    a, wa, _ = _plan_both(aligned, 28, 4, 128, num_cus=8)
+    e, we, _ = _plan_both(aligned, 28, 4, 128, num_cus=8, skew=-1)
+    assert (a.num_workers, a.num_work, a.num_combine) == (32, 32, 0) and np.array_equal(wa, we)
+    rng = np.random.default_rng(5)
+    lens = np.exp(rng.normal(np.log(1500), 1.0, size=24)).astype(np.int64).clip(16, 12000)
+    s, ws, _ = _plan_both(lens, 28, 4, 128, num_cus=8)
+    e, we, _ = _plan_both(lens, 28, 4, 128, num_cus=8, skew=-1)
+    assert s.chunk_pages > e.chunk_pages                     # kept: even workers own more
+    assert s.num_combine - e.num_combine <= s.num_workers // 8
+
+
 @pytest.mark.parametrize("skew", [-1, 1, 50, 250])
 def test_plan_matches_rederivation_parity_skew(skew):
     rng = np.random.default_rng(40 + skew)
@@ -105,8 +121,8 @@ def test_plan_matches_rederivation_parity_skew(skew):
     info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=64, skew=skew)
     _assert_same(info, work, ref)
     # a forced slice size ignores the skew: the same plan with and without it
-    a, wa, _ = _plan_both(lens, 28, 4, 128, chunk=37, skew=skew)
-    b, wb, _ = _plan_both(lens, 28, 4, 128, chunk=37, skew=-1)
+    a, wa, _ = _plan_both(lens, 28, 4, 128, chunk=400, skew=skew)
+    b, wb, _ = _plan_both(lens, 28, 4, 128, chunk=400, skew=-1)
     assert a.num_workers == b.num_workers and np.array_equal(wa, wb)
 
 

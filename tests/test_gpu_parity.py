@@ -437,6 +437,31 @@ def test_runner_ring_reuse_with_growing_and_shrinking_plans():
         assert_close(l, ref[1], f"ring step {i} lse")
 
 
+def test_runner_takes_every_plan_option():
+    """DecodeAttention hands all of its planner options to its native runner:
+    its plan (widest slice, cut pairs) is the host planner's for the same
+    options, with the XCD-parity skew off, at its default and at 200 per
+    mille. Every plan against the oracle."""
+    rng = np.random.default_rng(5)
+    lens = np.exp(rng.normal(np.log(1500), 1.0, size=24)).astype(np.int64).clip(16, 12000)
+    b = build_batch(lens, 28, 4, 128, 78)
+    ref = run_oracle(b)
+    desc = B.make_desc(b.num_seqs, 28, 4, 128, b.block_table.shape[1], b.num_pages, b.scale)
+    widest = set()
+    for skew in (-1, 0, 200):
+        opts = B.make_opts(num_cus=8, xcd_parity_skew=skew)
+        host, _ = B.sf_decode_attn_plan(desc, b.seq_lens, opts)
+        runner = B.DecodeAttention(28, 4, 128, opts=opts)
+        out, lse, _ = run_gpu(b, runner=runner)
+        assert_close(out, ref[0], f"skew {skew} out")
+        assert_close(lse, ref[1], f"skew {skew} lse")
+        got = runner.last_info
+        assert (got.num_workers, got.num_work, got.num_combine, got.chunk_pages) == \
+            (host.num_workers, host.num_work, host.num_combine, host.chunk_pages)
+        widest.add(got.chunk_pages)
+    assert len(widest) == 3   # three different plans reached the kernels
+
+
 def test_runner_steps_switching_streams_in_order():
     """Forty runner steps that move between two streams every five steps, each
     switch ordered by an event wait on the stream before (no host
