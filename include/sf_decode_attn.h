@@ -84,8 +84,8 @@ typedef struct sf_plan_opts {
   int32_t chunk_pages;      /* > 0 forces the pages per worker: workers = ceil(T / chunk_pages) */
   int32_t workers_per_cu;   /* default 4: attention waves per CU (one per SIMD) */
   int32_t min_chunk_pages;  /* default 8: fewer workers rather than slices thinner than this */
-  int32_t xcd_parity_skew;  /* p in the slice rule below, per mille: 0 = default 20, -1 = none,
-                               at most 250; ignored (none) when chunk_pages > 0 */
+  int32_t xcd_parity_skew;  /* p in the slice rule below, per mille, -250 .. 250: default 0
+                               (equal slices); ignored when chunk_pages > 0 */
 } sf_plan_opts;
 
 /* Filled by the planner; passed back unchanged to the other calls. */
@@ -116,12 +116,13 @@ typedef struct sf_plan_info {
  * [floor(T C(w) / C(W)), floor(T C(w + 1) / C(W))) with C(v) = 1000 v +
  * p (v mod 2): every worker reads its share of the pages however skewed the
  * lengths are, 1000 + p per mille of the mean for an even w, 1000 - p for an
- * odd one (p = opts->xcd_parity_skew, default 20; p = 0, equal slices within
- * one page, when chunk_pages is forced, and also when the skewed slices would
- * cut more than floor(W / 8) more pairs than the equal ones: equal lengths
- * can put every equal boundary on a pair boundary). Worker w runs as workgroup w, and
- * workgroups are spread over the 8 XCDs round-robin: on MI355X the odd XCDs
- * took 3-4 % longer than their even neighbours on the same work. A worker's range is
+ * odd one (p = opts->xcd_parity_skew, default 0: equal slices, within one
+ * page; p is also 0 when chunk_pages is forced, and when the skewed slices
+ * would cut more than floor(W / 8) more pairs than the equal ones: equal
+ * lengths can put every equal boundary on a pair boundary). Worker w runs as
+ * workgroup w, and workgroup w runs on XCD w mod 8: a GPU whose odd (p > 0)
+ * or even (p < 0) XCDs are slower on the same work can give them less. How
+ * much slower, and which, differs from one MI355X to the next. A worker's range is
  * cut at pair boundaries into segments, each a work item on one pair; a pair
  * crossing k worker boundaries has n_p = k + 1 segments. Empty pairs
  * (L_s = 0) get one item each, handed to worker e mod W for the e-th empty

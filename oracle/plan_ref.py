@@ -11,9 +11,9 @@ planner, so the two can be compared bit for bit:
       else min(workers_per_cu * num_cus, ceil(T / min_chunk))   (1 if T = 0 < #pairs)
   worker w owns global pages [floor(T*C(w)/C(W)), floor(T*C(w+1)/C(W))) with
   C(v) = 1000*v + p*(v % 2): even workers weigh 1000 + p, odd ones 1000 - p
-  (p = xcd_parity_skew per mille, default 20, -1 for none; none when
-  chunk_pages is forced, or when these slices cut more than W // 8 pairs more
-  than the equal ones, p = 0, would); cut at pair boundaries into segments (items); empty
+  (p = xcd_parity_skew per mille, -250 .. 250, default 0; 0 when chunk_pages
+  is forced, or when these slices cut more than W // 8 pairs more than the
+  equal ones, p = 0, would); cut at pair boundaries into segments (items); empty
   pairs go to worker e mod W after its segments; n_p = segments of pair p
   partial slots for pairs with n_p > 1 in pair order, segment c -> base + c
 
@@ -27,7 +27,7 @@ from __future__ import annotations
 import numpy as np
 
 PAGE = 16
-DEFAULTS = dict(workers_per_cu=4, min_chunk=8, xcd_parity_skew=20)
+DEFAULTS = dict(workers_per_cu=4, min_chunk=8)
 
 
 def _ceil(a, b):
@@ -42,9 +42,7 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
          workers_per_cu=None, min_chunk=None, xcd_parity_skew=0):
     wpc = workers_per_cu or DEFAULTS["workers_per_cu"]
     mn = min_chunk or DEFAULTS["min_chunk"]
-    skew = xcd_parity_skew or DEFAULTS["xcd_parity_skew"]
-    if skew < 0 or chunk_pages > 0:
-        skew = 0
+    skew = 0 if chunk_pages > 0 else int(xcd_parity_skew)
     lens = [int(x) for x in seq_lens]
     pairs = [(s, kvh) for s in range(len(lens)) for kvh in range(num_kv_heads)]
     pages = [_ceil(lens[s], PAGE) for s, _ in pairs]

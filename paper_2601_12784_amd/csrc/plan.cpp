@@ -76,16 +76,17 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   const int32_t B = desc->num_seqs;
   const int32_t hkv = desc->num_kv_heads;
   int32_t num_cus = kDefaultNumCus, forced = 0, wpc = kDefaultWorkersPerCu, mn = kDefaultMinChunk;
-  int32_t skew = kDefaultParitySkew;
+  int32_t skew = 0;
   if (opts) {
     if (opts->num_cus < 0 || opts->chunk_pages < 0 || opts->workers_per_cu < 0 ||
-        opts->min_chunk_pages < 0 || opts->xcd_parity_skew < -1 || opts->xcd_parity_skew > kMaxParitySkew)
+        opts->min_chunk_pages < 0 || opts->xcd_parity_skew < -kMaxParitySkew ||
+        opts->xcd_parity_skew > kMaxParitySkew)
       return SF_ERR_INVALID_ARG;
     if (opts->num_cus) num_cus = opts->num_cus;
     forced = opts->chunk_pages;
     if (opts->workers_per_cu) wpc = opts->workers_per_cu;
     if (opts->min_chunk_pages) mn = opts->min_chunk_pages;
-    if (opts->xcd_parity_skew) skew = opts->xcd_parity_skew < 0 ? 0 : opts->xcd_parity_skew;
+    skew = opts->xcd_parity_skew;
   }
 
   // Pages per sequence (every KV head of a sequence has the same count).
@@ -117,9 +118,10 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
 
   // Worker range starts lo(w) = floor(T C(w) / C(W)) with the cumulative
   // weight C(v) = 1000 v + p (v mod 2): worker v weighs 1000 + p if v is
-  // even, 1000 - p if odd (p = 0 for a forced slice size). Walked forward
-  // without divisions: T C(v) grows by T (1000 + p) or T (1000 - p), each
-  // below 2^51, and quotient and remainder advance by those over C(W).
+  // even, 1000 - p if odd (|p| <= 250; p = 0 for a forced slice size).
+  // Walked forward without divisions: T C(v) grows by T (1000 + p) or
+  // T (1000 - p), each positive and below 2^51, and quotient and remainder
+  // advance by those over C(W) > 0.
   if (forced > 0) skew = 0;
   struct Cuts {
     int64_t q = 0, r = 0, den = 1, idx = 0;
@@ -183,7 +185,7 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   thread_local std::vector<int32_t> nseg_buf, nseg_alt;
   nseg_buf.resize(size_t(num_pairs));
   int32_t* nseg = nseg_buf.data();
-  if (skew > 0 && workers > 1) {
+  if (skew != 0 && workers > 1) {
     // The skew moves every boundary off the equal cuts; where those fall on
     // pair boundaries (equal lengths, page-aligned) it would cut pairs the
     // equal slices leave whole. Keep it unless it cuts more than W / 8 pairs

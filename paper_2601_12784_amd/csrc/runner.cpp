@@ -154,7 +154,8 @@ extern "C" sf_status sf_runner_create(const sf_attn_desc* shape, const sf_plan_o
   probe.num_pages = probe.num_pages >= 0 ? probe.num_pages : 0;
   sf_status st = sf::validate_desc(&probe);
   if (st != SF_OK) return st;
-  if (opts && (opts->xcd_parity_skew < -1 || opts->xcd_parity_skew > sf::kMaxParitySkew)) return SF_ERR_INVALID_ARG;
+  if (opts && (opts->xcd_parity_skew < -sf::kMaxParitySkew || opts->xcd_parity_skew > sf::kMaxParitySkew))
+    return SF_ERR_INVALID_ARG;
   sf_runner* r = new (std::nothrow) sf_runner();
   if (!r) return SF_ERR_HIP;
   r->shape = probe;

@@ -18,10 +18,8 @@ constexpr int kMaxGroup = 16;   // query heads per KV head handled by one MFMA c
 constexpr int kDefaultNumCus = 256;
 constexpr int kDefaultWorkersPerCu = 4;  // attention waves per CU (one per SIMD)
 constexpr int kDefaultMinChunk = 8;      // pages: fewer workers rather than thinner slices
-// Per-mille of a worker's weight moved from odd-indexed to even-indexed
-// workers: workgroups go to the 8 XCDs round-robin, and odd XCDs ran the
-// same work 3-4 % slower than their even neighbours.
-constexpr int kDefaultParitySkew = 20;
+// Largest per-mille shift of page share between even- and odd-indexed
+// workers (sf_plan_opts.xcd_parity_skew; none by default).
 constexpr int kMaxParitySkew = 250;
 
 sf_status validate_desc(const sf_attn_desc* d);

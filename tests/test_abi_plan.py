@@ -99,30 +99,32 @@ def test_plan_matches_rederivation_knobs():
 
 
 def test_plan_skew_kept_or_dropped_by_cut_count():
-    """The default skew is dropped where equal slices fall on pair boundaries
-    (equal, page-aligned lengths: one pair per worker, no cut) and it would
-    cut more than W / 8 pairs more; on skewed lengths it is kept."""
+    """A skew is dropped where equal slices fall on pair boundaries (equal,
+    page-aligned lengths: one pair per worker, no cut) and it would cut more
+    than W / 8 pairs more; on skewed lengths it is kept."""
     aligned = [1600] * 8
-    a, wa, _ = _plan_both(aligned, 28, 4, 128, num_cus=8)
-    e, we, _ = _plan_both(aligned, 28, 4, 128, num_cus=8, skew=-1)
-    assert (a.num_workers, a.num_work, a.num_combine) == (32, 32, 0) and np.array_equal(wa, we)
+    for skew in (20, -20):
+        a, wa, _ = _plan_both(aligned, 28, 4, 128, num_cus=8, skew=skew)
+        e, we, _ = _plan_both(aligned, 28, 4, 128, num_cus=8)
+        assert (a.num_workers, a.num_work, a.num_combine) == (32, 32, 0) and np.array_equal(wa, we)
     rng = np.random.default_rng(5)
     lens = np.exp(rng.normal(np.log(1500), 1.0, size=24)).astype(np.int64).clip(16, 12000)
-    s, ws, _ = _plan_both(lens, 28, 4, 128, num_cus=8)
-    e, we, _ = _plan_both(lens, 28, 4, 128, num_cus=8, skew=-1)
-    assert s.chunk_pages > e.chunk_pages                     # kept: even workers own more
-    assert s.num_combine - e.num_combine <= s.num_workers // 8
+    e, we, _ = _plan_both(lens, 28, 4, 128, num_cus=8)
+    for skew in (20, -20):
+        s, ws, _ = _plan_both(lens, 28, 4, 128, num_cus=8, skew=skew)
+        assert s.chunk_pages > e.chunk_pages                 # kept: the favoured workers own more
+        assert s.num_combine - e.num_combine <= s.num_workers // 8
 
 
-@pytest.mark.parametrize("skew", [-1, 1, 50, 250])
+@pytest.mark.parametrize("skew", [-250, -30, 1, 50, 250])
 def test_plan_matches_rederivation_parity_skew(skew):
-    rng = np.random.default_rng(40 + skew)
+    rng = np.random.default_rng(400 + skew)
     lens = np.exp(rng.normal(np.log(2000), 1.0, size=180)).astype(np.int64).clip(0, 16384)
     info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=64, skew=skew)
     _assert_same(info, work, ref)
     # a forced slice size ignores the skew: the same plan with and without it
     a, wa, _ = _plan_both(lens, 28, 4, 128, chunk=400, skew=skew)
-    b, wb, _ = _plan_both(lens, 28, 4, 128, chunk=400, skew=-1)
+    b, wb, _ = _plan_both(lens, 28, 4, 128, chunk=400)
     assert a.num_workers == b.num_workers and np.array_equal(wa, wb)
 
 
@@ -162,11 +164,11 @@ def test_tiny_plan_by_hand():
     assert info.workspace_bytes == 5 * 4 * 64 * 4 + 256
 
 
-@pytest.mark.parametrize("seed,skew", [(0, 0), (1, 0), (2, -1), (3, -1), (4, 120)])
+@pytest.mark.parametrize("seed,skew", [(0, 0), (1, 0), (2, -40), (3, 0), (4, 120)])
 def test_plan_invariants(seed, skew):
     """Every worker owns its share of the T pages to within one page: T / W
-    without the parity skew, T (1000 + p) / (1000 W) for an even worker and
-    T (1000 - p) / (1000 W) for an odd one with it (W even; one more odd
+    without a parity skew, T (1000 + p) / (1000 W) for an even worker and
+    T (1000 - p) / (1000 W) for an odd one with skew p (W even; one more even
     worker's weight of 1000 + p in the total otherwise); the slices tile
     [0, T) in order; each pair's segments tile [0, pages) in worker order;
     slots of cut pairs are consecutive; every pair appears; empty pairs have
@@ -185,7 +187,7 @@ def test_plan_invariants(seed, skew):
     W = info.num_workers
     assert np.array_equal(tab[:, 0], np.concatenate([[0], np.cumsum(tab[:, 1])[:-1]]))
     assert tab[:, 1].sum() == info.num_work
-    p = {0: 20, -1: 0}.get(skew, skew)
+    p = skew
     weight = [1000 + p if w % 2 == 0 else 1000 - p for w in range(W)]
     owned = []
     for w in range(W):
@@ -223,7 +225,7 @@ def test_plan_rejects_bad_knobs(lib):
     lens = np.array([10, 20], np.int32)
     info = B.sf_plan_info()
     for field, value in (("num_cus", -1), ("chunk_pages", -1), ("workers_per_cu", -1),
-                         ("min_chunk_pages", -1), ("xcd_parity_skew", -2), ("xcd_parity_skew", 251)):
+                         ("min_chunk_pages", -1), ("xcd_parity_skew", -251), ("xcd_parity_skew", 251)):
         opts = B.make_opts()
         setattr(opts, field, value)
         assert lib.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts), None, 0,

@@ -440,15 +440,15 @@ def test_runner_ring_reuse_with_growing_and_shrinking_plans():
 def test_runner_takes_every_plan_option():
     """DecodeAttention hands all of its planner options to its native runner:
     its plan (widest slice, cut pairs) is the host planner's for the same
-    options, with the XCD-parity skew off, at its default and at 200 per
-    mille. Every plan against the oracle."""
+    options, with no XCD-parity skew and with -120 and 200 per mille. Every
+    plan against the oracle."""
     rng = np.random.default_rng(5)
     lens = np.exp(rng.normal(np.log(1500), 1.0, size=24)).astype(np.int64).clip(16, 12000)
     b = build_batch(lens, 28, 4, 128, 78)
     ref = run_oracle(b)
     desc = B.make_desc(b.num_seqs, 28, 4, 128, b.block_table.shape[1], b.num_pages, b.scale)
     widest = set()
-    for skew in (-1, 0, 200):
+    for skew in (-120, 0, 200):
         opts = B.make_opts(num_cus=8, xcd_parity_skew=skew)
         host, _ = B.sf_decode_attn_plan(desc, b.seq_lens, opts)
         runner = B.DecodeAttention(28, 4, 128, opts=opts)

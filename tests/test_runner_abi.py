@@ -21,7 +21,7 @@ def test_runner_rejects_bad_arguments_without_a_device():
     assert L.sf_runner_create(ctypes.byref(bad), None, ctypes.byref(r)) == 1
     odd = B.make_desc(0, 4, 1, 96, 1, 0, 1.0)               # head_dim 96 is not built
     assert L.sf_runner_create(ctypes.byref(odd), None, ctypes.byref(r)) == 2
-    opts = B.sf_plan_opts(0, 0, 0, 0, -2)                    # parity skew below -1
+    opts = B.sf_plan_opts(0, 0, 0, 0, -251)                  # parity skew below -250
     good = B.make_desc(0, 4, 1, 128, 1, 0, 1.0)
     assert L.sf_runner_create(ctypes.byref(good), ctypes.byref(opts), ctypes.byref(r)) == 1
     desc = B.make_desc(1, 4, 1, 128, 1, 1, 1.0)
