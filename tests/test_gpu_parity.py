@@ -278,6 +278,20 @@ def test_ragged_shapes(hq, hkv, d):
     check_batch(b, ref, chunk_pages=3)
 
 
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (8, 1)])
+def test_one_very_long_sequence(hq, hkv):
+    """A 200k-token sequence next to a 1-token one: the default plan cuts each
+    of the long sequence's pairs into hundreds of segments (about a thousand
+    with one KV head), so one combine row merges that many partials."""
+    lens = np.array([200_000, 1], np.int64)
+    b = build_batch(lens, hq, hkv, 128, 44)
+    ref = run_oracle(b)
+    _say(f"very long sequence hq={hq} hkv={hkv}")
+    out, lse, info = check_batch(b, ref)
+    assert info.num_combine == hkv
+    assert info.num_partials >= 250 * hkv
+
+
 def test_sharp_softmax_scaled_keys():
     """Keys scaled by 3 (the 32B-like workload's sharpening) at mid size."""
     lens = np.random.default_rng(9).integers(1, 6000, size=24)
