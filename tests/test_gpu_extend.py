@@ -93,6 +93,17 @@ def test_extend_small(case, shape):
     assert_close(out, lse, run_oracle(eb), f"{case} {shape}")
 
 
+@pytest.mark.parametrize("shape", [(28, 4, 128), (16, 1, 128)], ids=lambda s: "x".join(map(str, s)))
+def test_extend_after_a_long_prefix(shape):
+    """New tokens after a 100k-token cache: the items walk about 6250 pages
+    of keys each, the longest key walks the kernel takes."""
+    hq, hkv, d = shape
+    eb = build_extend([100_000, 5_000], [40, 700], hq, hkv, d, seed=91 + hq)
+    _say(f"extend after a long prefix hq={hq} hkv={hkv}")
+    out, lse, *_ = run_gpu(eb)
+    assert_close(out, lse, run_oracle(eb), f"long prefix {shape}")
+
+
 def test_extend_with_no_new_tokens_launches_nothing():
     eb = build_extend([40, 16], [0, 0], 8, 2, 64, seed=3)
     _say("extend empty")
