@@ -82,6 +82,19 @@ def test_fp8_attention_split_pairs(chunk):
     assert_close(lse, rl, f"chunk {chunk} lse")
 
 
+def test_fp8_attention_one_very_long_sequence():
+    """A 200k-token sequence beside a 1-token one over the fp8 cache: each
+    pair is cut into hundreds of segments (eight workers per CU)."""
+    batch = build_batch([200_000, 1], 28, 4, 128, seed=45)
+    cache = random_fp8_cache(batch, seed=46)
+    _say("fp8 attention, one very long sequence")
+    out, lse, info = run_fp8(batch, cache)
+    assert info.num_combine == 4 and info.num_partials >= 1000
+    ro, rl = ref_fp8(batch, cache)
+    assert_close(out, ro, "very long out")
+    assert_close(lse, rl, "very long lse")
+
+
 @pytest.mark.parametrize("shape", [(8, 2, 64), (16, 1, 128), (7, 7, 64), (5, 1, 64)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_fp8_attention_head_shapes(shape):
