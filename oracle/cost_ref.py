@@ -23,7 +23,7 @@ The staleness manager's check for an initial trajectory is modelled as
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 
 
 @dataclass
