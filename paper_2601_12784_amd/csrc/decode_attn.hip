@@ -306,6 +306,10 @@ __device__ __forceinline__ void store_token(uint16_t* k_dst, uint16_t* v_dst, co
 }
 
 // The fields of a segment row that the attention pass uses.
+// Lane of the calling thread in its wave (a workgroup may hold several waves,
+// one worker each).
+__device__ __forceinline__ int lane_id() { return int(threadIdx.x) & 63; }
+
 struct Segment {
   int seq, kvh, pb, pe, len, slot;
 };
@@ -331,6 +335,7 @@ __device__ __forceinline__ Segment segment_at(int v, int i) {
 }
 
 struct WorkerRows {
+  int worker;     // this wave's worker: workgroup * waves per workgroup + wave
   int first;      // index of the worker's first item
   int count;      // its items
   Segment head;   // item 0, from the table row
@@ -342,33 +347,55 @@ struct WorkerRows {
 // The side job: this worker's 64 ints of the merge rows, requested once its
 // first segment's first loads are out (like the work-list rows) and stored
 // after its last result.
-__device__ __forceinline__ bool copies_rows(const AttnArgs& a) {
-  return a.copy_dst != nullptr && int(blockIdx.x) * 64 + int(threadIdx.x) < a.copy_ints;
+__device__ __forceinline__ bool copies_rows(const AttnArgs& a, const WorkerRows& w) {
+  return a.copy_dst != nullptr && w.worker * 64 + lane_id() < a.copy_ints;
 }
 
 __device__ __forceinline__ void row_copy_load(const AttnArgs& a, WorkerRows& w) {
-  if (copies_rows(a)) w.copy_val = a.copy_src[int(blockIdx.x) * 64 + int(threadIdx.x)];
+  if (copies_rows(a, w)) w.copy_val = a.copy_src[w.worker * 64 + lane_id()];
 }
 
 __device__ __forceinline__ void row_copy_store(const AttnArgs& a, const WorkerRows& w) {
-  if (copies_rows(a)) a.copy_dst[int(blockIdx.x) * 64 + int(threadIdx.x)] = w.copy_val;
+  if (copies_rows(a, w)) a.copy_dst[w.worker * 64 + lane_id()] = w.copy_val;
 }
 
-__device__ __forceinline__ WorkerRows worker_rows(const AttnArgs& a) {
-  const const_i32_ptr wt = as_constant(a.worker_table) + size_t(blockIdx.x) * kItemInts;
-  WorkerRows w;
-  w.first = wt[0];
-  w.count = wt[1];
-  w.head.seq = wt[2];
-  w.head.kvh = wt[3];
-  w.head.pb = wt[4];
-  w.head.pe = wt[5];
-  w.head.len = wt[6];
-  w.head.slot = wt[7];
+// The table rows of a workgroup's kWG workers are consecutive: with kWG > 1
+// the first wave reads all of them in one vector load (one request of up to
+// 256 bytes over PCIe instead of one per worker: at eight workers per CU the
+// per-worker reads queued for several microseconds) and shares them through
+// LDS. Returns false for a wave past the last worker (the last workgroup may
+// be partial); it must then leave without touching anything else.
+template <int kWG>
+__device__ __forceinline__ bool worker_rows(const AttnArgs& a, int32_t* rows_lds, WorkerRows& w) {
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  w.worker = int(blockIdx.x) * kWG + wave;
+  int32_t r[kItemInts];
+  if constexpr (kWG == 1) {
+    const const_i32_ptr wt = as_constant(a.worker_table) + size_t(w.worker) * kItemInts;
+#pragma unroll
+    for (int i = 0; i < kItemInts; ++i) r[i] = wt[i];
+  } else {
+    const int first = int(blockIdx.x) * kWG;
+    const int nrows = min(kWG, a.num_workers - first);
+    if (int(threadIdx.x) < nrows * kItemInts)
+      rows_lds[threadIdx.x] = a.worker_table[size_t(first) * kItemInts + threadIdx.x];
+    __syncthreads();
+    if (w.worker >= a.num_workers) return false;
+#pragma unroll
+    for (int i = 0; i < kItemInts; ++i) r[i] = __builtin_amdgcn_readfirstlane(rows_lds[wave * kItemInts + i]);
+  }
+  w.first = r[0];
+  w.count = r[1];
+  w.head.seq = r[2];
+  w.head.kvh = r[3];
+  w.head.pb = r[4];
+  w.head.pe = r[5];
+  w.head.len = r[6];
+  w.head.slot = r[7];
   w.v = 0;
   w.group = -1;
   w.copy_val = 0;
-  return w;
+  return true;
 }
 
 // Requests the group of rows that holds item i (1 <= i < count), unless held.
@@ -379,7 +406,7 @@ __device__ __forceinline__ void request_rows(const AttnArgs& a, WorkerRows& w, i
   const int b = 1 + group * kRowsPerLoad;
   const int n = min(w.count - b, kRowsPerLoad);
   const int32_t* rows = a.items + size_t(w.first + b) * kItemInts;
-  const int lane = threadIdx.x;
+  const int lane = lane_id();
   w.v = lane < n * kItemInts ? rows[lane] : 0;
   w.group = group;
 }
@@ -396,7 +423,7 @@ __device__ __forceinline__ Segment worker_item(const WorkerRows& w, int i) {
 // takes it from new_pages and stores the token there).
 template <int D, bool kAppend>
 __device__ __forceinline__ ChunkCtx<D> segment_ctx(const AttnArgs& a, const Segment& sg, int& len_pages) {
-  const int lane = threadIdx.x;
+  const int lane = lane_id();
   const int col = lane & 15;
   const int grp = lane >> 4;
   ChunkCtx<D> c;
@@ -434,7 +461,7 @@ struct SegmentRegs {
 template <int D, bool kAppend>
 __device__ __forceinline__ void fetch_segment_start(const AttnArgs& a, const Segment& sg, const ChunkCtx<D>& c,
                                                     SegmentRegs<D>& r) {
-  const int lane = threadIdx.x;
+  const int lane = lane_id();
   const int col = lane & 15;
   const int grp = lane >> 4;
   const int g = a.group;
@@ -459,7 +486,7 @@ __device__ __forceinline__ void fetch_segment_start(const AttnArgs& a, const Seg
 template <int D>
 __device__ __forceinline__ void write_result(const AttnArgs& a, const Segment& sg, const f32x4* o, float l) {
   constexpr int JB = Shape<D>::JB;
-  const int lane = threadIdx.x;
+  const int lane = lane_id();
   const int col = lane & 15;
   const int grp = lane >> 4;
   const int g = a.group;
@@ -483,7 +510,7 @@ __device__ __forceinline__ void write_result(const AttnArgs& a, const Segment& s
 template <int D>
 __device__ __forceinline__ void flush_stash(const AttnArgs& a, const Segment& sg, const float* stash) {
   constexpr int JB = Shape<D>::JB;
-  const int lane = threadIdx.x;
+  const int lane = lane_id();
   f32x4 o[JB];
 #pragma unroll
   for (int jb = 0; jb < JB; ++jb)
@@ -505,7 +532,7 @@ template <int D, bool kAppend>
 __device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment& item, WorkerRows& w, int index,
                                                SegmentRegs<D>& r, bool& primed, float* stash) {
   constexpr int JB = Shape<D>::JB;
-  const int lane = threadIdx.x;
+  const int lane = lane_id();
   const int grp = lane >> 4;   // MFMA k-group
 
   const int pb = item.pb;
@@ -580,16 +607,19 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, const Segment&
 // Two waves per SIMD (at most 256 registers) keep 2048 workers resident.
 // The appending variant reads the newest tokens from k_new / v_new and
 // stores nothing: the stores come in the merge launch that follows.
-template <int D, bool kAppend>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_kernel(AttnArgs a) {
+template <int D, bool kAppend, int kWG>
+__global__ __launch_bounds__(64 * kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_kernel(AttnArgs a) {
   // A worker's first segment is usually the tail of a pair cut by the
   // previous worker, and short: its result would be written early, into the
   // middle of the launch's read stream, which costs more than its bytes.
   // It waits in LDS and is stored after the worker's last segment.
-  __shared__ float stash[(4 * Shape<D>::JB + 1) * 64];
+  __shared__ float stash_all[kWG][(4 * Shape<D>::JB + 1) * 64];
+  __shared__ int32_t rows_lds[kWG * kItemInts];
+  WorkerRows w;
+  if (!worker_rows<kWG>(a, rows_lds, w)) return;
+  float* stash = stash_all[w.worker - int(blockIdx.x) * kWG];
   SegmentRegs<D> regs;
   bool primed = false;
-  WorkerRows w = worker_rows(a);
   Segment sg = w.head;
   for (int i = 0; i < w.count; ++i) {
     attend_segment<D, kAppend>(a, sg, w, i, regs, primed, i == 0 && w.count > 1 ? stash : nullptr);
@@ -717,7 +747,7 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
                                                    float* stash) {
   constexpr int KB = Shape<D>::KB;
   constexpr int JB = Shape<D>::JB;
-  const int lane = threadIdx.x;
+  const int lane = lane_id();
   const int col = lane & 15;
   const int grp = lane >> 4;
   const int seq = item.seq;
@@ -814,11 +844,14 @@ __device__ __forceinline__ void attend_segment_fp8(const AttnArgs& a, const Segm
   write_result<D>(a, item, o, l);
 }
 
-template <int D>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_fp8_kernel(AttnArgs a) {
+template <int D, int kWG>
+__global__ __launch_bounds__(64 * kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_worker_fp8_kernel(AttnArgs a) {
   // The worker's first result waits in LDS, as in attn_worker_kernel.
-  __shared__ float stash[(4 * Shape<D>::JB + 1) * 64];
-  WorkerRows w = worker_rows(a);
+  __shared__ float stash_all[kWG][(4 * Shape<D>::JB + 1) * 64];
+  __shared__ int32_t rows_lds[kWG * kItemInts];
+  WorkerRows w;
+  if (!worker_rows<kWG>(a, rows_lds, w)) return;
+  float* stash = stash_all[w.worker - int(blockIdx.x) * kWG];
   Segment sg = w.head;
   for (int i = 0; i < w.count; ++i) {
     attend_segment_fp8<D, 3>(a, sg, w, i, i == 0 && w.count > 1 ? stash : nullptr);
@@ -1063,7 +1096,7 @@ __global__ __launch_bounds__(256) void merge_append_kernel(CombineArgs a) {
   }
 
   if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
+    const int lane = lane_id();
     store_token<D>(a.k_dst, a.v_dst, a.k_new, a.v_new, a.num_kv_heads, seq, kvh, page, t % kPage, lane);
     if (fresh >= 0 && kvh == 0 && lane == 0) a.bt_dst[entry] = fresh;
   }
@@ -1090,16 +1123,24 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
 
 }  // namespace
 
+// Waves (workers) per workgroup: the kernels run two waves per SIMD at most,
+// so a launch with at least 8 (fp8) or 4 (bf16) workers per CU packs that
+// many into each workgroup, which then share one read of their table rows;
+// smaller launches keep one worker per workgroup, spread over every CU.
+template <int kWG>
+void (*pick_attention(const AttnArgs& a))(AttnArgs) {
+  if (a.k_scale) return a.head_dim == 128 ? attn_worker_fp8_kernel<128, kWG> : attn_worker_fp8_kernel<64, kWG>;
+  if (a.k_new) return a.head_dim == 128 ? attn_worker_kernel<128, true, kWG> : attn_worker_kernel<64, true, kWG>;
+  return a.head_dim == 128 ? attn_worker_kernel<128, false, kWG> : attn_worker_kernel<64, false, kWG>;
+}
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
   if (a.num_workers == 0) return hipSuccess;
-  const dim3 grid(a.num_workers), block(64);
-  void (*kernel)(AttnArgs);
-  if (a.k_scale)
-    kernel = a.head_dim == 128 ? attn_worker_fp8_kernel<128> : attn_worker_fp8_kernel<64>;
-  else if (a.k_new)
-    kernel = a.head_dim == 128 ? attn_worker_kernel<128, true> : attn_worker_kernel<64, true>;
-  else
-    kernel = a.head_dim == 128 ? attn_worker_kernel<128, false> : attn_worker_kernel<64, false>;
+  const int per_group = a.k_scale && a.num_workers >= 8 * kDefaultNumCus ? 8
+                        : a.num_workers >= 4 * kDefaultNumCus ? 4 : 1;
+  const dim3 grid((a.num_workers + per_group - 1) / per_group), block(64 * per_group);
+  void (*kernel)(AttnArgs) = per_group == 8 ? pick_attention<8>(a) : per_group == 4 ? pick_attention<4>(a)
+                                                                                     : pick_attention<1>(a);
   if (start || stop)
     hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, a);
   else
