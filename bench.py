@@ -412,7 +412,7 @@ def fp8_bench(batch, steps, warmup, bf16_kernel_us):
             "kernel_speedup_vs_bf16": round(bf16_kernel_us / (k_mean * 1e3), 3),
             "quantize_ms_whole_cache": round(quant_ms, 3),
             "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                         "frac": round(achieved / PEAK_HBM_GBPS, 4), "kernel": "attn_worker_fp8_kernel<128>"}}
+                         "frac": round(achieved / PEAK_HBM_GBPS, 4), "kernel": "attn_worker_fp8_kernel<128, 8>"}}
 
 
 def read_ceiling(nbytes, grids=(2048, 4096, 8192), reps=15, warmup=3):
@@ -497,7 +497,8 @@ def stored_traffic(kv_bytes_per_launch):
     return doc.get("traffic_bytes_per_launch")
 
 
-ATTN_KERNEL = "attn_worker_kernel<128, false>"
+# the long-tail launch: head_dim 128, no append, 4 waves (workers) per workgroup
+ATTN_KERNEL = "attn_worker_kernel<128, false, 4>"
 COMBINE_KERNEL = "combine_kernel"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
