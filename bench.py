@@ -39,7 +39,7 @@ def kernel_source_hash(path=None) -> str:
 class Stepper:
     """Runs plan -> upload -> attention (+ merge) for a fixed batch on one stream."""
 
-    def __init__(self, batch, chunk_pages=0, workers_per_cu=0, fp8=None, rotate=1):
+    def __init__(self, batch, chunk_pages=0, workers_per_cu=0, fp8=None, rotate=1, skew=0):
         """fp8 = (k8, v8, k_scale, v_scale) device tensors: step over that fp8
         cache instead of the batch's bf16 pools. rotate > 1 keeps that many
         device copies of the pools and moves to the next copy every step, so a
@@ -56,14 +56,22 @@ class Stepper:
         self.lens = np.ascontiguousarray(batch.seq_lens, dtype=np.int32)
         self.chunk = chunk_pages or None
         cus = torch.cuda.get_device_properties(0).multi_processor_count
-        self.runner = B.DecodeAttention(batch.num_q_heads, batch.num_kv_heads, batch.head_dim,
-                                        opts=B.make_opts(num_cus=cus, workers_per_cu=workers_per_cu))
+        self.cus = cus
+        self.workers_per_cu = workers_per_cu
+        self.runner = self.make_runner(skew)
         self.stream = torch.cuda.Stream()  # default priority
         self.out = torch.empty((batch.num_seqs, batch.num_q_heads, batch.head_dim), dtype=torch.float32,
                                device="cuda")
         self.lse = torch.empty((batch.num_seqs, batch.num_q_heads), dtype=torch.float32, device="cuda")
         self.step()
         self.info0 = self.runner.last_info
+
+    def make_runner(self, skew):
+        from paper_2601_12784_amd import binding as B
+        b = self.batch
+        return B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim,
+                                 opts=B.make_opts(num_cus=self.cus, workers_per_cu=self.workers_per_cu,
+                                                  xcd_parity_skew=skew))
 
     def step(self, ev_attn=None):
         """One decode step; ev_attn = (start, end) events bracketing the attention kernel."""
@@ -100,6 +108,40 @@ def time_steps(stepper, steps, warmup, every=EVENT_EVERY):
     wall = time.perf_counter() - t0
     attn_ms = [a.elapsed_time(b) for a, b in evs.values()]
     return wall / steps * 1e3, float(np.mean(attn_ms)), float(np.median(attn_ms))
+
+
+SKEW_CANDIDATES = (-40, -20, 0, 20, 40)
+
+
+def calibrate_skew(stepper, candidates=SKEW_CANDIDATES, rounds=3, steps=200, warmup=100, min_gain=0.0025):
+    """Picks the plan's group-parity skew (sf_plan_opts.xcd_parity_skew) for
+    this GPU and workload by timing it: one runner per candidate, all on the
+    stepper's stream (one hardware queue), in rotated order for `rounds`
+    rounds; the score is the median over rounds of each round's median
+    attention-kernel time. A candidate is taken only if it beats equal slices
+    (0) by at least `min_gain`; the stepper keeps the chosen runner. Which
+    sign helps, and how much, differs between GPUs and between the bf16 and
+    fp8 kernels, so it is measured rather than fixed."""
+    runners = {p: (stepper.runner if p == 0 else stepper.make_runner(p)) for p in candidates}
+    times = {p: [] for p in candidates}
+    for _ in range(600):                 # out of the idle clocks first
+        stepper.step()
+    stepper.torch.cuda.synchronize()
+    for r in range(rounds):
+        order = list(candidates[r % len(candidates):]) + list(candidates[:r % len(candidates)])
+        for p in order:
+            stepper.runner = runners[p]
+            _, _, k_med = time_steps(stepper, steps, warmup)
+            times[p].append(k_med * 1e3)
+    score = {p: float(np.median(v)) for p, v in times.items()}
+    best = min(score, key=score.get)
+    chosen = best if score[best] < score[0] * (1.0 - min_gain) else 0
+    stepper.runner = runners[chosen]
+    return {"chosen": chosen, "kernel_us_median": {str(p): round(s, 2) for p, s in score.items()},
+            "what": "plan option xcd_parity_skew (per mille; workers of even launch groups weigh 1000 + p, of odd "
+                    "groups 1000 - p) chosen by timing each candidate on this GPU before the timed steps: "
+                    f"{rounds} rounds x {steps} steps per candidate, one stream; taken only if it beats equal "
+                    f"slices by {100 * min_gain:.2f} %"}
 
 
 def decode_loop_bench(reps=5):
@@ -375,7 +417,7 @@ def reprefill_bench(reps=20, warmup=5):
                          "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "kernel": EXTEND_KERNEL}}
 
 
-def fp8_bench(batch, steps, warmup, bf16_kernel_us):
+def fp8_bench(batch, steps, warmup, bf16_kernel_us, skew=None):
     """The same decode step over an fp8 (E4M3) copy of the batch's cache,
     made by the library's quantizer (every page a sequence holds). Bytes per
     step: one byte per cached element plus the K and V scale of every
@@ -402,7 +444,8 @@ def fp8_bench(batch, steps, warmup, bf16_kernel_us):
     e1.synchronize()
     quant_ms = e0.elapsed_time(e1) / 5
     del kq, vq
-    st = Stepper(batch, fp8=(k8, v8, ks, vs))
+    st = Stepper(batch, fp8=(k8, v8, ks, vs), skew=skew or 0)
+    cal = calibrate_skew(st) if skew is None else None
     ms_step, k_mean, k_med = time_steps(st, steps, warmup)
     tokens = int(batch.seq_lens.sum())
     tiles = int((-(-batch.seq_lens.astype(np.int64) // 16)).sum()) * hkv
@@ -418,6 +461,7 @@ def fp8_bench(batch, steps, warmup, bf16_kernel_us):
             "seq_steps_per_s": round(batch.num_seqs / (ms_step * 1e-3), 1),
             "kernel_speedup_vs_bf16": round(bf16_kernel_us / (k_mean * 1e3), 3),
             "quantize_ms_whole_cache": round(quant_ms, 3),
+            "xcd_parity_skew": cal["chosen"] if cal else skew, "skew_calibration": cal,
             "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                          "frac": round(achieved / PEAK_HBM_GBPS, 4), "kernel": "attn_worker_fp8_kernel<128, 8>"}}
 
@@ -730,6 +774,10 @@ def main():
                     help="untimed steps first (the GPU leaves its idle clocks during these)")
     ap.add_argument("--chunk-pages", type=int, default=0, help="force the pages per worker")
     ap.add_argument("--workers-per-cu", type=int, default=0, help="planner workers (waves) per CU")
+    ap.add_argument("--skew", type=int, default=None,
+                    help="plan group-parity skew (per mille) of the long-tail leg; default: chosen by "
+                         "timing candidates on this GPU before the timed steps")
+    ap.add_argument("--fp8-skew", type=int, default=None, help="the same for the fp8 leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-skew", action="store_true", help="skip the equal-bytes uniform batch")
     ap.add_argument("--no-loop", action="store_true", help="skip the growing-cache decode loop")
@@ -798,9 +846,15 @@ def main():
     batch = make_batch("longtail")
     kv = batch.kv_bytes()
     log(f"  {batch.num_seqs} seqs, {int(batch.seq_lens.sum())} tokens, {kv / 1e9:.3f} GB KV/step")
-    st = Stepper(batch, chunk_pages=args.chunk_pages, workers_per_cu=args.workers_per_cu)
+    st = Stepper(batch, chunk_pages=args.chunk_pages, workers_per_cu=args.workers_per_cu, skew=args.skew or 0)
+    calibration = None
+    if args.skew is None and not args.chunk_pages:
+        log("  choosing the plan's group-parity skew for this GPU (untimed)")
+        calibration = calibrate_skew(st)
+        log(f"  skew {calibration['chosen']}: {calibration['kernel_us_median']}")
+    skew = calibration["chosen"] if calibration else (args.skew or 0)
     ms_step, attn_ms_mean, attn_ms_med = time_steps(st, args.steps, args.warmup)
-    info = st.info0
+    info = st.runner.last_info
     log(f"  step {ms_step * 1e3:.1f} us, attention kernel {attn_ms_mean * 1e3:.1f} us (median "
         f"{attn_ms_med * 1e3:.1f}), {info.num_workers} workers x {info.chunk_pages} pages, "
         f"{info.num_work} segments, {info.num_combine} cut pairs")
@@ -833,11 +887,13 @@ def main():
                                "bf16 N(0,1), one decode step",
                    "seed": batch.seed, "kv_bytes_per_step": kv, "tokens": int(batch.seq_lens.sum()),
                    "workers": info.num_workers, "pages_per_worker": info.chunk_pages,
+                   "xcd_parity_skew": skew,
                    "segments": info.num_work, "cut_pairs": info.num_combine},
         "seq_steps_per_s": round(batch.num_seqs / (ms_step * 1e-3), 1),
         "pct_of_peak_hbm": round(100.0 * kv / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2),
         "attn_kernel_us": round(attn_ms_mean * 1e3, 2),
         "host_plan_us": round(plan_us, 2),
+        "skew_calibration": calibration,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic},
@@ -856,7 +912,7 @@ def main():
         lens_u = uniform_lengths_like(batch.seq_lens.astype(np.int64))
         log("generating equal-token uniform batch")
         ub = build_batch(lens_u, 28, 4, 128, batch.seed + 100, name="uniform")
-        su = Stepper(ub, chunk_pages=args.chunk_pages, workers_per_cu=args.workers_per_cu)
+        su = Stepper(ub, chunk_pages=args.chunk_pages, workers_per_cu=args.workers_per_cu, skew=skew)
         ms_u, attn_u, _ = time_steps(su, args.steps, args.warmup)
         result["skew"] = {"uniform_ms_per_step": round(ms_u, 5), "uniform_kv_bytes": ub.kv_bytes(),
                           "skewed_over_uniform": round(ms_step / ms_u, 4),
@@ -873,7 +929,8 @@ def main():
 
     if not args.no_fp8:
         log("fp8 (E4M3) cache: the same step over the library-quantized cache")
-        f8 = fp8_bench(batch, max(100, args.steps // 2), max(100, args.warmup // 2), attn_ms_mean * 1e3)
+        f8 = fp8_bench(batch, max(100, args.steps // 2), max(100, args.warmup // 2), attn_ms_mean * 1e3,
+                       skew=args.fp8_skew)
         result["fp8"] = f8
         log(f"  step {f8['ms_per_step'] * 1e3:.1f} us, kernel {f8['attn_kernel_us']} us "
             f"({f8['roofline']['achieved']} GB/s of fp8 codes, {f8['kernel_speedup_vs_bf16']}x the bf16 kernel; "

@@ -95,7 +95,7 @@ typedef struct sf_plan_info {
   int32_t num_combine;       /* (seq, KV head) pairs cut into more than one segment */
   int32_t num_partials;      /* partial-result slots = sum of their segment counts */
   int32_t chunk_pages;       /* the most pages any worker owns (0 if T = 0) */
-  int32_t reserved;          /* 0 */
+  int32_t workers_per_group; /* G: waves per attention workgroup, 1, 4 or 8 (rule below) */
   uint64_t work_bytes;       /* bytes of the work list:
                                 (num_workers + num_work + num_combine) * 32 */
   uint64_t workspace_bytes;  /* device scratch sf_decode_attn needs (0 if no partials) */
@@ -112,17 +112,20 @@ typedef struct sf_plan_info {
  * T = sum_p pages_p global pages. With
  *   W = ceil(T / chunk_pages)                                   if chunk_pages > 0
  *   W = min(workers_per_cu * num_cus, ceil(T / min_chunk_pages)) otherwise
- * (W = 1 if T = 0 but B * Hkv > 0), worker w owns the global pages
+ * (W = 1 if T = 0 but B * Hkv > 0), and G = 8 if W >= 8 num_cus, 4 if
+ * W >= 4 num_cus, else 1, worker w owns the global pages
  * [floor(T C(w) / C(W)), floor(T C(w + 1) / C(W))) with C(v) = 1000 v +
- * p (v mod 2): every worker reads its share of the pages however skewed the
- * lengths are, 1000 + p per mille of the mean for an even w, 1000 - p for an
- * odd one (p = opts->xcd_parity_skew, default 0: equal slices, within one
- * page; p is also 0 when chunk_pages is forced, and when the skewed slices
- * would cut more than floor(W / 8) more pairs than the equal ones: equal
- * lengths can put every equal boundary on a pair boundary). Worker w runs as
- * workgroup w, and workgroup w runs on XCD w mod 8: a GPU whose odd (p > 0)
- * or even (p < 0) XCDs are slower on the same work can give them less. How
- * much slower, and which, differs from one MI355X to the next. A worker's range is
+ * p D(v), D(v) = v mod G if floor(v / G) is even, else G - v mod G: every
+ * worker reads its share of the pages however skewed the lengths are, 1000 + p
+ * per mille of the mean if floor(w / G) is even, 1000 - p if it is odd
+ * (p = opts->xcd_parity_skew, default 0: equal slices, within one page; p is
+ * also 0 when chunk_pages is forced, and when the skewed slices would cut
+ * more than floor(W / 8) more pairs than the equal ones: equal lengths can put
+ * every equal boundary on a pair boundary). The attention launch runs workers
+ * G b .. G b + G - 1 as workgroup b, and workgroup b runs on XCD b mod 8: a
+ * GPU whose odd (p > 0) or even (p < 0) XCDs are slower on the same work can
+ * give them less. How much slower, and which, differs from one MI355X to the
+ * next. A worker's range is
  * cut at pair boundaries into segments, each a work item on one pair; a pair
  * crossing k worker boundaries has n_p = k + 1 segments. Empty pairs
  * (L_s = 0) get one item each, handed to worker e mod W for the e-th empty

@@ -9,8 +9,10 @@ planner, so the two can be compared bit for bit:
   pairs p = (s, kvh), s-major; pages_p = ceil(L_s / 16); T = sum_p pages_p
   W = ceil(T / chunk_pages) if chunk_pages > 0
       else min(workers_per_cu * num_cus, ceil(T / min_chunk))   (1 if T = 0 < #pairs)
+  G = 8 if W >= 8*num_cus, 4 if W >= 4*num_cus, else 1 (workers per launch group)
   worker w owns global pages [floor(T*C(w)/C(W)), floor(T*C(w+1)/C(W))) with
-  C(v) = 1000*v + p*(v % 2): even workers weigh 1000 + p, odd ones 1000 - p
+  C(v) = 1000*v + p*D(v), D(v) = v % G if (v // G) is even else G - v % G:
+  workers of even groups weigh 1000 + p, of odd groups 1000 - p
   (p = xcd_parity_skew per mille, -250 .. 250, default 0; 0 when chunk_pages
   is forced, or when these slices cut more than W // 8 pairs more than the
   equal ones, p = 0, would); cut at pair boundaries into segments (items); empty
@@ -56,12 +58,15 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
     else:
         workers = min(wpc * num_cus, _ceil(total, mn))
 
+    group = 8 if workers >= 8 * num_cus else 4 if workers >= 4 * num_cus else 1
+
     # every (worker, pair) overlap is a segment
     starts = np.cumsum([0] + pages)
 
     def cuts_for(p):
         def weight_upto(v):      # C(v): the weights of workers 0 .. v - 1
-            return 1000 * v + p * (v % 2)
+            r = v % group
+            return 1000 * v + p * (r if (v // group) % 2 == 0 else group - r)
         return [total * weight_upto(w) // weight_upto(workers) for w in range(workers + 1)] if workers else [0]
 
     def pairs_cut(bounds):       # pairs with a worker boundary strictly inside them
@@ -123,7 +128,7 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
     comb = np.array(combine, dtype=np.int32).reshape(-1, 8)
     g = num_q_heads // num_kv_heads
     ws = _align(slot * g * head_dim * 4) + _align(slot * g * 4) if slot else 0
-    return dict(table=table, items=items, combine=comb, num_workers=workers,
+    return dict(table=table, items=items, combine=comb, num_workers=workers, workers_per_group=group,
                 chunk_pages=max(b - a for a, b in zip(bounds, bounds[1:])) if workers and total else 0,
                 num_partials=slot, workspace_bytes=ws,
                 work_bytes=(table.shape[0] + items.shape[0] + comb.shape[0]) * 8 * 4)

@@ -48,7 +48,7 @@ class sf_plan_opts(ctypes.Structure):
 class sf_plan_info(ctypes.Structure):
     _fields_ = [("num_workers", ctypes.c_int32), ("num_work", ctypes.c_int32),
                 ("num_combine", ctypes.c_int32), ("num_partials", ctypes.c_int32),
-                ("chunk_pages", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("chunk_pages", ctypes.c_int32), ("workers_per_group", ctypes.c_int32),
                 ("work_bytes", ctypes.c_uint64), ("workspace_bytes", ctypes.c_uint64),
                 ("desc_key", ctypes.c_uint64)]
 

@@ -17,7 +17,8 @@ sf_status check_plan(const sf_attn_desc* d, const sf_plan_info* info) {
   if (info->desc_key != desc_key(d)) return SF_ERR_PLAN_MISMATCH;
   if (info->num_workers < 0 || info->num_work < 0 || info->num_combine < 0 || info->num_partials < 0)
     return SF_ERR_INVALID_ARG;
-  if (info->reserved != 0 || info->work_bytes != uint64_t(table_rows(info->num_workers) + info->num_work +
+  if ((info->workers_per_group != 1 && info->workers_per_group != 4 && info->workers_per_group != 8) ||
+      info->work_bytes != uint64_t(table_rows(info->num_workers) + info->num_work +
                                                           info->num_combine) * kItemInts * 4)
     return SF_ERR_PLAN_MISMATCH;
   return SF_OK;
@@ -132,6 +133,7 @@ sf_status attend(const sf_attn_desc* desc, const sf_plan_info* info, const int32
   a.worker_table = work_dev;
   a.items = work_dev + table_rows(info->num_workers) * kItemInts;
   a.num_workers = info->num_workers;
+  a.workers_per_group = info->workers_per_group;
   a.q = static_cast<const uint16_t*>(q);
   a.k_pool = static_cast<const uint16_t*>(k_pool);
   a.v_pool = static_cast<const uint16_t*>(v_pool);

@@ -116,19 +116,26 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   }
   if (workers > INT32_MAX / 2) return SF_ERR_INVALID_ARG;
 
+  // The attention launch runs workers G b .. G b + G - 1 as workgroup b
+  // (one wave each), and workgroup b runs on XCD b mod 8.
+  const int32_t group = workers >= 8 * int64_t(num_cus) ? 8 : workers >= 4 * int64_t(num_cus) ? 4 : 1;
+
   // Worker range starts lo(w) = floor(T C(w) / C(W)) with the cumulative
-  // weight C(v) = 1000 v + p (v mod 2): worker v weighs 1000 + p if v is
-  // even, 1000 - p if odd (|p| <= 250; p = 0 for a forced slice size).
-  // Walked forward without divisions: T C(v) grows by T (1000 + p) or
-  // T (1000 - p), each positive and below 2^51, and quotient and remainder
-  // advance by those over C(W) > 0.
+  // weight C(v) = 1000 v + p D(v), D(v) = v mod G if floor(v / G) is even,
+  // else G - v mod G: a worker of an even group weighs 1000 + p, of an odd
+  // group 1000 - p (|p| <= 250; p = 0 for a forced slice size). Walked
+  // forward without divisions: T C(v) grows by T (1000 + p) or T (1000 - p),
+  // each positive and below 2^51, and quotient and remainder advance by
+  // those over C(W) > 0.
   if (forced > 0) skew = 0;
   struct Cuts {
-    int64_t q = 0, r = 0, den = 1, idx = 0;
-    int64_t dq[2] = {0, 0}, dr[2] = {0, 0};   // [v mod 2]: step from C(v) to C(v + 1)
-    void init(int64_t t, int64_t w, int64_t p) {
+    int64_t q = 0, r = 0, den = 1, idx = 0, g = 1;
+    int64_t dq[2] = {0, 0}, dr[2] = {0, 0};   // [group parity of v]: step from C(v) to C(v + 1)
+    void init(int64_t t, int64_t w, int64_t p, int64_t grp) {
       q = r = idx = 0;
-      den = w > 0 ? 1000 * w + p * (w & 1) : 1;
+      g = grp;
+      const int64_t rem = w % g;
+      den = w > 0 ? 1000 * w + p * (((w / g) & 1) ? g - rem : rem) : 1;
       for (int k = 0; k < 2; ++k) {
         const int64_t inc = t * (k == 0 ? 1000 + p : 1000 - p);
         dq[k] = inc / den;
@@ -136,8 +143,9 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
       }
     }
     void next() {
-      q += dq[idx & 1];
-      r += dr[idx & 1];
+      const int k = int((idx / g) & 1);
+      q += dq[k];
+      r += dr[k];
       if (r >= den) {
         r -= den;
         ++q;
@@ -152,7 +160,7 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   // Returns the number of cut pairs.
   auto segments = [&](int64_t p_skew, int32_t* nseg) -> int64_t {
     Cuts next_lo;           // lo(cur + 1)
-    next_lo.init(total, workers, p_skew);
+    next_lo.init(total, workers, p_skew, group);
     next_lo.next();
     int64_t cur = 0;        // worker whose range holds `start`
     int64_t start = 0;      // global page where the current pair starts
@@ -217,9 +225,9 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   info->num_combine = int32_t(n_comb);
   info->num_partials = int32_t(n_part);
   {
-    // the widest slice (an even worker's when the slices are skewed)
+    // the widest slice (an even group's worker's when the slices are skewed)
     Cuts c;
-    c.init(total, workers, skew);
+    c.init(total, workers, skew, group);
     int64_t prev = 0, widest = 0;
     for (int64_t w = 0; w < workers; ++w) {
       c.next();
@@ -228,7 +236,7 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
     }
     info->chunk_pages = int32_t(widest);
   }
-  info->reserved = 0;
+  info->workers_per_group = group;
   info->work_bytes = uint64_t(table_rows + n_work + n_comb) * kItemInts * 4;
   info->workspace_bytes =
       n_part ? align256(uint64_t(n_part) * g * desc->head_dim * 4) + align256(uint64_t(n_part) * g * 4) : 0;
@@ -294,8 +302,8 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   int64_t row = 0, pstart = 0;
   int32_t seg_c = 0;  // segment index within the current pair
   Cuts lo_w, hi_w;
-  lo_w.init(total, workers, skew);
-  hi_w.init(total, workers, skew);
+  lo_w.init(total, workers, skew, group);
+  hi_w.init(total, workers, skew, group);
   hi_w.next();
   for (int64_t w = 0; w < workers; ++w, lo_w.next(), hi_w.next()) {
     const int64_t lo = lo_w.q, hi = hi_w.q;

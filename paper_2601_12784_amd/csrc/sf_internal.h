@@ -38,6 +38,7 @@ struct AttnArgs {
   const int32_t* worker_table;  // (first item, item count) per worker
   const int32_t* items;         // segment rows
   int32_t num_workers;
+  int32_t workers_per_group;    // waves per workgroup (1, 4 or 8; the plan's choice)
   const uint16_t* q;
   const uint16_t* k_pool;
   const uint16_t* v_pool;

@@ -60,6 +60,7 @@ def _split(info, work):
 
 def _assert_same(info, work, ref):
     assert info.num_workers == ref["num_workers"]
+    assert info.workers_per_group == ref["workers_per_group"]
     assert info.chunk_pages == ref["chunk_pages"]
     assert info.num_work == ref["items"].shape[0]
     assert info.num_combine == ref["combine"].shape[0]
@@ -117,10 +118,12 @@ def test_plan_skew_kept_or_dropped_by_cut_count():
 
 
 @pytest.mark.parametrize("skew", [-250, -30, 1, 50, 250])
-def test_plan_matches_rederivation_parity_skew(skew):
+@pytest.mark.parametrize("num_cus,wpc,group,nseq", [(64, 0, 4, 180), (64, 8, 8, 180), (2048, 0, 1, 40)])
+def test_plan_matches_rederivation_parity_skew(skew, num_cus, wpc, group, nseq):
     rng = np.random.default_rng(400 + skew)
-    lens = np.exp(rng.normal(np.log(2000), 1.0, size=180)).astype(np.int64).clip(0, 16384)
-    info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=64, skew=skew)
+    lens = np.exp(rng.normal(np.log(2000), 1.0, size=nseq)).astype(np.int64).clip(0, 16384)
+    info, work, ref = _plan_both(lens, 28, 4, 128, num_cus=num_cus, wpc=wpc, skew=skew)
+    assert info.workers_per_group == group
     _assert_same(info, work, ref)
     # a forced slice size ignores the skew: the same plan with and without it
     a, wa, _ = _plan_both(lens, 28, 4, 128, chunk=400, skew=skew)
@@ -164,20 +167,22 @@ def test_tiny_plan_by_hand():
     assert info.workspace_bytes == 5 * 4 * 64 * 4 + 256
 
 
-@pytest.mark.parametrize("seed,skew", [(0, 0), (1, 0), (2, -40), (3, 0), (4, 120)])
-def test_plan_invariants(seed, skew):
+@pytest.mark.parametrize("seed,skew,wpc", [(0, 0, 0), (1, 0, 0), (2, -40, 0), (3, 0, 8), (4, 120, 0),
+                                           (5, 60, 8), (6, -90, 4)])
+def test_plan_invariants(seed, skew, wpc):
     """Every worker owns its share of the T pages to within one page: T / W
-    without a parity skew, T (1000 + p) / (1000 W) for an even worker and
-    T (1000 - p) / (1000 W) for an odd one with skew p (W even; one more even
-    worker's weight of 1000 + p in the total otherwise); the slices tile
-    [0, T) in order; each pair's segments tile [0, pages) in worker order;
-    slots of cut pairs are consecutive; every pair appears; empty pairs have
-    one empty item."""
+    without a parity skew; with skew p, a worker of group floor(w / G) weighs
+    1000 + p if the group is even and 1000 - p if it is odd, and owns T times
+    its weight over the sum of all weights; G is 8, 4 or 1 as W reaches 8 or
+    4 workers per CU; the slices tile [0, T) in order; each pair's segments
+    tile [0, pages) in worker order; slots of cut pairs are consecutive; every
+    pair appears; empty pairs have one empty item."""
     rng = np.random.default_rng(100 + seed)
     lens = rng.integers(0, 20000, size=int(rng.integers(1, 200)))
     lens[rng.random(lens.size) < 0.1] = 0
     hkv = 4
-    info, work, _ = _plan_both(lens, 28, hkv, 128, num_cus=int(rng.integers(1, 300)), skew=skew)
+    num_cus = int(rng.integers(1, 300))
+    info, work, _ = _plan_both(lens, 28, hkv, 128, num_cus=num_cus, wpc=wpc, skew=skew)
     table, items, comb = _split(info, work)
     tab = table[:, :2]
     # each worker's row repeats the first six ints of its first item
@@ -187,8 +192,10 @@ def test_plan_invariants(seed, skew):
     W = info.num_workers
     assert np.array_equal(tab[:, 0], np.concatenate([[0], np.cumsum(tab[:, 1])[:-1]]))
     assert tab[:, 1].sum() == info.num_work
+    G = info.workers_per_group
+    assert G == (8 if W >= 8 * num_cus else 4 if W >= 4 * num_cus else 1)
     p = skew
-    weight = [1000 + p if w % 2 == 0 else 1000 - p for w in range(W)]
+    weight = [1000 + p if (w // G) % 2 == 0 else 1000 - p for w in range(W)]
     owned = []
     for w in range(W):
         seg = items[tab[w, 0]: tab[w, 0] + tab[w, 1]]
