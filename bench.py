@@ -560,7 +560,7 @@ def _csv_rows(path):
         return list(csv.DictReader(f))
 
 
-def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTERS_FILE):
+def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTERS_FILE, skew=None):
     """Per-launch HBM traffic of the attention kernel from two rocprofv3 --pmc
     runs (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what
     the same counter reads for a plain device copy of copy_mib MiB."""
@@ -612,13 +612,17 @@ def summarize_counters(fetch_csv, write_csv, copy_mib, kv_bytes, out_path=COUNTE
     md = out_path[:-len(".json")] + ".md"
     cmd = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
            "-d $OUT/{d} -o {o} -- python3 $REPO/bench.py --steps 5 --warmup 2 --no-cpu-baseline "
-           "--no-skew --no-loop --no-cost --no-reprefill --no-fp8 --no-configs --copy-probe " + str(int(copy_mib)))
+           "--no-skew --no-loop --no-cost --no-reprefill --no-fp8 --no-configs" +
+           ("" if skew is None else f" --skew {int(skew)}") + " --copy-probe " + str(int(copy_mib)))
     lines = [f"# HBM traffic of {ATTN_KERNEL} on the long-tail batch (rocprofv3 counters)", "",
              "Two counter passes (one counter each), then the summary:", "", "```",
              cmd.format(c="FETCH_SIZE", d="pmc_fetch", o="f"), cmd.format(c="WRITE_SIZE", d="pmc_write", o="w"),
              "python bench.py --summarize-counters $OUT/pmc_fetch/f_counter_collection.csv "
-             f"$OUT/pmc_write/w_counter_collection.csv --copy-probe {int(copy_mib)}", "```", "",
-             "($REPO: the repository root; $OUT: any directory for the profiler's output.)", "",
+             f"$OUT/pmc_write/w_counter_collection.csv --copy-probe {int(copy_mib)}" +
+             ("" if skew is None else f" --skew {int(skew)}"), "```", "",
+             "($REPO: the repository root; $OUT: any directory for the profiler's output.)" +
+             ("" if skew is None else f" The plan skew {int(skew)} is the one the default run chose on the same "
+                                      "GPU just before (it moves slice boundaries, not the bytes read)."), "",
              f"Kernel source sha256[:16]: `{doc['kernel_source_sha256_16']}`", "",
              "Calibration: a plain device copy (`__amd_rocclr_copyBuffer`) of "
              f"{int(copy_mib)} MiB reads FETCH_SIZE = {doc['raw_counter_bytes_per_launch']['copy_FETCH_SIZE']} B "
@@ -739,8 +743,12 @@ def summarize_trace(stats_csv, command, out_md, bench_json=None):
              else "# Kernel trace: the decode step on the long-tail batch, bf16 and fp8 caches" if fp8
              else f"# Kernel trace: {ATTN_KERNEL} on the long-tail batch")
     src = EXTEND_SRC if reprefill else KERNEL_SRC
-    lines = [title, "", "Command (from the repository root):", "", "```", command, "```", "",
-             f"Kernel source sha256[:16]: `{kernel_source_hash(src)}`", "",
+    lines = [title, "", "Command (from the repository root):", "", "```", command, "```", ""]
+    if "--skew" in command:
+        lines += ["The plan skews in the command are the ones a default run (which times the candidates first) "
+                  "chose on the same GPU just before; fixing them keeps those calibration launches out of the "
+                  "trace.", ""]
+    lines += [f"Kernel source sha256[:16]: `{kernel_source_hash(src)}`", "",
              "| kernel | calls | average us | min us | max us | share % |", "|---|---|---|---|---|---|"]
     for r in rows:
         lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
@@ -802,7 +810,8 @@ def main():
         from paper_2601_12784_amd.workloads import config_seed, sample_lengths
         lens = sample_lengths("longtail", np.random.Generator(np.random.PCG64(config_seed("longtail"))))
         kv = int(lens.sum()) * 4 * 128 * 2 * 2  # 4 KV heads, head_dim 128, K and V, bf16
-        print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_probe or 1024, kv), indent=1))
+        print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_probe or 1024, kv, skew=args.skew),
+                         indent=1))
         return
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace, bench_json=args.bench_json)
