@@ -144,7 +144,7 @@ def calibrate_skew(stepper, candidates=SKEW_CANDIDATES, rounds=3, steps=200, war
                     f"slices by {100 * min_gain:.2f} %"}
 
 
-def decode_loop_bench(reps=5):
+def decode_loop_bench(reps=5, skew=0):
     """The extreme-straggler lengths and caps as a growing-cache decode loop:
     512 sequences, 64 steps, one appended token per active sequence per step.
     Returns seq-steps/s over whole loops, host bookkeeping and planning
@@ -165,7 +165,8 @@ def decode_loop_bench(reps=5):
     kv_read = sum(b.kv_bytes(L) for L in lens)
     out = torch.empty((b.num_seqs, b.num_q_heads, b.head_dim), dtype=torch.float32, device="cuda")
     stream = torch.cuda.Stream()
-    attn = B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim)   # one runner for every loop
+    attn = B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim,   # one runner for every loop
+                             opts=B.make_opts(xcd_parity_skew=skew))
     times, issue = [], []
     sink = torch.zeros(64, dtype=torch.uint8, device="cuda")
     for rep in range(reps + 1):
@@ -192,7 +193,7 @@ def decode_loop_bench(reps=5):
             issue.append(t1 - t0)
     wall = float(np.median(times))
     seq_steps = run.seq_steps()
-    return {"workload": f"growing-cache decode loop: {b.num_seqs} sequences (502 x U[1,2048] + 10 x 32768 "
+    return {"xcd_parity_skew": skew, "workload": f"growing-cache decode loop: {b.num_seqs} sequences (502 x U[1,2048] + 10 x 32768 "
                         f"tokens at step 0), caps +U[0,64], {run.steps} steps, 28 q / 4 kv heads, "
                         "head_dim 128; each step appends one token per active sequence",
             "seq_steps": seq_steps, "loop_ms": round(wall * 1e3, 3),
@@ -204,7 +205,7 @@ def decode_loop_bench(reps=5):
 LLC_BYTES = 256 << 20   # MI355X last-level (Infinity) cache
 
 
-def config_bench(name, steps, warmup):
+def config_bench(name, steps, warmup, skew=0):
     """One decode step of a named workload (tiny, gqa7b, gqa32b), timed as the
     long-tail step is: plan -> attention -> combine back to back on one
     stream, wall time per step, attention kernel from HIP events. Batches
@@ -218,12 +219,12 @@ def config_bench(name, steps, warmup):
     rotate = 1 if pool_bytes > 2 * LLC_BYTES else max(4, -(-4 * LLC_BYTES // pool_bytes))
     if name == "tiny":
         rotate = 1   # 130 KB: a latency figure, cache-resident by nature
-    st = Stepper(b, rotate=rotate)
+    st = Stepper(b, rotate=rotate, skew=skew)
     ms_step, k_mean, k_med = time_steps(st, steps, warmup)
     info = st.info0
     gbs = kv / (k_mean * 1e-3) / 1e9
     _, bsz, hq, hkv, d = CONFIGS[name]
-    res = {"workload": f"{name}: {bsz} sequences, {hq} q / {hkv} kv heads, head_dim {d}, page 16",
+    res = {"xcd_parity_skew": skew, "workload": f"{name}: {bsz} sequences, {hq} q / {hkv} kv heads, head_dim {d}, page 16",
            "tokens": int(b.seq_lens.sum()), "kv_bytes_per_step": kv, "pool_copies_rotated": rotate,
            "ms_per_step": round(ms_step, 5), "attn_kernel_us": round(k_mean * 1e3, 2),
            "attn_kernel_us_median": round(k_med * 1e3, 2),
@@ -236,7 +237,7 @@ def config_bench(name, steps, warmup):
     return res
 
 
-def straggler_bench(reps=5):
+def straggler_bench(reps=5, skew=0):
     """The extreme-straggler schedule over its pre-filled pool: 64 decode
     steps, the batch shrinking as sequences reach their caps. Every step's
     queries and compacted block table are uploaded before timing; the timed
@@ -257,7 +258,7 @@ def straggler_bench(reps=5):
     seq_steps = run.seq_steps()
     out = torch.empty((b.num_seqs, b.num_q_heads, b.head_dim), dtype=torch.float32, device="cuda")
     stream = torch.cuda.Stream()
-    attn = B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim)
+    attn = B.DecodeAttention(b.num_q_heads, b.num_kv_heads, b.head_dim, opts=B.make_opts(xcd_parity_skew=skew))
 
     def loop(events=None):
         for t, (q, bt, lens) in enumerate(dev):
@@ -277,7 +278,7 @@ def straggler_bench(reps=5):
     torch.cuda.synchronize()
     kernel_ms = float(sum(a.elapsed_time(z) for a, z in evs))
     wall = float(np.median(times))
-    return {"workload": f"extreme straggler, pre-filled pool: {b.num_seqs} sequences at step 0 (502 x U[1,2048] "
+    return {"xcd_parity_skew": skew, "workload": f"extreme straggler, pre-filled pool: {b.num_seqs} sequences at step 0 (502 x U[1,2048] "
                         f"+ 10 x 32768 tokens), caps +U[0,64], {run.steps} steps, finished sequences dropped, "
                         "28 q / 4 kv heads, head_dim 128",
             "seq_steps": seq_steps, "loop_ms": round(wall * 1e3, 3),
@@ -838,7 +839,7 @@ def main():
         print(json.dumps(reprefill_bench()), flush=True)
         return
     if args.only_config:
-        print(json.dumps(config_bench(args.only_config, args.steps, args.warmup)), flush=True)
+        print(json.dumps(config_bench(args.only_config, args.steps, args.warmup, skew=args.skew or 0)), flush=True)
         return
 
     if args.copy_probe:
@@ -949,12 +950,12 @@ def main():
         legs = {}
         for name in ("tiny", "gqa7b", "gqa32b"):
             log(f"config {name}")
-            legs[name] = config_bench(name, args.steps, min(args.warmup, 500))
+            legs[name] = config_bench(name, args.steps, min(args.warmup, 500), skew=skew)
             log(f"  step {legs[name]['ms_per_step'] * 1e3:.1f} us, kernel {legs[name]['attn_kernel_us']} us, "
                 f"{legs[name]['kv_gb_per_s_kernel']} GB/s ({legs[name]['pct_of_peak_hbm_kernel']} % of peak), "
                 f"{legs[name]['seq_steps_per_s']} seq-steps/s")
         log("config straggler (pre-filled, 64 steps)")
-        legs["straggler"] = straggler_bench()
+        legs["straggler"] = straggler_bench(skew=skew)
         log(f"  {legs['straggler']['loop_ms']} ms per loop, {legs['straggler']['seq_steps_per_s']} seq-steps/s, "
             f"{legs['straggler']['kv_gb_per_s']} GB/s")
         result["configs"] = legs
@@ -968,7 +969,7 @@ def main():
 
     if not args.no_loop:
         log("growing-cache decode loop (straggler lengths, 64 steps)")
-        result["decode_loop"] = decode_loop_bench()
+        result["decode_loop"] = decode_loop_bench(skew=skew)
         log(f"  {result['decode_loop']['seq_steps_per_s']} seq-steps/s, "
             f"{result['decode_loop']['loop_ms']} ms per loop")
 

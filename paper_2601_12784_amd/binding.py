@@ -670,7 +670,7 @@ class DecodeAttention:
         desc = make_desc(lens.size, self.hq, self.hkv, self.d, block_table_stride, num_pages, 1.0)
         o = self.opts
         wpc = o.workers_per_cu or (8 if fp8 else 0)
-        opts = sf_plan_opts(o.num_cus, int(chunk_pages or 0), wpc, o.min_chunk_pages, 0)
+        opts = sf_plan_opts(o.num_cus, int(chunk_pages or 0), wpc, o.min_chunk_pages, o.xcd_parity_skew)
         info = sf_plan_info()
         st = self.L.sf_decode_attn_plan(ctypes.byref(desc), lens.ctypes.data, ctypes.byref(opts), None, 0,
                                         ctypes.byref(info))
