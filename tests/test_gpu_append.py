@@ -42,14 +42,15 @@ def assert_close(gpu, ref, what):
     return worst
 
 
-def run_loop(run, check_steps, chunk_pages=None):
+def run_loop(run, check_steps, chunk_pages=None, opts=None):
     b = run.base
     hq, hkv, d = b.num_q_heads, b.num_kv_heads, b.head_dim
     ref = append_ref.DecodeLoopRef(b.seq_lens, run.caps, bf16_bits(b.k_pool).copy(), bf16_bits(b.v_pool).copy(),
                                    b.block_table.copy(), bf16_bits(run.k_new), bf16_bits(run.v_new))
     k, v = b.k_pool.cuda(), b.v_pool.cuda()
     bt = torch.from_numpy(b.block_table).cuda()
-    runner = B.DecodeLoopRunner(hq, hkv, d, k, v, bt, b.block_table, b.seq_lens, b.scale)
+    attn = B.DecodeAttention(hq, hkv, d, opts=opts) if opts is not None else None
+    runner = B.DecodeLoopRunner(hq, hkv, d, k, v, bt, b.block_table, b.seq_lens, b.scale, attn=attn)
     if chunk_pages is not None:
         runner.attn.opts.chunk_pages = chunk_pages
     q_all, k_new, v_new = run.q_all.cuda(), run.k_new.cuda(), run.v_new.cuda()
@@ -93,6 +94,16 @@ def test_decode_loop_split_pairs(chunk):
     _say(f"decode loop chunk={chunk}")
     run = make_decode_loop(lens=[5, 16, 100, 333], steps=20, cap_extra_max=20, seed=22)
     run_loop(run, check_steps=set(range(20)), chunk_pages=chunk)
+
+
+def test_decode_loop_eight_wave_groups_with_skew():
+    """Appending steps launched as eight-wave workgroups (eight workers per CU
+    on an 8-CU plan) with a group-parity skew: pools, tables and every step
+    against the oracle."""
+    _say("decode loop, groups of 8, skew 40")
+    run = make_decode_loop(lens=[1, 15, 16, 17, 40, 200, 3, 700, 33, 2047, 5000, 90], steps=24, cap_extra_max=24,
+                           seed=23)
+    run_loop(run, check_steps=set(range(24)), opts=B.make_opts(num_cus=8, workers_per_cu=8, xcd_parity_skew=40))
 
 
 def test_decode_loop_full_straggler():

@@ -44,8 +44,8 @@ def assert_close(gpu, ref, what):
     assert worst <= 1.0, f"{what}: tolerance exceeded ({worst:.3f} of bound)"
 
 
-def run_fp8(batch, cache, chunk_pages=None):
-    runner = B.DecodeAttention(batch.num_q_heads, batch.num_kv_heads, batch.head_dim)
+def run_fp8(batch, cache, chunk_pages=None, opts=None):
+    runner = B.DecodeAttention(batch.num_q_heads, batch.num_kv_heads, batch.head_dim, opts=opts)
     lse = torch.empty((batch.num_seqs, batch.num_q_heads), dtype=torch.float32, device="cuda")
     out = runner(batch.q.cuda(), cache.k8.cuda(), cache.v8.cuda(), torch.from_numpy(batch.block_table).cuda(),
                  batch.seq_lens, batch.scale, lse=lse, chunk_pages=chunk_pages,
@@ -93,6 +93,24 @@ def test_fp8_attention_one_very_long_sequence():
     ro, rl = ref_fp8(batch, cache)
     assert_close(out, ro, "very long out")
     assert_close(lse, rl, "very long lse")
+
+
+@pytest.mark.parametrize("wpc,group", [(1, 1), (4, 4), (0, 8)])
+def test_fp8_attention_every_launch_group_size(wpc, group):
+    """fp8 steps plan eight workers per CU by default (eight waves per
+    workgroup); four and one per CU give groups of 4 and 1. Each, with equal
+    slices and with a group-parity skew, against the oracle."""
+    rng = np.random.default_rng(7)
+    lens = np.exp(rng.normal(np.log(1500), 1.0, size=24)).astype(np.int64).clip(16, 12000)
+    batch = build_batch(lens, 28, 4, 128, 80)
+    cache = random_fp8_cache(batch, seed=47)
+    ro, rl = ref_fp8(batch, cache)
+    for skew in (0, -60):
+        out, lse, info = run_fp8(batch, cache, opts=B.make_opts(num_cus=8, workers_per_cu=wpc, xcd_parity_skew=skew))
+        _say(f"fp8 group {group} skew {skew}: {info.num_workers} workers, {info.num_combine} cut pairs")
+        assert info.workers_per_group == group
+        assert_close(out, ro, f"fp8 group {group} skew {skew} out")
+        assert_close(lse, rl, f"fp8 group {group} skew {skew} lse")
 
 
 @pytest.mark.parametrize("shape", [(8, 2, 64), (16, 1, 128), (7, 7, 64), (5, 1, 64)],

@@ -476,6 +476,26 @@ def test_runner_takes_every_plan_option():
     assert len(widest) == 3   # three different plans reached the kernels
 
 
+@pytest.mark.parametrize("wpc,group", [(1, 1), (4, 4), (8, 8)])
+def test_every_launch_group_size(wpc, group):
+    """The plan packs 1, 4 or 8 workers into each attention workgroup as it
+    reaches 4 or 8 workers per CU; the launch takes that size from the plan.
+    Each size, with equal slices and with a group-parity skew, against the
+    oracle."""
+    rng = np.random.default_rng(6)
+    lens = np.exp(rng.normal(np.log(1500), 1.0, size=24)).astype(np.int64).clip(16, 12000)
+    b = build_batch(lens, 28, 4, 128, 79)
+    ref = run_oracle(b)
+    for skew in (0, 60):
+        runner = B.DecodeAttention(28, 4, 128, opts=B.make_opts(num_cus=8, workers_per_cu=wpc, xcd_parity_skew=skew))
+        out, lse, _ = run_gpu(b, runner=runner)
+        info = runner.last_info
+        _say(f"group {group} skew {skew}: {info.num_workers} workers, {info.num_combine} cut pairs")
+        assert info.workers_per_group == group and info.num_workers == 8 * wpc
+        assert_close(out, ref[0], f"group {group} skew {skew} out")
+        assert_close(lse, ref[1], f"group {group} skew {skew} lse")
+
+
 def test_runner_steps_switching_streams_in_order():
     """Forty runner steps that move between two streams every five steps, each
     switch ordered by an event wait on the stream before (no host
