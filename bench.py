@@ -715,6 +715,13 @@ def _events_vs_trace(rows, kernel, event_us):
             f"({100 * (event_us / tr - 1):+.1f} %) from it (the start event is a marker ahead of the dispatch)"]
 
 
+def _skew_note(command):
+    if "--skew" not in command:
+        return []
+    return ["The plan skews in the command are the ones a default run (which times the candidates first) chose "
+            "on the same GPU just before; fixing them keeps those calibration launches out of the trace.", ""]
+
+
 def summarize_trace(stats_csv, command, out_md, bench_json=None):
     """Markdown summary of a rocprofv3 --kernel-trace --stats run (the decode
     step, the re-prefill leg when the bench line is an --only-reprefill one,
@@ -723,7 +730,8 @@ def summarize_trace(stats_csv, command, out_md, bench_json=None):
     b = json.load(open(bench_json)) if bench_json else None
     if b is not None and "pool_copies_rotated" in b:
         lines = [f"# Kernel trace: the decode step on {b['workload']}", "", "Command (from the repository root):",
-                 "", "```", command, "```", "", f"Kernel source sha256[:16]: `{kernel_source_hash()}`", "",
+                 "", "```", command, "```", ""] + _skew_note(command) + [
+                 f"Kernel source sha256[:16]: `{kernel_source_hash()}`", "",
                  "| kernel | calls | average us | min us | max us | share % |", "|---|---|---|---|---|---|"]
         for r in rows:
             lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
@@ -744,11 +752,7 @@ def summarize_trace(stats_csv, command, out_md, bench_json=None):
              else "# Kernel trace: the decode step on the long-tail batch, bf16 and fp8 caches" if fp8
              else f"# Kernel trace: {ATTN_KERNEL} on the long-tail batch")
     src = EXTEND_SRC if reprefill else KERNEL_SRC
-    lines = [title, "", "Command (from the repository root):", "", "```", command, "```", ""]
-    if "--skew" in command:
-        lines += ["The plan skews in the command are the ones a default run (which times the candidates first) "
-                  "chose on the same GPU just before; fixing them keeps those calibration launches out of the "
-                  "trace.", ""]
+    lines = [title, "", "Command (from the repository root):", "", "```", command, "```", ""] + _skew_note(command)
     lines += [f"Kernel source sha256[:16]: `{kernel_source_hash(src)}`", "",
              "| kernel | calls | average us | min us | max us | share % |", "|---|---|---|---|---|---|"]
     for r in rows:
