@@ -317,6 +317,10 @@ def test_attn_rejects_mismatched_plan(lib):
     bad = B.sf_plan_info.from_buffer_copy(info)
     bad.work_bytes += 32
     assert _call(lib, desc, bad) == 4
+    for group in (0, 2, 16):           # the launch packs 1, 4 or 8 waves per workgroup, nothing else
+        bad = B.sf_plan_info.from_buffer_copy(info)
+        bad.workers_per_group = group
+        assert _call(lib, desc, bad) == 4
 
 
 def test_combine_rejects_bad_arguments(lib):
