@@ -95,7 +95,7 @@ typedef struct sf_plan_info {
   int32_t num_combine;       /* (seq, KV head) pairs cut into more than one segment */
   int32_t num_partials;      /* partial-result slots = sum of their segment counts */
   int32_t chunk_pages;       /* the most pages any worker owns (0 if T = 0) */
-  int32_t workers_per_group; /* G: waves per attention workgroup, 1, 4 or 8 (rule below) */
+  int32_t workers_per_group; /* G: waves per attention workgroup, 1, 2, 4 or 8 (rule below) */
   uint64_t work_bytes;       /* bytes of the work list:
                                 (num_workers + num_work + num_combine) * 32 */
   uint64_t workspace_bytes;  /* device scratch sf_decode_attn needs (0 if no partials) */
@@ -112,8 +112,8 @@ typedef struct sf_plan_info {
  * T = sum_p pages_p global pages. With
  *   W = ceil(T / chunk_pages)                                   if chunk_pages > 0
  *   W = min(workers_per_cu * num_cus, ceil(T / min_chunk_pages)) otherwise
- * (W = 1 if T = 0 but B * Hkv > 0), and G = 8 if W >= 8 num_cus, 4 if
- * W >= 4 num_cus, else 1, worker w owns the global pages
+ * (W = 1 if T = 0 but B * Hkv > 0), and G the largest of 8, 4, 2 for which
+ * W is a positive multiple of G num_cus (else G = 1), worker w owns the global pages
  * [floor(T C(w) / C(W)), floor(T C(w + 1) / C(W))) with C(v) = 1000 v +
  * p D(v), D(v) = v mod G if floor(v / G) is even, else G - v mod G: every
  * worker reads its share of the pages however skewed the lengths are, 1000 + p

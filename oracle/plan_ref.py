@@ -9,7 +9,7 @@ planner, so the two can be compared bit for bit:
   pairs p = (s, kvh), s-major; pages_p = ceil(L_s / 16); T = sum_p pages_p
   W = ceil(T / chunk_pages) if chunk_pages > 0
       else min(workers_per_cu * num_cus, ceil(T / min_chunk))   (1 if T = 0 < #pairs)
-  G = 8 if W >= 8*num_cus, 4 if W >= 4*num_cus, else 1 (workers per launch group)
+  G = the largest of 8, 4, 2 with W a positive multiple of G*num_cus, else 1 (workers per launch group)
   worker w owns global pages [floor(T*C(w)/C(W)), floor(T*C(w+1)/C(W))) with
   C(v) = 1000*v + p*D(v), D(v) = v % G if (v // G) is even else G - v % G:
   workers of even groups weigh 1000 + p, of odd groups 1000 - p
@@ -58,7 +58,7 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
     else:
         workers = min(wpc * num_cus, _ceil(total, mn))
 
-    group = 8 if workers >= 8 * num_cus else 4 if workers >= 4 * num_cus else 1
+    group = next((g for g in (8, 4, 2) if workers >= g * num_cus and workers % (g * num_cus) == 0), 1)
 
     # every (worker, pair) overlap is a segment
     starts = np.cumsum([0] + pages)

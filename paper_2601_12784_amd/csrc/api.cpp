@@ -17,7 +17,8 @@ sf_status check_plan(const sf_attn_desc* d, const sf_plan_info* info) {
   if (info->desc_key != desc_key(d)) return SF_ERR_PLAN_MISMATCH;
   if (info->num_workers < 0 || info->num_work < 0 || info->num_combine < 0 || info->num_partials < 0)
     return SF_ERR_INVALID_ARG;
-  if ((info->workers_per_group != 1 && info->workers_per_group != 4 && info->workers_per_group != 8) ||
+  const int32_t grp = info->workers_per_group;
+  if ((grp != 1 && grp != 2 && grp != 4 && grp != 8) ||
       info->work_bytes != uint64_t(table_rows(info->num_workers) + info->num_work +
                                                           info->num_combine) * kItemInts * 4)
     return SF_ERR_PLAN_MISMATCH;

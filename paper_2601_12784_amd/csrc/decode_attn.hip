@@ -1124,10 +1124,11 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
 }  // namespace
 
 // Waves (workers) per workgroup, as the plan chose it: the kernels run two
-// waves per SIMD at most, so a plan with at least 8 or 4 workers per CU
-// packs that many into each workgroup, which then share one read of their
-// table rows; smaller plans keep one worker per workgroup, spread over every
-// CU. Workgroup b holds workers G b .. G b + G - 1 and runs on XCD b mod 8.
+// waves per SIMD at most, so a plan with 8, 4 or 2 workers per CU (or a
+// multiple) packs that many into each workgroup, which then share one read
+// of their table rows; other plans keep one worker per workgroup, spread
+// over every CU. Workgroup b holds workers G b .. G b + G - 1 and runs on
+// XCD b mod 8.
 template <int kWG>
 void (*pick_attention(const AttnArgs& a))(AttnArgs) {
   if (a.k_scale) return a.head_dim == 128 ? attn_worker_fp8_kernel<128, kWG> : attn_worker_fp8_kernel<64, kWG>;
@@ -1137,10 +1138,12 @@ void (*pick_attention(const AttnArgs& a))(AttnArgs) {
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
   if (a.num_workers == 0) return hipSuccess;
-  const int per_group = a.workers_per_group;   // 1, 4 or 8 (checked with the plan)
+  const int per_group = a.workers_per_group;   // 1, 2, 4 or 8 (checked with the plan)
   const dim3 grid((a.num_workers + per_group - 1) / per_group), block(64 * per_group);
-  void (*kernel)(AttnArgs) = per_group == 8 ? pick_attention<8>(a) : per_group == 4 ? pick_attention<4>(a)
-                                                                                     : pick_attention<1>(a);
+  void (*kernel)(AttnArgs) = per_group == 8   ? pick_attention<8>(a)
+                             : per_group == 4 ? pick_attention<4>(a)
+                             : per_group == 2 ? pick_attention<2>(a)
+                                              : pick_attention<1>(a);
   if (start || stop)
     hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, a);
   else

@@ -117,8 +117,16 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
   if (workers > INT32_MAX / 2) return SF_ERR_INVALID_ARG;
 
   // The attention launch runs workers G b .. G b + G - 1 as workgroup b
-  // (one wave each), and workgroup b runs on XCD b mod 8.
-  const int32_t group = workers >= 8 * int64_t(num_cus) ? 8 : workers >= 4 * int64_t(num_cus) ? 4 : 1;
+  // (one wave each), and workgroup b runs on XCD b mod 8. G is the largest
+  // of 8, 4, 2 that packs the workers into whole rounds of one workgroup per
+  // CU (W a multiple of G num_cus), else 1: a partial round would leave some
+  // CUs with one group more than others.
+  int32_t group = 1;
+  for (const int32_t g : {8, 4, 2})
+    if (workers >= g * int64_t(num_cus) && workers % (g * int64_t(num_cus)) == 0) {
+      group = g;
+      break;
+    }
 
   // Worker range starts lo(w) = floor(T C(w) / C(W)) with the cumulative
   // weight C(v) = 1000 v + p D(v), D(v) = v mod G if floor(v / G) is even,

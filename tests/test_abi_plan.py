@@ -118,7 +118,8 @@ def test_plan_skew_kept_or_dropped_by_cut_count():
 
 
 @pytest.mark.parametrize("skew", [-250, -30, 1, 50, 250])
-@pytest.mark.parametrize("num_cus,wpc,group,nseq", [(64, 0, 4, 180), (64, 8, 8, 180), (2048, 0, 1, 40)])
+@pytest.mark.parametrize("num_cus,wpc,group,nseq", [(64, 0, 4, 180), (64, 8, 8, 180), (64, 6, 2, 180),
+                                                   (64, 5, 1, 180), (2048, 0, 1, 40)])
 def test_plan_matches_rederivation_parity_skew(skew, num_cus, wpc, group, nseq):
     rng = np.random.default_rng(400 + skew)
     lens = np.exp(rng.normal(np.log(2000), 1.0, size=nseq)).astype(np.int64).clip(0, 16384)
@@ -168,7 +169,7 @@ def test_tiny_plan_by_hand():
 
 
 @pytest.mark.parametrize("seed,skew,wpc", [(0, 0, 0), (1, 0, 0), (2, -40, 0), (3, 0, 8), (4, 120, 0),
-                                           (5, 60, 8), (6, -90, 4)])
+                                           (5, 60, 8), (6, -90, 4), (7, 70, 6), (8, -50, 2), (9, 30, 5)])
 def test_plan_invariants(seed, skew, wpc):
     """Every worker owns its share of the T pages to within one page: T / W
     without a parity skew; with skew p, a worker of group floor(w / G) weighs
@@ -193,7 +194,7 @@ def test_plan_invariants(seed, skew, wpc):
     assert np.array_equal(tab[:, 0], np.concatenate([[0], np.cumsum(tab[:, 1])[:-1]]))
     assert tab[:, 1].sum() == info.num_work
     G = info.workers_per_group
-    assert G == (8 if W >= 8 * num_cus else 4 if W >= 4 * num_cus else 1)
+    assert G == next((g for g in (8, 4, 2) if W >= g * num_cus and W % (g * num_cus) == 0), 1)
     p = skew
     weight = [1000 + p if (w // G) % 2 == 0 else 1000 - p for w in range(W)]
     owned = []
@@ -317,7 +318,7 @@ def test_attn_rejects_mismatched_plan(lib):
     bad = B.sf_plan_info.from_buffer_copy(info)
     bad.work_bytes += 32
     assert _call(lib, desc, bad) == 4
-    for group in (0, 2, 16):           # the launch packs 1, 4 or 8 waves per workgroup, nothing else
+    for group in (0, 3, 16):           # the launch packs 1, 2, 4 or 8 waves per workgroup, nothing else
         bad = B.sf_plan_info.from_buffer_copy(info)
         bad.workers_per_group = group
         assert _call(lib, desc, bad) == 4

@@ -95,7 +95,7 @@ def test_fp8_attention_one_very_long_sequence():
     assert_close(lse, rl, "very long lse")
 
 
-@pytest.mark.parametrize("wpc,group", [(1, 1), (4, 4), (0, 8)])
+@pytest.mark.parametrize("wpc,group", [(1, 1), (2, 2), (4, 4), (6, 2), (0, 8)])
 def test_fp8_attention_every_launch_group_size(wpc, group):
     """fp8 steps plan eight workers per CU by default (eight waves per
     workgroup); four and one per CU give groups of 4 and 1. Each, with equal

@@ -476,10 +476,11 @@ def test_runner_takes_every_plan_option():
     assert len(widest) == 3   # three different plans reached the kernels
 
 
-@pytest.mark.parametrize("wpc,group", [(1, 1), (4, 4), (8, 8)])
+@pytest.mark.parametrize("wpc,group", [(1, 1), (2, 2), (4, 4), (5, 1), (6, 2), (8, 8)])
 def test_every_launch_group_size(wpc, group):
-    """The plan packs 1, 4 or 8 workers into each attention workgroup as it
-    reaches 4 or 8 workers per CU; the launch takes that size from the plan.
+    """The plan packs 8, 4 or 2 workers into each attention workgroup when
+    that fills whole rounds of one workgroup per CU, else 1; the launch takes
+    that size from the plan.
     Each size, with equal slices and with a group-parity skew, against the
     oracle."""
     rng = np.random.default_rng(6)
