@@ -210,7 +210,8 @@ def config_bench(name, steps, warmup, skew=0):
     long-tail step is: plan -> attention -> combine back to back on one
     stream, wall time per step, attention kernel from HIP events. Batches
     whose pools would fit in the last-level cache rotate over enough device
-    copies (at least 4) that every step reads its bytes from HBM."""
+    copies (at least 4) that every step reads its bytes from HBM. skew=None
+    chooses the plan skew for this workload by timing (calibrate_skew)."""
     import torch
     from paper_2601_12784_amd.workloads import make_batch, CONFIGS
     b = make_batch(name, poison=False)
@@ -219,9 +220,11 @@ def config_bench(name, steps, warmup, skew=0):
     rotate = 1 if pool_bytes > 2 * LLC_BYTES else max(4, -(-4 * LLC_BYTES // pool_bytes))
     if name == "tiny":
         rotate = 1   # 130 KB: a latency figure, cache-resident by nature
-    st = Stepper(b, rotate=rotate, skew=skew)
+    st = Stepper(b, rotate=rotate, skew=skew or 0)
+    cal = calibrate_skew(st) if skew is None else None
+    skew = cal["chosen"] if cal else skew
     ms_step, k_mean, k_med = time_steps(st, steps, warmup)
-    info = st.info0
+    info = st.runner.last_info
     gbs = kv / (k_mean * 1e-3) / 1e9
     _, bsz, hq, hkv, d = CONFIGS[name]
     res = {"xcd_parity_skew": skew, "workload": f"{name}: {bsz} sequences, {hq} q / {hkv} kv heads, head_dim {d}, page 16",
@@ -231,7 +234,8 @@ def config_bench(name, steps, warmup, skew=0):
            "kv_gb_per_s_step": round(kv / (ms_step * 1e-3) / 1e9, 2),
            "kv_gb_per_s_kernel": round(gbs, 2), "pct_of_peak_hbm_kernel": round(100 * gbs / PEAK_HBM_GBPS, 2),
            "seq_steps_per_s": round(b.num_seqs / (ms_step * 1e-3), 1),
-           "workers": info.num_workers, "segments": info.num_work, "cut_pairs": info.num_combine}
+           "workers": info.num_workers, "segments": info.num_work, "cut_pairs": info.num_combine,
+           "skew_calibration": cal}
     del st
     torch.cuda.empty_cache()
     return res
@@ -954,7 +958,9 @@ def main():
         legs = {}
         for name in ("tiny", "gqa7b", "gqa32b"):
             log(f"config {name}")
-            legs[name] = config_bench(name, args.steps, min(args.warmup, 500), skew=skew)
+            # the single-step configs choose their own skew (unless --skew fixes it); tiny is latency only
+            legs[name] = config_bench(name, args.steps, min(args.warmup, 500),
+                                      skew=(skew if args.skew is not None or name == "tiny" else None))
             log(f"  step {legs[name]['ms_per_step'] * 1e3:.1f} us, kernel {legs[name]['attn_kernel_us']} us, "
                 f"{legs[name]['kv_gb_per_s_kernel']} GB/s ({legs[name]['pct_of_peak_hbm_kernel']} % of peak), "
                 f"{legs[name]['seq_steps_per_s']} seq-steps/s")
