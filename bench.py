@@ -847,7 +847,8 @@ def main():
         print(json.dumps(reprefill_bench()), flush=True)
         return
     if args.only_config:
-        print(json.dumps(config_bench(args.only_config, args.steps, args.warmup, skew=args.skew or 0)), flush=True)
+        fixed = args.skew if args.skew is not None else (0 if args.only_config == "tiny" else None)
+        print(json.dumps(config_bench(args.only_config, args.steps, args.warmup, skew=fixed)), flush=True)
         return
 
     if args.copy_probe:
