@@ -353,8 +353,8 @@ sf_status sf_kv_quantize_fp8(const sf_attn_desc* desc, const void* k_pool, const
  * entries 0 .. ceil(L_s / 16) - 1 of every sequence with E_s > 0 are read.
  */
 typedef struct sf_extend_info {
-  int32_t num_items;        /* work items (one 512-thread block each, up to 256 rows) */
-  int32_t tokens_per_item;  /* new tokens per item: floor(256 / g) */
+  int32_t num_items;        /* work items (one 768-thread block each, up to 384 rows) */
+  int32_t tokens_per_item;  /* new tokens per item: floor(384 / g) */
   int32_t num_q_rows;       /* T */
   int32_t reserved;         /* 0 */
   uint64_t work_bytes;      /* num_items * 32 */
@@ -364,7 +364,7 @@ typedef struct sf_extend_info {
 /*
  * Builds the extend work list on the host (no device calls).
  *
- * Rule: each sequence's new tokens are cut into blocks of n = floor(256 / g)
+ * Rule: each sequence's new tokens are cut into blocks of n = floor(384 / g)
  * (the last block shorter), and each (sequence, KV head, block) is one item,
  * whose rows are the block's tokens times the group's g query heads. An item
  * whose block starts at new token t0 with nt tokens reads the keys

@@ -134,9 +134,9 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
                 work_bytes=(table.shape[0] + items.shape[0] + comb.shape[0]) * 8 * 4)
 
 
-def extend_plan(seq_lens, q_lens, num_kv_heads, num_q_heads, rows_per_item=256):
+def extend_plan(seq_lens, q_lens, num_kv_heads, num_q_heads, rows_per_item=384):
     """The extend work list, re-derived from its rule: new tokens cut into
-    blocks of floor(256 / g) per (sequence, KV head); an item starting at new
+    blocks of floor(384 / g) per (sequence, KV head); an item starting at new
     token t0 with nt tokens reads ceil((P_s + t0 + nt) / 32) blocks of 32
     keys; items by that count, largest first, ties in (s, kvh, t0) order.
     Rows: (seq, kv_head, t0, nt, P_s, cu_s, steps, 0)."""

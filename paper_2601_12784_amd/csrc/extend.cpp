@@ -3,7 +3,7 @@
 // A re-prefill recomputes a resumed trajectory's KV cache (Sec. 2.3, partial
 // rollout and migration). Its cost per new token grows with the token's
 // position, so a sequence's new tokens are cut into blocks of
-// floor(256 / g) tokens, one work item per (sequence, KV head, block), and
+// floor(384 / g) tokens, one work item per (sequence, KV head, block), and
 // the items are launched longest first: the GPU starts the longest key walks
 // early and fills the tail with the short ones. The rule is stated in
 // sf_decode_attn.h next to sf_extend_attn_plan.

@@ -10,21 +10,23 @@
 // Unlike a decode step this is a dense contraction: every key tile is used by
 // all new tokens after it, so the work runs on the matrix cores. A work item
 // is one (sequence, KV head, block of new tokens); its rows are the block's
-// tokens times the g query heads of the group (token-major), at most 256 rows,
-// 32 per wave (8 waves). The item walks the keys in steps of 32 (two pages),
-// two steps per barrier: the waves stage the K and V tiles of both steps
-// (32 KiB at D = 128) through LDS, double buffered, and each wave computes,
-// per step and 16-row tile,
+// tokens times the g query heads of the group (token-major), at most 384 rows,
+// 32 per wave (12 waves, three per SIMD). The item walks the keys in steps of
+// 32 (two pages), one step per barrier: eight of the waves stage the K and V
+// tiles of the next step (16 KiB at D = 128) through LDS, double buffered, and
+// each wave computes, per step and 16-row tile,
 //
 //   S^T[32 keys][16 rows] = K Q^T        2 x (D/32) v_mfma_f32_16x16x32_bf16
 //   online softmax in base 2             (row = lane column; lazily moved reference)
 //   O^T[D][16 rows]      += V^T P^T      (D/16) v_mfma_f32_16x16x32_f16
 //
-// with each K and V operand read from LDS once per wave and used for both of
-// its row tiles, and the two tiles pipelined so that one tile's matrix-core
-// work overlaps the other's exponentials. The operand mapping is the decode
-// kernel's: each lane's eight scores are keys 4*grp .. 4*grp+3 of both
-// pages, the eight P^T values its P.V operand needs.
+// with each K and V operand read from LDS once per wave, just before the
+// MFMAs of both row tiles that use it. Three waves per SIMD (168 registers
+// each) hide the latencies that a wave's own schedule would otherwise have
+// to: with two waves per SIMD and the row tiles software-pipelined inside
+// each wave the same work took 17 % longer. The operand mapping is the
+// decode kernel's: each lane's eight scores are keys 4*grp .. 4*grp+3 of
+// both pages, the eight P^T values its P.V operand needs.
 //
 // The P.V product runs on fp16 operands. The weights P are rounded to fp16
 // (relative error 2^-11) instead of bf16 (2^-8): with bf16 weights a row
@@ -39,7 +41,9 @@
 // Measured alternatives (full re-prefill of 32 long-tail trajectories):
 // 64 rows per wave (4 waves, one per SIMD) halves the LDS operand reads but
 // leaves no second wave per SIMD to overlap with, and is 1.5x slower; items
-// of 128 rows double the K/V staging per row and are 2x slower.
+// of 128 rows double the K/V staging per row and are 2x slower; 16 rows per
+// wave (16 waves, four per SIMD) doubles the LDS operand reads per row and
+// is 12 % slower than three waves of 32 rows.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -58,11 +62,12 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(4))) const int32_t* const_i32_ptr;
 
 constexpr float kLn2 = 0.69314718055994530942f;
-constexpr int kWaves = 8;
+constexpr int kWaves = 12;
+constexpr int kStageWaves = 8;    // waves that stage K and V (the other four only compute)
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowTiles = 2;      // 16-row MFMA tiles per wave
 constexpr int kStepKeys = 2 * kPage;   // keys per step (two pages)
-constexpr int kSub = 2;                // steps per barrier interval
+constexpr int kSub = 1;                // steps per barrier interval
 constexpr float kRescaleMax = 32768.f; // headroom of the lazily moved softmax reference, 2^15 (fp16 weights)
 static_assert(kWaves * kRowTiles * 16 == kExtendRows, "rows per item");
 
@@ -107,9 +112,9 @@ struct Tiles {
   static constexpr int kElems = kPage * D;            // bf16 per (page, KV head) tile
   static constexpr int kChunks = kElems / 8;          // 16-byte pieces per tile
   // A step stages four tiles (K and V of two pages); each is moved by
-  // kWaves / 4 waves, kWaveChunks wave-wide 1 KiB chunks (64 pieces) each.
-  static constexpr int kWaveChunks = kChunks / 64 / (kWaves / 4);
-  static_assert(kWaveChunks * 64 * kWaves == 4 * kChunks, "staging split");
+  // kStageWaves / 4 waves, kWaveChunks wave-wide 1 KiB chunks (64 pieces) each.
+  static constexpr int kWaveChunks = kChunks / 64 / (kStageWaves / 4);
+  static_assert(kWaveChunks * 64 * kStageWaves == 4 * kChunks, "staging split");
 };
 
 // Sum of a lane's eight weights of a step.
@@ -201,22 +206,8 @@ __device__ __forceinline__ u32x4 settle(TileWeights& t, float c, float& m, float
                pack_f16(t.p[6], t.p[7])};
 }
 
-// Scheduling hints: n times {one MFMA, then k vector ALU ops}, so the
-// vector work of one row tile issues while the matrix core works on the
-// other (the matrix core runs an MFMA for 16 cycles; a wave issues other
-// independent work meanwhile only if it comes next in program order).
-// (n must be a compile-time constant once the caller's loops are unrolled.)
-template <int K>
-__device__ __forceinline__ void interleave_mfma_valu(int n) {
-#pragma unroll
-  for (int i = 0; i < n; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, K, 0);
-  }
-}
-
 template <int D>
-__global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 3))) void extend_attn_kernel(ExtendArgs a) {
   constexpr int KB = D / 32;
   constexpr int JB = D / 16;
   constexpr int TE = Tiles<D>::kElems;
@@ -279,18 +270,18 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
     lsum[rt] = 0.f;
   }
 
-  // Staging: wave w moves tile w / 2 of each step (0: K of the step's first
-  // page, 1: K of its second, 2 and 3: V of the two pages), in 1 KiB chunks
-  // (w % 2) * NC .. + NC - 1. The tile and its page are wave-uniform, so the
-  // global address is a scalar base plus a fixed per-lane offset, and every
-  // LDS address is fixed per lane: no per-step address arithmetic. A page past
-  // the item's last is replaced by its first page (always in range); its keys
-  // lie past kend and are masked.
-  // The keys are walked in intervals of kSub steps with one barrier each:
-  // a wave's work between barriers is then long enough for the two waves
-  // that share a SIMD to fall out of step (one on the matrix core while the
-  // other exponentiates).
-  const int stile = wave >> 1;
+  // Staging: wave w < 8 moves tile w / 2 of each step (0: K of the step's
+  // first page, 1: K of its second, 2 and 3: V of the two pages), in 1 KiB
+  // chunks (w % 2) * NC .. + NC - 1; waves 8 .. 11 stage nothing. The tile and
+  // its page are wave-uniform, so the global address is a scalar base plus a
+  // fixed per-lane offset, and every LDS address is fixed per lane: no
+  // per-step address arithmetic. A page past the item's last is replaced by
+  // its first page (always in range); its keys lie past kend and are masked.
+  // The keys are walked in intervals of kSub steps with one barrier each (one
+  // step: two would need prefetch registers that the three-waves-per-SIMD
+  // budget does not have).
+  const bool stager = wave < kStageWaves;
+  const int stile = (stager ? wave : 0) >> 1;
   const uint16_t* const spool = stile < 2 ? a.k_pool : a.v_pool;
   int soff[NC];    // element offset of this lane's piece in the tile
   int sdst0[NC];   // LDS element offset of the piece (K) or of its first 8-byte half (V)
@@ -364,68 +355,67 @@ __global__ __launch_bounds__(kThreads) void extend_attn_kernel(ExtendArgs a) {
     }
   };
 
-  // One step: keys key0 .. key0 + 31 from the given LDS slice. The row
-  // tiles are pipelined: the scores of tile rt + 1 and the P.V product of
-  // tile rt - 1 run on the matrix core while tile rt is exponentiated.
+  // One step, operands read from LDS just before use: the scores of both
+  // row tiles per 32 dims of K, then the softmax of both, then P.V per
+  // 16 dims of V (the third wave on each SIMD hides the latencies).
   auto compute = [&](const uint16_t* L, int key0) {
-    // K operands of both pages and V operands of the step.
-    u32x4 kf0[KB], kf1[KB], vf[JB];
+    f32x4 s0[kRowTiles], s1[kRowTiles];
+#pragma unroll
+    for (int rt = 0; rt < kRowTiles; ++rt) {
+      s0[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s1[rt] = s0[rt];
+    }
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       const int ko = ((4 * kb + grp) * kPage + col) * 8;
-      kf0[kb] = *reinterpret_cast<const u32x4*>(L + ko);
-      kf1[kb] = *reinterpret_cast<const u32x4*>(L + TE + ko);
-    }
-    const int vo = 2 * TE + col * 32 + (grp ^ v_swizzle(col)) * 8;
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) vf[jb] = *reinterpret_cast<const u32x4*>(L + vo + jb * 16 * 32);
-    // Scores S^T of row tile rt: lane holds row `col`, keys key0 + 4*grp + e
-    // of page 0 (s0) and page 1 (s1).
-    f32x4 s0[kRowTiles], s1[kRowTiles];
-    auto scores = [&](int rt) {
-      s0[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s1[rt] = s0[rt];
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        s0[rt] = mfma_bf16(kf0[kb], qf[rt][kb], s0[rt]);
-        s1[rt] = mfma_bf16(kf1[kb], qf[rt][kb], s1[rt]);
-      }
-    };
-    scores(0);
-    auto pipeline = [&](auto masked_tag) {
-      constexpr bool kMasked = decltype(masked_tag)::value;
+      const u32x4 k0 = *reinterpret_cast<const u32x4*>(L + ko);
+      const u32x4 k1 = *reinterpret_cast<const u32x4*>(L + TE + ko);
 #pragma unroll
       for (int rt = 0; rt < kRowTiles; ++rt) {
-        if (rt + 1 < kRowTiles) scores(rt + 1);
-        TileWeights t = exponentiate<kMasked>(s0[rt], s1[rt], key0, grp, limit[rt], c, m[rt]);
-        interleave_mfma_valu<3>((rt + 1 < kRowTiles ? 2 * KB : 0) + (rt > 0 ? JB : 0));
-        const u32x4 pf = settle<D, kMasked>(t, c, m[rt], lsum[rt], o[rt]);
+        s0[rt] = mfma_bf16(k0, qf[rt][kb], s0[rt]);
+        s1[rt] = mfma_bf16(k1, qf[rt][kb], s1[rt]);
+      }
+    }
+    const int vo = 2 * TE + col * 32 + (grp ^ v_swizzle(col)) * 8;
+    auto tail = [&](auto masked_tag) {
+      constexpr bool kMasked = decltype(masked_tag)::value;
+      u32x4 pf[kRowTiles];
 #pragma unroll
-        for (int jb = 0; jb < JB; ++jb) o[rt][jb] = mfma_f16(vf[jb], pf, o[rt][jb]);
+      for (int rt = 0; rt < kRowTiles; ++rt) {
+        TileWeights t = exponentiate<kMasked>(s0[rt], s1[rt], key0, grp, limit[rt], c, m[rt]);
+        pf[rt] = settle<D, kMasked>(t, c, m[rt], lsum[rt], o[rt]);
+      }
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(L + vo + jb * 16 * 32);
+#pragma unroll
+        for (int rt = 0; rt < kRowTiles; ++rt) o[rt][jb] = mfma_f16(v, pf[rt], o[rt][jb]);
       }
     };
     if (key0 + kStepKeys - 1 > wave_kmin)
-      pipeline(std::true_type{});
+      tail(std::true_type{});
     else
-      pipeline(std::false_type{});
+      tail(std::false_type{});
   };
 
   const int nint = (nsteps + kSub - 1) / kSub;
-  fetch(0);
-  stage(lds[0], 0);
+  if (stager) {
+    fetch(0);
+    stage(lds[0], 0);
+  }
   __syncthreads();
 
   // One interval from buffer `cur` while the next is staged into `nxt`; the
   // loop is unrolled by two so that both buffers' addresses are constants.
   auto interval = [&](int j, uint16_t (*cur)[4 * TE], uint16_t (*nxt)[4 * TE]) {
-    if (j + 1 < nint) fetch(j + 1);
+    if (stager && j + 1 < nint) fetch(j + 1);
 #pragma unroll
     for (int u = 0; u < kSub; ++u) {
       const int js = kSub * j + u;
       const int key0 = js * kStepKeys;
       if (js < nsteps && key0 <= wave_kmax) compute(cur[u], key0);
     }
-    if (j + 1 < nint) stage(nxt, j + 1);
+    if (stager && j + 1 < nint) stage(nxt, j + 1);
     __syncthreads();
   };
   for (int j = 0; j < nint; j += 2) {

@@ -165,7 +165,7 @@ struct ExtendArgs {
 };
 
 // Rows (tokens x query heads of a group) of one extend work item.
-constexpr int kExtendRows = 256;
+constexpr int kExtendRows = 384;
 
 // start / stop (hipEvent_t, may be NULL) take the kernel's own start and end
 // times: the launch records them from its dispatch (hipExtLaunchKernel), so

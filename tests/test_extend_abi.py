@@ -52,16 +52,19 @@ def test_plan_covers_every_new_token_once_per_kv_head():
 
 
 def test_plan_tiny_by_hand():
-    # g = 128/8 = 16 -> 16 tokens per item; sequence 0: P = 10, E = 20 -> blocks t0 = 0 (16), 16 (4)
+    # g = 16 -> floor(384 / 16) = 24 tokens per item; sequence 0: P = 10, E = 20 -> one block (t0 = 0, 20 tokens)
     desc, info, work = _plan([30, 3], [20, 3], 16, 1, d=64)
-    assert info.tokens_per_item == 16
-    # keys [0, 26) and [0, 30): one step of 32 each, so the tie keeps t0 order
-    assert work.tolist() == [[0, 0, 0, 16, 10, 0, 1, 0],
-                             [0, 0, 16, 4, 10, 0, 1, 0],
+    assert info.tokens_per_item == 24
+    # keys [0, 30) and [0, 3): one step of 32 each, so the tie keeps sequence order
+    assert work.tolist() == [[0, 0, 0, 20, 10, 0, 1, 0],
                              [1, 0, 0, 3, 0, 20, 1, 0]]
     desc, info, work = _plan([60, 3], [40, 3], 16, 1, d=64)
-    # P = 20: blocks t0 = 0 (keys [0, 36): 2 steps), 16 (keys [0, 52): 2), 32 (8 tokens, keys [0, 60): 2)
-    assert work[:, 2].tolist() == [0, 16, 32, 0] and work[:, 6].tolist() == [2, 2, 2, 1]
+    # P = 20: blocks t0 = 0 (24 tokens, keys [0, 44): 2 steps), 24 (16 tokens, keys [0, 60): 2 steps)
+    assert work[:, 2].tolist() == [0, 24, 0] and work[:, 3].tolist() == [24, 16, 3]
+    assert work[:, 6].tolist() == [2, 2, 1]
+    desc, info, work = _plan([100, 3], [80, 3], 16, 1, d=64)
+    # P = 20: blocks t0 = 0 (keys [0, 44): 2 steps), 24 ([0, 68): 3), 48 ([0, 92): 3), 72 (8 tokens, [0, 100): 4)
+    assert work[:, 2].tolist() == [72, 24, 48, 0, 0] and work[:, 6].tolist() == [4, 3, 3, 2, 1]
 
 
 @pytest.mark.parametrize("lens,qls", [([10], [11]), ([10], [-1]), ([40], [3])])
