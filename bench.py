@@ -1,8 +1,10 @@
 """Decode-attention benchmark on the long-tail rollout batch (one MI355X).
 
 One step = the whole hot path for one decode step of the batch: host plan
-(length-aware split-K) -> work-list upload -> attention kernel -> LSE combine.
-Inputs (q, paged K/V pools, block table) are resident in HBM before timing.
+(length-aware split-K, written to pinned memory that the kernels read in
+place) -> attention kernel -> LSE combine. Inputs (q, paged K/V pools, block
+table) are resident in HBM before timing. Before its timed steps each leg may
+time the plan's group-parity skew candidates (untimed calibration).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1]
 
