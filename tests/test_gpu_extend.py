@@ -79,6 +79,8 @@ CASES = {
     "reprefill": ([37, 300, 64, 1], [37, 300, 64, 1]),
     "chunked": ([900, 233, 517, 48], [200, 1, 117, 16]),
     "mixed": ([40, 16, 1, 0, 700], [0, 9, 1, 0, 333]),
+    # with one query head per KV head an item holds 384 tokens: several full items and ragged tails
+    "wide": ([1000, 777], [900, 777]),
 }
 
 
