@@ -119,9 +119,11 @@ typedef struct sf_plan_info {
  * worker reads its share of the pages however skewed the lengths are, 1000 + p
  * per mille of the mean if floor(w / G) is even, 1000 - p if it is odd
  * (p = opts->xcd_parity_skew, default 0: equal slices, within one page; p is
- * also 0 when chunk_pages is forced, and when the skewed slices would cut
- * more than floor(W / 8) more pairs than the equal ones: equal lengths can put
- * every equal boundary on a pair boundary). The attention launch runs workers
+ * also 0 when chunk_pages is forced, when the skewed slices would leave a
+ * worker without a page (slices near one page; the equal ones give each
+ * worker at least one, so every worker has a segment), and when they would
+ * cut more than floor(W / 8) more pairs than the equal ones: equal lengths can
+ * put every equal boundary on a pair boundary). The attention launch runs workers
  * G b .. G b + G - 1 as workgroup b, and workgroup b runs on XCD b mod 8: a
  * GPU whose odd (p > 0) or even (p < 0) XCDs are slower on the same work can
  * give them less. How much slower, and which, differs from one MI355X to the

@@ -14,8 +14,9 @@ planner, so the two can be compared bit for bit:
   C(v) = 1000*v + p*D(v), D(v) = v % G if (v // G) is even else G - v % G:
   workers of even groups weigh 1000 + p, of odd groups 1000 - p
   (p = xcd_parity_skew per mille, -250 .. 250, default 0; 0 when chunk_pages
-  is forced, or when these slices cut more than W // 8 pairs more than the
-  equal ones, p = 0, would); cut at pair boundaries into segments (items); empty
+  is forced, when these slices would leave a worker no page, or when they cut
+  more than W // 8 pairs more than the equal ones, p = 0, would); cut at pair
+  boundaries into segments (items); empty
   pairs go to worker e mod W after its segments; n_p = segments of pair p
   partial slots for pairs with n_p > 1 in pair order, segment c -> base + c
 
@@ -79,7 +80,8 @@ def plan(seq_lens, num_kv_heads, num_q_heads, head_dim, num_cus, chunk_pages=0,
     bounds = cuts_for(skew)
     if skew and workers > 1:
         equal = cuts_for(0)
-        if pairs_cut(bounds) - pairs_cut(equal) > workers // 8:
+        leaves_one_empty = any(bounds[w + 1] == bounds[w] for w in range(workers))
+        if leaves_one_empty or pairs_cut(bounds) - pairs_cut(equal) > workers // 8:
             bounds = equal
     per_worker = [[] for _ in range(workers)]
     seg_of_pair = {p: [] for p in range(len(pairs))}

@@ -198,6 +198,22 @@ extern "C" sf_status sf_decode_attn_plan(const sf_attn_desc* desc, const int32_t
     }
     return cut;
   };
+  if (skew != 0 && workers > 1) {
+    // Slices near one page: a skew that would leave a worker without a page
+    // falls back to equal slices (which give every worker at least one, since
+    // W <= T), so every worker has a segment.
+    Cuts c;
+    c.init(total, workers, skew, group);
+    int64_t prev = 0;
+    for (int64_t w = 0; w < workers; ++w) {
+      c.next();
+      if (c.q == prev) {
+        skew = 0;
+        break;
+      }
+      prev = c.q;
+    }
+  }
   thread_local std::vector<int32_t> nseg_buf, nseg_alt;
   nseg_buf.resize(size_t(num_pairs));
   int32_t* nseg = nseg_buf.data();

@@ -117,6 +117,31 @@ def test_plan_skew_kept_or_dropped_by_cut_count():
         assert s.num_combine - e.num_combine <= s.num_workers // 8
 
 
+def test_plan_skew_dropped_where_a_worker_would_get_no_page():
+    """Slices near one page (minimum slice 1, as many workers as pages): a skew
+    would leave some workers without a page, so the plan takes equal slices.
+    Every worker then has at least one segment and no segment is empty, and
+    the plan oracle agrees. Where the skew leaves every worker a page, it is
+    kept."""
+    lens = [48] * 40                      # 2 KV heads x 40 x 3 pages: T = 240
+    for skew in (100, -100, 250):
+        s, ws, ref = _plan_both(lens, 4, 2, 128, num_cus=64, wpc=4, mn=1, skew=skew)
+        e, we, _ = _plan_both(lens, 4, 2, 128, num_cus=64, wpc=4, mn=1)
+        _assert_same(s, ws, ref)
+        assert s.num_workers == 240 and np.array_equal(ws, we)
+        table, items, _ = _split(s, ws)
+        assert table[:, 1].min() >= 1 and np.all(items[:, 3] > items[:, 2])
+    # three pages per worker on skewed lengths: 750 per mille still leaves each two
+    rng = np.random.default_rng(5)
+    skewed = np.exp(rng.normal(np.log(300), 1.0, size=24)).astype(np.int64).clip(16, 3000)
+    s, ws, ref = _plan_both(skewed, 4, 2, 128, num_cus=256, wpc=8, mn=3, skew=250)
+    e, we, _ = _plan_both(skewed, 4, 2, 128, num_cus=256, wpc=8, mn=3)
+    _assert_same(s, ws, ref)
+    assert s.num_workers == e.num_workers and s.chunk_pages > e.chunk_pages
+    table, items, _ = _split(s, ws)
+    assert table[:, 1].min() >= 1 and np.all(items[:, 3] > items[:, 2])
+
+
 @pytest.mark.parametrize("skew", [-250, -30, 1, 50, 250])
 @pytest.mark.parametrize("num_cus,wpc,group,nseq", [(64, 0, 4, 180), (64, 8, 8, 180), (64, 6, 2, 180),
                                                    (64, 5, 1, 180), (2048, 0, 1, 40)])
