@@ -129,3 +129,73 @@ def test_sweep_attention_matches_oracle(seed):
           f"{info8.num_work} segments, {info8.num_combine} cut pairs", flush=True)
     _assert_close(out8.cpu().numpy(), ro8, "fp8 out")
     _assert_close(lse8.cpu().numpy(), rl8, "fp8 lse")
+
+
+# ---------------------------------------------------------------------------
+# extend (re-prefill) attention: drawn prefixes and new-token counts
+# ---------------------------------------------------------------------------
+EXTEND_SEEDS = range(12)
+
+
+def extend_case(seed):
+    rng = np.random.default_rng(2000 + seed)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    g = int(rng.choice([1, 2, 3, 5, 7, 8, 16]))
+    while hkv * g > 64:
+        hkv //= 2
+    d = int(rng.choice([64, 128]))
+    b = int(rng.integers(1, 7))
+    prefix = np.where(rng.random(b) < 0.3, 0, rng.integers(0, 1500, size=b))
+    new = rng.integers(0, 500, size=b)
+    u = rng.random(b)
+    new[u < 0.15] = 0
+    new[(u >= 0.15) & (u < 0.3)] = 1
+    lens = prefix + new
+    scale = float(rng.choice([1.0, -1.0, 2.0])) / math.sqrt(d)
+    return dict(seed=seed, hq=hkv * g, hkv=hkv, d=d, lens=lens, q_lens=new, scale=scale,
+                k_mult=float(rng.choice([1.0, 3.0])), store=bool(rng.random() < 0.5))
+
+
+@pytest.mark.parametrize("seed", EXTEND_SEEDS)
+def test_sweep_extend_plan_matches_oracle(seed):
+    c = extend_case(seed)
+    lens = c["lens"].astype(np.int32)
+    stride = max(1, int(-(-lens.max() // PAGE)))
+    pages = max(1, int((-(-lens.astype(np.int64) // PAGE)).sum()))
+    desc = B.make_desc(lens.size, c["hq"], c["hkv"], c["d"], stride, pages, c["scale"])
+    info, work = B.sf_extend_attn_plan(desc, lens, c["q_lens"])
+    want, per = plan_ref.extend_plan(lens, c["q_lens"], c["hkv"], c["hq"])
+    assert info.tokens_per_item == per and info.num_items == want.shape[0]
+    assert np.array_equal(np.asarray(work)[: info.work_bytes // 4].reshape(-1, 8), want)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("seed", EXTEND_SEEDS)
+def test_sweep_extend_matches_oracle(seed):
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from oracle import extend_ref
+    from paper_2601_12784_amd.workloads import build_extend
+    c = extend_case(seed)
+    print(f"extend sweep {seed}: hq={c['hq']} hkv={c['hkv']} d={c['d']} lens={c['lens'].tolist()} "
+          f"new={c['q_lens'].tolist()} scale={c['scale']:+.4f} k_mult={c['k_mult']} store={c['store']}", flush=True)
+    eb = build_extend(c["lens"], c["q_lens"], c["hq"], c["hkv"], c["d"], seed=7000 + seed, k_mult=c["k_mult"])
+    b = eb.batch
+    runner = B.ExtendAttention(c["hq"], c["hkv"], c["d"])
+    kp, vp = b.k_pool.cuda(), b.v_pool.cuda()
+    rows = eb.num_rows
+    lse = torch.empty((rows, c["hq"]), dtype=torch.float32, device="cuda")
+    out = runner(eb.q.cuda(), kp, vp, torch.from_numpy(b.block_table).cuda(), b.seq_lens, eb.q_lens, c["scale"],
+                 lse=lse, k_new=eb.k_new.cuda() if c["store"] else None,
+                 v_new=eb.v_new.cuda() if c["store"] else None)
+    torch.cuda.synchronize()
+    ro, rl = extend_ref.extend_attn(bf16_bits(eb.q), bf16_bits(b.k_pool), bf16_bits(b.v_pool), b.block_table,
+                                    b.seq_lens, eb.q_lens, c["scale"])
+    assert out.shape == (rows, c["hq"], c["d"])
+    if rows:
+        _assert_close(out.cpu().numpy(), ro, "extend out")
+        _assert_close(lse.cpu().numpy(), rl, "extend lse")
+    # the new tokens' keys and values are copies of their pool slots: a store
+    # leaves the pools bit for bit as they were
+    assert np.array_equal(bf16_bits(kp.cpu()), bf16_bits(b.k_pool))
+    assert np.array_equal(bf16_bits(vp.cpu()), bf16_bits(b.v_pool))
