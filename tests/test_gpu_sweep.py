@@ -199,3 +199,46 @@ def test_sweep_extend_matches_oracle(seed):
     # leaves the pools bit for bit as they were
     assert np.array_equal(bf16_bits(kp.cpu()), bf16_bits(b.k_pool))
     assert np.array_equal(bf16_bits(vp.cpu()), bf16_bits(b.v_pool))
+
+
+# ---------------------------------------------------------------------------
+# growing-cache decode loop (append): drawn batches, caps and planner options
+# ---------------------------------------------------------------------------
+LOOP_SEEDS = range(8)
+
+
+def loop_case(seed):
+    rng = np.random.default_rng(3000 + seed)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    g = int(rng.choice([1, 2, 3, 7, 8, 16]))
+    while hkv * g > 64:
+        hkv //= 2
+    d = int(rng.choice([64, 128]))
+    b = int(rng.integers(2, 21))
+    median = float(np.exp(rng.uniform(np.log(5), np.log(800))))
+    lens = np.exp(rng.normal(np.log(median), 1.0, size=b)).astype(np.int64).clip(1, 3000)
+    opts = dict(num_cus=int(rng.choice([1, 8, 64, 256])),
+                workers_per_cu=int(rng.choice([0, 1, 2, 4, 6, 8])),
+                chunk_pages=int(rng.integers(1, 9)) if rng.random() < 0.25 else 0,
+                min_chunk_pages=int(rng.choice([0, 1, 4])),
+                xcd_parity_skew=int(rng.choice([0, 40, -40, 250])))
+    return dict(seed=seed, hq=hkv * g, hkv=hkv, d=d, lens=lens, steps=int(rng.integers(6, 21)),
+                cap_extra_max=int(rng.choice([3, 10, 40])), opts=opts)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("seed", LOOP_SEEDS)
+def test_sweep_decode_loop_matches_oracle(seed):
+    """Every step's out and lse against the fp64 oracle on the oracle's own
+    appended pools; the final pools, block tables and free-page count bit for
+    bit (the growing-cache loop's checks, with drawn options)."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2601_12784_amd.workloads import make_decode_loop
+    from test_gpu_append import run_loop
+    c = loop_case(seed)
+    print(f"loop sweep {seed}: hq={c['hq']} hkv={c['hkv']} d={c['d']} B={c['lens'].size} "
+          f"steps={c['steps']} caps+{c['cap_extra_max']} opts={c['opts']}", flush=True)
+    run = make_decode_loop(lens=c["lens"], steps=c["steps"], cap_extra_max=c["cap_extra_max"], seed=8000 + seed,
+                           num_q_heads=c["hq"], num_kv_heads=c["hkv"], head_dim=c["d"])
+    run_loop(run, check_steps=set(range(c["steps"])), opts=B.make_opts(**c["opts"]))
