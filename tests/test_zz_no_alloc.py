@@ -99,3 +99,31 @@ def test_scratch_step_rejects_a_plan_beyond_its_array():
                                  torch.from_numpy(b.block_table).cuda(), out)
     assert e.value.status == 3   # SF_ERR_CAPACITY
     del dev
+
+
+def test_scratch_step_over_the_sweep_cases():
+    """The seeded sweep's drawn decode cases (head layouts, head dims, length
+    mixes, scales of either sign, planner options), one call after another on
+    the one array, large and small in turn: each equal to the workspace path
+    bit for bit and within the bound of the oracle. Cases whose partials do
+    not fit the array are left out (the refusal has its own test)."""
+    import dataclasses
+    from test_gpu_sweep import SEEDS, sweep_case
+    from paper_2601_12784_amd.workloads import PAGE
+    ran = 0
+    for seed in SEEDS:
+        c = sweep_case(seed)
+        b = build_batch(c["lens"], c["hq"], c["hkv"], c["d"], 5000 + seed,
+                        pool_pages=int(((c["lens"] + PAGE - 1) // PAGE).sum()) + 5)
+        b = dataclasses.replace(b, scale=c["scale"])
+        opts = B.make_opts(**c["opts"])
+        desc = B.make_desc(b.num_seqs, b.num_q_heads, b.num_kv_heads, b.head_dim, b.block_table.shape[1],
+                           b.num_pages, b.scale)
+        info, _ = B.sf_decode_attn_plan(desc, b.seq_lens, opts)
+        if info.workspace_bytes > B.SCRATCH_BYTES:
+            continue
+        _say(f"scratch sweep {seed}: hq={c['hq']} hkv={c['hkv']} d={c['d']} B={b.num_seqs} opts={c['opts']}")
+        info, ws, sc = _step_both_ways(b, opts)
+        _check(b, info, ws, sc, f"sweep {seed}")
+        ran += 1
+    assert ran >= len(SEEDS) // 2
